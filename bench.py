@@ -1,0 +1,232 @@
+#!/usr/bin/env python3
+"""Benchmark of the RRS W4A4 linear layer on one MI355X.
+
+A step is one pass of the whole hot path on one batch: rotate + runtime smooth
++ per-token INT4 quantization (rrs_rotate_smooth_quant) followed by the
+smoothing-fused W4A4 GEMM (rrs_w4a4_gemm), i.e. exactly what rrs_linear runs.
+Workload: the LLaMA-7B-shaped fused QKV projection, M=2048 tokens, K=4096,
+N=12288, smoothing group 128, on seeded synthetic outlier-laden activations and
+random N(0, 0.02^2) weights (offline weight preparation is outside the timed
+region). Inputs are resident in HBM before timing starts.
+
+value = 2*M*N*K / (time per step), effective TOPS of the whole step.
+The roofline object covers the dominant kernel (the GEMM): its average
+duration is taken from HIP events recorded around it on the launch stream.
+A decode-shaped measurement (M=8, K=8192, N=28672) reports HBM GB/s of the
+GEMM over algorithmic bytes, cycling through 4 weight copies (470 MB, more
+than the 256 MB Infinity Cache) so that every call streams its weight from HBM.
+
+Prints one JSON line.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "effective W4A4 TOPS at M=2048,K=4096,N=12288; HBM GB/s at M=8 decode"
+INT8_MFMA_PEAK_TOPS = 5000.0   # MI355X dense int8 MFMA, 5.0 POP/s
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-decode", action="store_true", help="skip the decode measurement")
+    ap.add_argument("--decode-steps", type=int, default=100)
+    return ap.parse_args()
+
+
+def qkv_step_bench(args, torch, rrs, synth):
+    w = synth.WORKLOADS["qkv"]
+    dev = torch.device("cuda:0")
+    log(f"workload qkv M={w.M} K={w.K} N={w.N} g={w.g}: generating inputs")
+    X = torch.from_numpy(synth.activations(w)).to(dev)
+    Wq, beta = rrs.prepare_weight(torch.from_numpy(synth.weights(w)).to(dev))
+    Xq = torch.empty((w.M, w.K // 2), dtype=torch.uint8, device=dev)
+    a = torch.empty((w.M,), dtype=torch.float32, device=dev)
+    s = torch.empty((w.G,), dtype=torch.float32, device=dev)
+    Y = torch.empty((w.M, w.N), dtype=torch.float16, device=dev)
+    ws = torch.empty((rrs.workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+
+    def step(evs=None):
+        if evs is not None:
+            evs[0].record()
+        rrs.rotate_smooth_quant(X, w.g, workspace=ws, out=(Xq, a, s))
+        if evs is not None:
+            evs[1].record()
+        rrs.w4a4_gemm(Xq, a, s, Wq, beta, w.g, out=Y)
+        if evs is not None:
+            evs[2].record()
+
+    log(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    log(f"timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    quant_ms = [e[0].elapsed_time(e[1]) for e in evs]
+    gemm_ms = [e[1].elapsed_time(e[2]) for e in evs]
+    step_ms = evs[0][0].elapsed_time(evs[-1][2]) / args.steps
+    return w, dict(step_ms=step_ms, wall_ms=wall * 1e3 / args.steps,
+                   quant_ms=sum(quant_ms) / len(quant_ms), gemm_ms=sum(gemm_ms) / len(gemm_ms),
+                   gemm_ms_min=min(gemm_ms), quant_ms_min=min(quant_ms))
+
+
+def decode_bench(args, torch, rrs, synth):
+    w = synth.WORKLOADS["decode"]
+    dev = torch.device("cuda:0")
+    log(f"decode M={w.M} K={w.K} N={w.N}: generating inputs")
+    X = torch.from_numpy(synth.activations(w)).to(dev)
+    Wq0, beta = rrs.prepare_weight(torch.from_numpy(synth.weights(w)).to(dev))
+    copies = [Wq0] + [Wq0.clone() for _ in range(3)]   # 4 x 117 MB > 256 MB MALL
+    Xq, a, s = rrs.rotate_smooth_quant(X, w.g)
+    Y = torch.empty((w.M, w.N), dtype=torch.float16, device=dev)
+    lws = torch.empty((rrs.linear_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
+                      device=dev)
+    for i in range(8):
+        rrs.w4a4_gemm(Xq, a, s, copies[i % 4], beta, w.g, out=Y)
+    torch.cuda.synchronize()
+    n = args.decode_steps
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    ev[0].record()
+    for i in range(n):
+        rrs.w4a4_gemm(Xq, a, s, copies[i % 4], beta, w.g, out=Y)
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    g_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(n)]
+    ev2 = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    ev2[0].record()
+    for i in range(n):
+        rrs.linear(X, copies[i % 4], beta, w.g, workspace=lws, out=Y)
+        ev2[i + 1].record()
+    torch.cuda.synchronize()
+    l_ms = [ev2[i].elapsed_time(ev2[i + 1]) for i in range(n)]
+    alg = (w.M * w.K // 2 + 4 * w.M + 4 * w.G + w.N * w.K // 2 + 4 * w.N + 2 * w.M * w.N)
+    gm = sum(g_ms) / n
+    lm = sum(l_ms) / n
+    return {
+        "config": {"workload": "decode", "M": w.M, "K": w.K, "N": w.N, "group_size": w.g},
+        "algorithmic_bytes": alg,
+        "gemm_us": round(gm * 1e3, 3),
+        "gemm_us_min": round(min(g_ms) * 1e3, 3),
+        "gemm_GBps": round(alg / (gm * 1e-3) / 1e9, 1),
+        "gemm_frac_hbm": round(alg / (gm * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "linear_us": round(lm * 1e3, 3),
+        "linear_GBps": round(alg / (lm * 1e-3) / 1e9, 1),
+        "weight_copies": 4,
+    }
+
+
+def cpu_baseline(synth):
+    """The CPU oracle as it stands, on a bounded sample of the same workload."""
+    import numpy as np
+    from oracle import rrs_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count() or 1
+    w = synth.WORKLOADS["qkv"]
+    X = synth.activations(w)
+    S = 128
+    cols = np.arange(w.N)
+    W = synth.weights(w)
+    wq = O.prepare_weight(W)          # offline, not timed
+    t0 = time.perf_counter()
+    act = O.rotate_smooth_quant(X, w.g)
+    t_quant = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    P = O.group_partials(act.q[:S], wq.q[:, cols], w.g)
+    O.output(P, act.s, act.alpha[:S], wq.beta, norm=w.K)
+    t_gemm = time.perf_counter() - t0
+    t_step = t_quant + t_gemm * (w.M / S)
+    ops = 2.0 * w.M * w.N * w.K
+    return {
+        "value": round(ops / t_step / 1e12, 6),
+        "unit": "TOPS",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": (f"quantization of all {w.M} tokens ({t_quant:.2f} s) + grouped integer "
+                   f"GEMM and epilogue for {S} of {w.M} tokens x all {w.N} outputs "
+                   f"({t_gemm:.2f} s), GEMM time scaled by {w.M // S}; step estimate "
+                   f"{t_step:.1f} s"),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    import paper_2409_20361_amd as rrs
+    import synth
+
+    if not torch.cuda.is_available():
+        sys.exit("bench.py needs a GPU")
+    rrs.lib()
+    w, r = qkv_step_bench(args, torch, rrs, synth)
+    ops = 2.0 * w.M * w.N * w.K
+    value = ops / (r["step_ms"] * 1e-3) / 1e12
+    gemm_tops = ops / (r["gemm_ms"] * 1e-3) / 1e12
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(r["step_ms"], 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int4",
+        "data": "synthetic",
+        "config": {"workload": "qkv", "M": w.M, "K": w.K, "N": w.N, "group_size": w.g,
+                   "step": "rrs_rotate_smooth_quant + rrs_w4a4_gemm"},
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "gemm_kernel (rrs_w4a4_gemm)",
+            "achieved": round(gemm_tops, 2),
+            "peak": INT8_MFMA_PEAK_TOPS,
+            "unit": "TOP/s",
+            "frac": round(gemm_tops / INT8_MFMA_PEAK_TOPS, 4),
+            "traffic": None,
+        },
+        "breakdown": {
+            "quant_us": round(r["quant_ms"] * 1e3, 2),
+            "gemm_us": round(r["gemm_ms"] * 1e3, 2),
+            "gemm_us_min": round(r["gemm_ms_min"] * 1e3, 2),
+            "wall_ms_per_step": round(r["wall_ms"], 5),
+        },
+    }
+    if not args.no_decode:
+        out["decode"] = decode_bench(args, torch, rrs, synth)
+    if not args.no_cpu:
+        log("timing the CPU oracle baseline")
+        out["cpu_baseline"] = cpu_baseline(synth)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,163 @@
+/*
+ * rrs.h - C ABI of the MI355X (gfx950) Rotated Runtime Smooth W4A4 linear layer.
+ *
+ * Method: "Rotated Runtime Smooth: Training-Free Activation Smoother for
+ * accurate INT4 inference" (arXiv 2409.20361). The online path of one linear
+ * layer rotates the activations with a Hadamard matrix (Section 3.3, Eq. 4),
+ * takes runtime channel maxima over the token batch as group smoothing scales
+ * (Eq. 1, Section 3.2), quantizes each token to symmetric INT4 (Section 2.1,
+ * Eq. 2), and multiplies against offline-rotated INT4 weights with the group
+ * scale applied to each block's integer partial sum (Eq. 3, Fig. 4 step (3)).
+ *
+ * Orientation: X is M x K (M tokens, K input channels), W is K x N (N output
+ * channels), Y = X W is M x N. (The paper writes X as N x K and W as M x K.)
+ *
+ * Conventions for every function below:
+ *  - Pointers are DEVICE pointers unless stated otherwise. The caller allocates
+ *    and owns every buffer; no function here allocates device memory or keeps
+ *    a pointer after it returns.
+ *  - Work is enqueued asynchronously on `stream` (a hipStream_t passed as
+ *    void*; NULL = the default stream). Outputs are valid once the stream has
+ *    reached that point. Calls on different streams with disjoint buffers may
+ *    run concurrently; the library holds no per-call state.
+ *  - Arguments are validated on the host before any device work, in this
+ *    order: null pointers, shapes, group size, alignment, workspace size,
+ *    device present, device architecture. The first failing check decides
+ *    the returned code and nothing is enqueued.
+ *  - Shapes: M >= 1; N >= 1 and N % 16 == 0; K a power of two with
+ *    512 <= K <= 16384. Group size g: g divides K and g is one of
+ *    64, 128, 256, 512. Every pointer must be 16-byte aligned.
+ *  - Preconditions not checked: inputs finite; `perm` a permutation of
+ *    0..K-1; buffers large enough for the stated sizes; no overlap between
+ *    inputs and outputs.
+ *  - Device-side faults surface at the caller's next synchronisation, as with
+ *    any HIP launch; launch failures are returned as RRS_ERR_HIP.
+ *
+ * Data layouts (fixed by this library; the paper does not specify them):
+ *  - X:  M x K float16, row-major.
+ *  - W:  K x N float16, row-major (the transpose of nn.Linear's weight).
+ *  - Xq: M x K/2 bytes, row-major; Wq: N x K/2 bytes, one row per output
+ *    channel. Codes are INT4 two's complement in [-7, 7], two per byte, the
+ *    low nibble holding the even channel index.
+ *  - a_scale: M float32 (per token); w_scale: N float32 (per output channel);
+ *    s_group: K/g float32 (one smoothing scale per channel group).
+ *  - Y:  M x N float16, row-major.
+ *
+ * Arithmetic: rotation, scales and epilogue in float32 with IEEE
+ * round-to-nearest-even, fp32 denormals preserved; integer partial sums are
+ * exact int32. The rotation is applied unnormalized (x H_K, entries +-1) and
+ * the 1/K of R R^T with R = H_K / sqrt(K) is folded into the output scale.
+ */
+#ifndef RRS_H_
+#define RRS_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t rrs_status;
+
+enum {
+  RRS_OK = 0,
+  RRS_ERR_NULL = -1,       /* a required pointer is NULL */
+  RRS_ERR_SHAPE = -2,      /* M, N or K outside the supported set */
+  RRS_ERR_GROUP = -3,      /* group size unsupported or not dividing K */
+  RRS_ERR_ALIGN = -4,      /* a pointer is not 16-byte aligned */
+  RRS_ERR_WORKSPACE = -5,  /* workspace smaller than the query returns */
+  RRS_ERR_NO_DEVICE = -6,  /* no HIP device visible */
+  RRS_ERR_ARCH = -7,       /* the current device is not gfx950 */
+  RRS_ERR_HIP = -8         /* a HIP runtime call or launch failed */
+};
+
+/* Human-readable name of a status code (static storage; never NULL). */
+const char* rrs_status_string(rrs_status status);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int rrs_version(void);
+
+/*
+ * Bytes of device workspace rrs_rotate_smooth_quant needs for this shape
+ * (per-workgroup channel-maximum partials plus the reduced channel maxima).
+ * Returns 0 when the shape or group size is invalid.
+ */
+size_t rrs_workspace_bytes(int M, int K, int group_size);
+
+/*
+ * Offline weight preparation (Section 3.3: weights are rotated offline and
+ * quantized per output channel; round-to-nearest stands in for GPTQ).
+ *   W       in : K x N float16, row-major.
+ *   perm    in : optional K int32 (NULL = identity). Row j of the rotated
+ *                weight becomes row perm[j]'s rotation (the static channel
+ *                reorder of Fig. 4 step (1)); pass the same perm to
+ *                rrs_rotate_smooth_quant / rrs_linear.
+ *   Wq      out: N x K/2 bytes, packed INT4 codes of u = H_K W per column.
+ *   w_scale out: N float32, beta_n = max_k |u_kn| / 7.
+ * Not on the timed path.
+ */
+rrs_status rrs_prepare_weight(const void* W, int K, int N, const int32_t* perm,
+                              void* Wq, float* w_scale, void* stream);
+
+/*
+ * Online rotate + runtime smooth + per-token INT4 quantization
+ * (Section 3.3 then Section 3.2; Eq. 1-2; Section 2.1).
+ *   X        in : M x K float16, row-major.
+ *   perm     in : optional K int32 (NULL = identity): position j of the
+ *                 rotated token takes channel perm[j].
+ *   Xq       out: M x K/2 bytes, packed codes.
+ *   a_scale  out: M float32, alpha_i.
+ *   s_group  out: K/g float32, s_b = the largest |rotated activation| over all
+ *                 M tokens and the g channels of group b.
+ *   workspace   : device scratch of at least rrs_workspace_bytes(M, K, g)
+ *                 bytes; contents on entry are ignored, on exit undefined.
+ */
+rrs_status rrs_rotate_smooth_quant(const void* X, int M, int K, int group_size,
+                                   const int32_t* perm, void* Xq, float* a_scale,
+                                   float* s_group, void* workspace,
+                                   size_t workspace_bytes, void* stream);
+
+/*
+ * W4A4 GEMM with Runtime Smooth fused into the block loop (Section 3.2,
+ * Eq. 3, Fig. 4 step (3)):
+ *   Y[i, n] = fp16( a_scale[i] * w_scale[n] / K * sum_b s_group[b] * P_b[i, n] ),
+ *   P_b[i, n] = sum over the g channels j of group b of q_x[i, j] * q_w[j, n],
+ * with every P_b an exact integer and the sum over b in float32.
+ *   Xq, a_scale, s_group: as written by rrs_rotate_smooth_quant.
+ *   Wq, w_scale         : as written by rrs_prepare_weight.
+ *   Y out               : M x N float16, row-major.
+ */
+rrs_status rrs_w4a4_gemm(const void* Xq, const float* a_scale, const float* s_group,
+                         const void* Wq, const float* w_scale, int M, int N, int K,
+                         int group_size, void* Y, void* stream);
+
+/*
+ * Bytes of workspace rrs_linear needs: rrs_workspace_bytes plus room for Xq,
+ * a_scale and s_group, each sub-buffer aligned to 256 bytes. 0 when invalid.
+ */
+size_t rrs_linear_workspace_bytes(int M, int K, int group_size);
+
+/*
+ * One RRS linear layer: rrs_rotate_smooth_quant followed by rrs_w4a4_gemm,
+ * with Xq, a_scale and s_group kept in the workspace.
+ *   X in: M x K float16; Wq, w_scale from rrs_prepare_weight (same perm);
+ *   Y out: M x N float16.
+ */
+rrs_status rrs_linear(const void* X, const void* Wq, const float* w_scale, int M, int N,
+                      int K, int group_size, const int32_t* perm, void* Y,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Test hook: the exact int32 group partials P[b][i][n] (b < K/g, i < M,
+ * n < N; G x M x N int32, row-major) from the same GEMM main loop as
+ * rrs_w4a4_gemm, before any scaling (Eq. 3's inner sums per block).
+ */
+rrs_status rrs_w4a4_gemm_partials(const void* Xq, const void* Wq, int M, int N, int K,
+                                  int group_size, int32_t* P, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RRS_H_ */

@@ -1,0 +1,34 @@
+"""MI355X (gfx950) Rotated Runtime Smooth W4A4 linear layer.
+
+A thin ctypes binding over librrs.so, the C-ABI HIP library declared in
+include/rrs.h. The binding only marshals arguments: it checks torch tensors
+(device, dtype, shape, contiguity), passes their device pointers and the
+current HIP stream, and raises RuntimeError on a non-zero status. Every step of
+the computation runs in the library's kernels. There is no fallback: if
+librrs.so is missing, every call raises.
+
+Paper: "Rotated Runtime Smooth: Training-Free Activation Smoother for accurate
+INT4 inference" (arXiv 2409.20361), Sections 3.1-3.3.
+"""
+from __future__ import annotations
+
+from ._binding import (  # noqa: F401
+    RRSError,
+    lib,
+    lib_path,
+    linear,
+    linear_workspace_bytes,
+    prepare_weight,
+    rotate_smooth_quant,
+    status_string,
+    version,
+    w4a4_gemm,
+    w4a4_gemm_partials,
+    workspace_bytes,
+)
+
+__all__ = [
+    "RRSError", "lib", "lib_path", "linear", "linear_workspace_bytes", "prepare_weight",
+    "rotate_smooth_quant", "status_string", "version", "w4a4_gemm", "w4a4_gemm_partials",
+    "workspace_bytes",
+]

@@ -1,0 +1,183 @@
+"""ctypes marshalling for librrs.so (names follow include/rrs.h without the prefix)."""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "librrs.so")
+_lib: Optional[ctypes.CDLL] = None
+
+_vp = ctypes.c_void_p
+_i = ctypes.c_int
+_sz = ctypes.c_size_t
+
+_SIGNATURES = {
+    "rrs_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
+    "rrs_version": (_i, []),
+    "rrs_workspace_bytes": (_sz, [_i, _i, _i]),
+    "rrs_linear_workspace_bytes": (_sz, [_i, _i, _i]),
+    "rrs_prepare_weight": (ctypes.c_int32, [_vp, _i, _i, _vp, _vp, _vp, _vp]),
+    "rrs_rotate_smooth_quant": (ctypes.c_int32,
+                                [_vp, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "rrs_w4a4_gemm": (ctypes.c_int32, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp]),
+    "rrs_linear": (ctypes.c_int32, [_vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp, _sz, _vp]),
+    "rrs_w4a4_gemm_partials": (ctypes.c_int32, [_vp, _vp, _i, _i, _i, _i, _vp, _vp]),
+}
+
+
+class RRSError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {status_string(code)} (status {code})")
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def lib() -> ctypes.CDLL:
+    """Load librrs.so from the package directory (built by build.py)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(
+                f"{_LIB_PATH} is missing: build it with `python -m paper_2409_20361_amd.build` "
+                "(there is no non-HIP fallback)")
+        handle = ctypes.CDLL(_LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def status_string(code: int) -> str:
+    return lib().rrs_status_string(code).decode()
+
+
+def version() -> int:
+    return lib().rrs_version()
+
+
+def workspace_bytes(M: int, K: int, g: int) -> int:
+    return lib().rrs_workspace_bytes(M, K, g)
+
+
+def linear_workspace_bytes(M: int, K: int, g: int) -> int:
+    return lib().rrs_linear_workspace_bytes(M, K, g)
+
+
+def _check(code: int, where: str) -> None:
+    if code != 0:
+        raise RRSError(code, where)
+
+
+def _stream(device: torch.device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _dev(t: torch.Tensor, name: str, dtype: torch.dtype, shape: Tuple[int, ...]) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor, got {t.device}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _perm_ptr(perm: Optional[torch.Tensor], K: int) -> Optional[int]:
+    if perm is None:
+        return None
+    return _dev(perm, "perm", torch.int32, (K,))
+
+
+def prepare_weight(W: torch.Tensor, perm: Optional[torch.Tensor] = None
+                   ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """W: K x N fp16 (the transpose of nn.Linear's weight) -> (Wq N x K/2 uint8, w_scale N f32)."""
+    K, N = W.shape
+    wp = _dev(W, "W", torch.float16, (K, N))
+    Wq = torch.empty((N, K // 2), dtype=torch.uint8, device=W.device)
+    ws = torch.empty((N,), dtype=torch.float32, device=W.device)
+    _check(lib().rrs_prepare_weight(wp, K, N, _perm_ptr(perm, K), Wq.data_ptr(), ws.data_ptr(),
+                                    _stream(W.device)), "rrs_prepare_weight")
+    return Wq, ws
+
+
+def rotate_smooth_quant(X: torch.Tensor, g: int, perm: Optional[torch.Tensor] = None,
+                        workspace: Optional[torch.Tensor] = None, out=None):
+    """X: M x K fp16 -> (Xq M x K/2 uint8, a_scale M f32, s_group K/g f32)."""
+    M, K = X.shape
+    xp = _dev(X, "X", torch.float16, (M, K))
+    if out is None:
+        Xq = torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
+        a = torch.empty((M,), dtype=torch.float32, device=X.device)
+        s = torch.empty((max(K // g, 1),), dtype=torch.float32, device=X.device)
+    else:
+        Xq, a, s = out
+    nbytes = workspace_bytes(M, K, g)
+    if workspace is None:
+        workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=X.device)
+    _check(lib().rrs_rotate_smooth_quant(
+        xp, M, K, g, _perm_ptr(perm, K), Xq.data_ptr(), a.data_ptr(), s.data_ptr(),
+        workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(X.device)),
+        "rrs_rotate_smooth_quant")
+    return Xq, a, s
+
+
+def w4a4_gemm(Xq: torch.Tensor, a_scale: torch.Tensor, s_group: torch.Tensor,
+              Wq: torch.Tensor, w_scale: torch.Tensor, g: int,
+              out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Y = fp16(a_i w_n / K * sum_b s_b P_b) (M x N)."""
+    M, Kh = Xq.shape
+    K = 2 * Kh
+    N = Wq.shape[0]
+    args = (_dev(Xq, "Xq", torch.uint8, (M, Kh)), _dev(a_scale, "a_scale", torch.float32, (M,)),
+            _dev(s_group, "s_group", torch.float32, (K // g,)),
+            _dev(Wq, "Wq", torch.uint8, (N, Kh)), _dev(w_scale, "w_scale", torch.float32, (N,)))
+    Y = out if out is not None else torch.empty((M, N), dtype=torch.float16, device=Xq.device)
+    yp = _dev(Y, "Y", torch.float16, (M, N))
+    _check(lib().rrs_w4a4_gemm(*args, M, N, K, g, yp, _stream(Xq.device)), "rrs_w4a4_gemm")
+    return Y
+
+
+def linear(X: torch.Tensor, Wq: torch.Tensor, w_scale: torch.Tensor, g: int,
+           perm: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+           out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """One RRS linear layer: X M x K fp16 -> Y M x N fp16."""
+    M, K = X.shape
+    N = Wq.shape[0]
+    xp = _dev(X, "X", torch.float16, (M, K))
+    wqp = _dev(Wq, "Wq", torch.uint8, (N, K // 2))
+    wsp = _dev(w_scale, "w_scale", torch.float32, (N,))
+    nbytes = linear_workspace_bytes(M, K, g)
+    if workspace is None:
+        workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=X.device)
+    Y = out if out is not None else torch.empty((M, N), dtype=torch.float16, device=X.device)
+    yp = _dev(Y, "Y", torch.float16, (M, N))
+    _check(lib().rrs_linear(xp, wqp, wsp, M, N, K, g, _perm_ptr(perm, K), yp,
+                            workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                            _stream(X.device)), "rrs_linear")
+    return Y
+
+
+def w4a4_gemm_partials(Xq: torch.Tensor, Wq: torch.Tensor, g: int) -> torch.Tensor:
+    """Exact int32 group partials P[b, i, n] from the GEMM main loop (test hook)."""
+    M, Kh = Xq.shape
+    K = 2 * Kh
+    N = Wq.shape[0]
+    xp = _dev(Xq, "Xq", torch.uint8, (M, Kh))
+    wp = _dev(Wq, "Wq", torch.uint8, (N, Kh))
+    P = torch.empty((K // g, M, N), dtype=torch.int32, device=Xq.device)
+    _check(lib().rrs_w4a4_gemm_partials(xp, wp, M, N, K, g, P.data_ptr(), _stream(Xq.device)),
+           "rrs_w4a4_gemm_partials")
+    return P

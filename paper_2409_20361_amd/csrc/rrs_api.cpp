@@ -1,0 +1,208 @@
+// C ABI of the RRS W4A4 linear layer: host-side validation, device and
+// architecture checks, workspace layout, and launches on the caller's stream.
+// Every check runs on the host before any device work is enqueued.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+
+#include "rrs.h"
+#include "rrs_internal.h"
+
+namespace {
+
+constexpr int kVersion = 100;  // 0.1.0
+constexpr int kMaxDevices = 64;
+
+bool is_aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool valid_k(int K) { return K >= 512 && K <= 16384 && (K & (K - 1)) == 0; }
+bool valid_m(int M) { return M >= 1; }
+bool valid_n(int N) { return N >= 1 && (N % 16) == 0; }
+bool valid_group(int K, int g) {
+  return (g == 64 || g == 128 || g == 256 || g == 512) && K % g == 0;
+}
+
+bool debug_enabled() {
+  static const bool on = [] {
+    const char* v = std::getenv("RRS_DEBUG");
+    return v != nullptr && v[0] != '\0' && v[0] != '0';
+  }();
+  return on;
+}
+
+// 0 = unknown, 1 = gfx950, 2 = other architecture.
+std::atomic<int> g_arch_cache[kMaxDevices];
+
+rrs_status check_device() {
+  int count = 0;
+  if (hipGetDeviceCount(&count) != hipSuccess || count <= 0) {
+    (void)hipGetLastError();
+    return RRS_ERR_NO_DEVICE;
+  }
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return RRS_ERR_NO_DEVICE;
+  }
+  int cached = (dev >= 0 && dev < kMaxDevices) ? g_arch_cache[dev].load() : 0;
+  if (cached == 0) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return RRS_ERR_HIP;
+    }
+    cached = (std::strncmp(prop.gcnArchName, "gfx950", 6) == 0) ? 1 : 2;
+    if (dev >= 0 && dev < kMaxDevices) g_arch_cache[dev].store(cached);
+  }
+  return cached == 1 ? RRS_OK : RRS_ERR_ARCH;
+}
+
+rrs_status from_hip(hipError_t e) { return e == hipSuccess ? RRS_OK : RRS_ERR_HIP; }
+
+size_t linear_ws_bytes(int M, int K, int g) {
+  return rrs::quant_workspace_bytes(M, K) + rrs::align256((size_t)M * (K / 2)) +
+         rrs::align256((size_t)M * 4) + rrs::align256((size_t)(K / g) * 4);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* rrs_status_string(rrs_status s) {
+  switch (s) {
+    case RRS_OK: return "RRS_OK";
+    case RRS_ERR_NULL: return "RRS_ERR_NULL: a required pointer is NULL";
+    case RRS_ERR_SHAPE:
+      return "RRS_ERR_SHAPE: need M >= 1, N >= 1 with N % 16 == 0, K a power of two in "
+             "[512, 16384]";
+    case RRS_ERR_GROUP: return "RRS_ERR_GROUP: group size must be 64, 128, 256 or 512 and divide K";
+    case RRS_ERR_ALIGN: return "RRS_ERR_ALIGN: every pointer must be 16-byte aligned";
+    case RRS_ERR_WORKSPACE: return "RRS_ERR_WORKSPACE: workspace smaller than required";
+    case RRS_ERR_NO_DEVICE: return "RRS_ERR_NO_DEVICE: no HIP device visible";
+    case RRS_ERR_ARCH: return "RRS_ERR_ARCH: current device is not gfx950";
+    case RRS_ERR_HIP: return "RRS_ERR_HIP: a HIP call or kernel launch failed";
+    default: return "RRS_ERR_UNKNOWN";
+  }
+}
+
+int rrs_version(void) { return kVersion; }
+
+size_t rrs_workspace_bytes(int M, int K, int group_size) {
+  if (!valid_m(M) || !valid_k(K) || !valid_group(K, group_size)) return 0;
+  return rrs::quant_workspace_bytes(M, K);
+}
+
+size_t rrs_linear_workspace_bytes(int M, int K, int group_size) {
+  if (!valid_m(M) || !valid_k(K) || !valid_group(K, group_size)) return 0;
+  return linear_ws_bytes(M, K, group_size);
+}
+
+rrs_status rrs_prepare_weight(const void* W, int K, int N, const int32_t* perm, void* Wq,
+                              float* w_scale, void* stream) {
+  if (debug_enabled())
+    std::fprintf(stderr, "[rrs] prepare_weight W=%p K=%d N=%d perm=%p Wq=%p w_scale=%p\n", W, K,
+                 N, (const void*)perm, Wq, (void*)w_scale);
+  if (!W || !Wq || !w_scale) return RRS_ERR_NULL;
+  if (!valid_k(K) || !valid_n(N)) return RRS_ERR_SHAPE;
+  if (!is_aligned(W) || !is_aligned(Wq) || !is_aligned(w_scale) || (perm && !is_aligned(perm)))
+    return RRS_ERR_ALIGN;
+  if (rrs_status s = check_device()) return s;
+  return from_hip(rrs::launch_prepare_weight(static_cast<const uint16_t*>(W), K, N, perm,
+                                             static_cast<uint8_t*>(Wq), w_scale,
+                                             static_cast<hipStream_t>(stream)));
+}
+
+rrs_status rrs_rotate_smooth_quant(const void* X, int M, int K, int group_size,
+                                   const int32_t* perm, void* Xq, float* a_scale,
+                                   float* s_group, void* workspace, size_t workspace_bytes,
+                                   void* stream) {
+  if (debug_enabled())
+    std::fprintf(stderr,
+                 "[rrs] rotate_smooth_quant X=%p M=%d K=%d g=%d perm=%p Xq=%p a=%p s=%p ws=%p "
+                 "(%zu B)\n",
+                 X, M, K, group_size, (const void*)perm, Xq, (void*)a_scale, (void*)s_group,
+                 workspace, workspace_bytes);
+  if (!X || !Xq || !a_scale || !s_group || !workspace) return RRS_ERR_NULL;
+  if (!valid_m(M) || !valid_k(K)) return RRS_ERR_SHAPE;
+  if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
+  if (!is_aligned(X) || !is_aligned(Xq) || !is_aligned(a_scale) || !is_aligned(s_group) ||
+      !is_aligned(workspace) || (perm && !is_aligned(perm)))
+    return RRS_ERR_ALIGN;
+  if (workspace_bytes < rrs::quant_workspace_bytes(M, K)) return RRS_ERR_WORKSPACE;
+  if (rrs_status s = check_device()) return s;
+  return from_hip(rrs::launch_rotate_smooth_quant(
+      static_cast<const uint16_t*>(X), M, K, group_size, perm, static_cast<uint8_t*>(Xq),
+      a_scale, s_group, workspace, static_cast<hipStream_t>(stream)));
+}
+
+rrs_status rrs_w4a4_gemm(const void* Xq, const float* a_scale, const float* s_group,
+                         const void* Wq, const float* w_scale, int M, int N, int K,
+                         int group_size, void* Y, void* stream) {
+  if (debug_enabled())
+    std::fprintf(stderr,
+                 "[rrs] w4a4_gemm Xq=%p a=%p s=%p Wq=%p w=%p M=%d N=%d K=%d g=%d Y=%p\n", Xq,
+                 (const void*)a_scale, (const void*)s_group, Wq, (const void*)w_scale, M, N, K,
+                 group_size, Y);
+  if (!Xq || !a_scale || !s_group || !Wq || !w_scale || !Y) return RRS_ERR_NULL;
+  if (!valid_m(M) || !valid_n(N) || !valid_k(K)) return RRS_ERR_SHAPE;
+  if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
+  if (!is_aligned(Xq) || !is_aligned(a_scale) || !is_aligned(s_group) || !is_aligned(Wq) ||
+      !is_aligned(w_scale) || !is_aligned(Y))
+    return RRS_ERR_ALIGN;
+  if (rrs_status s = check_device()) return s;
+  return from_hip(rrs::launch_w4a4_gemm(
+      static_cast<const uint8_t*>(Xq), a_scale, s_group, static_cast<const uint8_t*>(Wq),
+      w_scale, M, N, K, group_size, static_cast<uint16_t*>(Y),
+      static_cast<hipStream_t>(stream)));
+}
+
+rrs_status rrs_linear(const void* X, const void* Wq, const float* w_scale, int M, int N,
+                      int K, int group_size, const int32_t* perm, void* Y, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+  if (debug_enabled())
+    std::fprintf(stderr,
+                 "[rrs] linear X=%p Wq=%p w=%p M=%d N=%d K=%d g=%d perm=%p Y=%p ws=%p (%zu B)\n",
+                 X, Wq, (const void*)w_scale, M, N, K, group_size, (const void*)perm, Y,
+                 workspace, workspace_bytes);
+  if (!X || !Wq || !w_scale || !Y || !workspace) return RRS_ERR_NULL;
+  if (!valid_m(M) || !valid_n(N) || !valid_k(K)) return RRS_ERR_SHAPE;
+  if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
+  if (!is_aligned(X) || !is_aligned(Wq) || !is_aligned(w_scale) || !is_aligned(Y) ||
+      !is_aligned(workspace) || (perm && !is_aligned(perm)))
+    return RRS_ERR_ALIGN;
+  if (workspace_bytes < linear_ws_bytes(M, K, group_size)) return RRS_ERR_WORKSPACE;
+  if (rrs_status s = check_device()) return s;
+
+  char* ws = static_cast<char*>(workspace);
+  void* qws = ws;
+  ws += rrs::quant_workspace_bytes(M, K);
+  uint8_t* xq = reinterpret_cast<uint8_t*>(ws);
+  ws += rrs::align256((size_t)M * (K / 2));
+  float* a = reinterpret_cast<float*>(ws);
+  ws += rrs::align256((size_t)M * 4);
+  float* s = reinterpret_cast<float*>(ws);
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = rrs::launch_rotate_smooth_quant(static_cast<const uint16_t*>(X), M, K,
+                                                 group_size, perm, xq, a, s, qws, st);
+  if (e != hipSuccess) return RRS_ERR_HIP;
+  return from_hip(rrs::launch_w4a4_gemm(xq, a, s, static_cast<const uint8_t*>(Wq), w_scale, M,
+                                        N, K, group_size, static_cast<uint16_t*>(Y), st));
+}
+
+rrs_status rrs_w4a4_gemm_partials(const void* Xq, const void* Wq, int M, int N, int K,
+                                  int group_size, int32_t* P, void* stream) {
+  if (!Xq || !Wq || !P) return RRS_ERR_NULL;
+  if (!valid_m(M) || !valid_n(N) || !valid_k(K)) return RRS_ERR_SHAPE;
+  if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
+  if (!is_aligned(Xq) || !is_aligned(Wq) || !is_aligned(P)) return RRS_ERR_ALIGN;
+  if (rrs_status s = check_device()) return s;
+  return from_hip(rrs::launch_w4a4_gemm_partials(static_cast<const uint8_t*>(Xq),
+                                                 static_cast<const uint8_t*>(Wq), M, N, K,
+                                                 group_size, P, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,190 @@
+// Internal device helpers shared by the rotate/quantize and weight-preparation
+// kernels: fp16 row loads, the register/LDS fast Walsh-Hadamard transform and
+// workgroup max reductions. gfx950 only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rrs {
+
+// Threads per workgroup for the row kernels: one row of K elements is spread
+// over 256 threads, E = K / 256 consecutive elements per thread.
+constexpr int kRowThreads = 256;
+constexpr int kLogRowThreads = 8;
+
+constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x >> 1); }
+
+// LDS row buffer: one pad word per 16 floats keeps the strided transposes of
+// the FWHT free of bank conflicts.
+__device__ __forceinline__ int lds_pad(int p) { return p + (p >> 4); }
+constexpr int lds_row_floats(int K) { return K + K / 16; }
+
+__device__ __forceinline__ float half_to_float(uint32_t bits16) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
+}
+
+// v[e] = float(src[e]) for e < E; src aligned to min(16, 2E) bytes.
+template <int E>
+__device__ __forceinline__ void load_halves(const uint16_t* __restrict__ src, float (&v)[E]) {
+  if constexpr (E >= 8) {
+    const uint4* s4 = reinterpret_cast<const uint4*>(src);
+#pragma unroll
+    for (int c = 0; c < E / 8; ++c) {
+      const uint4 w = s4[c];
+      const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        v[c * 8 + 2 * m] = half_to_float(ws[m] & 0xFFFFu);
+        v[c * 8 + 2 * m + 1] = half_to_float(ws[m] >> 16);
+      }
+    }
+  } else if constexpr (E == 4) {
+    const uint2 w = *reinterpret_cast<const uint2*>(src);
+    v[0] = half_to_float(w.x & 0xFFFFu);
+    v[1] = half_to_float(w.x >> 16);
+    v[2] = half_to_float(w.y & 0xFFFFu);
+    v[3] = half_to_float(w.y >> 16);
+  } else {
+    static_assert(E == 2, "E must be a power of two >= 2");
+    const uint32_t w = *reinterpret_cast<const uint32_t*>(src);
+    v[0] = half_to_float(w & 0xFFFFu);
+    v[1] = half_to_float(w >> 16);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Fast Walsh-Hadamard transform of one row (y = x H_K, unnormalized).
+//
+// Stage order is h = 1, 2, 4, ..., K/2 and every butterfly output is a single
+// rounded fp32 add or subtract, so the result is bit-identical to the
+// canonical sequential definition. The K = 2^(8+L) indices are covered by
+// "windows" of L = log2(E) index bits: in the window starting at bit `lo`,
+// thread t holds the E elements
+//   p(t, e) = (t mod 2^lo) | (e << lo) | ((t >> lo) << (lo + L)),
+// so the window's stages are in-register butterflies. Windows advance through
+// the bits in increasing order (the last one is shifted down to end at bit
+// log2 K and only applies the stages not yet done); between windows the row
+// goes through LDS.
+// ---------------------------------------------------------------------------
+
+template <int E, int J>
+__device__ __forceinline__ void fwht_stage(float (&v)[E]) {
+  constexpr int h = 1 << J;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    if ((e & h) == 0) {
+      const float a = v[e];
+      const float b = v[e + h];
+      v[e] = a + b;
+      v[e + h] = a - b;
+    }
+  }
+}
+
+template <int E, int J0, int J1>
+__device__ __forceinline__ void fwht_stages(float (&v)[E]) {
+  if constexpr (J0 < J1) {
+    fwht_stage<E, J0>(v);
+    fwht_stages<E, J0 + 1, J1>(v);
+  }
+}
+
+__device__ __forceinline__ int window_index(int t, int e, int lo, int L) {
+  return (t & ((1 << lo) - 1)) | (e << lo) | ((t >> lo) << (lo + L));
+}
+
+template <int K>
+struct FwhtShape {
+  static constexpr int E = K / kRowThreads;
+  static constexpr int L = ilog2(E);
+  static constexpr int LOGK = ilog2(K);
+  static constexpr int kWindows = (LOGK + L - 1) / L;
+  static constexpr int kFinalLo = LOGK - L;  // == kLogRowThreads
+  static_assert(E >= 2 && (1 << L) == E, "K must be 2^(8+L), L >= 1");
+};
+
+template <int K, int W>
+__device__ __forceinline__ void fwht_windows(float (&v)[FwhtShape<K>::E], float* lds, int t) {
+  using S = FwhtShape<K>;
+  if constexpr (W < S::kWindows) {
+    constexpr int prev_lo = (W - 1) * S::L;
+    constexpr int lo = (W * S::L < S::LOGK - S::L) ? W * S::L : S::LOGK - S::L;
+    constexpr int first = W * S::L - lo;  // first e-bit not yet transformed
+    __syncthreads();  // earlier readers of lds are done
+#pragma unroll
+    for (int e = 0; e < S::E; ++e) lds[lds_pad(window_index(t, e, prev_lo, S::L))] = v[e];
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < S::E; ++e) v[e] = lds[lds_pad(window_index(t, e, lo, S::L))];
+    fwht_stages<S::E, first, S::L>(v);
+    fwht_windows<K, W + 1>(v, lds, t);
+  }
+}
+
+// On entry v[e] holds element t*E + e of the row. On exit v[e] holds element
+// t + e * 256 of x H_K. `lds` must hold lds_row_floats(K) floats; it is
+// clobbered. Must be called by all 256 threads of the workgroup.
+template <int K>
+__device__ __forceinline__ void fwht_row(float (&v)[FwhtShape<K>::E], float* lds, int t) {
+  using S = FwhtShape<K>;
+  fwht_stages<S::E, 0, S::L>(v);
+  fwht_windows<K, 1>(v, lds, t);
+}
+
+// ---------------------------------------------------------------------------
+// Reductions (values are non-negative and finite, so fmaxf is exact).
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+
+// Max over the 256 threads of the workgroup; `red` is 4 floats of LDS.
+__device__ __forceinline__ float block_max256(float x, float* red) {
+  x = wave_max(x);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+// Symmetric INT4 code of v: clamp(rint(v), -7, 7) as a 4-bit two's complement nibble.
+__device__ __forceinline__ uint32_t int4_nibble(float v) {
+  const float q = fminf(fmaxf(__builtin_rintf(v), -7.0f), 7.0f);
+  return (uint32_t)((int)q) & 0xFu;
+}
+
+// Store E/2 packed bytes (E nibbles, low nibble = even index) at dst.
+template <int E>
+__device__ __forceinline__ void store_nibbles(uint8_t* __restrict__ dst, const uint32_t (&nib)[E]) {
+  if constexpr (E >= 8) {
+    uint32_t words[E / 8];
+#pragma unroll
+    for (int w = 0; w < E / 8; ++w) {
+      uint32_t x = 0;
+#pragma unroll
+      for (int n = 0; n < 8; ++n) x |= nib[w * 8 + n] << (4 * n);
+      words[w] = x;
+    }
+    if constexpr (E == 8) {
+      *reinterpret_cast<uint32_t*>(dst) = words[0];
+    } else if constexpr (E == 16) {
+      *reinterpret_cast<uint2*>(dst) = make_uint2(words[0], words[1]);
+    } else {
+#pragma unroll
+      for (int c = 0; c < E / 32; ++c)
+        reinterpret_cast<uint4*>(dst)[c] =
+            make_uint4(words[4 * c], words[4 * c + 1], words[4 * c + 2], words[4 * c + 3]);
+    }
+  } else if constexpr (E == 4) {
+    const uint32_t x = nib[0] | (nib[1] << 4) | (nib[2] << 8) | (nib[3] << 12);
+    *reinterpret_cast<uint16_t*>(dst) = (uint16_t)x;
+  } else {
+    *dst = (uint8_t)(nib[0] | (nib[1] << 4));
+  }
+}
+
+}  // namespace rrs

@@ -1,0 +1,32 @@
+// Internal launchers called by the C ABI layer (rrs_api.cpp). Each one
+// enqueues kernels on `stream` and returns hipGetLastError(). Arguments are
+// already validated by the caller.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace rrs {
+
+// Channel-max partials: one row of K floats per workgroup of the first pass.
+int quant_partial_rows(int M);
+size_t quant_workspace_bytes(int M, int K);
+
+hipError_t launch_rotate_smooth_quant(const uint16_t* X, int M, int K, int g,
+                                      const int32_t* perm, uint8_t* Xq, float* a_scale,
+                                      float* s_group, void* workspace, hipStream_t stream);
+
+hipError_t launch_prepare_weight(const uint16_t* W, int K, int N, const int32_t* perm,
+                                 uint8_t* Wq, float* w_scale, hipStream_t stream);
+
+hipError_t launch_w4a4_gemm(const uint8_t* Xq, const float* a_scale, const float* s_group,
+                            const uint8_t* Wq, const float* w_scale, int M, int N, int K,
+                            int g, uint16_t* Y, hipStream_t stream);
+
+hipError_t launch_w4a4_gemm_partials(const uint8_t* Xq, const uint8_t* Wq, int M, int N,
+                                     int K, int g, int32_t* P, hipStream_t stream);
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+}  // namespace rrs

@@ -1,0 +1,94 @@
+// Offline weight preparation (Section 3.3: weights are rotated offline and
+// quantized per output channel; round-to-nearest stands in for GPTQ).
+//
+// For each output channel n (a column of W, K x N row-major):
+//   u = H_K W[:, n]                 (same FWHT and stage order as activations)
+//   u'_j = u_{perm[j]}              (optional static reorder, Fig. 4 step (1))
+//   b_n = max_j |u_j|, winv = fl(7 / b_n), beta_n = fl(b_n / 7)
+//   code_j = clamp(rint(fl(u'_j * winv)), -7, 7), packed into Wq[n][j / 2].
+// A workgroup stages C = 32768 / K whole columns in LDS (139 KB), then
+// transforms and quantizes them one after another.
+#include "rrs_device.h"
+#include "rrs_internal.h"
+
+namespace rrs {
+namespace {
+
+template <int K>
+__global__ __launch_bounds__(kRowThreads) void prep_weight_kernel(
+    const uint16_t* __restrict__ W, int N, const int32_t* __restrict__ perm,
+    uint8_t* __restrict__ Wq, float* __restrict__ w_scale) {
+  using S = FwhtShape<K>;
+  constexpr int E = S::E;
+  constexpr int C = 32768 / K;
+  constexpr int kCol = lds_row_floats(K);
+  __shared__ float lds[C * kCol];
+  __shared__ float red[4];
+  const int t = threadIdx.x;
+  const int n0 = blockIdx.x * C;
+
+  // Stage C columns, column c at lds[c * kCol + pad(k)].
+  for (int idx = t; idx < K * C; idx += kRowThreads) {
+    const int c = idx % C;
+    const int k = idx / C;
+    const int n = n0 + c;
+    const float w = (n < N) ? half_to_float(W[(size_t)k * N + n]) : 0.0f;
+    lds[c * kCol + lds_pad(k)] = w;
+  }
+  __syncthreads();
+
+  int src[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) src[e] = perm ? perm[t * E + e] : t * E + e;
+
+  for (int c = 0; c < C; ++c) {
+    const int n = n0 + c;
+    if (n >= N) break;  // uniform across the workgroup
+    float* col = lds + c * kCol;
+    float v[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) v[e] = col[lds_pad(t * E + e)];
+    fwht_row<K>(v, col, t);
+    float lm = 0.0f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) lm = fmaxf(lm, fabsf(v[e]));
+    const float b = block_max256(lm, red);  // contains barriers
+#pragma unroll
+    for (int e = 0; e < E; ++e) col[lds_pad(t + e * kRowThreads)] = v[e];
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < E; ++e) v[e] = col[lds_pad(src[e])];
+    const float winv = (b == 0.0f) ? 0.0f : __fdiv_rn(7.0f, b);
+    uint32_t nib[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) nib[e] = int4_nibble(v[e] * winv);
+    store_nibbles<E>(Wq + (size_t)n * (K / 2) + (size_t)t * (E / 2), nib);
+    if (t == 0) w_scale[n] = __fdiv_rn(b, 7.0f);
+  }
+}
+
+template <int K>
+hipError_t launch_k(const uint16_t* W, int N, const int32_t* perm, uint8_t* Wq,
+                    float* w_scale, hipStream_t stream) {
+  constexpr int C = 32768 / K;
+  const int grid = (N + C - 1) / C;
+  prep_weight_kernel<K><<<grid, kRowThreads, 0, stream>>>(W, N, perm, Wq, w_scale);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_prepare_weight(const uint16_t* W, int K, int N, const int32_t* perm,
+                                 uint8_t* Wq, float* w_scale, hipStream_t stream) {
+  switch (K) {
+    case 512: return launch_k<512>(W, N, perm, Wq, w_scale, stream);
+    case 1024: return launch_k<1024>(W, N, perm, Wq, w_scale, stream);
+    case 2048: return launch_k<2048>(W, N, perm, Wq, w_scale, stream);
+    case 4096: return launch_k<4096>(W, N, perm, Wq, w_scale, stream);
+    case 8192: return launch_k<8192>(W, N, perm, Wq, w_scale, stream);
+    case 16384: return launch_k<16384>(W, N, perm, Wq, w_scale, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace rrs

@@ -1,0 +1,185 @@
+"""Host-only checks of the C ABI (no GPU needed): librrs.so loads, exports
+every function include/rrs.h declares, and rejects invalid arguments with the
+documented status code before touching any device.
+
+The fake pointers used here are never dereferenced: every call below fails a
+host-side check that comes before the device check. The one test that reaches
+the device check only runs where no GPU is visible.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2409_20361_amd as rrs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rrs.h")
+
+OK, NULL, SHAPE, GROUP, ALIGN, WS, NODEV, ARCH, HIP = 0, -1, -2, -3, -4, -5, -6, -7, -8
+P = 0x10000     # 16-byte aligned fake pointer (never dereferenced)
+MIS = 0x10004   # misaligned fake pointer
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(rrs_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = rrs.lib()
+    names = _declared()
+    assert {"rrs_rotate_smooth_quant", "rrs_w4a4_gemm", "rrs_linear"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+    # and they are real dynamic symbols of the shared object
+    raw = ctypes.CDLL(rrs.lib_path())
+    for n in names:
+        getattr(raw, n)
+
+
+def test_status_strings_and_version():
+    for code in (OK, NULL, SHAPE, GROUP, ALIGN, WS, NODEV, ARCH, HIP):
+        s = rrs.status_string(code)
+        assert s.startswith("RRS_")
+    assert rrs.status_string(-99) == "RRS_ERR_UNKNOWN"
+    assert rrs.version() >= 100
+
+
+def test_workspace_queries():
+    lib = rrs.lib()
+    for M, K, g in ((16, 512, 128), (2048, 4096, 128), (8, 8192, 128), (8192, 8192, 64),
+                    (3, 16384, 512)):
+        q = lib.rrs_workspace_bytes(M, K, g)
+        # 256 partial rows of K floats plus the K channel maxima, 256-byte aligned
+        assert q == 256 * K * 4 + ((K * 4 + 255) // 256) * 256
+        lw = lib.rrs_linear_workspace_bytes(M, K, g)
+        a256 = lambda x: (x + 255) // 256 * 256  # noqa: E731
+        assert lw == q + a256(M * K // 2) + a256(4 * M) + a256(4 * (K // g))
+    for bad in ((0, 512, 128), (16, 500, 128), (16, 256, 64), (16, 32768, 128),
+                (16, 512, 32), (16, 512, 1024), (16, 512, 96)):
+        assert lib.rrs_workspace_bytes(*bad) == 0
+        assert lib.rrs_linear_workspace_bytes(*bad) == 0
+
+
+def _rsq(**kw):
+    a = dict(X=P, M=16, K=512, g=128, perm=None, Xq=P, a=P, s=P, ws=P, wsb=1 << 30)
+    a.update(kw)
+    return rrs.lib().rrs_rotate_smooth_quant(a["X"], a["M"], a["K"], a["g"], a["perm"], a["Xq"],
+                                             a["a"], a["s"], a["ws"], a["wsb"], None)
+
+
+def _gemm(**kw):
+    a = dict(Xq=P, a=P, s=P, Wq=P, w=P, M=16, N=512, K=512, g=128, Y=P)
+    a.update(kw)
+    return rrs.lib().rrs_w4a4_gemm(a["Xq"], a["a"], a["s"], a["Wq"], a["w"], a["M"], a["N"],
+                                   a["K"], a["g"], a["Y"], None)
+
+
+def _lin(**kw):
+    a = dict(X=P, Wq=P, w=P, M=16, N=512, K=512, g=128, perm=None, Y=P, ws=P, wsb=1 << 30)
+    a.update(kw)
+    return rrs.lib().rrs_linear(a["X"], a["Wq"], a["w"], a["M"], a["N"], a["K"], a["g"],
+                                a["perm"], a["Y"], a["ws"], a["wsb"], None)
+
+
+def _prep(**kw):
+    a = dict(W=P, K=512, N=512, perm=None, Wq=P, w=P)
+    a.update(kw)
+    return rrs.lib().rrs_prepare_weight(a["W"], a["K"], a["N"], a["perm"], a["Wq"], a["w"], None)
+
+
+def _parts(**kw):
+    a = dict(Xq=P, Wq=P, M=16, N=512, K=512, g=128, P=P)
+    a.update(kw)
+    return rrs.lib().rrs_w4a4_gemm_partials(a["Xq"], a["Wq"], a["M"], a["N"], a["K"], a["g"],
+                                            a["P"], None)
+
+
+@pytest.mark.parametrize("fn,key", [
+    (_rsq, "X"), (_rsq, "Xq"), (_rsq, "a"), (_rsq, "s"), (_rsq, "ws"),
+    (_gemm, "Xq"), (_gemm, "a"), (_gemm, "s"), (_gemm, "Wq"), (_gemm, "w"), (_gemm, "Y"),
+    (_lin, "X"), (_lin, "Wq"), (_lin, "w"), (_lin, "Y"), (_lin, "ws"),
+    (_prep, "W"), (_prep, "Wq"), (_prep, "w"),
+    (_parts, "Xq"), (_parts, "Wq"), (_parts, "P"),
+])
+def test_null_pointers(fn, key):
+    assert fn(**{key: None}) == NULL
+
+
+@pytest.mark.parametrize("kw", [dict(M=0), dict(M=-3), dict(K=500), dict(K=256),
+                                dict(K=32768), dict(K=0)])
+def test_bad_shapes_quant(kw):
+    assert _rsq(**kw) == SHAPE
+
+
+@pytest.mark.parametrize("fn", [_gemm, _lin, _parts])
+@pytest.mark.parametrize("kw", [dict(N=0), dict(N=24), dict(N=-16), dict(M=0), dict(K=768),
+                                dict(K=131072)])
+def test_bad_shapes_gemm(fn, kw):
+    assert fn(**kw) == SHAPE
+
+
+@pytest.mark.parametrize("kw", [dict(K=1000), dict(N=8), dict(N=0)])
+def test_bad_shapes_prep(kw):
+    assert _prep(**kw) == SHAPE
+
+
+@pytest.mark.parametrize("fn", [_rsq, _gemm, _lin, _parts])
+@pytest.mark.parametrize("g", [0, 1, 32, 96, 1024, -128])
+def test_bad_group(fn, g):
+    assert fn(g=g) == GROUP
+
+
+def test_group_must_divide_k():
+    # g = K passes the group check and fails the later workspace check
+    assert _rsq(K=512, g=512, wsb=0) == WS
+    assert _rsq(K=512, g=1024) == GROUP
+    assert _rsq(K=16384, g=512, wsb=0) == WS
+
+
+@pytest.mark.parametrize("fn,key", [
+    (_rsq, "X"), (_rsq, "Xq"), (_rsq, "a"), (_rsq, "s"), (_rsq, "ws"), (_rsq, "perm"),
+    (_gemm, "Xq"), (_gemm, "Wq"), (_gemm, "Y"), (_gemm, "w"),
+    (_lin, "X"), (_lin, "Y"), (_lin, "perm"), (_lin, "ws"),
+    (_prep, "W"), (_prep, "Wq"), (_prep, "perm"),
+    (_parts, "P"),
+])
+def test_misaligned(fn, key):
+    assert fn(**{key: MIS}) == ALIGN
+
+
+def test_workspace_too_small():
+    need = rrs.workspace_bytes(16, 512, 128)
+    assert _rsq(wsb=need - 1) == WS
+    assert _rsq(wsb=0) == WS
+    need_l = rrs.linear_workspace_bytes(16, 512, 128)
+    assert _lin(wsb=need_l - 1) == WS
+
+
+def test_check_order():
+    # null beats shape beats group beats alignment beats workspace
+    assert _rsq(X=None, M=0, g=3, Xq=MIS, wsb=0) == NULL
+    assert _rsq(M=0, g=3, Xq=MIS, wsb=0) == SHAPE
+    assert _rsq(g=3, Xq=MIS, wsb=0) == GROUP
+    assert _rsq(Xq=MIS, wsb=0) == ALIGN
+
+
+def _gpu_visible():
+    try:
+        import torch
+        return torch.cuda.device_count() > 0
+    except Exception:  # pragma: no cover
+        return False
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="reaches the device check; only meaningful "
+                    "(and only safe with fake pointers) where no GPU is visible")
+def test_no_device():
+    assert _rsq() == NODEV
+    assert _gemm() == NODEV
+    assert _lin() == NODEV
+    assert _prep() == NODEV
+    assert _parts() == NODEV

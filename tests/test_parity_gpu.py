@@ -1,0 +1,260 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Codes (Xq, Wq), scales (alpha, beta, s) and the int32 group partials must be
+bit-exact with the oracle's canonical binary32 mode; a code may differ only at a
+flagged rounding boundary (counted). Outputs Y must be within the tolerance of
+tests/_gpu_util.check_y. Inputs come from the seeded generators in synth/.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import rrs_oracle as O
+from tests._gpu_util import check_codes, check_y, to_gpu, to_np
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2409_20361_amd as rrs
+    rrs.lib()
+
+
+def _rrs():
+    import paper_2409_20361_amd as rrs
+    return rrs
+
+
+def _quant_case(X, g, perm=None, label=""):
+    rrs = _rrs()
+    print(f"[case] quant {label} M={X.shape[0]} K={X.shape[1]} g={g} perm={perm is not None}",
+          flush=True)
+    act = O.rotate_smooth_quant(X, g, perm=perm)
+    Xq, a, s = rrs.rotate_smooth_quant(to_gpu(X), g,
+                                       perm=None if perm is None else to_gpu(perm))
+    np.testing.assert_array_equal(to_np(s), act.s, err_msg=f"{label}: s_group")
+    np.testing.assert_array_equal(to_np(a), act.alpha, err_msg=f"{label}: alpha")
+    flips = check_codes(to_np(Xq), act, label)
+    assert flips == 0 or flips < 1e-6 * X.size
+    return act, (Xq, a, s)
+
+
+# ------------------------------------------------------------------ quantization
+
+@pytest.mark.parametrize("seed", [1, 2, 3, 4])
+def test_quant_tiny(seed):
+    w = synth.WORKLOADS["tiny"]
+    _quant_case(synth.activations(w, seed), w.g, label=f"tiny/{seed}")
+
+
+@pytest.mark.parametrize("name", ["qkv", "decode", "gateup", "large"])
+def test_quant_full_size(name):
+    w = synth.WORKLOADS[name]
+    _quant_case(synth.activations(w), w.g, label=name)
+
+
+@pytest.mark.parametrize("M,K,g", [
+    (1, 512, 64), (3, 1024, 128), (37, 2048, 256), (300, 4096, 512), (5, 8192, 64),
+    (2, 16384, 128), (257, 512, 512), (1, 16384, 64),
+])
+def test_quant_ragged(M, K, g):
+    w = synth.custom("r", M, K, 16, g, 100 + M + K, n_chan=max(1, K // 100),
+                     n_spike=max(1, M * K // 5000), spike_mag=(100, 500))
+    _quant_case(synth.activations(w), g, label=f"ragged {M}x{K}/g{g}")
+
+
+@pytest.mark.parametrize("K,g", [(512, 128), (4096, 128), (8192, 64)])
+def test_quant_with_perm(K, g):
+    w = synth.custom("p", 33, K, 16, g, 7 + K, n_chan=8, n_spike=4)
+    _quant_case(synth.activations(w), g, perm=synth.permutation(K, K), label=f"perm K={K}")
+
+
+def test_quant_degenerate_rows_and_groups():
+    # an all-zero token (alpha = 0, codes 0) and all-ones tokens, which rotate
+    # to [K, 0, ..., 0]: every group but the first has s_b = 0 (codes 0).
+    K = 4096
+    X = np.zeros((6, K), np.float16)
+    X[1] = 1.0
+    X[4] = -2.0
+    _quant_case(X, 128, label="degenerate")
+
+
+def test_quant_single_spike_eq4():
+    # Eq. 4: a lone spike rotates to +-|O| everywhere -> all codes +-7.
+    K = 4096
+    X = np.zeros((2, K), np.float16)
+    X[0, 123] = 300.0
+    X[1, 7] = -12.0
+    act, (Xq, _, _) = _quant_case(X, 128, label="spike")
+    assert np.all(np.abs(O.unpack_int4(to_np(Xq))) == 7)
+
+
+def test_quant_deterministic():
+    w = synth.WORKLOADS["qkv"]
+    rrs = _rrs()
+    Xg = to_gpu(synth.activations(w))
+    a = rrs.rotate_smooth_quant(Xg, w.g)
+    b = rrs.rotate_smooth_quant(Xg, w.g)
+    for u, v in zip(a, b):
+        assert torch.equal(u, v)
+
+
+# ------------------------------------------------------------------ weights
+
+def _weight_case(w, cols=None, perm=None, label=""):
+    rrs = _rrs()
+    print(f"[case] weight {label} K={w.K} N={w.N}", flush=True)
+    W = synth.weights(w)
+    Wq, beta = rrs.prepare_weight(to_gpu(W), None if perm is None else to_gpu(perm))
+    Wq = to_np(Wq)
+    beta = to_np(beta)
+    Ws = W if cols is None else W[:, cols]
+    ref = O.prepare_weight(Ws, perm=perm)
+    sel = slice(None) if cols is None else cols
+    np.testing.assert_array_equal(beta[sel], ref.beta, err_msg=f"{label}: beta")
+    gq = O.unpack_int4(Wq[sel]).T  # K x n
+    diff = gq != ref.q
+    if diff.any():
+        v = (ref.u * ref.winv[None, :]).astype(np.float64)
+        from tests._gpu_util import near_half_integer
+        assert not (diff & ~near_half_integer(v)).any(), f"{label}: weight code mismatch"
+    return Wq, beta, ref
+
+
+@pytest.mark.parametrize("name", ["tiny", "qkv"])
+def test_weight_prep(name):
+    _weight_case(synth.WORKLOADS[name], label=name)
+
+
+@pytest.mark.parametrize("name", ["decode", "large"])
+def test_weight_prep_sampled_columns(name):
+    w = synth.WORKLOADS[name]
+    cols = np.sort(np.random.default_rng(3).choice(w.N, 96, replace=False))
+    _weight_case(w, cols=cols, label=name)
+
+
+@pytest.mark.parametrize("K,N", [(512, 16), (1024, 48), (16384, 32), (2048, 400)])
+def test_weight_prep_ragged(K, N):
+    _weight_case(synth.custom("w", 4, K, N, 64, K + N, n_chan=1), label=f"{K}x{N}")
+
+
+def test_weight_prep_perm():
+    K = 4096
+    w = synth.custom("w", 4, K, 64, 128, 9)
+    _weight_case(w, perm=synth.permutation(K, 1), label="perm")
+
+
+# ------------------------------------------------------------------ GEMM
+
+def _partials_case(qx, qw, g, label):
+    """qx: M x K codes, qw: K x N codes (oracle's); GPU partials from packed codes."""
+    rrs = _rrs()
+    print(f"[case] partials {label} M={qx.shape[0]} K={qx.shape[1]} N={qw.shape[1]} g={g}",
+          flush=True)
+    Pg = rrs.w4a4_gemm_partials(to_gpu(O.pack_int4(qx)), to_gpu(O.pack_int4(qw.T)), g)
+    np.testing.assert_array_equal(to_np(Pg), O.group_partials(qx, qw, g), err_msg=label)
+
+
+@pytest.mark.parametrize("M,K,N,g", [
+    (16, 512, 512, 128), (1, 512, 16, 64), (7, 1024, 144, 256), (129, 2048, 272, 512),
+    (200, 4096, 128, 128), (3, 8192, 48, 64),
+])
+def test_partials_random_codes(M, K, N, g):
+    rng = np.random.default_rng(M * 7 + N)
+    qx = rng.integers(-7, 8, size=(M, K)).astype(np.int8)
+    qw = rng.integers(-7, 8, size=(K, N)).astype(np.int8)
+    _partials_case(qx, qw, g, f"random {M}x{K}x{N}")
+
+
+def test_partials_extremes():
+    # |P_b| = 49 g, the int32 bound the epilogue relies on.
+    M, K, N, g = 32, 1024, 32, 512
+    qx = np.full((M, K), -7, np.int8)
+    qw = np.full((K, N), 7, np.int8)
+    qx[1::2] = 7
+    _partials_case(qx, qw, g, "extremes")
+
+
+def _linear_case(w, X=None, W=None, row_sample=None, col_sample=None, label=""):
+    """Quantize + GEMM on the GPU (separately and through rrs_linear) vs the oracle."""
+    rrs = _rrs()
+    print(f"[case] linear {label} M={w.M} K={w.K} N={w.N} g={w.g}", flush=True)
+    X = synth.activations(w) if X is None else X
+    W = synth.weights(w) if W is None else W
+    Xg = to_gpu(X)
+    Wq, beta = rrs.prepare_weight(to_gpu(W))
+    Xq, a, s = rrs.rotate_smooth_quant(Xg, w.g)
+    Y = rrs.w4a4_gemm(Xq, a, s, Wq, beta, w.g)
+    Y2 = rrs.linear(Xg, Wq, beta, w.g)
+    assert torch.equal(Y, Y2), f"{label}: rrs_linear differs from quant + gemm"
+    Y = to_np(Y).astype(np.float32)
+
+    act = O.rotate_smooth_quant(X, w.g)
+    rows = np.arange(w.M) if row_sample is None else row_sample
+    cols = np.arange(w.N) if col_sample is None else col_sample
+    wq = O.prepare_weight(W[:, cols])
+    np.testing.assert_array_equal(to_np(a), act.alpha)
+    np.testing.assert_array_equal(to_np(s), act.s)
+    check_codes(to_np(Xq), act, label)
+    np.testing.assert_array_equal(to_np(beta)[cols], wq.beta)
+    P = O.group_partials(act.q[rows], wq.q, w.g)
+    y_ref = O.output(P, act.s, act.alpha[rows], wq.beta, norm=w.K)
+    nw = check_y(Y[np.ix_(rows, cols)], y_ref, P, act.s, act.alpha[rows], wq.beta, w.K, label)
+    print(f"{label}: normwise |dY|/|Y| = {nw:.3e}")
+
+
+def test_linear_tiny():
+    _linear_case(synth.WORKLOADS["tiny"], label="tiny")
+
+
+@pytest.mark.parametrize("seed", [2, 3, 4])
+def test_linear_tiny_seeds(seed):
+    w = synth.WORKLOADS["tiny"]
+    _linear_case(w, X=synth.activations(w, seed), W=synth.weights(w, seed), label=f"tiny/{seed}")
+
+
+@pytest.mark.parametrize("M,K,N,g", [
+    (1, 512, 16, 64), (5, 1024, 48, 256), (130, 2048, 400, 512), (77, 4096, 272, 128),
+    (300, 512, 1040, 64), (9, 16384, 64, 128),
+])
+def test_linear_ragged(M, K, N, g):
+    w = synth.custom("l", M, K, N, g, M + N + K, n_chan=max(1, K // 100),
+                     chan_factor=(20, 100), n_spike=max(1, M * K // 10000),
+                     spike_mag=(100, 500))
+    _linear_case(w, label=f"ragged {M}x{K}x{N}/g{g}")
+
+
+@pytest.mark.parametrize("name", ["qkv", "decode"])
+def test_linear_full_size_sampled(name):
+    # The benchmark's shapes and launch configuration; outputs checked on a
+    # sample of rows x columns (plus the first/last row and column).
+    w = synth.WORKLOADS[name]
+    rng = np.random.default_rng(11)
+    rows = np.unique(np.concatenate([[0, w.M - 1], rng.choice(w.M, min(w.M, 48),
+                                                               replace=False)]))
+    cols = np.unique(np.concatenate([[0, w.N - 1], rng.choice(w.N, 160, replace=False)]))
+    _linear_case(w, row_sample=rows, col_sample=cols, label=name)
+
+
+def test_linear_large_sampled():
+    w = synth.WORKLOADS["large"]
+    rng = np.random.default_rng(12)
+    rows = np.unique(np.concatenate([[0, w.M - 1], rng.choice(w.M, 32, replace=False)]))
+    cols = np.unique(np.concatenate([[0, w.N - 1], rng.choice(w.N, 64, replace=False)]))
+    _linear_case(w, row_sample=rows, col_sample=cols, label="large")
+
+
+def test_gemm_deterministic():
+    rrs = _rrs()
+    w = synth.WORKLOADS["qkv"]
+    Xg = to_gpu(synth.activations(w))
+    Wq, beta = rrs.prepare_weight(to_gpu(synth.weights(w)))
+    Xq, a, s = rrs.rotate_smooth_quant(Xg, w.g)
+    y1 = rrs.w4a4_gemm(Xq, a, s, Wq, beta, w.g)
+    y2 = rrs.w4a4_gemm(Xq, a, s, Wq, beta, w.g)
+    assert torch.equal(y1, y2)
