@@ -3,20 +3,39 @@
 //   Y[i, n] = fp16( alpha_i * beta_n / K * sum_b s_b * P_b[i, n] )
 //   P_b[i, n] = sum_{j in group b} qx[i, j] * qw[j, n]   (exact int32)
 //
-// Both operands are K-contiguous packed INT4 (Xq: M x K/2, Wq: N x K/2).
-// Tile 128 x 128 per 256-thread workgroup, four waves of 64 x 64, K step 64.
-// Global -> registers (16 B per thread per operand) -> unpacked to int8 ->
-// LDS (double-buffered) -> v_mfma_i32_32x32x32_i8.
+// Main kernel: 512 threads (8 waves, two per SIMD), output tile 256 x 128,
+// each wave 64 x 64 as 2 x 2 blocks of v_mfma_i32_32x32x32_i8. K advances in
+// tiles of 128 (four MFMA k-steps of 32).
 //
-// Unpacking: a nibble n of a packed byte is moved into the high half of an
-// int8 lane, i.e. the byte holds 16 * q. Low nibbles: (w << 4) & 0xF0F0F0F0,
-// high nibbles: w & 0xF0F0F0F0. Each MFMA product is then 256 q w, exact in
-// int32 (|256 * 49 * 512| < 2^23); the 2^-8 is folded into the output scale.
-// The unpack permutes K inside each 8-element chunk, identically for both
-// operands, so every dot product is unchanged.
+// Data path: packed INT4 (Xq: M x K/2, Wq: N x K/2, K contiguous) is loaded
+// from HBM into registers one tile ahead, unpacked to int8 and stored in a
+// double-buffered LDS stage whose rows are padded to 144 bytes (conflict-free
+// 128-bit fragment reads at immediate offsets). A nibble is unpacked into the
+// high half of its int8 lane (the byte holds 16 q): low nibbles are
+// (w << 4) & 0xF0F0F0F0, high nibbles w & 0xF0F0F0F0, three VALU ops per
+// eight codes. Products are 256 q w, exact in int32 for every group size here;
+// the 2^-8 is folded into the output scale. The unpack permutes K inside each
+// 16-element chunk identically for both operands, so every dot product is
+// unchanged.
 //
-// At the end of each smoothing group the int32 accumulators are converted
-// and added into fp32 accumulators with one FMA by s_b, then restart at 0.
+// Runtime Smooth: each group of g channels gets fresh int32 accumulators; at
+// the end of the group they are converted and added into fp32 accumulators
+// with one FMA by s_b. For g <= 256 the conversion is free of v_cvt_f32_i32
+// (a slow instruction): the group's first MFMA starts from C = bits of
+// 1.5 * 2^23 instead of 0, so the int32 result 0x4B400000 + 256 P is, read
+// as a float, exactly 1.5 * 2^23 + 256 P (|256 P| <= 256 * 49 * 256 < 2^22
+// keeps it in the binade whose ulp is 1), and one exact subtraction recovers
+// 256 P. For g = 512 the accumulators start from 0 and are converted. That rescale costs as
+// much VALU time as the group's MFMAs cost matrix time, so it must run in
+// their shadow. Each wave splits its tile into two row halves (H0: rows 0-31,
+// H1: rows 32-63) that take turns over every chunk of k-steps: while H0 runs
+// its MFMAs, the VALU rescales H1's finished group, and the other way round.
+// Only one set of int32 accumulators is live at a time (64 registers), and
+// the B fragments of a chunk are read once and used by both halves.
+//
+// Workgroups are mapped to tiles XCD by XCD: the hardware deals workgroup ids
+// round-robin to the 8 XCDs, so each XCD is given a contiguous run of tiles,
+// ordered in column strips of 4 row tiles to share A and B in its L2.
 #include "rrs_internal.h"
 
 namespace rrs {
@@ -24,157 +43,305 @@ namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
+typedef float v16f __attribute__((ext_vector_type(16)));
 
-constexpr int BM = 128;
+constexpr int kThreads = 512;
+constexpr int BM = 256;
 constexpr int BN = 128;
-constexpr int BK = 64;             // INT4 elements of K per tile
-constexpr int KBYTES = BK / 2;     // packed bytes per row per tile
-constexpr int LROW = 2 * KBYTES + 16;  // LDS bytes per row: 64 int8 + 16 pad
+constexpr int BK = 128;                 // INT4 elements of K per tile
+constexpr int ROWP = BK + 16;           // LDS bytes per row: 128 int8 + 16 pad
+constexpr int A_BYTES = BM * ROWP;      // 36864
+constexpr int B_BYTES = BN * ROWP;      // 18432
+constexpr int STAGE = A_BYTES + B_BYTES;
+constexpr int kGroupM = 4;              // row tiles per column strip
 
-__device__ __forceinline__ uint4 unpack_lo(uint4 w) {
-  return make_uint4((w.x << 4) & 0xF0F0F0F0u, w.x & 0xF0F0F0F0u,
-                    (w.y << 4) & 0xF0F0F0F0u, w.y & 0xF0F0F0F0u);
-}
-__device__ __forceinline__ uint4 unpack_hi(uint4 w) {
-  return make_uint4((w.z << 4) & 0xF0F0F0F0u, w.z & 0xF0F0F0F0u,
-                    (w.w << 4) & 0xF0F0F0F0u, w.w & 0xF0F0F0F0u);
+__device__ __forceinline__ uint4 unpack_pair(uint32_t w0, uint32_t w1) {
+  return make_uint4((w0 << 4) & 0xF0F0F0F0u, w0 & 0xF0F0F0F0u, (w1 << 4) & 0xF0F0F0F0u,
+                    w1 & 0xF0F0F0F0u);
 }
 
 __device__ __forceinline__ uint16_t float_to_half_bits(float x) {
   return __builtin_bit_cast(uint16_t, (_Float16)x);
 }
 
-template <bool kPartials>
-__global__ __launch_bounds__(256) void gemm_kernel(
+struct TileMap {
+  int m0, n0;
+  bool valid;
+};
+
+// XCD-aware tile order (see the file comment).
+__device__ __forceinline__ TileMap map_tile(int M, int N) {
+  const int tm = (M + BM - 1) / BM;
+  const int tn = (N + BN - 1) / BN;
+  const int T = tm * tn;
+  const int w = blockIdx.x;
+  const int per = (T + 7) >> 3;
+  const int lin = (w & 7) * per + (w >> 3);
+  TileMap r;
+  r.valid = lin < T;
+  const int strip = kGroupM * tn;
+  const int first_m = (lin / strip) * kGroupM;
+  const int gm = min(tm - first_m, kGroupM);
+  const int rem = lin % strip;
+  r.m0 = (first_m + rem % gm) * BM;
+  r.n0 = (rem / gm) * BN;
+  return r;
+}
+
+// Row / column of accumulator register r of block (h, j) for this lane.
+__device__ __forceinline__ int acc_row(int m0, int wm, int h, int r, int lane) {
+  return m0 + wm * 64 + h * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+}
+__device__ __forceinline__ int acc_col(int n0, int wn, int j, int lane) {
+  return n0 + wn * 64 + j * 32 + (lane & 31);
+}
+
+// GS = g / 32 MFMA k-steps per smoothing group.
+template <int GS, bool kPartials>
+__global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
-    const float* __restrict__ w_scale, int M, int N, int K, int g,
-    uint16_t* __restrict__ Y, int32_t* __restrict__ P) {
-  __shared__ __attribute__((aligned(16))) uint8_t sA[2][BM * LROW];
-  __shared__ __attribute__((aligned(16))) uint8_t sB[2][BN * LROW];
+    const float* __restrict__ w_scale, int M, int N, int K, uint16_t* __restrict__ Y,
+    int32_t* __restrict__ P) {
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * STAGE];
+
+  const TileMap tile = map_tile(M, N);
+  if (!tile.valid) return;
+  const int m0 = tile.m0;
+  const int n0 = tile.n0;
 
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int wave = t >> 6;
-  const int wm = wave >> 1;
-  const int wn = wave & 1;
-  const int m0 = blockIdx.y * BM;
-  const int n0 = blockIdx.x * BN;
-  const size_t kbytes_row = (size_t)K / 2;
+  const int wm = wave & 3;   // 64-row slice of the 256-row tile
+  const int wn = wave >> 2;  // 64-column slice of the 128-column tile
+  const size_t krow = (size_t)K / 2;
 
-  // Global load slots: row t/2, bytes [16 * (t & 1), +16) of the tile's 32.
-  const int lrow = t >> 1;
-  const int lhalf = t & 1;
-  const bool a_ok = (m0 + lrow) < M;
-  const bool b_ok = (n0 + lrow) < N;
-  const uint8_t* gA = Xq + (size_t)(a_ok ? m0 + lrow : 0) * kbytes_row + lhalf * 16;
-  const uint8_t* gB = Wq + (size_t)(b_ok ? n0 + lrow : 0) * kbytes_row + lhalf * 16;
-  const int st_off = lrow * LROW + lhalf * 32;
+  // Global -> LDS slots. A: row t/2, 32 packed bytes; B: row t/4, 16 bytes.
+  // Rows past M (or N) load the last valid row instead: their results are
+  // never stored, and the loop stays free of divergent branches.
+  const int arow = t >> 1;
+  const int ahalf = t & 1;
+  const int brow = t >> 2;
+  const int bq = t & 3;
+  const uint8_t* ga = Xq + (size_t)min(m0 + arow, M - 1) * krow + ahalf * 32;
+  const uint8_t* gb = Wq + (size_t)min(n0 + brow, N - 1) * krow + bq * 16;
+  const int a_st = arow * ROWP + ahalf * 64;
+  const int b_st = A_BYTES + brow * ROWP + bq * 32;
 
-  uint4 ra = make_uint4(0, 0, 0, 0);
-  uint4 rb = make_uint4(0, 0, 0, 0);
+  // Fragment read offsets (per lane) inside a stage.
+  const int frow = lane & 31;
+  const int fk = (lane >> 5) * 16;
+  const int a_fr = (wm * 64 + frow) * ROWP + fk;       // H0; H1 is + 32 rows
+  const int b_fr = A_BYTES + (wn * 64 + frow) * ROWP + fk;  // B0; B1 is + 32 rows
 
+  // Packed tiles in flight: two register sets, tile kt lives in set kt & 1.
+  uint4 ra0[2], ra1[2], rb0[2];
+  auto gload = [&](int set, int kt) {
+    const uint4* p = reinterpret_cast<const uint4*>(ga + (size_t)kt * (BK / 2));
+    ra0[set] = p[0];
+    ra1[set] = p[1];
+    rb0[set] = *reinterpret_cast<const uint4*>(gb + (size_t)kt * (BK / 2));
+  };
+  auto lstore = [&](int set, int stage) {
+    uint8_t* s = lds + stage * STAGE;
+    *reinterpret_cast<uint4*>(s + a_st) = unpack_pair(ra0[set].x, ra0[set].y);
+    *reinterpret_cast<uint4*>(s + a_st + 16) = unpack_pair(ra0[set].z, ra0[set].w);
+    *reinterpret_cast<uint4*>(s + a_st + 32) = unpack_pair(ra1[set].x, ra1[set].y);
+    *reinterpret_cast<uint4*>(s + a_st + 48) = unpack_pair(ra1[set].z, ra1[set].w);
+    *reinterpret_cast<uint4*>(s + b_st) = unpack_pair(rb0[set].x, rb0[set].y);
+    *reinterpret_cast<uint4*>(s + b_st + 16) = unpack_pair(rb0[set].z, rb0[set].w);
+  };
+  auto afrag = [&](int stage, int h, int ks) -> v4i {
+    return *reinterpret_cast<const v4i*>(lds + stage * STAGE + a_fr + h * 32 * ROWP + ks * 32);
+  };
+  auto bfrag = [&](int stage, int j, int ks) -> v4i {
+    return *reinterpret_cast<const v4i*>(lds + stage * STAGE + b_fr + j * 32 * ROWP + ks * 32);
+  };
+
+  // acc[h][j]: int32 accumulators of block (h, j); f[h][j][r]: fp32 results.
   v16i acc[2][2];
   float f[2][2][16];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        acc[i][j][r] = 0;
-        f[i][j][r] = 0.0f;
+        acc[h][j][r] = (kPartials || GS > 8) ? 0 : 0x4B400000;
+        f[h][j][r] = 0.0f;
+      }
+
+  const int nsteps = K / 32;
+  const int ntiles = K / BK;
+  const v16i zero = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+  constexpr int kMagic = 0x4B400000;  // bits of 1.5 * 2^23 (= 12582912.0f)
+  const v16i magic = {kMagic, kMagic, kMagic, kMagic, kMagic, kMagic, kMagic, kMagic,
+                      kMagic, kMagic, kMagic, kMagic, kMagic, kMagic, kMagic, kMagic};
+
+  constexpr int PH = GS < 4 ? GS : 4;            // k-steps per chunk
+  constexpr int U = GS > 8 ? GS : 8;             // k-steps per unrolled loop trip
+  constexpr int CONV = 32 / PH;                  // rescale elements per k-step
+
+  // Rescale one slice of half h's accumulators: elements [q0, q0 + CONV) of 32.
+  auto rescale = [&](int h, int q0, float s, int grp) {
+    if constexpr (!kPartials) {
+#pragma unroll
+      for (int q = 0; q < CONV; ++q) {
+        const int e = q0 + q;
+        // Bit-cast the whole vector, then index: bit-casting a single element
+        // of an ext_vector is miscompiled (every element reads element 0).
+        const v16f accf = __builtin_bit_cast(v16f, acc[h][e >> 4]);
+        const float pv = GS > 8 ? (float)acc[h][e >> 4][e & 15] : accf[e & 15] - 12582912.0f;
+        f[h][e >> 4][e & 15] = __builtin_fmaf(s, pv, f[h][e >> 4][e & 15]);
+        // Pin the update here: otherwise the compiler sinks all rescales of a
+        // loop trip to its end, where they force copies of the accumulators.
+        asm volatile("" : "+v"(f[h][e >> 4][e & 15]));
+      }
+    } else {
+      int32_t* Pg = P + (size_t)grp * (size_t)M * (size_t)N;
+#pragma unroll
+      for (int q = 0; q < CONV; ++q) {
+        const int e = q0 + q;
+        const int row = acc_row(m0, wm, h, e & 15, lane);
+        const int col = acc_col(n0, wn, e >> 4, lane);
+        if (row < M && col < N) Pg[(size_t)row * N + col] = acc[h][e >> 4][e & 15] >> 8;
       }
     }
+  };
 
-  const int nkt = K / BK;
-  const int tiles_per_group = g / BK;
-  const int frag_row = lane & 31;
-  const int frag_k = (lane >> 5) * 16;
+  // Prologue: tile 0 staged, tiles 1 and 2 in flight, fragments of chunk 0 read.
+  gload(0, 0);
+  lstore(0, 0);
+  gload(1, min(1, ntiles - 1));
+  gload(0, min(2, ntiles - 1));
+  __syncthreads();
+  v4i fb[PH][2], fa0[PH], fa1[PH];
+#pragma unroll
+  for (int s = 0; s < PH; ++s) {
+    fb[s][0] = bfrag(0, 0, s);
+    fb[s][1] = bfrag(0, 1, s);
+    fa0[s] = afrag(0, 0, s);
+  }
 
-  if (a_ok) ra = *reinterpret_cast<const uint4*>(gA);
-  if (b_ok) rb = *reinterpret_cast<const uint4*>(gB);
-
-  for (int kt = 0; kt < nkt; ++kt) {
-    const int st = kt & 1;
-    *reinterpret_cast<uint4*>(&sA[st][st_off]) = unpack_lo(ra);
-    *reinterpret_cast<uint4*>(&sA[st][st_off + 16]) = unpack_hi(ra);
-    *reinterpret_cast<uint4*>(&sB[st][st_off]) = unpack_lo(rb);
-    *reinterpret_cast<uint4*>(&sB[st][st_off + 16]) = unpack_hi(rb);
-    __syncthreads();
-    if (kt + 1 < nkt) {
-      if (a_ok) ra = *reinterpret_cast<const uint4*>(gA + (size_t)(kt + 1) * KBYTES);
-      if (b_ok) rb = *reinterpret_cast<const uint4*>(gB + (size_t)(kt + 1) * KBYTES);
-    }
+  for (int base = 0; base < nsteps; base += U) {
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      v4i a[2], b[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        a[i] = *reinterpret_cast<const v4i*>(
-            &sA[st][(wm * 64 + i * 32 + frag_row) * LROW + ks * 32 + frag_k]);
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        b[j] = *reinterpret_cast<const v4i*>(
-            &sB[st][(wn * 64 + j * 32 + frag_row) * LROW + ks * 32 + frag_k]);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-    if ((kt + 1) % tiles_per_group == 0) {
-      const int grp = kt / tiles_per_group;
-      if constexpr (kPartials) {
-        int32_t* Pg = P + (size_t)grp * (size_t)M * (size_t)N;
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-              const int col = n0 + wn * 64 + j * 32 + (lane & 31);
-              if (row < M && col < N) Pg[(size_t)row * N + col] = acc[i][j][r] >> 8;
-            }
-      } else {
-        const float s = s_group[grp];
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-              f[i][j][r] = __builtin_fmaf(s, (float)acc[i][j][r], f[i][j][r]);
+    for (int c0 = 0; c0 < U; c0 += PH) {  // one chunk of PH k-steps
+      const int stage = (c0 >> 2) & 1;
+      const int ks0 = c0 & 3;
+      const int j0 = base + c0;             // first global k-step of the chunk
+      const int grp = j0 / GS;
+      const bool g_first = (c0 % GS) == 0;  // chunk opens a group (H1 closed one)
+      const bool g_last = ((c0 + PH) % GS) == 0;  // chunk closes a group
+      const bool tile_end = ks0 + PH == 4;
+      float s_cur = 0.0f, s_prev = 0.0f;
+      if constexpr (!kPartials) {
+        if (g_last) s_cur = s_group[grp];
+        if (g_first) s_prev = grp > 0 ? s_group[grp - 1] : 0.0f;
       }
+      __builtin_amdgcn_sched_barrier(0);
+
+      // Phase H0: MFMAs of rows 0-31; A fragments of rows 32-63 are read;
+      // rescale of H1's group closed by the previous chunk (for the very
+      // first chunk acc[1] and s_prev are 0).
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int s = 0; s < PH; ++s) {
+        const bool fresh = g_first && s == 0;
+        acc[0][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa0[s], fb[s][0], fresh ? ((kPartials || GS > 8) ? zero : magic) : acc[0][0], 0, 0, 0);
+        acc[0][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa0[s], fb[s][1], fresh ? ((kPartials || GS > 8) ? zero : magic) : acc[0][1], 0, 0, 0);
+        fa1[s] = afrag(stage, 1, ks0 + s);
+        if (g_first) {
+          if (!kPartials || grp > 0) rescale(1, s * CONV, s_prev, grp - 1);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+
+      // End of a tile: every wave has read this tile's fragments, so the
+      // next tile goes into the other stage now; the one after is fetched.
+      // (On the last tile this stages a duplicate that is never read.)
+      if (tile_end) {
+        const int kt = j0 >> 2;
+        lstore((kt + 1) & 1, stage ^ 1);
+        __syncthreads();
+        gload((kt + 1) & 1, min(kt + 3, ntiles - 1));
+      }
+      const int nstage = tile_end ? stage ^ 1 : stage;
+      const int nks0 = (ks0 + PH) & 3;
+      __builtin_amdgcn_sched_barrier(0);
+
+      // Phase H1: MFMAs of rows 32-63; the next chunk's B and A0 fragments
+      // are read into the registers each k-step frees; rescale of H0's group
+      // if this chunk closed it.
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
+      for (int s = 0; s < PH; ++s) {
+        const bool fresh = g_first && s == 0;
+        acc[1][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa1[s], fb[s][0], fresh ? ((kPartials || GS > 8) ? zero : magic) : acc[1][0], 0, 0, 0);
+        acc[1][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa1[s], fb[s][1], fresh ? ((kPartials || GS > 8) ? zero : magic) : acc[1][1], 0, 0, 0);
+        fb[s][0] = bfrag(nstage, 0, nks0 + s);
+        fb[s][1] = bfrag(nstage, 1, nks0 + s);
+        fa0[s] = afrag(nstage, 0, nks0 + s);
+        if (g_last) rescale(0, s * CONV, s_cur, grp);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
+  }
+  // H1's last group.
+  {
+    const int G = nsteps / GS;
+    const float s_last = kPartials ? 0.0f : s_group[G - 1];
+#pragma unroll
+    for (int s = 0; s < 32; s += CONV) rescale(1, s, s_last, G - 1);
   }
 
   if constexpr (!kPartials) {
-    // 2^-8 undoes the 16x16 of the unpacked operands, 1/K the unnormalized rotation.
+    // 2^-8 undoes the 16 x 16 of the unpacked operands, 1/K the unnormalized rotation.
     const float inv = __builtin_ldexpf(1.0f, -8) / (float)K;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int j = 0; j < 2; ++j) {
+      const int col = acc_col(n0, wn, j, lane);
+      const float bcol = col < N ? w_scale[col] : 0.0f;
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int col = n0 + wn * 64 + j * 32 + (lane & 31);
-        const float bcol = col < N ? w_scale[col] : 0.0f;
+      for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          const int row = acc_row(m0, wm, h, r, lane);
           if (row < M && col < N) {
             const float sc = a_scale[row] * inv;
-            Y[(size_t)row * N + col] = float_to_half_bits((f[i][j][r] * sc) * bcol);
+            Y[(size_t)row * N + col] = float_to_half_bits((f[h][j][r] * sc) * bcol);
           }
         }
-      }
+    }
   }
+}
+
+template <bool kPartials>
+hipError_t launch_main(const uint8_t* Xq, const float* a_scale, const float* s_group,
+                       const uint8_t* Wq, const float* w_scale, int M, int N, int K, int g,
+                       uint16_t* Y, int32_t* P, hipStream_t stream) {
+  const int tm = (M + BM - 1) / BM;
+  const int tn = (N + BN - 1) / BN;
+  const int T = tm * tn;
+  const int grid = 8 * ((T + 7) / 8);
+  switch (g) {
+#define RRS_CASE(G_)                                                                       \
+  case G_:                                                                                 \
+    gemm_main_kernel<G_ / 32, kPartials><<<grid, kThreads, 0, stream>>>(                   \
+        Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, P);                                 \
+    break;
+    RRS_CASE(64)
+    RRS_CASE(128)
+    RRS_CASE(256)
+    RRS_CASE(512)
+#undef RRS_CASE
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+// The main kernel unrolls max(8, g / 32) k-steps per loop trip.
+bool main_kernel_fits(int K, int g) {
+  const int U = (g / 32 > 8) ? g / 32 : 8;
+  return (K / 32) % U == 0;
 }
 
 }  // namespace
@@ -182,18 +349,16 @@ __global__ __launch_bounds__(256) void gemm_kernel(
 hipError_t launch_w4a4_gemm(const uint8_t* Xq, const float* a_scale, const float* s_group,
                             const uint8_t* Wq, const float* w_scale, int M, int N, int K,
                             int g, uint16_t* Y, hipStream_t stream) {
-  dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
-  gemm_kernel<false><<<grid, 256, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale, M, N, K,
-                                               g, Y, nullptr);
-  return hipGetLastError();
+  if (!main_kernel_fits(K, g))
+    return launch_w4a4_gemm_small(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, stream);
+  return launch_main<false>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, nullptr, stream);
 }
 
 hipError_t launch_w4a4_gemm_partials(const uint8_t* Xq, const uint8_t* Wq, int M, int N,
                                      int K, int g, int32_t* P, hipStream_t stream) {
-  dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
-  gemm_kernel<true><<<grid, 256, 0, stream>>>(Xq, nullptr, nullptr, Wq, nullptr, M, N, K, g,
-                                              nullptr, P);
-  return hipGetLastError();
+  if (!main_kernel_fits(K, g))
+    return launch_w4a4_gemm_partials_small(Xq, Wq, M, N, K, g, P, stream);
+  return launch_main<true>(Xq, nullptr, nullptr, Wq, nullptr, M, N, K, g, nullptr, P, stream);
 }
 
 }  // namespace rrs

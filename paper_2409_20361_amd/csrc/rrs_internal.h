@@ -27,6 +27,16 @@ hipError_t launch_w4a4_gemm(const uint8_t* Xq, const float* a_scale, const float
 hipError_t launch_w4a4_gemm_partials(const uint8_t* Xq, const uint8_t* Wq, int M, int N,
                                      int K, int g, int32_t* P, hipStream_t stream);
 
+// Simple 128 x 128 tile kernel: the fallback for shapes the main kernel's
+// unrolling does not cover (K / 32 not a multiple of max(8, g / 16)).
+hipError_t launch_w4a4_gemm_small(const uint8_t* Xq, const float* a_scale,
+                                  const float* s_group, const uint8_t* Wq,
+                                  const float* w_scale, int M, int N, int K, int g,
+                                  uint16_t* Y, hipStream_t stream);
+hipError_t launch_w4a4_gemm_partials_small(const uint8_t* Xq, const uint8_t* Wq, int M,
+                                           int N, int K, int g, int32_t* P,
+                                           hipStream_t stream);
+
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 }  // namespace rrs
