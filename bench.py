@@ -29,8 +29,21 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "effective W4A4 TOPS at M=2048,K=4096,N=12288; HBM GB/s at M=8 decode"
+# HBM bytes per launch of the GEMM kernel on this workload, from two rocprofv3
+# --pmc runs (FETCH_SIZE, WRITE_SIZE) scaled by a 256 MiB copy-kernel
+# calibration (profiles/gemm_main_kernel_qkv.md), keyed by the sha1 prefix of
+# the kernel source they were measured on. Any other source reports null.
+GEMM_TRAFFIC_BYTES = {"7b5795b19fe6": 160.75e6}
 INT8_MFMA_PEAK_TOPS = 5000.0   # MI355X dense int8 MFMA, 5.0 POP/s
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+
+
+def gemm_traffic():
+    import hashlib
+    src = os.path.join(ROOT, "paper_2409_20361_amd", "csrc", "rrs_gemm.hip")
+    with open(src, "rb") as f:
+        sha = hashlib.sha1(f.read()).hexdigest()[:12]
+    return GEMM_TRAFFIC_BYTES.get(sha)
 
 
 def log(msg):
@@ -234,7 +247,7 @@ def main():
             "peak": INT8_MFMA_PEAK_TOPS,
             "unit": "TOP/s",
             "frac": round(gemm_tops / INT8_MFMA_PEAK_TOPS, 4),
-            "traffic": None,
+            "traffic": gemm_traffic(),
         },
         "breakdown": {
             "quant_us": round(r["quant_ms"] * 1e3, 2),

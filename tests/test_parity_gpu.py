@@ -163,6 +163,7 @@ def _partials_case(qx, qw, g, label):
 @pytest.mark.parametrize("M,K,N,g", [
     (16, 512, 512, 128), (1, 512, 16, 64), (7, 1024, 144, 256), (129, 2048, 272, 512),
     (200, 4096, 128, 128), (3, 8192, 48, 64),
+    (5, 512, 32, 512),   # K = g = 512: the 128 x 128 fallback kernel
 ])
 def test_partials_random_codes(M, K, N, g):
     rng = np.random.default_rng(M * 7 + N)
@@ -221,6 +222,7 @@ def test_linear_tiny_seeds(seed):
 @pytest.mark.parametrize("M,K,N,g", [
     (1, 512, 16, 64), (5, 1024, 48, 256), (130, 2048, 400, 512), (77, 4096, 272, 128),
     (300, 512, 1040, 64), (9, 16384, 64, 128),
+    (33, 512, 96, 512),   # K = g = 512: the 128 x 128 fallback kernel
 ])
 def test_linear_ragged(M, K, N, g):
     w = synth.custom("l", M, K, N, g, M + N + K, n_chan=max(1, K // 100),
@@ -247,6 +249,29 @@ def test_linear_large_sampled():
     rows = np.unique(np.concatenate([[0, w.M - 1], rng.choice(w.M, 32, replace=False)]))
     cols = np.unique(np.concatenate([[0, w.N - 1], rng.choice(w.N, 64, replace=False)]))
     _linear_case(w, row_sample=rows, col_sample=cols, label="large")
+
+
+@pytest.mark.parametrize("g", [64, 128, 256, 512])
+def test_gemm_extreme_partials(g):
+    # Every code +-7, so |P_b| = 49 g: the largest partial sums any input can
+    # give, which bounds the accumulator encodings the kernels rely on.
+    rrs = _rrs()
+    M, K, N = 96, 2048, 160
+    rng = np.random.default_rng(g)
+    qx = np.where(rng.random((M, K)) < 0.5, -7, 7).astype(np.int8)
+    qx[::3] = 7
+    qw = np.where(rng.random((K, N)) < 0.5, -7, 7).astype(np.int8)
+    qw[:, ::4] = 7
+    alpha = (rng.random(M) + 0.5).astype(np.float32)
+    beta = (rng.random(N) * 0.01 + 0.001).astype(np.float32)
+    s = (rng.random(K // g) * 3 + 0.25).astype(np.float32)
+    print(f"[case] extreme partials g={g}", flush=True)
+    Y = rrs.w4a4_gemm(to_gpu(O.pack_int4(qx)), to_gpu(alpha), to_gpu(s),
+                      to_gpu(O.pack_int4(qw.T)), to_gpu(beta), g)
+    P = O.group_partials(qx, qw, g)
+    assert np.abs(P).max() == 49 * g
+    y_ref = O.output(P, s, alpha, beta, norm=K)
+    check_y(to_np(Y).astype(np.float32), y_ref, P, s, alpha, beta, K, f"extreme g={g}")
 
 
 def test_gemm_deterministic():
