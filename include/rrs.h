@@ -80,7 +80,7 @@ int rrs_version(void);
 
 /*
  * Bytes of device workspace rrs_rotate_smooth_quant needs for this shape
- * (per-workgroup channel-maximum partials plus the reduced channel maxima).
+ * (per-workgroup group-maximum partials: up to 256 rows of K/64 floats).
  * Returns 0 when the shape or group size is invalid.
  */
 size_t rrs_workspace_bytes(int M, int K, int group_size);

@@ -1,16 +1,21 @@
 // Online rotate + runtime smooth + per-token INT4 quantization
 // (Section 3.3 then Section 3.2; Eq. 1-2; Section 2.1).
 //
-// Three launches on the caller's stream:
-//   1. colmax: each workgroup rotates its rows (FWHT) and keeps the running
-//      per-channel max |y| in registers; it writes one partial row of K floats.
-//   2. reduce: per channel, the max over the partial rows -> c_j (Eq. 1).
-//   3. quant:  each workgroup derives the group scales s_b = max_{j in b} c_j
-//      (Section 3.2) and r_b = 1/s_b, then re-rotates its rows (bit-identical
-//      to pass 1), takes the per-token max of |y| r_b, and writes the INT4
-//      codes, alpha_i and (workgroup 0) s_b.
-// The channel max needs every token before any token can be quantized, hence
-// the split; the second read of X mostly hits the 256 MB Infinity Cache.
+// The smoothing scale of group b is the largest |rotated activation| over
+// every token of the call and every channel of the group (Eq. 1 with the
+// group maximum of Section 3.2), so no token can be quantized before all
+// tokens are rotated. Two launches on the caller's stream:
+//   1. rot_max: each workgroup rotates its rows (FWHT, canonical stage order),
+//      keeps per-channel maxima in registers, combines its teams in LDS, and
+//      writes one row of per-group maxima (G floats; with a static reorder the
+//      groups are formed over the reordered positions);
+//   2. quant: each workgroup reduces those rows to s_b and r_b = fl(1/s_b),
+//      then re-rotates its rows (identical code, identical bits; X mostly
+//      comes from the MALL the second time), takes the per-token maximum of
+//      fl(|y_ij| r_b), and writes alpha_i and the packed INT4 codes.
+// A workgroup holds 1, 2 or 4 teams of 256 threads (K = 16384, 8192, <= 4096:
+// a thread's share of a row stays in registers); each team works on one row at
+// a time. Cross-team and cross-wave reductions go through LDS, no atomics.
 #include "rrs_device.h"
 #include "rrs_internal.h"
 
@@ -18,126 +23,230 @@ namespace rrs {
 namespace {
 
 constexpr int kMaxPartialRows = 256;
-constexpr int kQuantMaxWgs = 1024;
 
 template <int K>
-__global__ __launch_bounds__(kRowThreads) void colmax_kernel(const uint16_t* __restrict__ X,
-                                                             int M, int rows_per_wg,
-                                                             float* __restrict__ partial) {
+struct Teams {
+  static constexpr int n = K <= 4096 ? 4 : (K == 8192 ? 2 : 1);
+  static constexpr int threads = n * kRowThreads;
+};
+
+// Row slots: one padded row per team, at least 1024 floats in all, so the
+// same LDS doubles as reduction scratch (indexed by channel and by thread)
+// when no row is in flight.
+template <int K>
+constexpr int slot_floats() {
+  return Teams<K>::n * lds_row_floats(K) > 1024 ? Teams<K>::n * lds_row_floats(K) : 1024;
+}
+
+// v = row r of X (this thread's E elements), or zeros past the last row r1.
+template <int K>
+__device__ __forceinline__ void load_row_or_zero(const uint16_t* __restrict__ X, int r, int r1,
+                                                 int t, float (&v)[FwhtShape<K>::E]) {
+  constexpr int E = FwhtShape<K>::E;
+  if (r < r1) {
+    load_halves<E>(X + (size_t)r * K + (size_t)t * E, v);
+  } else {
+#pragma unroll
+    for (int e = 0; e < E; ++e) v[e] = 0.0f;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 1. rotate + per-workgroup group maxima
+// ---------------------------------------------------------------------------
+template <int K>
+__global__ __launch_bounds__(Teams<K>::threads) void rot_max_kernel(
+    const uint16_t* __restrict__ X, int M, int g, int rows_per_wg,
+    const int32_t* __restrict__ perm, float* __restrict__ gpart) {
   using S = FwhtShape<K>;
-  __shared__ float lds[lds_row_floats(K)];
-  const int t = threadIdx.x;
+  constexpr int E = S::E;
+  constexpr int RF = lds_row_floats(K);
+  constexpr int kTeams = Teams<K>::n;
+  constexpr int kThreads = Teams<K>::threads;
+  __shared__ float slots[slot_floats<K>()];
+  float* cbuf = slots;  // reduction scratch once the rows are done
+  const int tid = threadIdx.x;
+  const int team = tid >> 8;
+  const int t = tid & (kRowThreads - 1);
+  const int iters = (rows_per_wg + kTeams - 1) / kTeams;
   const int r0 = blockIdx.x * rows_per_wg;
   const int r1 = min(M, r0 + rows_per_wg);
-  float cm[S::E];
+  float* slot = slots + team * RF;
+
+  float cm[E];
 #pragma unroll
-  for (int e = 0; e < S::E; ++e) cm[e] = 0.0f;
-  for (int r = r0; r < r1; ++r) {
-    float v[S::E];
-    load_halves<S::E>(X + (size_t)r * K + (size_t)t * S::E, v);
-    fwht_row<K>(v, lds, t);
+  for (int e = 0; e < E; ++e) cm[e] = 0.0f;
+  float vn[E];  // next row, loaded while the current one is transformed
+  load_row_or_zero<K>(X, r0 + team, r1, t, vn);
+  for (int it = 0; it < iters; ++it) {
+    float v[E];
 #pragma unroll
-    for (int e = 0; e < S::E; ++e) cm[e] = fmaxf(cm[e], fabsf(v[e]));
+    for (int e = 0; e < E; ++e) v[e] = vn[e];
+    if (it + 1 < iters) load_row_or_zero<K>(X, r0 + (it + 1) * kTeams + team, r1, t, vn);
+    fwht_row<K>(v, slot, t);  // v[e] = y[t + 256 e]
+#pragma unroll
+    for (int e = 0; e < E; ++e) cm[e] = fmaxf(cm[e], fabsf(v[e]));
   }
-  float* out = partial + (size_t)blockIdx.x * K;
-#pragma unroll
-  for (int e = 0; e < S::E; ++e) out[t + e * kRowThreads] = cm[e];
-}
-
-// c[j] = max over the partial rows; 64 channels per workgroup, 4 row slices.
-__global__ __launch_bounds__(256) void reduce_kernel(const float* __restrict__ partial,
-                                                     int nparts, int K,
-                                                     float* __restrict__ cmax) {
-  __shared__ float red[4][64];
-  const int t = threadIdx.x;
-  const int j = blockIdx.x * 64 + (t & 63);
-  const int slice = t >> 6;
-  float m = 0.0f;
-  for (int i = slice; i < nparts; i += 4) m = fmaxf(m, partial[(size_t)i * K + j]);
-  red[slice][t & 63] = m;
+  // Per-channel maxima of the workgroup: teams combined in LDS.
   __syncthreads();
-  if (t < 64) cmax[j] = fmaxf(fmaxf(red[0][t], red[1][t]), fmaxf(red[2][t], red[3][t]));
+  if (team == 0) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) cbuf[t + e * kRowThreads] = cm[e];
+  }
+  __syncthreads();
+  for (int tm = 1; tm < kTeams; ++tm) {
+    if (team == tm) {
+#pragma unroll
+      for (int e = 0; e < E; ++e)
+        cbuf[t + e * kRowThreads] = fmaxf(cbuf[t + e * kRowThreads], cm[e]);
+    }
+    __syncthreads();
+  }
+  // Group maxima over the (reordered) positions. The first NA threads cover
+  // P consecutive positions each, all inside one group (P <= 64 <= g).
+  constexpr int NA = K < kThreads ? K : kThreads;
+  constexpr int P = K / NA;
+  float pm = 0.0f;
+  if (tid < NA) {
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      const int j = tid * P + q;
+      pm = fmaxf(pm, cbuf[perm ? perm[j] : j]);
+    }
+  }
+  __syncthreads();
+  cbuf[tid] = pm;  // tid < kThreads <= slot_floats
+  __syncthreads();
+  const int G = K / g;
+  if (tid < G) {
+    const int per = g / P;  // threads per group
+    float s = 0.0f;
+    for (int u = 0; u < per; ++u) s = fmaxf(s, cbuf[tid * per + u]);
+    gpart[(size_t)blockIdx.x * G + tid] = s;
+  }
 }
 
+// ---------------------------------------------------------------------------
+// 2. group scales, per-token scale, codes
+// ---------------------------------------------------------------------------
 template <int K>
-__global__ __launch_bounds__(kRowThreads) void quant_kernel(
-    const uint16_t* __restrict__ X, int M, int g, int rows_per_wg,
-    const int32_t* __restrict__ perm, const float* __restrict__ cmax,
+__global__ __launch_bounds__(Teams<K>::threads) void quant_kernel(
+    const uint16_t* __restrict__ X, int M, int g, int rows_per_wg, int nparts,
+    const int32_t* __restrict__ perm, const float* __restrict__ gpart,
     uint8_t* __restrict__ Xq, float* __restrict__ a_scale, float* __restrict__ s_group) {
   using S = FwhtShape<K>;
   constexpr int E = S::E;
-  __shared__ float lds[lds_row_floats(K)];
-  __shared__ float rgrp[kRowThreads];
-  __shared__ float red[4];
-  const int t = threadIdx.x;
+  constexpr int RF = lds_row_floats(K);
+  constexpr int kTeams = Teams<K>::n;
+  constexpr int kThreads = Teams<K>::threads;
+  __shared__ float slots[slot_floats<K>()];
+  __shared__ float rg[256];
+  __shared__ float red[16];
+  float* cbuf = slots;  // reduction scratch before the rows start
+  const int tid = threadIdx.x;
+  const int team = tid >> 8;
+  const int t = tid & (kRowThreads - 1);
   const int G = K / g;
+  float* slot = slots + team * RF;
 
-  // Position j = t*E + e of the (reordered) row reads channel src[e].
-  int src[E];
+  // s_b = max over the partial rows; threads split (group, row slice).
+  {
+    const int nsl = kThreads / G;  // G <= 256 <= kThreads
+    const int b = tid % G;
+    const int sl = tid / G;
+    float m = 0.0f;
+    if (sl < nsl)
+      for (int i = sl; i < nparts; i += nsl) m = fmaxf(m, gpart[(size_t)i * G + b]);
+    cbuf[tid] = m;
+    __syncthreads();
+    if (tid < G) {
+      float s = cbuf[tid];
+      for (int q = 1; q < nsl; ++q) s = fmaxf(s, cbuf[q * G + tid]);
+      rg[tid] = (s == 0.0f) ? 0.0f : __fdiv_rn(1.0f, s);
+      if (blockIdx.x == 0) s_group[tid] = s;
+    }
+    __syncthreads();
+  }
+  int src[E];  // position t*E + e of the reordered row reads channel src[e]
 #pragma unroll
   for (int e = 0; e < E; ++e) src[e] = perm ? perm[t * E + e] : t * E + e;
+  const float rb = rg[(t * E) / g];  // this thread's positions lie in one group
 
-  // Group smoothing scales: this thread's E positions lie in one group (E <= g).
-  float cl = 0.0f;
-#pragma unroll
-  for (int e = 0; e < E; ++e) cl = fmaxf(cl, cmax[src[e]]);
-  lds[t] = cl;
-  __syncthreads();
-  if (t < G) {
-    const int per = g / E;
-    float s = 0.0f;
-    for (int u = 0; u < per; ++u) s = fmaxf(s, lds[t * per + u]);
-    rgrp[t] = (s == 0.0f) ? 0.0f : __fdiv_rn(1.0f, s);
-    if (blockIdx.x == 0) s_group[t] = s;
-  }
-  __syncthreads();
-  const float rb = rgrp[(t * E) / g];
-
+  const int iters = (rows_per_wg + kTeams - 1) / kTeams;
   const int r0 = blockIdx.x * rows_per_wg;
   const int r1 = min(M, r0 + rows_per_wg);
-  for (int r = r0; r < r1; ++r) {
+  float vn[E];  // next row, loaded while the current one is processed
+  load_row_or_zero<K>(X, r0 + team, r1, t, vn);
+  for (int it = 0; it < iters; ++it) {
+    const int r = r0 + it * kTeams + team;
+    const bool live = r < r1;
     float v[E];
-    load_halves<E>(X + (size_t)r * K + (size_t)t * E, v);
-    fwht_row<K>(v, lds, t);
-    // back to natural order (and apply the static reorder)
+#pragma unroll
+    for (int e = 0; e < E; ++e) v[e] = vn[e];
+    if (it + 1 < iters) load_row_or_zero<K>(X, r0 + (it + 1) * kTeams + team, r1, t, vn);
+    fwht_row<K>(v, slot, t);
+    // back to natural order through LDS, with the static reorder applied
     __syncthreads();
 #pragma unroll
-    for (int e = 0; e < E; ++e) lds[lds_pad(t + e * kRowThreads)] = v[e];
+    for (int e = 0; e < E; ++e) slot[lds_pad(t + e * kRowThreads)] = v[e];
     __syncthreads();
 #pragma unroll
-    for (int e = 0; e < E; ++e) v[e] = lds[lds_pad(src[e])];
-
+    for (int e = 0; e < E; ++e) v[e] = slot[lds_pad(src[e])];
     float lm = 0.0f;
 #pragma unroll
     for (int e = 0; e < E; ++e) lm = fmaxf(lm, fabsf(v[e]));
-    lm = lm * rb;  // fl(M_ib * r_b)
-    const float a = block_max256(lm, red);
+    lm = wave_max(lm * rb);  // fl(M_ib * r_b), max over the wave
+    if ((tid & 63) == 0) red[tid >> 6] = lm;
+    __syncthreads();
+    const float a = fmaxf(fmaxf(red[team * 4], red[team * 4 + 1]),
+                          fmaxf(red[team * 4 + 2], red[team * 4 + 3]));  // 4 waves per team
     const float inv = (a == 0.0f) ? 0.0f : __fdiv_rn(7.0f, a);
     const float m = rb * inv;  // fl(r_b * inv_i)
-    uint32_t nib[E];
+    if (live) {
+      uint32_t nib[E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) nib[e] = int4_nibble(v[e] * m);
-    store_nibbles<E>(Xq + (size_t)r * (K / 2) + (size_t)t * (E / 2), nib);
-    if (t == 0) a_scale[r] = __fdiv_rn(a, 7.0f);
+      for (int e = 0; e < E; ++e) nib[e] = int4_nibble(v[e] * m);
+      store_nibbles<E>(Xq + (size_t)r * (K / 2) + (size_t)t * (E / 2), nib);
+      if (t == 0) a_scale[r] = __fdiv_rn(a, 7.0f);
+    }
   }
+}
+
+int g_num_cus = 0;
+
+int num_cus() {
+  if (g_num_cus == 0) {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        cus > 0)
+      g_num_cus = cus;
+    else
+      g_num_cus = 256;
+  }
+  return g_num_cus;
 }
 
 template <int K>
 hipError_t launch_k(const uint16_t* X, int M, int g, const int32_t* perm, uint8_t* Xq,
                     float* a_scale, float* s_group, void* workspace, hipStream_t stream) {
-  const int nparts = quant_partial_rows(M);
-  const int rows_a = (M + nparts - 1) / nparts;
-  const int grid_a = (M + rows_a - 1) / rows_a;
-  float* partial = static_cast<float*>(workspace);
-  float* cmax = reinterpret_cast<float*>(static_cast<char*>(workspace) +
-                                         align256((size_t)kMaxPartialRows * K * 4));
-  colmax_kernel<K><<<grid_a, kRowThreads, 0, stream>>>(X, M, rows_a, partial);
-  reduce_kernel<<<K / 64, 256, 0, stream>>>(partial, grid_a, K, cmax);
-  const int wgs_c = M < kQuantMaxWgs ? M : kQuantMaxWgs;
-  const int rows_c = (M + wgs_c - 1) / wgs_c;
-  const int grid_c = (M + rows_c - 1) / rows_c;
-  quant_kernel<K><<<grid_c, kRowThreads, 0, stream>>>(X, M, g, rows_c, perm, cmax, Xq,
-                                                      a_scale, s_group);
+  constexpr int kTeams = Teams<K>::n;
+  // Pass 1 writes one partial row per workgroup: at most 256 of them, so the
+  // reduction every pass-2 workgroup repeats stays small. Pass 2 has no such
+  // limit: up to 4 workgroups per CU, one row per team where possible.
+  auto split = [&](int cap, int* rows_per_wg) {
+    int wgs = (M + kTeams - 1) / kTeams;
+    wgs = wgs < cap ? wgs : cap;
+    *rows_per_wg = (M + wgs - 1) / wgs;
+    return (M + *rows_per_wg - 1) / *rows_per_wg;
+  };
+  int rpw1 = 0, rpw2 = 0;
+  const int wgs1 = split(kMaxPartialRows, &rpw1);
+  const int wgs2 = split(4 * num_cus(), &rpw2);
+  float* gpart = static_cast<float*>(workspace);
+  rot_max_kernel<K><<<wgs1, Teams<K>::threads, 0, stream>>>(X, M, g, rpw1, perm, gpart);
+  quant_kernel<K><<<wgs2, Teams<K>::threads, 0, stream>>>(X, M, g, rpw2, wgs1, perm, gpart, Xq,
+                                                          a_scale, s_group);
   return hipGetLastError();
 }
 
@@ -147,7 +256,8 @@ int quant_partial_rows(int M) { return M < kMaxPartialRows ? M : kMaxPartialRows
 
 size_t quant_workspace_bytes(int M, int K) {
   (void)M;
-  return align256((size_t)kMaxPartialRows * K * 4) + align256((size_t)K * 4);
+  // per-workgroup group maxima: at most 256 rows of K / 64 floats
+  return align256((size_t)kMaxPartialRows * (K / 64) * 4);
 }
 
 hipError_t launch_rotate_smooth_quant(const uint16_t* X, int M, int K, int g,

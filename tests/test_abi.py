@@ -53,8 +53,8 @@ def test_workspace_queries():
     for M, K, g in ((16, 512, 128), (2048, 4096, 128), (8, 8192, 128), (8192, 8192, 64),
                     (3, 16384, 512)):
         q = lib.rrs_workspace_bytes(M, K, g)
-        # 256 partial rows of K floats plus the K channel maxima, 256-byte aligned
-        assert q == 256 * K * 4 + ((K * 4 + 255) // 256) * 256
+        # per-workgroup group maxima: 256 rows of K / 64 floats, 256-byte aligned
+        assert q == ((256 * (K // 64) * 4 + 255) // 256) * 256
         lw = lib.rrs_linear_workspace_bytes(M, K, g)
         a256 = lambda x: (x + 255) // 256 * 256  # noqa: E731
         assert lw == q + a256(M * K // 2) + a256(4 * M) + a256(4 * (K // g))
