@@ -36,6 +36,8 @@
 // Workgroups are mapped to tiles XCD by XCD: the hardware deals workgroup ids
 // round-robin to the 8 XCDs, so each XCD is given a contiguous run of tiles,
 // ordered in column strips of 4 row tiles to share A and B in its L2.
+#include <type_traits>
+
 #include "rrs_internal.h"
 
 namespace rrs {
@@ -104,6 +106,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
     const float* __restrict__ w_scale, int M, int N, int K, uint16_t* __restrict__ Y,
     int32_t* __restrict__ P) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[2 * STAGE];
+  __shared__ float scale_tab[BM + BN];  // alpha of the tile's rows, then beta of its columns
 
   const TileMap tile = map_tile(M, N);
   if (!tile.valid) return;
@@ -210,7 +213,15 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
     }
   };
 
-  // Prologue: tile 0 staged, tiles 1 and 2 in flight, fragments of chunk 0 read.
+  // Prologue: the tile's output scales into LDS (read only by the epilogue,
+  // after many barriers); tile 0 staged, tiles 1 and 2 in flight, fragments
+  // of chunk 0 read.
+  if constexpr (!kPartials) {
+    if (t < BM)
+      scale_tab[t] = a_scale[min(m0 + t, M - 1)];
+    else if (t < BM + BN)
+      scale_tab[t] = w_scale[min(n0 + t - BM, N - 1)];
+  }
   gload(0, 0);
   lstore(0, 0);
   gload(1, min(1, ntiles - 1));
@@ -296,21 +307,41 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
   if constexpr (!kPartials) {
     // 2^-8 undoes the 16 x 16 of the unpacked operands, 1/K the unnormalized rotation.
     const float inv = __builtin_ldexpf(1.0f, -8) / (float)K;
+    // Scales come from LDS, so no store waits on a global load: this lane's
+    // 32 rows are eight runs of 4 consecutive ones (128-bit reads). A tile
+    // that lies wholly inside Y stores without per-element bounds checks.
+    float4 arow4[2][4];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int col = acc_col(n0, wn, j, lane);
-      const float bcol = col < N ? w_scale[col] : 0.0f;
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+      for (int q = 0; q < 4; ++q)
+        arow4[h][q] = *reinterpret_cast<const float4*>(
+            &scale_tab[acc_row(0, wm, h, 4 * q, lane)]);
+    float bcol2[2];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = acc_row(m0, wm, h, r, lane);
-          if (row < M && col < N) {
-            const float sc = a_scale[row] * inv;
-            Y[(size_t)row * N + col] = float_to_half_bits((f[h][j][r] * sc) * bcol);
+    for (int j = 0; j < 2; ++j) bcol2[j] = scale_tab[BM + acc_col(0, wn, j, lane)];
+    auto store = [&](auto full) {
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int col = acc_col(n0, wn, j, lane);
+        const float bcol = bcol2[j];
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = acc_row(m0, wm, h, r, lane);
+            const float4 a4 = arow4[h][r >> 2];
+            const float ar = (r & 3) == 0 ? a4.x : (r & 3) == 1 ? a4.y : (r & 3) == 2 ? a4.z : a4.w;
+            const float sc = ar * inv;
+            const uint16_t v = float_to_half_bits((f[h][j][r] * sc) * bcol);
+            if (decltype(full)::value || (row < M && col < N)) Y[(size_t)row * N + col] = v;
           }
-        }
-    }
+      }
+    };
+    if (m0 + BM <= M && n0 + BN <= N)
+      store(std::true_type{});
+    else
+      store(std::false_type{});
   }
 }
 
