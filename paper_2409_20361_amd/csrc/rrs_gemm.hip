@@ -8,9 +8,11 @@
 // tiles of 128 (four MFMA k-steps of 32).
 //
 // Data path: packed INT4 (Xq: M x K/2, Wq: N x K/2, K contiguous) is loaded
-// from HBM into registers one tile ahead, unpacked to int8 and stored in a
+// from HBM into registers two tiles ahead, unpacked to int8 and stored in a
 // double-buffered LDS stage whose rows are padded to 144 bytes (conflict-free
-// 128-bit fragment reads at immediate offsets). A nibble is unpacked into the
+// 128-bit fragment reads at immediate offsets). The unpack and the LDS stores
+// of the next tile are spread over the MFMAs of the current tile's H0 phase
+// (below), so the matrix core is not idle while they run. A nibble is unpacked into the
 // high half of its int8 lane (the byte holds 16 q): low nibbles are
 // (w << 4) & 0xF0F0F0F0, high nibbles w & 0xF0F0F0F0, three VALU ops per
 // eight codes. Products are 256 q w, exact in int32 for every group size here;
@@ -155,6 +157,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
     *reinterpret_cast<uint4*>(s + b_st) = unpack_pair(rb0[set].x, rb0[set].y);
     *reinterpret_cast<uint4*>(s + b_st + 16) = unpack_pair(rb0[set].z, rb0[set].w);
   };
+  // One sixth of lstore: piece i of this thread's six 16-byte LDS stores.
+  auto lpiece = [&](int set, int stage, int i) {
+    uint8_t* s = lds + stage * STAGE;
+    if (i == 0) *reinterpret_cast<uint4*>(s + a_st) = unpack_pair(ra0[set].x, ra0[set].y);
+    if (i == 1) *reinterpret_cast<uint4*>(s + a_st + 16) = unpack_pair(ra0[set].z, ra0[set].w);
+    if (i == 2) *reinterpret_cast<uint4*>(s + b_st) = unpack_pair(rb0[set].x, rb0[set].y);
+    if (i == 3) *reinterpret_cast<uint4*>(s + a_st + 32) = unpack_pair(ra1[set].x, ra1[set].y);
+    if (i == 4) *reinterpret_cast<uint4*>(s + a_st + 48) = unpack_pair(ra1[set].z, ra1[set].w);
+    if (i == 5) *reinterpret_cast<uint4*>(s + b_st + 16) = unpack_pair(rb0[set].z, rb0[set].w);
+  };
   auto afrag = [&](int stage, int h, int ks) -> v4i {
     return *reinterpret_cast<const v4i*>(lds + stage * STAGE + a_fr + h * 32 * ROWP + ks * 32);
   };
@@ -254,7 +266,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
 
       // Phase H0: MFMAs of rows 0-31; A fragments of rows 32-63 are read;
       // rescale of H1's group closed by the previous chunk (for the very
-      // first chunk acc[1] and s_prev are 0).
+      // first chunk acc[1] and s_prev are 0); in a tile's last chunk, the
+      // next tile is unpacked into the other LDS stage.
 #pragma unroll
       for (int s = 0; s < PH; ++s) {
         const bool fresh = g_first && s == 0;
@@ -264,15 +277,20 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
         if (g_first) {
           if (!kPartials || grp > 0) rescale(1, s * CONV, s_prev, grp - 1);
         }
+        if (tile_end) {
+          const int kt = j0 >> 2;
+#pragma unroll
+          for (int i = s * 6 / PH; i < (s + 1) * 6 / PH; ++i) lpiece((kt + 1) & 1, stage ^ 1, i);
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
 
-      // End of a tile: every wave has read this tile's fragments, so the
-      // next tile goes into the other stage now; the one after is fetched.
-      // (On the last tile this stages a duplicate that is never read.)
+      // End of a tile: every wave has read this tile's fragments and staged
+      // its pieces of the next tile (in the other stage) during phase H0;
+      // after the barrier the tile after next is fetched. (On the last tile
+      // this stages a duplicate that is never read.)
       if (tile_end) {
         const int kt = j0 >> 2;
-        lstore((kt + 1) & 1, stage ^ 1);
         __syncthreads();
         gload((kt + 1) & 1, min(kt + 3, ntiles - 1));
       }
