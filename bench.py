@@ -77,6 +77,20 @@ def copy_calibration(torch):
     log(f"copy calibration: 5 copies of {n} bytes")
 
 
+def prewarm(torch, fn, seconds=0.3):
+    """Run `fn` untimed for a fixed wall time before the warmup steps: the GPU
+    takes tens of milliseconds of load to reach its steady clock, far longer
+    than a few warmup steps of a sub-millisecond workload."""
+    t0 = time.perf_counter()
+    n = 0
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(20):
+            fn()
+        torch.cuda.synchronize()
+        n += 20
+    log(f"pre-warm: {n} untimed calls in {time.perf_counter() - t0:.2f} s")
+
+
 def qkv_step_bench(args, torch, rrs, synth):
     w = synth.WORKLOADS["qkv"]
     dev = torch.device("cuda:0")
@@ -100,6 +114,7 @@ def qkv_step_bench(args, torch, rrs, synth):
         if evs is not None:
             evs[2].record()
 
+    prewarm(torch, step)
     log(f"warmup {args.warmup} steps")
     for _ in range(args.warmup):
         step()
@@ -131,8 +146,8 @@ def decode_bench(args, torch, rrs, synth):
     Y = torch.empty((w.M, w.N), dtype=torch.float16, device=dev)
     lws = torch.empty((rrs.linear_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
                       device=dev)
-    for i in range(8):
-        rrs.w4a4_gemm(Xq, a, s, copies[i % 4], beta, w.g, out=Y)
+    it = iter(range(1 << 30))
+    prewarm(torch, lambda: rrs.w4a4_gemm(Xq, a, s, copies[next(it) % 4], beta, w.g, out=Y))
     torch.cuda.synchronize()
     n = args.decode_steps
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]

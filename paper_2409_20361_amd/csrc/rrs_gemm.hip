@@ -398,6 +398,8 @@ bool main_kernel_fits(int K, int g) {
 hipError_t launch_w4a4_gemm(const uint8_t* Xq, const float* a_scale, const float* s_group,
                             const uint8_t* Wq, const float* w_scale, int M, int N, int K,
                             int g, uint16_t* Y, hipStream_t stream) {
+  if (decode_kernel_fits(M))
+    return launch_w4a4_gemm_decode(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, stream);
   if (!main_kernel_fits(K, g))
     return launch_w4a4_gemm_small(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, stream);
   return launch_main<false>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, nullptr, stream);

@@ -9,7 +9,7 @@
 
 namespace rrs {
 
-// Channel-max partials: one row of K floats per workgroup of the first pass.
+// Group-max partials: one row of K / g floats per workgroup of the first pass.
 int quant_partial_rows(int M);
 size_t quant_workspace_bytes(int M, int K);
 
@@ -36,6 +36,13 @@ hipError_t launch_w4a4_gemm_small(const uint8_t* Xq, const float* a_scale,
 hipError_t launch_w4a4_gemm_partials_small(const uint8_t* Xq, const uint8_t* Wq, int M,
                                            int N, int K, int g, int32_t* P,
                                            hipStream_t stream);
+
+// Few-token kernel (decode): streams Wq once, for M <= 16.
+bool decode_kernel_fits(int M);
+hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
+                                   const float* s_group, const uint8_t* Wq,
+                                   const float* w_scale, int M, int N, int K, int g,
+                                   uint16_t* Y, hipStream_t stream);
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 

@@ -149,14 +149,32 @@ __global__ __launch_bounds__(Teams<K>::threads) void quant_kernel(
   const int G = K / g;
   float* slot = slots + team * RF;
 
-  // s_b = max over the partial rows; threads split (group, row slice).
+  // This team's first row is requested before anything else, so its load
+  // latency overlaps the reduction below.
+  const int iters = (rows_per_wg + kTeams - 1) / kTeams;
+  const int r0 = blockIdx.x * rows_per_wg;
+  const int r1 = min(M, r0 + rows_per_wg);
+  float vn[E];  // next row, loaded while the current one is processed
+  load_row_or_zero<K>(X, r0 + team, r1, t, vn);
+
+  // s_b = max over the partial rows; threads split (group, row slice) and
+  // issue their loads eight at a time so the latencies overlap.
   {
     const int nsl = kThreads / G;  // G <= 256 <= kThreads
     const int b = tid % G;
     const int sl = tid / G;
     float m = 0.0f;
-    if (sl < nsl)
-      for (int i = sl; i < nparts; i += nsl) m = fmaxf(m, gpart[(size_t)i * G + b]);
+    if (sl < nsl) {
+      int i = sl;
+      for (; i + 7 * nsl < nparts; i += 8 * nsl) {
+        float x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x[u] = gpart[(size_t)(i + u * nsl) * G + b];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) m = fmaxf(m, x[u]);
+      }
+      for (; i < nparts; i += nsl) m = fmaxf(m, gpart[(size_t)i * G + b]);
+    }
     cbuf[tid] = m;
     __syncthreads();
     if (tid < G) {
@@ -172,11 +190,6 @@ __global__ __launch_bounds__(Teams<K>::threads) void quant_kernel(
   for (int e = 0; e < E; ++e) src[e] = perm ? perm[t * E + e] : t * E + e;
   const float rb = rg[(t * E) / g];  // this thread's positions lie in one group
 
-  const int iters = (rows_per_wg + kTeams - 1) / kTeams;
-  const int r0 = blockIdx.x * rows_per_wg;
-  const int r1 = min(M, r0 + rows_per_wg);
-  float vn[E];  // next row, loaded while the current one is processed
-  load_row_or_zero<K>(X, r0 + team, r1, t, vn);
   for (int it = 0; it < iters; ++it) {
     const int r = r0 + it * kTeams + team;
     const bool live = r < r1;

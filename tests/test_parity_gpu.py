@@ -274,6 +274,62 @@ def test_gemm_extreme_partials(g):
     check_y(to_np(Y).astype(np.float32), y_ref, P, s, alpha, beta, K, f"extreme g={g}")
 
 
+def _gemm_codes_case(qx, qw, g, seed, label):
+    """rrs_w4a4_gemm on given codes with random positive scales vs the oracle."""
+    rrs = _rrs()
+    M, K = qx.shape
+    N = qw.shape[1]
+    rng = np.random.default_rng(seed)
+    alpha = (rng.random(M) + 0.5).astype(np.float32)
+    beta = (rng.random(N) * 0.01 + 0.001).astype(np.float32)
+    s = (rng.random(K // g) * 3 + 0.25).astype(np.float32)
+    print(f"[case] gemm {label} M={M} K={K} N={N} g={g}", flush=True)
+    Y = rrs.w4a4_gemm(to_gpu(O.pack_int4(qx)), to_gpu(alpha), to_gpu(s),
+                      to_gpu(O.pack_int4(qw.T)), to_gpu(beta), g)
+    P = O.group_partials(qx, qw, g)
+    y_ref = O.output(P, s, alpha, beta, norm=K)
+    check_y(to_np(Y).astype(np.float32), y_ref, P, s, alpha, beta, K, label)
+    return P
+
+
+@pytest.mark.parametrize("M", [1, 8, 16])
+@pytest.mark.parametrize("g", [64, 128, 256, 512])
+def test_gemm_few_tokens_extreme(M, g):
+    # Few-token (decode) kernel with every code +-7: |P_b| = 49 g.
+    K, N = 2048, 160
+    rng = np.random.default_rng(1000 + M * 10 + g)
+    qx = np.where(rng.random((M, K)) < 0.5, -7, 7).astype(np.int8)
+    qx[0] = 7
+    qw = np.where(rng.random((K, N)) < 0.5, -7, 7).astype(np.int8)
+    qw[:, 0] = 7
+    P = _gemm_codes_case(qx, qw, g, g + M, f"few-token extreme M={M} g={g}")
+    assert np.abs(P).max() == 49 * g
+
+
+@pytest.mark.parametrize("M,K,N,g", [
+    (1, 512, 16, 512), (2, 512, 48, 64), (3, 1024, 272, 128), (8, 8192, 144, 128),
+    (13, 4096, 64, 256), (16, 16384, 32, 64), (16, 2048, 1040, 512), (17, 2048, 80, 128),
+])
+def test_gemm_few_tokens_random(M, K, N, g):
+    # M <= 16 runs the few-token kernel (M = 17 the main kernel): every K
+    # split, group size and ragged column count, against the oracle.
+    rng = np.random.default_rng(M * 31 + K + N)
+    qx = rng.integers(-7, 8, size=(M, K)).astype(np.int8)
+    qw = rng.integers(-7, 8, size=(K, N)).astype(np.int8)
+    _gemm_codes_case(qx, qw, g, M + N, f"few-token random {M}x{K}x{N}")
+
+
+def test_gemm_few_tokens_deterministic():
+    rrs = _rrs()
+    w = synth.WORKLOADS["decode"]
+    Xg = to_gpu(synth.activations(w))
+    Wq, beta = rrs.prepare_weight(to_gpu(synth.weights(w)))
+    Xq, a, s = rrs.rotate_smooth_quant(Xg, w.g)
+    y1 = rrs.w4a4_gemm(Xq, a, s, Wq, beta, w.g)
+    y2 = rrs.w4a4_gemm(Xq, a, s, Wq, beta, w.g)
+    assert torch.equal(y1, y2)
+
+
 def test_gemm_deterministic():
     rrs = _rrs()
     w = synth.WORKLOADS["qkv"]
