@@ -6,17 +6,19 @@
 // With a handful of tokens the work is streaming Wq (N x K/2 bytes) through
 // the chip once; the matrix core only has to keep up. The kernel therefore
 // maximizes the weight bytes in flight and never stages them in LDS:
-//   - a workgroup owns 16 output columns (16 rows of Wq); its four waves
-//     split K into quarters (whole smoothing groups each) and add their
-//     fp32 partial sums in a fixed order at the end (deterministic);
+//   - a workgroup owns two blocks of 16 output columns (rows of Wq); its four
+//     waves split K into quarters (whole smoothing groups each) and add their
+//     fp32 partial sums in a fixed order at the end (deterministic); each
+//     wave unpacks its token codes once for both blocks;
 //   - per group, lane (c, q) (c = lane % 16, q = lane / 16) loads the g/8
 //     contiguous bytes [q g/8, (q+1) g/8) of the group in Wq row n0 + c, and
 //     the same bytes of Xq row c (zero for c >= M). MFMA k-step s of the group
 //     (v_mfma_i32_16x16x64_i8, 64 codes) takes bytes [8 s, 8 s + 8) of every
 //     lane, so each k-step stays inside one group and A and B pair the same
 //     codes;
-//   - loads run several groups ahead of the MFMAs (about 64 bytes of Wq per
-//     lane in flight, tens of KB per CU).
+//   - loads run several groups ahead of the MFMAs (about 48 bytes of Wq per
+//     lane in flight, tens of KB per CU), with no branch between a load and
+//     its use, so each wait is for exactly the group about to be used.
 // Codes are unpacked into the high nibble of each int8 lane (16 q), as in the
 // main kernel; the 2^-8 is folded into the output scale. The group rescale
 // uses the same magic-number seed: the group's first MFMA starts from the bits
@@ -30,8 +32,9 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 256;  // 4 waves: K quarters of the same 16 columns
-constexpr int kCols = 16;
+constexpr int kThreads = 256;  // 4 waves: K quarters of the same columns
+constexpr int kCols = 16;      // columns per MFMA block
+constexpr int kBlocks = 2;     // column blocks per workgroup (they share the A unpack)
 
 __device__ __forceinline__ v4i unpack_pair(uint32_t w0, uint32_t w1) {
   v4i r;
@@ -61,93 +64,158 @@ __device__ __forceinline__ void load_words(const uint8_t* __restrict__ p, uint32
   }
 }
 
-// GS = g / 64 MFMA k-steps per group.
-template <int GS>
+// Groups per wave: whole groups, K split in quarters (one group each when K
+// has fewer than four groups; waves past the last group get none).
+__host__ __device__ inline int groups_per_wave(int K, int g) { return K / g >= 4 ? K / g / 4 : 1; }
+// LDS bytes per row of one wave's slice of Xq: its groups, padded by 16 bytes
+// so the 16 rows a lane quarter reads start in different banks.
+__host__ __device__ inline int a_row_bytes(int K, int g) {
+  return groups_per_wave(K, g) * (g / 2) + 16;
+}
+constexpr int kMaxLdsA = 10240;  // per wave; four workgroups per CU fit in LDS
+constexpr int kPartBytes = 4 * kBlocks * 64 * 16;
+
+// GS = g / 64 MFMA k-steps per group. kLdsA: each wave first copies its K
+// quarter of Xq into LDS (when it fits), so the token fragments are LDS reads
+// instead of vector-memory loads queued behind the weight stream.
+template <int GS, bool kLdsA>
 __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
     const float* __restrict__ w_scale, int M, int N, int K, uint16_t* __restrict__ Y) {
   constexpr int g = GS * 64;
-  constexpr int NW = g / 32;                 // words per lane per group
-  constexpr int D = NW >= 16 ? 1 : 16 / NW;  // groups in flight (64 bytes per lane)
-  __shared__ v4f part[4][64];
+  constexpr int NW = g / 32;                  // words per lane per group and block
+  constexpr int D = NW >= 16 ? 1 : (NW >= 8 ? 2 : 4);  // groups in flight
+  // Token slices during the loop; the partial sums reuse the space after it.
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsA ? 4 * kMaxLdsA : kPartBytes];
+  v4f(*part)[kBlocks][64] = reinterpret_cast<v4f(*)[kBlocks][64]>(lds);
 
   const int t = threadIdx.x;
   const int lane = t & 63;
-  const int kq = t >> 6;  // K quarter of this wave
+  // K quarter of this wave; uniform, so group indices and scales are scalar.
+  const int kq = __builtin_amdgcn_readfirstlane(t >> 6);
   const int c = lane & 15;
   const int q = lane >> 4;
-  const int n0 = blockIdx.x * kCols;
+  const int n0 = blockIdx.x * (kBlocks * kCols);
   const size_t krow = (size_t)K / 2;
   const int G = K / g;
-  const int per = G >= 4 ? G / 4 : 1;  // groups per wave
+  const int per = groups_per_wave(K, g);  // the same for every wave
   const int b0 = kq * per;
-  const int b1 = min(G, b0 + per);
+  const int nb = min(G, b0 + per) - b0;  // groups this wave really has (<= 0 past K)
+  const int steps = (per + D - 1) / D * D;
 
-  const uint8_t* pb = Wq + (size_t)(n0 + c) * krow + q * (g / 8);
-  const bool arow = c < M;
-  const uint8_t* pa = Xq + (size_t)(arow ? c : 0) * krow + q * (g / 8);
-
-  uint32_t wb[D][NW], wa[D][NW];
-  auto load = [&](int d, int b) {
-    load_words<NW>(pb + (size_t)b * (g / 2), wb[d]);
-    if (arow) {
-      load_words<NW>(pa + (size_t)b * (g / 2), wa[d]);
-    } else {
+  // The loop is free of branches around loads, so the compiler can count the
+  // loads in flight and wait for exactly the group it needs. Steps past this
+  // wave's groups load a valid group and add it with scale 0 (exactly 0: the
+  // partial sums are finite). Token rows >= M load row M - 1; they only feed
+  // output rows that are never stored. Column blocks past N load block 0 and
+  // are never stored.
+  const uint8_t* pa = Xq + (size_t)min(c, M - 1) * krow + q * (g / 8);
+  const uint8_t* pb[kBlocks];
 #pragma unroll
-      for (int i = 0; i < NW; ++i) wa[d][i] = 0u;
+  for (int j = 0; j < kBlocks; ++j) {
+    const int n = n0 + j * kCols < N ? n0 + j * kCols : 0;
+    pb[j] = Wq + (size_t)(n + c) * krow + q * (g / 8);
+  }
+
+  // Wave-private copy of this wave's K quarter of Xq: row r < M at
+  // r * a_row_bytes(K); lanes then read their row min(c, M - 1).
+  uint8_t* aq = lds + kq * kMaxLdsA;
+  const int arb = a_row_bytes(K, g);
+  if constexpr (kLdsA) {
+    const int qb = max(nb, 0) * (g / 2);  // bytes of this wave's groups in a row
+    const uint8_t* src = Xq + (size_t)b0 * (g / 2);
+    for (int e = lane * 16; e < M * qb; e += 64 * 16) {
+      const int r = e / qb;
+      const int o = e - r * qb;
+      *reinterpret_cast<uint4*>(aq + r * arb + o) =
+          *reinterpret_cast<const uint4*>(src + (size_t)r * krow + o);
     }
+  }
+  const uint8_t* pal = aq + min(c, M - 1) * arb + q * (g / 8);
+
+  uint32_t wa[D][NW], wb[D][kBlocks][NW];
+  auto load = [&](int d, int i) {
+    const size_t off = (size_t)min(b0 + i, G - 1) * (g / 2);
+    if constexpr (!kLdsA) load_words<NW>(pa + off, wa[d]);
+#pragma unroll
+    for (int j = 0; j < kBlocks; ++j) load_words<NW>(pb[j] + off, wb[d][j]);
+  };
+  // Token words from LDS, read just before use (the quarter starts at group b0;
+  // padded steps past this wave's groups reread its last group).
+  auto read_a = [&](int d, int i) {
+    const int li = min(i, max(nb, 1) - 1);
+    load_words<NW>(pal + li * (g / 2), wa[d]);
   };
 
   constexpr int kMagic = 0x4B400000;  // bits of 1.5 * 2^23
   const v4i seed = GS > 4 ? v4i{0, 0, 0, 0} : v4i{kMagic, kMagic, kMagic, kMagic};
-  float f[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  float f[kBlocks][4];
+#pragma unroll
+  for (int j = 0; j < kBlocks; ++j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) f[j][r] = 0.0f;
 
+  auto consume = [&](int d, int i) {
+    if constexpr (kLdsA) read_a(d, i);
+    const float s = i < nb ? s_group[min(b0 + i, G - 1)] : 0.0f;
+    v4i acc[kBlocks];
 #pragma unroll
-  for (int d = 0; d < D; ++d)
-    if (b0 + d < b1) load(d, b0 + d);
-
-  for (int b = b0; b < b1; b += D) {
+    for (int j = 0; j < kBlocks; ++j) acc[j] = seed;
 #pragma unroll
-    for (int d = 0; d < D; ++d) {
-      const int bb = b + d;
-      if (bb < b1) {
-        const float s = s_group[bb];
-        v4i acc = seed;
+    for (int st = 0; st < GS; ++st) {
+      const v4i a = unpack_pair(wa[d][2 * st], wa[d][2 * st + 1]);
 #pragma unroll
-        for (int st = 0; st < GS; ++st)
-          acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(unpack_pair(wa[d][2 * st], wa[d][2 * st + 1]),
-                                                     unpack_pair(wb[d][2 * st], wb[d][2 * st + 1]),
-                                                     acc, 0, 0, 0);
-        if (bb + D < b1) load(d, bb + D);
-        // Bit-cast the whole vector, then index: bit-casting a single element
-        // of an ext_vector is miscompiled (every element reads element 0).
-        const v4f accf = __builtin_bit_cast(v4f, acc);
+      for (int j = 0; j < kBlocks; ++j)
+        acc[j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(
+            a, unpack_pair(wb[d][j][2 * st], wb[d][j][2 * st + 1]), acc[j], 0, 0, 0);
+    }
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float pv = GS > 4 ? (float)acc[r] : accf[r] - 12582912.0f;
-          f[r] = __builtin_fmaf(s, pv, f[r]);
-        }
+    for (int j = 0; j < kBlocks; ++j) {
+      // Bit-cast the whole vector, then index: bit-casting a single element
+      // of an ext_vector is miscompiled (every element reads element 0).
+      const v4f accf = __builtin_bit_cast(v4f, acc[j]);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float pv = GS > 4 ? (float)acc[j][r] : accf[r] - 12582912.0f;
+        f[j][r] = __builtin_fmaf(s, pv, f[j][r]);
       }
     }
+  };
+
+#pragma unroll
+  for (int d = 0; d < D; ++d) load(d, d);
+  int i = 0;
+  for (; i < steps - D; i += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      consume(d, i + d);
+      load(d, i + d + D);
+    }
   }
+#pragma unroll
+  for (int d = 0; d < D; ++d) consume(d, i + d);
 
   // Partial sums of the four K quarters, added in a fixed order.
-  part[kq][lane] = v4f{f[0], f[1], f[2], f[3]};
-  __syncthreads();
-  if (kq == 0) {
-    v4f sum = part[0][lane];
+  if constexpr (kLdsA) __syncthreads();  // every wave is done with its token slice
 #pragma unroll
-    for (int w = 1; w < 4; ++w) {
-      const v4f p = part[w][lane];
-      sum.x += p.x;
-      sum.y += p.y;
-      sum.z += p.z;
-      sum.w += p.w;
+  for (int j = 0; j < kBlocks; ++j) part[kq][j][lane] = v4f{f[j][0], f[j][1], f[j][2], f[j][3]};
+  __syncthreads();
+  // Wave w stores column block w (if any): sums in the order kq = 0, 1, 2, 3.
+  const int w = t >> 6;
+  if (w < kBlocks && n0 + w * kCols < N) {
+    v4f sum = part[0][w][lane];
+#pragma unroll
+    for (int p = 1; p < 4; ++p) {
+      const v4f x = part[p][w][lane];
+      sum.x += x.x;
+      sum.y += x.y;
+      sum.z += x.z;
+      sum.w += x.w;
     }
     // 2^-8 undoes the 16 x 16 of the unpacked operands, 1/K the unnormalized rotation.
     const float inv = __builtin_ldexpf(1.0f, -8) / (float)K;
-    const int col = n0 + c;
+    const int col = n0 + w * kCols + c;
     const float bcol = w_scale[col];
     const float sv[4] = {sum.x, sum.y, sum.z, sum.w};
 #pragma unroll
@@ -169,23 +237,21 @@ hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
                                    const float* s_group, const uint8_t* Wq,
                                    const float* w_scale, int M, int N, int K, int g,
                                    uint16_t* Y, hipStream_t stream) {
-  const int grid = N / kCols;  // N % 16 == 0 is an API precondition
+  const int grid = (N / kCols + kBlocks - 1) / kBlocks;  // N % 16 == 0 (API precondition)
+  const bool lds_a = (size_t)M * a_row_bytes(K, g) <= (size_t)kMaxLdsA;
+#define RRS_DECODE(GS_)                                                                  \
+  (lds_a ? (gemm_decode_kernel<GS_, true><<<grid, kThreads, 0, stream>>>(                 \
+               Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y), 0)                        \
+         : (gemm_decode_kernel<GS_, false><<<grid, kThreads, 0, stream>>>(                \
+               Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y), 0))
   switch (g) {
-    case 64:
-      gemm_decode_kernel<1><<<grid, kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y);
-      break;
-    case 128:
-      gemm_decode_kernel<2><<<grid, kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y);
-      break;
-    case 256:
-      gemm_decode_kernel<4><<<grid, kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y);
-      break;
-    case 512:
-      gemm_decode_kernel<8><<<grid, kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y);
-      break;
-    default:
-      return hipErrorInvalidValue;
+    case 64: RRS_DECODE(1); break;
+    case 128: RRS_DECODE(2); break;
+    case 256: RRS_DECODE(4); break;
+    case 512: RRS_DECODE(8); break;
+    default: return hipErrorInvalidValue;
   }
+#undef RRS_DECODE
   return hipGetLastError();
 }
 
