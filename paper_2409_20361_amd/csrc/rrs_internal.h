@@ -17,6 +17,12 @@ hipError_t launch_rotate_smooth_quant(const uint16_t* X, int M, int K, int g,
                                       const int32_t* perm, uint8_t* Xq, float* a_scale,
                                       float* s_group, void* workspace, hipStream_t stream);
 
+// One-wave-per-row variant for K <= 4096 (same two passes, same bits).
+hipError_t launch_rotate_smooth_quant_wave(const uint16_t* X, int M, int K, int g,
+                                           const int32_t* perm, uint8_t* Xq, float* a_scale,
+                                           float* s_group, void* workspace, int max_partials,
+                                           int max_quant_wgs, hipStream_t stream);
+
 hipError_t launch_prepare_weight(const uint16_t* W, int K, int N, const int32_t* perm,
                                  uint8_t* Wq, float* w_scale, hipStream_t stream);
 

@@ -13,9 +13,11 @@
 //      then re-rotates its rows (identical code, identical bits; X mostly
 //      comes from the MALL the second time), takes the per-token maximum of
 //      fl(|y_ij| r_b), and writes alpha_i and the packed INT4 codes.
-// A workgroup holds 1, 2 or 4 teams of 256 threads (K = 16384, 8192, <= 4096:
-// a thread's share of a row stays in registers); each team works on one row at
-// a time. Cross-team and cross-wave reductions go through LDS, no atomics.
+// In this file a workgroup holds 1, 2 or 4 teams of 256 threads (K = 16384,
+// 8192, <= 2048: a thread's share of a row stays in registers); each team
+// works on one row at a time. Cross-team and cross-wave reductions go through
+// LDS, no atomics. K = 4096 (and K = 2048 with many rows) takes the
+// one-wave-per-row kernels of rrs_quant_wave.hip instead.
 #include "rrs_device.h"
 #include "rrs_internal.h"
 
@@ -276,11 +278,15 @@ size_t quant_workspace_bytes(int M, int K) {
 hipError_t launch_rotate_smooth_quant(const uint16_t* X, int M, int K, int g,
                                       const int32_t* perm, uint8_t* Xq, float* a_scale,
                                       float* s_group, void* workspace, hipStream_t stream) {
+  // One wave per row wins at K = 4096, and at K = 2048 once there are enough
+  // rows; elsewhere the team kernels below are faster (measured).
+  if (K == 4096 || (K == 2048 && M >= 512))
+    return launch_rotate_smooth_quant_wave(X, M, K, g, perm, Xq, a_scale, s_group, workspace,
+                                           kMaxPartialRows, 2 * num_cus(), stream);
   switch (K) {
     case 512: return launch_k<512>(X, M, g, perm, Xq, a_scale, s_group, workspace, stream);
     case 1024: return launch_k<1024>(X, M, g, perm, Xq, a_scale, s_group, workspace, stream);
     case 2048: return launch_k<2048>(X, M, g, perm, Xq, a_scale, s_group, workspace, stream);
-    case 4096: return launch_k<4096>(X, M, g, perm, Xq, a_scale, s_group, workspace, stream);
     case 8192: return launch_k<8192>(X, M, g, perm, Xq, a_scale, s_group, workspace, stream);
     case 16384: return launch_k<16384>(X, M, g, perm, Xq, a_scale, s_group, workspace, stream);
     default: return hipErrorInvalidValue;

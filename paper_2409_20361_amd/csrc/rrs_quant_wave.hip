@@ -1,0 +1,332 @@
+// Online rotate + runtime smooth + per-token INT4 quantization for K <= 4096
+// (Section 3.3 then Section 3.2; Eq. 1-2; Section 2.1): one wave per row.
+//
+// The same two launches as for large K (see rrs_quant.hip): rot_max writes one
+// row of group maxima per workgroup, quant reduces them to s_b and r_b and
+// writes the codes. What differs is how a row is rotated: here a row belongs
+// to R = K/64 lanes of one wave (a wave holds 64/R rows), so the whole
+// transform needs no workgroup barrier:
+//   layout 1: lane l of the row holds elements i = 64 l + e (e = 0..63), i.e.
+//             64 contiguous values (eight 16-byte loads); FWHT stages
+//             h = 1..32 are in-register butterflies;
+//   layout 2: after a transpose through a wave-private LDS region, lane l
+//             holds i = l + R e; stages h = 64..K/2 (index bits 6 .. log2 K - 1,
+//             register bits 6 - log2 R .. 5) are in-register butterflies.
+// Stage order stays h = 1, 2, ..., K/2 with one rounded fp32 add or subtract
+// per butterfly output, so the result is bit-identical to the canonical
+// sequential transform (and to the team kernels for large K). quant then
+// transposes back to layout 1 (or gathers the statically reordered positions)
+// so each lane quantizes and packs 64 consecutive codes into 32 bytes.
+//
+// LDS row region: element i at A(i) = i + 4 floor(i / 64) (16-byte aligned runs
+// of 64, conflict-free 128-bit writes of layout 1 and 32-bit reads of layout 2);
+// rows of one wave are 16 floats further apart so they start in other banks.
+#include "rrs_device.h"
+#include "rrs_internal.h"
+
+namespace rrs {
+namespace {
+
+template <int K>
+struct WaveRow {
+  static constexpr int R = K / 64;             // lanes per row
+  static constexpr int LR = ilog2(R);          // 3 .. 6
+  static constexpr int RW = 64 / R;            // rows per wave
+  static constexpr int RF = K + K / 16 + 16;   // LDS floats per row region
+  static constexpr int LOGK = ilog2(K);
+  static_assert(K >= 512 && K <= 4096 && (1 << LOGK) == K, "wave path: K in 512..4096");
+};
+
+__device__ __forceinline__ int lds_a(int i) { return i + ((i >> 6) << 2); }
+
+// Raw halves of 64 consecutive elements (128 bytes) of a row, or zeros.
+__device__ __forceinline__ void load_raw64(const uint16_t* __restrict__ src, bool live,
+                                           uint4 (&raw)[8]) {
+  if (live) {
+#pragma unroll
+    for (int c = 0; c < 8; ++c) raw[c] = reinterpret_cast<const uint4*>(src)[c];
+  } else {
+#pragma unroll
+    for (int c = 0; c < 8; ++c) raw[c] = make_uint4(0u, 0u, 0u, 0u);
+  }
+}
+
+__device__ __forceinline__ void raw_to_float(const uint4 (&raw)[8], float (&v)[64]) {
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    const uint32_t w[4] = {raw[c].x, raw[c].y, raw[c].z, raw[c].w};
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      v[c * 8 + 2 * m] = half_to_float(w[m] & 0xFFFFu);
+      v[c * 8 + 2 * m + 1] = half_to_float(w[m] >> 16);
+    }
+  }
+}
+
+// Rotate one row held in layout 1 (v[e] = x[64 l + e]); on exit layout 2
+// (v[e] = y[l + R e]). `row` is this row's LDS region (wave-private).
+template <int K>
+__device__ __forceinline__ void fwht_wave_row(float (&v)[64], float* row, int l) {
+  using S = WaveRow<K>;
+  fwht_stages<64, 0, 6>(v);
+#pragma unroll
+  for (int m = 0; m < 16; ++m)
+    *reinterpret_cast<float4*>(row + lds_a(64 * l + 4 * m)) =
+        make_float4(v[4 * m], v[4 * m + 1], v[4 * m + 2], v[4 * m + 3]);
+#pragma unroll
+  for (int e = 0; e < 64; ++e) v[e] = row[lds_a(l + S::R * e)];
+  fwht_stages<64, 6 - S::LR, 6>(v);
+}
+
+// Max over the R lanes of each row of the wave (aligned groups of R lanes).
+template <int R>
+__device__ __forceinline__ float row_max(float x) {
+#pragma unroll
+  for (int o = 1; o < R; o <<= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+
+// ---------------------------------------------------------------------------
+// 1. rotate + per-workgroup group maxima (8 waves per workgroup)
+// ---------------------------------------------------------------------------
+constexpr int kRotWaves = 8;
+
+template <int K>
+__global__ __launch_bounds__(kRotWaves * 64) void rot_max_wave_kernel(
+    const uint16_t* __restrict__ X, int M, int g, int rows_per_wg,
+    const int32_t* __restrict__ perm, float* __restrict__ gpart) {
+  using S = WaveRow<K>;
+  __shared__ __attribute__((aligned(16))) float rows[kRotWaves * S::RW * S::RF];
+  __shared__ uint32_t cbuf[K];     // channel maxima (bits of non-negative floats)
+  __shared__ float red[kRotWaves * 64];
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  const int sub = lane >> S::LR;   // row of the wave
+  const int l = lane & (S::R - 1);  // lane within the row
+  float* row = rows + (wave * S::RW + sub) * S::RF;
+  for (int i = tid; i < K; i += kRotWaves * 64) cbuf[i] = 0u;
+
+  const int r0 = blockIdx.x * rows_per_wg;
+  const int r1 = min(M, r0 + rows_per_wg);
+  const int per_pass = kRotWaves * S::RW;
+  const int passes = (rows_per_wg + per_pass - 1) / per_pass;
+  auto row_of = [&](int p) { return r0 + (p * kRotWaves + wave) * S::RW + sub; };
+
+  float cm[64];
+#pragma unroll
+  for (int e = 0; e < 64; ++e) cm[e] = 0.0f;
+  uint4 raw[8];
+  {
+    const int r = row_of(0);
+    load_raw64(X + (size_t)min(r, M - 1) * K + 64 * l, r < r1, raw);
+  }
+  for (int p = 0; p < passes; ++p) {
+    float v[64];
+    raw_to_float(raw, v);
+    if (p + 1 < passes) {
+      const int r = row_of(p + 1);
+      load_raw64(X + (size_t)min(r, M - 1) * K + 64 * l, r < r1, raw);
+    }
+    fwht_wave_row<K>(v, row, l);  // v[e] = y[l + R e]
+#pragma unroll
+    for (int e = 0; e < 64; ++e) cm[e] = fmaxf(cm[e], fabsf(v[e]));
+  }
+  // Rows of the same wave hold the same channels: combine them in registers.
+#pragma unroll
+  for (int e = 0; e < 64; ++e)
+#pragma unroll
+    for (int o = S::R; o < 64; o <<= 1) cm[e] = fmaxf(cm[e], __shfl_xor(cm[e], o, 64));
+  __syncthreads();  // cbuf zeroed
+  if (sub == 0) {
+#pragma unroll
+    for (int e = 0; e < 64; ++e) atomicMax(&cbuf[l + S::R * e], __float_as_uint(cm[e]));
+  }
+  __syncthreads();
+  // Group maxima over the (reordered) positions: thread t covers P = K / 512
+  // (at least 1) consecutive positions, all in one group (P <= 8 < g).
+  constexpr int NT = kRotWaves * 64;
+  constexpr int P = K >= NT ? K / NT : 1;
+  static_assert(K / P == NT, "every thread covers P positions");
+  float pm = 0.0f;
+  if (perm) {
+    int idx[P];  // all loads first, so their latencies overlap
+#pragma unroll
+    for (int q = 0; q < P; ++q) idx[q] = perm[tid * P + q];
+#pragma unroll
+    for (int q = 0; q < P; ++q) pm = fmaxf(pm, __uint_as_float(cbuf[idx[q]]));
+  } else {
+#pragma unroll
+    for (int q = 0; q < P; ++q) pm = fmaxf(pm, __uint_as_float(cbuf[tid * P + q]));
+  }
+  red[tid] = pm;
+  __syncthreads();
+  const int G = K / g;
+  if (tid < G) {
+    const int npos = g / P;  // threads per group
+    float s = 0.0f;
+    for (int u = 0; u < npos; ++u) s = fmaxf(s, red[tid * npos + u]);
+    gpart[(size_t)blockIdx.x * G + tid] = s;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 2. group scales, per-token scale, codes (4 waves per workgroup)
+// ---------------------------------------------------------------------------
+constexpr int kQuantWaves = 4;
+
+template <int K>
+__global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
+    const uint16_t* __restrict__ X, int M, int g, int rows_per_wg, int nparts,
+    const int32_t* __restrict__ perm, const float* __restrict__ gpart,
+    uint8_t* __restrict__ Xq, float* __restrict__ a_scale, float* __restrict__ s_group) {
+  using S = WaveRow<K>;
+  constexpr int NT = kQuantWaves * 64;
+  constexpr int GMAX = K / 64;  // groups at g = 64
+  __shared__ __attribute__((aligned(16))) float rows[kQuantWaves * S::RW * S::RF];
+  __shared__ float rg[GMAX];
+  __shared__ float red[NT];
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  const int sub = lane >> S::LR;
+  const int l = lane & (S::R - 1);
+  float* row = rows + (wave * S::RW + sub) * S::RF;
+  const int G = K / g;
+
+  const int r0 = blockIdx.x * rows_per_wg;
+  const int r1 = min(M, r0 + rows_per_wg);
+  const int per_pass = kQuantWaves * S::RW;
+  const int passes = (rows_per_wg + per_pass - 1) / per_pass;
+  auto row_of = [&](int p) { return r0 + (p * kQuantWaves + wave) * S::RW + sub; };
+
+  // This wave's first row is requested before anything else.
+  uint4 raw[8];
+  {
+    const int r = row_of(0);
+    load_raw64(X + (size_t)min(r, M - 1) * K + 64 * l, r < r1, raw);
+  }
+
+  // s_b = max over the partial rows. Thread t takes group b = t % GMAX and
+  // rows t / GMAX + k NS (NS = 256 / GMAX slices) with a fixed number of
+  // unconditional loads (row indices clamped to the last row, entries for
+  // b >= G read neighbouring rows and are ignored: every index stays inside
+  // the 256 x K/64 workspace), then the slices are combined through LDS.
+  {
+    constexpr int NS = NT / GMAX;
+    constexpr int NL = (256 + NS - 1) / NS;  // loads per thread for up to 256 rows
+    const int b = tid % GMAX;
+    const int sl = tid / GMAX;
+    float x[NL];
+#pragma unroll
+    for (int k = 0; k < NL; ++k) {
+      const int i = min(sl + k * NS, nparts - 1);
+      x[k] = gpart[(size_t)i * G + b];
+    }
+    float m = 0.0f;
+#pragma unroll
+    for (int k = 0; k < NL; ++k) m = fmaxf(m, x[k]);
+    red[tid] = m;
+    __syncthreads();
+    if (tid < G) {
+      float sv = red[tid];
+      for (int q = 1; q < NS; ++q) sv = fmaxf(sv, red[q * GMAX + tid]);
+      rg[tid] = (sv == 0.0f) ? 0.0f : __fdiv_rn(1.0f, sv);
+      if (blockIdx.x == 0) s_group[tid] = sv;
+    }
+    __syncthreads();
+  }
+  // Positions 64 l .. 64 l + 63 of a row lie in one group (g >= 64).
+  const float rb = rg[(64 * l) / g];
+
+  for (int p = 0; p < passes; ++p) {
+    const int r = row_of(p);
+    const bool live = r < r1;
+    float v[64];
+    raw_to_float(raw, v);
+    if (p + 1 < passes) {
+      const int rn = row_of(p + 1);
+      load_raw64(X + (size_t)min(rn, M - 1) * K + 64 * l, rn < r1, raw);
+    }
+    fwht_wave_row<K>(v, row, l);  // v[e] = y[l + R e]
+    // back to layout 1 through LDS, with the static reorder applied
+#pragma unroll
+    for (int e = 0; e < 64; ++e) row[lds_a(l + S::R * e)] = v[e];
+    if (perm) {
+      const int4* pp = reinterpret_cast<const int4*>(perm + 64 * l);
+#pragma unroll
+      for (int m = 0; m < 16; ++m) {
+        const int4 c = pp[m];
+        v[4 * m] = row[lds_a(c.x)];
+        v[4 * m + 1] = row[lds_a(c.y)];
+        v[4 * m + 2] = row[lds_a(c.z)];
+        v[4 * m + 3] = row[lds_a(c.w)];
+      }
+    } else {
+#pragma unroll
+      for (int m = 0; m < 16; ++m) {
+        const float4 c = *reinterpret_cast<const float4*>(row + lds_a(64 * l + 4 * m));
+        v[4 * m] = c.x;
+        v[4 * m + 1] = c.y;
+        v[4 * m + 2] = c.z;
+        v[4 * m + 3] = c.w;
+      }
+    }
+    float lm = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 64; ++e) lm = fmaxf(lm, fabsf(v[e]));
+    const float a = row_max<S::R>(lm * rb);  // max over the row's groups of fl(M_ib r_b)
+    const float inv = (a == 0.0f) ? 0.0f : __fdiv_rn(7.0f, a);
+    const float m = rb * inv;                // fl(r_b * inv_i)
+    if (live) {
+      uint32_t nib[64];
+#pragma unroll
+      for (int e = 0; e < 64; ++e) nib[e] = int4_nibble(v[e] * m);
+      store_nibbles<64>(Xq + (size_t)r * (K / 2) + 32 * l, nib);
+      if (l == 0) a_scale[r] = __fdiv_rn(a, 7.0f);
+    }
+  }
+}
+
+template <int K>
+hipError_t launch_wave(const uint16_t* X, int M, int g, const int32_t* perm, uint8_t* Xq,
+                       float* a_scale, float* s_group, void* workspace, int max_partials,
+                       int max_quant_wgs, hipStream_t stream) {
+  using S = WaveRow<K>;
+  // rot_max: at most max_partials workgroups (one partial row each).
+  const int rows_wg_min1 = kRotWaves * S::RW;
+  int wgs1 = (M + rows_wg_min1 - 1) / rows_wg_min1;
+  wgs1 = wgs1 < max_partials ? wgs1 : max_partials;
+  const int rpw1 = (M + wgs1 - 1) / wgs1;
+  wgs1 = (M + rpw1 - 1) / rpw1;
+  // quant: one row per wave where the grid allows it.
+  const int rows_wg_min2 = kQuantWaves * S::RW;
+  int wgs2 = (M + rows_wg_min2 - 1) / rows_wg_min2;
+  wgs2 = wgs2 < max_quant_wgs ? wgs2 : max_quant_wgs;
+  const int rpw2 = (M + wgs2 - 1) / wgs2;
+  wgs2 = (M + rpw2 - 1) / rpw2;
+  float* gpart = static_cast<float*>(workspace);
+  rot_max_wave_kernel<K><<<wgs1, kRotWaves * 64, 0, stream>>>(X, M, g, rpw1, perm, gpart);
+  quant_wave_kernel<K><<<wgs2, kQuantWaves * 64, 0, stream>>>(X, M, g, rpw2, wgs1, perm, gpart,
+                                                               Xq, a_scale, s_group);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_rotate_smooth_quant_wave(const uint16_t* X, int M, int K, int g,
+                                           const int32_t* perm, uint8_t* Xq, float* a_scale,
+                                           float* s_group, void* workspace, int max_partials,
+                                           int max_quant_wgs, hipStream_t stream) {
+  switch (K) {
+    case 512: return launch_wave<512>(X, M, g, perm, Xq, a_scale, s_group, workspace, max_partials, max_quant_wgs, stream);
+    case 1024: return launch_wave<1024>(X, M, g, perm, Xq, a_scale, s_group, workspace, max_partials, max_quant_wgs, stream);
+    case 2048: return launch_wave<2048>(X, M, g, perm, Xq, a_scale, s_group, workspace, max_partials, max_quant_wgs, stream);
+    case 4096: return launch_wave<4096>(X, M, g, perm, Xq, a_scale, s_group, workspace, max_partials, max_quant_wgs, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace rrs
