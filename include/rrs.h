@@ -21,9 +21,9 @@
  *    reached that point. Calls on different streams with disjoint buffers may
  *    run concurrently; the library holds no per-call state.
  *  - Arguments are validated on the host before any device work, in this
- *    order: null pointers, shapes, group size, alignment, workspace size,
- *    device present, device architecture. The first failing check decides
- *    the returned code and nothing is enqueued.
+ *    order: null pointers, shapes, group size, flags (the _ex functions),
+ *    alignment, workspace size, device present, device architecture. The
+ *    first failing check decides the returned code and nothing is enqueued.
  *  - Shapes: M >= 1; N >= 1 and N % 16 == 0; K a power of two with
  *    512 <= K <= 16384. Group size g: g divides K and g is one of
  *    64, 128, 256, 512. Every pointer must be 16-byte aligned.
@@ -69,8 +69,24 @@ enum {
   RRS_ERR_WORKSPACE = -5,  /* workspace smaller than the query returns */
   RRS_ERR_NO_DEVICE = -6,  /* no HIP device visible */
   RRS_ERR_ARCH = -7,       /* the current device is not gfx950 */
-  RRS_ERR_HIP = -8         /* a HIP runtime call or launch failed */
+  RRS_ERR_HIP = -8,        /* a HIP runtime call or launch failed */
+  RRS_ERR_FLAGS = -9       /* unknown or unsupported flag bits (_ex functions) */
 };
+
+/*
+ * Ablation switches for the _ex functions (the paper's own baselines,
+ * Section 3.1 and Section 2.3; Tables 1 and 4). 0 selects RRS itself.
+ *  - RRS_SKIP_ROTATION: no Hadamard rotation of activations or weights
+ *    (plain Runtime Smooth); the GEMM output drops the 1/K.
+ *  - RRS_SKIP_SMOOTHING: every smoothing scale is 1 (rotation followed by
+ *    per-token quantization only, the QuaRot scheme); rrs_rotate_smooth_quant_ex
+ *    then makes one pass over X instead of two and writes s_group = 1.
+ * Pass the same flags to the quantization, weight-preparation and GEMM calls
+ * of one layer (weight preparation and the GEMM take only RRS_SKIP_ROTATION
+ * into account; RRS_SKIP_SMOOTHING is accepted and has no effect there, except
+ * that rrs_prepare_weight_ex rejects it: weights are never smoothed).
+ */
+enum { RRS_SKIP_ROTATION = 1, RRS_SKIP_SMOOTHING = 2 };
 
 /* Human-readable name of a status code (static storage; never NULL). */
 const char* rrs_status_string(rrs_status status);
@@ -100,6 +116,11 @@ size_t rrs_workspace_bytes(int M, int K, int group_size);
 rrs_status rrs_prepare_weight(const void* W, int K, int N, const int32_t* perm,
                               void* Wq, float* w_scale, void* stream);
 
+/* rrs_prepare_weight with flags: RRS_SKIP_ROTATION quantizes W itself
+ * (u = W) for the ablation without rotation; any other bit -> RRS_ERR_FLAGS. */
+rrs_status rrs_prepare_weight_ex(const void* W, int K, int N, const int32_t* perm, int flags,
+                                 void* Wq, float* w_scale, void* stream);
+
 /*
  * Online rotate + runtime smooth + per-token INT4 quantization
  * (Section 3.3 then Section 3.2; Eq. 1-2; Section 2.1).
@@ -118,6 +139,13 @@ rrs_status rrs_rotate_smooth_quant(const void* X, int M, int K, int group_size,
                                    float* s_group, void* workspace,
                                    size_t workspace_bytes, void* stream);
 
+/* rrs_rotate_smooth_quant with ablation flags (RRS_SKIP_ROTATION: y = x;
+ * RRS_SKIP_SMOOTHING: s_b = r_b = 1). Same buffers and workspace. */
+rrs_status rrs_rotate_smooth_quant_ex(const void* X, int M, int K, int group_size,
+                                      const int32_t* perm, int flags, void* Xq, float* a_scale,
+                                      float* s_group, void* workspace, size_t workspace_bytes,
+                                      void* stream);
+
 /*
  * W4A4 GEMM with Runtime Smooth fused into the block loop (Section 3.2,
  * Eq. 3, Fig. 4 step (3)):
@@ -131,6 +159,13 @@ rrs_status rrs_rotate_smooth_quant(const void* X, int M, int K, int group_size,
 rrs_status rrs_w4a4_gemm(const void* Xq, const float* a_scale, const float* s_group,
                          const void* Wq, const float* w_scale, int M, int N, int K,
                          int group_size, void* Y, void* stream);
+
+/* rrs_w4a4_gemm with ablation flags: with RRS_SKIP_ROTATION the operands are
+ * unrotated and the output is a_scale[i] * w_scale[n] * sum_b s_group[b] P_b
+ * (no 1/K). RRS_SKIP_SMOOTHING has no effect (the scales come from s_group). */
+rrs_status rrs_w4a4_gemm_ex(const void* Xq, const float* a_scale, const float* s_group,
+                            const void* Wq, const float* w_scale, int M, int N, int K,
+                            int group_size, int flags, void* Y, void* stream);
 
 /*
  * Bytes of workspace rrs_linear needs: rrs_workspace_bytes plus room for Xq,
@@ -147,6 +182,13 @@ size_t rrs_linear_workspace_bytes(int M, int K, int group_size);
 rrs_status rrs_linear(const void* X, const void* Wq, const float* w_scale, int M, int N,
                       int K, int group_size, const int32_t* perm, void* Y,
                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* rrs_linear with ablation flags (quantization and GEMM as in their _ex
+ * forms); Wq and w_scale must come from rrs_prepare_weight_ex with the same
+ * RRS_SKIP_ROTATION bit. */
+rrs_status rrs_linear_ex(const void* X, const void* Wq, const float* w_scale, int M, int N,
+                         int K, int group_size, const int32_t* perm, int flags, void* Y,
+                         void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * Test hook: the exact int32 group partials P[b][i][n] (b < K/g, i < M,

@@ -13,6 +13,8 @@ INT4 inference" (arXiv 2409.20361), Sections 3.1-3.3.
 from __future__ import annotations
 
 from ._binding import (  # noqa: F401
+    SKIP_ROTATION,
+    SKIP_SMOOTHING,
     RRSError,
     lib,
     lib_path,
@@ -28,7 +30,7 @@ from ._binding import (  # noqa: F401
 )
 
 __all__ = [
-    "RRSError", "lib", "lib_path", "linear", "linear_workspace_bytes", "prepare_weight",
-    "rotate_smooth_quant", "status_string", "version", "w4a4_gemm", "w4a4_gemm_partials",
-    "workspace_bytes",
+    "SKIP_ROTATION", "SKIP_SMOOTHING", "RRSError", "lib", "lib_path", "linear",
+    "linear_workspace_bytes", "prepare_weight", "rotate_smooth_quant", "status_string",
+    "version", "w4a4_gemm", "w4a4_gemm_partials", "workspace_bytes",
 ]

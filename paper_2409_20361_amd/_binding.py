@@ -26,7 +26,18 @@ _SIGNATURES = {
     "rrs_w4a4_gemm": (ctypes.c_int32, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp]),
     "rrs_linear": (ctypes.c_int32, [_vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp, _sz, _vp]),
     "rrs_w4a4_gemm_partials": (ctypes.c_int32, [_vp, _vp, _i, _i, _i, _i, _vp, _vp]),
+    "rrs_prepare_weight_ex": (ctypes.c_int32, [_vp, _i, _i, _vp, _i, _vp, _vp, _vp]),
+    "rrs_rotate_smooth_quant_ex": (ctypes.c_int32,
+                                   [_vp, _i, _i, _i, _vp, _i, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "rrs_w4a4_gemm_ex": (ctypes.c_int32,
+                         [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp]),
+    "rrs_linear_ex": (ctypes.c_int32,
+                      [_vp, _vp, _vp, _i, _i, _i, _i, _vp, _i, _vp, _vp, _sz, _vp]),
 }
+
+# Ablation switches (include/rrs.h): 0 is RRS itself.
+SKIP_ROTATION = 1    # plain Runtime Smooth: no Hadamard rotation
+SKIP_SMOOTHING = 2   # rotation + per-token quantization only (smoothing scales all 1)
 
 
 class RRSError(RuntimeError):
@@ -101,20 +112,20 @@ def _perm_ptr(perm: Optional[torch.Tensor], K: int) -> Optional[int]:
     return _dev(perm, "perm", torch.int32, (K,))
 
 
-def prepare_weight(W: torch.Tensor, perm: Optional[torch.Tensor] = None
+def prepare_weight(W: torch.Tensor, perm: Optional[torch.Tensor] = None, flags: int = 0
                    ) -> Tuple[torch.Tensor, torch.Tensor]:
     """W: K x N fp16 (the transpose of nn.Linear's weight) -> (Wq N x K/2 uint8, w_scale N f32)."""
     K, N = W.shape
     wp = _dev(W, "W", torch.float16, (K, N))
     Wq = torch.empty((N, K // 2), dtype=torch.uint8, device=W.device)
     ws = torch.empty((N,), dtype=torch.float32, device=W.device)
-    _check(lib().rrs_prepare_weight(wp, K, N, _perm_ptr(perm, K), Wq.data_ptr(), ws.data_ptr(),
-                                    _stream(W.device)), "rrs_prepare_weight")
+    _check(lib().rrs_prepare_weight_ex(wp, K, N, _perm_ptr(perm, K), flags, Wq.data_ptr(),
+                                       ws.data_ptr(), _stream(W.device)), "rrs_prepare_weight")
     return Wq, ws
 
 
 def rotate_smooth_quant(X: torch.Tensor, g: int, perm: Optional[torch.Tensor] = None,
-                        workspace: Optional[torch.Tensor] = None, out=None):
+                        workspace: Optional[torch.Tensor] = None, out=None, flags: int = 0):
     """X: M x K fp16 -> (Xq M x K/2 uint8, a_scale M f32, s_group K/g f32)."""
     M, K = X.shape
     xp = _dev(X, "X", torch.float16, (M, K))
@@ -127,8 +138,8 @@ def rotate_smooth_quant(X: torch.Tensor, g: int, perm: Optional[torch.Tensor] = 
     nbytes = workspace_bytes(M, K, g)
     if workspace is None:
         workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=X.device)
-    _check(lib().rrs_rotate_smooth_quant(
-        xp, M, K, g, _perm_ptr(perm, K), Xq.data_ptr(), a.data_ptr(), s.data_ptr(),
+    _check(lib().rrs_rotate_smooth_quant_ex(
+        xp, M, K, g, _perm_ptr(perm, K), flags, Xq.data_ptr(), a.data_ptr(), s.data_ptr(),
         workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(X.device)),
         "rrs_rotate_smooth_quant")
     return Xq, a, s
@@ -136,8 +147,8 @@ def rotate_smooth_quant(X: torch.Tensor, g: int, perm: Optional[torch.Tensor] = 
 
 def w4a4_gemm(Xq: torch.Tensor, a_scale: torch.Tensor, s_group: torch.Tensor,
               Wq: torch.Tensor, w_scale: torch.Tensor, g: int,
-              out: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Y = fp16(a_i w_n / K * sum_b s_b P_b) (M x N)."""
+              out: Optional[torch.Tensor] = None, flags: int = 0) -> torch.Tensor:
+    """Y = fp16(a_i w_n / K * sum_b s_b P_b) (M x N; no 1/K with SKIP_ROTATION)."""
     M, Kh = Xq.shape
     K = 2 * Kh
     N = Wq.shape[0]
@@ -146,13 +157,14 @@ def w4a4_gemm(Xq: torch.Tensor, a_scale: torch.Tensor, s_group: torch.Tensor,
             _dev(Wq, "Wq", torch.uint8, (N, Kh)), _dev(w_scale, "w_scale", torch.float32, (N,)))
     Y = out if out is not None else torch.empty((M, N), dtype=torch.float16, device=Xq.device)
     yp = _dev(Y, "Y", torch.float16, (M, N))
-    _check(lib().rrs_w4a4_gemm(*args, M, N, K, g, yp, _stream(Xq.device)), "rrs_w4a4_gemm")
+    _check(lib().rrs_w4a4_gemm_ex(*args, M, N, K, g, flags, yp, _stream(Xq.device)),
+           "rrs_w4a4_gemm")
     return Y
 
 
 def linear(X: torch.Tensor, Wq: torch.Tensor, w_scale: torch.Tensor, g: int,
            perm: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
-           out: Optional[torch.Tensor] = None) -> torch.Tensor:
+           out: Optional[torch.Tensor] = None, flags: int = 0) -> torch.Tensor:
     """One RRS linear layer: X M x K fp16 -> Y M x N fp16."""
     M, K = X.shape
     N = Wq.shape[0]
@@ -164,9 +176,9 @@ def linear(X: torch.Tensor, Wq: torch.Tensor, w_scale: torch.Tensor, g: int,
         workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=X.device)
     Y = out if out is not None else torch.empty((M, N), dtype=torch.float16, device=X.device)
     yp = _dev(Y, "Y", torch.float16, (M, N))
-    _check(lib().rrs_linear(xp, wqp, wsp, M, N, K, g, _perm_ptr(perm, K), yp,
-                            workspace.data_ptr(), workspace.numel() * workspace.element_size(),
-                            _stream(X.device)), "rrs_linear")
+    _check(lib().rrs_linear_ex(xp, wqp, wsp, M, N, K, g, _perm_ptr(perm, K), flags, yp,
+                               workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                               _stream(X.device)), "rrs_linear")
     return Y
 
 

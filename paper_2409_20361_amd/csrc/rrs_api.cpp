@@ -6,6 +6,7 @@
 #include <atomic>
 #include <cstdio>
 #include <cstdlib>
+#include <cmath>
 #include <cstring>
 
 #include "rrs.h"
@@ -13,7 +14,7 @@
 
 namespace {
 
-constexpr int kVersion = 100;  // 0.1.0
+constexpr int kVersion = 200;  // 0.2.0: ablation (_ex) entry points
 constexpr int kMaxDevices = 64;
 
 bool is_aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -23,6 +24,17 @@ bool valid_m(int M) { return M >= 1; }
 bool valid_n(int N) { return N >= 1 && (N % 16) == 0; }
 bool valid_group(int K, int g) {
   return (g == 64 || g == 128 || g == 256 || g == 512) && K % g == 0;
+}
+bool valid_flags(int flags, int allowed) { return (flags & ~allowed) == 0; }
+constexpr int kAllFlags = RRS_SKIP_ROTATION | RRS_SKIP_SMOOTHING;
+static_assert(RRS_SKIP_ROTATION == rrs::kSkipRotation && RRS_SKIP_SMOOTHING == rrs::kSkipSmoothing,
+              "public and internal flag values agree");
+
+// Output scale of the GEMM: 2^-8 undoes the 16 x 16 of the unpacked int8
+// operands, 1/K the unnormalized rotation (absent without rotation).
+float out_scale(int K, int flags) {
+  const float s = std::ldexp(1.0f, -8);
+  return (flags & RRS_SKIP_ROTATION) ? s : s / (float)K;
 }
 
 bool debug_enabled() {
@@ -84,6 +96,7 @@ const char* rrs_status_string(rrs_status s) {
     case RRS_ERR_NO_DEVICE: return "RRS_ERR_NO_DEVICE: no HIP device visible";
     case RRS_ERR_ARCH: return "RRS_ERR_ARCH: current device is not gfx950";
     case RRS_ERR_HIP: return "RRS_ERR_HIP: a HIP call or kernel launch failed";
+    case RRS_ERR_FLAGS: return "RRS_ERR_FLAGS: unknown or unsupported flag bits";
     default: return "RRS_ERR_UNKNOWN";
   }
 }
@@ -100,76 +113,102 @@ size_t rrs_linear_workspace_bytes(int M, int K, int group_size) {
   return linear_ws_bytes(M, K, group_size);
 }
 
-rrs_status rrs_prepare_weight(const void* W, int K, int N, const int32_t* perm, void* Wq,
-                              float* w_scale, void* stream) {
+rrs_status rrs_prepare_weight_ex(const void* W, int K, int N, const int32_t* perm, int flags,
+                                 void* Wq, float* w_scale, void* stream) {
   if (debug_enabled())
-    std::fprintf(stderr, "[rrs] prepare_weight W=%p K=%d N=%d perm=%p Wq=%p w_scale=%p\n", W, K,
-                 N, (const void*)perm, Wq, (void*)w_scale);
+    std::fprintf(stderr,
+                 "[rrs] prepare_weight W=%p K=%d N=%d perm=%p flags=%d Wq=%p w_scale=%p\n", W,
+                 K, N, (const void*)perm, flags, Wq, (void*)w_scale);
   if (!W || !Wq || !w_scale) return RRS_ERR_NULL;
   if (!valid_k(K) || !valid_n(N)) return RRS_ERR_SHAPE;
+  if (!valid_flags(flags, RRS_SKIP_ROTATION)) return RRS_ERR_FLAGS;
   if (!is_aligned(W) || !is_aligned(Wq) || !is_aligned(w_scale) || (perm && !is_aligned(perm)))
     return RRS_ERR_ALIGN;
   if (rrs_status s = check_device()) return s;
-  return from_hip(rrs::launch_prepare_weight(static_cast<const uint16_t*>(W), K, N, perm,
-                                             static_cast<uint8_t*>(Wq), w_scale,
-                                             static_cast<hipStream_t>(stream)));
+  return from_hip(rrs::launch_prepare_weight(
+      static_cast<const uint16_t*>(W), K, N, perm, !(flags & RRS_SKIP_ROTATION),
+      static_cast<uint8_t*>(Wq), w_scale, static_cast<hipStream_t>(stream)));
 }
 
-rrs_status rrs_rotate_smooth_quant(const void* X, int M, int K, int group_size,
-                                   const int32_t* perm, void* Xq, float* a_scale,
-                                   float* s_group, void* workspace, size_t workspace_bytes,
-                                   void* stream) {
+rrs_status rrs_prepare_weight(const void* W, int K, int N, const int32_t* perm, void* Wq,
+                              float* w_scale, void* stream) {
+  return rrs_prepare_weight_ex(W, K, N, perm, 0, Wq, w_scale, stream);
+}
+
+rrs_status rrs_rotate_smooth_quant_ex(const void* X, int M, int K, int group_size,
+                                      const int32_t* perm, int flags, void* Xq, float* a_scale,
+                                      float* s_group, void* workspace, size_t workspace_bytes,
+                                      void* stream) {
   if (debug_enabled())
     std::fprintf(stderr,
-                 "[rrs] rotate_smooth_quant X=%p M=%d K=%d g=%d perm=%p Xq=%p a=%p s=%p ws=%p "
-                 "(%zu B)\n",
-                 X, M, K, group_size, (const void*)perm, Xq, (void*)a_scale, (void*)s_group,
-                 workspace, workspace_bytes);
+                 "[rrs] rotate_smooth_quant X=%p M=%d K=%d g=%d perm=%p flags=%d Xq=%p a=%p "
+                 "s=%p ws=%p (%zu B)\n",
+                 X, M, K, group_size, (const void*)perm, flags, Xq, (void*)a_scale,
+                 (void*)s_group, workspace, workspace_bytes);
   if (!X || !Xq || !a_scale || !s_group || !workspace) return RRS_ERR_NULL;
   if (!valid_m(M) || !valid_k(K)) return RRS_ERR_SHAPE;
   if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
+  if (!valid_flags(flags, kAllFlags)) return RRS_ERR_FLAGS;
   if (!is_aligned(X) || !is_aligned(Xq) || !is_aligned(a_scale) || !is_aligned(s_group) ||
       !is_aligned(workspace) || (perm && !is_aligned(perm)))
     return RRS_ERR_ALIGN;
   if (workspace_bytes < rrs::quant_workspace_bytes(M, K)) return RRS_ERR_WORKSPACE;
   if (rrs_status s = check_device()) return s;
   return from_hip(rrs::launch_rotate_smooth_quant(
-      static_cast<const uint16_t*>(X), M, K, group_size, perm, static_cast<uint8_t*>(Xq),
+      static_cast<const uint16_t*>(X), M, K, group_size, perm, flags, static_cast<uint8_t*>(Xq),
       a_scale, s_group, workspace, static_cast<hipStream_t>(stream)));
 }
 
-rrs_status rrs_w4a4_gemm(const void* Xq, const float* a_scale, const float* s_group,
-                         const void* Wq, const float* w_scale, int M, int N, int K,
-                         int group_size, void* Y, void* stream) {
+rrs_status rrs_rotate_smooth_quant(const void* X, int M, int K, int group_size,
+                                   const int32_t* perm, void* Xq, float* a_scale,
+                                   float* s_group, void* workspace, size_t workspace_bytes,
+                                   void* stream) {
+  return rrs_rotate_smooth_quant_ex(X, M, K, group_size, perm, 0, Xq, a_scale, s_group,
+                                    workspace, workspace_bytes, stream);
+}
+
+rrs_status rrs_w4a4_gemm_ex(const void* Xq, const float* a_scale, const float* s_group,
+                            const void* Wq, const float* w_scale, int M, int N, int K,
+                            int group_size, int flags, void* Y, void* stream) {
   if (debug_enabled())
     std::fprintf(stderr,
-                 "[rrs] w4a4_gemm Xq=%p a=%p s=%p Wq=%p w=%p M=%d N=%d K=%d g=%d Y=%p\n", Xq,
-                 (const void*)a_scale, (const void*)s_group, Wq, (const void*)w_scale, M, N, K,
-                 group_size, Y);
+                 "[rrs] w4a4_gemm Xq=%p a=%p s=%p Wq=%p w=%p M=%d N=%d K=%d g=%d flags=%d "
+                 "Y=%p\n",
+                 Xq, (const void*)a_scale, (const void*)s_group, Wq, (const void*)w_scale, M, N,
+                 K, group_size, flags, Y);
   if (!Xq || !a_scale || !s_group || !Wq || !w_scale || !Y) return RRS_ERR_NULL;
   if (!valid_m(M) || !valid_n(N) || !valid_k(K)) return RRS_ERR_SHAPE;
   if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
+  if (!valid_flags(flags, kAllFlags)) return RRS_ERR_FLAGS;
   if (!is_aligned(Xq) || !is_aligned(a_scale) || !is_aligned(s_group) || !is_aligned(Wq) ||
       !is_aligned(w_scale) || !is_aligned(Y))
     return RRS_ERR_ALIGN;
   if (rrs_status s = check_device()) return s;
   return from_hip(rrs::launch_w4a4_gemm(
       static_cast<const uint8_t*>(Xq), a_scale, s_group, static_cast<const uint8_t*>(Wq),
-      w_scale, M, N, K, group_size, static_cast<uint16_t*>(Y),
+      w_scale, M, N, K, group_size, static_cast<uint16_t*>(Y), out_scale(K, flags),
       static_cast<hipStream_t>(stream)));
 }
 
-rrs_status rrs_linear(const void* X, const void* Wq, const float* w_scale, int M, int N,
-                      int K, int group_size, const int32_t* perm, void* Y, void* workspace,
-                      size_t workspace_bytes, void* stream) {
+rrs_status rrs_w4a4_gemm(const void* Xq, const float* a_scale, const float* s_group,
+                         const void* Wq, const float* w_scale, int M, int N, int K,
+                         int group_size, void* Y, void* stream) {
+  return rrs_w4a4_gemm_ex(Xq, a_scale, s_group, Wq, w_scale, M, N, K, group_size, 0, Y, stream);
+}
+
+rrs_status rrs_linear_ex(const void* X, const void* Wq, const float* w_scale, int M, int N,
+                         int K, int group_size, const int32_t* perm, int flags, void* Y,
+                         void* workspace, size_t workspace_bytes, void* stream) {
   if (debug_enabled())
     std::fprintf(stderr,
-                 "[rrs] linear X=%p Wq=%p w=%p M=%d N=%d K=%d g=%d perm=%p Y=%p ws=%p (%zu B)\n",
-                 X, Wq, (const void*)w_scale, M, N, K, group_size, (const void*)perm, Y,
+                 "[rrs] linear X=%p Wq=%p w=%p M=%d N=%d K=%d g=%d perm=%p flags=%d Y=%p ws=%p "
+                 "(%zu B)\n",
+                 X, Wq, (const void*)w_scale, M, N, K, group_size, (const void*)perm, flags, Y,
                  workspace, workspace_bytes);
   if (!X || !Wq || !w_scale || !Y || !workspace) return RRS_ERR_NULL;
   if (!valid_m(M) || !valid_n(N) || !valid_k(K)) return RRS_ERR_SHAPE;
   if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
+  if (!valid_flags(flags, kAllFlags)) return RRS_ERR_FLAGS;
   if (!is_aligned(X) || !is_aligned(Wq) || !is_aligned(w_scale) || !is_aligned(Y) ||
       !is_aligned(workspace) || (perm && !is_aligned(perm)))
     return RRS_ERR_ALIGN;
@@ -187,10 +226,18 @@ rrs_status rrs_linear(const void* X, const void* Wq, const float* w_scale, int M
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = rrs::launch_rotate_smooth_quant(static_cast<const uint16_t*>(X), M, K,
-                                                 group_size, perm, xq, a, s, qws, st);
+                                                 group_size, perm, flags, xq, a, s, qws, st);
   if (e != hipSuccess) return RRS_ERR_HIP;
   return from_hip(rrs::launch_w4a4_gemm(xq, a, s, static_cast<const uint8_t*>(Wq), w_scale, M,
-                                        N, K, group_size, static_cast<uint16_t*>(Y), st));
+                                        N, K, group_size, static_cast<uint16_t*>(Y),
+                                        out_scale(K, flags), st));
+}
+
+rrs_status rrs_linear(const void* X, const void* Wq, const float* w_scale, int M, int N,
+                      int K, int group_size, const int32_t* perm, void* Y, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+  return rrs_linear_ex(X, Wq, w_scale, M, N, K, group_size, perm, 0, Y, workspace,
+                       workspace_bytes, stream);
 }
 
 rrs_status rrs_w4a4_gemm_partials(const void* Xq, const void* Wq, int M, int N, int K,

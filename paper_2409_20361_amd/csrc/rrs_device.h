@@ -104,7 +104,7 @@ struct FwhtShape {
   static_assert(E >= 2 && (1 << L) == E, "K must be 2^(8+L), L >= 1");
 };
 
-template <int K, int W>
+template <int K, int W, bool kRot>
 __device__ __forceinline__ void fwht_windows(float (&v)[FwhtShape<K>::E], float* lds, int t) {
   using S = FwhtShape<K>;
   if constexpr (W < S::kWindows) {
@@ -117,19 +117,21 @@ __device__ __forceinline__ void fwht_windows(float (&v)[FwhtShape<K>::E], float*
     __syncthreads();
 #pragma unroll
     for (int e = 0; e < S::E; ++e) v[e] = lds[lds_pad(window_index(t, e, lo, S::L))];
-    fwht_stages<S::E, first, S::L>(v);
-    fwht_windows<K, W + 1>(v, lds, t);
+    if constexpr (kRot) fwht_stages<S::E, first, S::L>(v);
+    fwht_windows<K, W + 1, kRot>(v, lds, t);
   }
 }
 
 // On entry v[e] holds element t*E + e of the row. On exit v[e] holds element
-// t + e * 256 of x H_K. `lds` must hold lds_row_floats(K) floats; it is
-// clobbered. Must be called by all 256 threads of the workgroup.
-template <int K>
+// t + e * 256 of x H_K (of x itself when kRot is false: the same data
+// movement without the butterflies, for the ablation without rotation).
+// `lds` must hold lds_row_floats(K) floats; it is clobbered. Must be called by
+// all 256 threads of the workgroup.
+template <int K, bool kRot = true>
 __device__ __forceinline__ void fwht_row(float (&v)[FwhtShape<K>::E], float* lds, int t) {
   using S = FwhtShape<K>;
-  fwht_stages<S::E, 0, S::L>(v);
-  fwht_windows<K, 1>(v, lds, t);
+  if constexpr (kRot) fwht_stages<S::E, 0, S::L>(v);
+  fwht_windows<K, 1, kRot>(v, lds, t);
 }
 
 // ---------------------------------------------------------------------------

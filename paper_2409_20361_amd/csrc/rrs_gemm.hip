@@ -106,7 +106,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
     const float* __restrict__ w_scale, int M, int N, int K, uint16_t* __restrict__ Y,
-    int32_t* __restrict__ P) {
+    int32_t* __restrict__ P, float out_scale) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[2 * STAGE];
   __shared__ float scale_tab[BM + BN];  // alpha of the tile's rows, then beta of its columns
 
@@ -323,8 +323,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
   }
 
   if constexpr (!kPartials) {
-    // 2^-8 undoes the 16 x 16 of the unpacked operands, 1/K the unnormalized rotation.
-    const float inv = __builtin_ldexpf(1.0f, -8) / (float)K;
+    // out_scale = 2^-8 (undoes the 16 x 16 of the unpacked operands) / K (the
+    // unnormalized rotation; 1 without rotation), an exact power of two.
+    const float inv = out_scale;
     // Scales come from LDS, so no store waits on a global load: this lane's
     // 32 rows are eight runs of 4 consecutive ones (128-bit reads). A tile
     // that lies wholly inside Y stores without per-element bounds checks.
@@ -366,7 +367,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
 template <bool kPartials>
 hipError_t launch_main(const uint8_t* Xq, const float* a_scale, const float* s_group,
                        const uint8_t* Wq, const float* w_scale, int M, int N, int K, int g,
-                       uint16_t* Y, int32_t* P, hipStream_t stream) {
+                       uint16_t* Y, int32_t* P, float out_scale, hipStream_t stream) {
   const int tm = (M + BM - 1) / BM;
   const int tn = (N + BN - 1) / BN;
   const int T = tm * tn;
@@ -375,7 +376,7 @@ hipError_t launch_main(const uint8_t* Xq, const float* a_scale, const float* s_g
 #define RRS_CASE(G_)                                                                       \
   case G_:                                                                                 \
     gemm_main_kernel<G_ / 32, kPartials><<<grid, kThreads, 0, stream>>>(                   \
-        Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, P);                                 \
+        Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, P, out_scale);                      \
     break;
     RRS_CASE(64)
     RRS_CASE(128)
@@ -397,19 +398,23 @@ bool main_kernel_fits(int K, int g) {
 
 hipError_t launch_w4a4_gemm(const uint8_t* Xq, const float* a_scale, const float* s_group,
                             const uint8_t* Wq, const float* w_scale, int M, int N, int K,
-                            int g, uint16_t* Y, hipStream_t stream) {
+                            int g, uint16_t* Y, float out_scale, hipStream_t stream) {
   if (decode_kernel_fits(M))
-    return launch_w4a4_gemm_decode(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, stream);
+    return launch_w4a4_gemm_decode(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, out_scale,
+                                   stream);
   if (!main_kernel_fits(K, g))
-    return launch_w4a4_gemm_small(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, stream);
-  return launch_main<false>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, nullptr, stream);
+    return launch_w4a4_gemm_small(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, out_scale,
+                                  stream);
+  return launch_main<false>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, nullptr,
+                            out_scale, stream);
 }
 
 hipError_t launch_w4a4_gemm_partials(const uint8_t* Xq, const uint8_t* Wq, int M, int N,
                                      int K, int g, int32_t* P, hipStream_t stream) {
   if (!main_kernel_fits(K, g))
     return launch_w4a4_gemm_partials_small(Xq, Wq, M, N, K, g, P, stream);
-  return launch_main<true>(Xq, nullptr, nullptr, Wq, nullptr, M, N, K, g, nullptr, P, stream);
+  return launch_main<true>(Xq, nullptr, nullptr, Wq, nullptr, M, N, K, g, nullptr, P, 0.0f,
+                           stream);
 }
 
 }  // namespace rrs

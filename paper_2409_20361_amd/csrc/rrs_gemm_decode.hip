@@ -82,7 +82,8 @@ template <int GS, bool kLdsA>
 __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
-    const float* __restrict__ w_scale, int M, int N, int K, uint16_t* __restrict__ Y) {
+    const float* __restrict__ w_scale, int M, int N, int K, uint16_t* __restrict__ Y,
+    float out_scale) {
   constexpr int g = GS * 64;
   constexpr int NW = g / 32;                  // words per lane per group and block
   constexpr int D = NW >= 16 ? 1 : (NW >= 8 ? 2 : 4);  // groups in flight
@@ -213,8 +214,9 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
       sum.z += x.z;
       sum.w += x.w;
     }
-    // 2^-8 undoes the 16 x 16 of the unpacked operands, 1/K the unnormalized rotation.
-    const float inv = __builtin_ldexpf(1.0f, -8) / (float)K;
+    // out_scale = 2^-8 (undoes the 16 x 16 of the unpacked operands) / K (the
+    // unnormalized rotation; 1 without rotation), an exact power of two.
+    const float inv = out_scale;
     const int col = n0 + w * kCols + c;
     const float bcol = w_scale[col];
     const float sv[4] = {sum.x, sum.y, sum.z, sum.w};
@@ -236,14 +238,14 @@ bool decode_kernel_fits(int M) { return M >= 1 && M <= kCols; }
 hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
                                    const float* s_group, const uint8_t* Wq,
                                    const float* w_scale, int M, int N, int K, int g,
-                                   uint16_t* Y, hipStream_t stream) {
+                                   uint16_t* Y, float out_scale, hipStream_t stream) {
   const int grid = (N / kCols + kBlocks - 1) / kBlocks;  // N % 16 == 0 (API precondition)
   const bool lds_a = (size_t)M * a_row_bytes(K, g) <= (size_t)kMaxLdsA;
 #define RRS_DECODE(GS_)                                                                  \
   (lds_a ? (gemm_decode_kernel<GS_, true><<<grid, kThreads, 0, stream>>>(                 \
-               Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y), 0)                        \
+               Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale), 0)             \
          : (gemm_decode_kernel<GS_, false><<<grid, kThreads, 0, stream>>>(                \
-               Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y), 0))
+               Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale), 0))
   switch (g) {
     case 64: RRS_DECODE(1); break;
     case 128: RRS_DECODE(2); break;

@@ -50,7 +50,7 @@ __global__ __launch_bounds__(256) void gemm_small_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
     const float* __restrict__ w_scale, int M, int N, int K, int g,
-    uint16_t* __restrict__ Y, int32_t* __restrict__ P) {
+    uint16_t* __restrict__ Y, int32_t* __restrict__ P, float out_scale) {
   __shared__ __attribute__((aligned(16))) uint8_t sA[2][BM * LROW];
   __shared__ __attribute__((aligned(16))) uint8_t sB[2][BN * LROW];
 
@@ -159,7 +159,7 @@ __global__ __launch_bounds__(256) void gemm_small_kernel(
 
   if constexpr (!kPartials) {
     // 2^-8 undoes the 16x16 of the unpacked operands, 1/K the unnormalized rotation.
-    const float inv = __builtin_ldexpf(1.0f, -8) / (float)K;
+    const float inv = out_scale;  // 2^-8 / K (2^-8 without rotation), exact
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -182,10 +182,10 @@ __global__ __launch_bounds__(256) void gemm_small_kernel(
 
 hipError_t launch_w4a4_gemm_small(const uint8_t* Xq, const float* a_scale, const float* s_group,
                             const uint8_t* Wq, const float* w_scale, int M, int N, int K,
-                            int g, uint16_t* Y, hipStream_t stream) {
+                            int g, uint16_t* Y, float out_scale, hipStream_t stream) {
   dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
   gemm_small_kernel<false><<<grid, 256, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale, M, N, K,
-                                               g, Y, nullptr);
+                                                     g, Y, nullptr, out_scale);
   return hipGetLastError();
 }
 
@@ -193,7 +193,7 @@ hipError_t launch_w4a4_gemm_partials_small(const uint8_t* Xq, const uint8_t* Wq,
                                      int K, int g, int32_t* P, hipStream_t stream) {
   dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
   gemm_small_kernel<true><<<grid, 256, 0, stream>>>(Xq, nullptr, nullptr, Wq, nullptr, M, N, K, g,
-                                              nullptr, P);
+                                                    nullptr, P, 0.0f);
   return hipGetLastError();
 }
 

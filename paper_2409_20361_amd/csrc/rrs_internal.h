@@ -13,22 +13,30 @@ namespace rrs {
 int quant_partial_rows(int M);
 size_t quant_workspace_bytes(int M, int K);
 
+// Ablation switches (the public RRS_SKIP_* flags).
+constexpr int kSkipRotation = 1;
+constexpr int kSkipSmoothing = 2;
+
 hipError_t launch_rotate_smooth_quant(const uint16_t* X, int M, int K, int g,
-                                      const int32_t* perm, uint8_t* Xq, float* a_scale,
-                                      float* s_group, void* workspace, hipStream_t stream);
+                                      const int32_t* perm, int flags, uint8_t* Xq,
+                                      float* a_scale, float* s_group, void* workspace,
+                                      hipStream_t stream);
 
 // One-wave-per-row variant for K <= 4096 (same two passes, same bits).
 hipError_t launch_rotate_smooth_quant_wave(const uint16_t* X, int M, int K, int g,
-                                           const int32_t* perm, uint8_t* Xq, float* a_scale,
-                                           float* s_group, void* workspace, int max_partials,
-                                           int max_quant_wgs, hipStream_t stream);
+                                           const int32_t* perm, int flags, uint8_t* Xq,
+                                           float* a_scale, float* s_group, void* workspace,
+                                           int max_partials, int max_quant_wgs,
+                                           hipStream_t stream);
 
 hipError_t launch_prepare_weight(const uint16_t* W, int K, int N, const int32_t* perm,
-                                 uint8_t* Wq, float* w_scale, hipStream_t stream);
+                                 bool rotate, uint8_t* Wq, float* w_scale, hipStream_t stream);
 
+// out_scale multiplies every output with alpha_i beta_n: 2^-8 / K for rotated
+// operands, 2^-8 without rotation (both exact powers of two).
 hipError_t launch_w4a4_gemm(const uint8_t* Xq, const float* a_scale, const float* s_group,
                             const uint8_t* Wq, const float* w_scale, int M, int N, int K,
-                            int g, uint16_t* Y, hipStream_t stream);
+                            int g, uint16_t* Y, float out_scale, hipStream_t stream);
 
 hipError_t launch_w4a4_gemm_partials(const uint8_t* Xq, const uint8_t* Wq, int M, int N,
                                      int K, int g, int32_t* P, hipStream_t stream);
@@ -38,7 +46,7 @@ hipError_t launch_w4a4_gemm_partials(const uint8_t* Xq, const uint8_t* Wq, int M
 hipError_t launch_w4a4_gemm_small(const uint8_t* Xq, const float* a_scale,
                                   const float* s_group, const uint8_t* Wq,
                                   const float* w_scale, int M, int N, int K, int g,
-                                  uint16_t* Y, hipStream_t stream);
+                                  uint16_t* Y, float out_scale, hipStream_t stream);
 hipError_t launch_w4a4_gemm_partials_small(const uint8_t* Xq, const uint8_t* Wq, int M,
                                            int N, int K, int g, int32_t* P,
                                            hipStream_t stream);
@@ -48,7 +56,7 @@ bool decode_kernel_fits(int M);
 hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
                                    const float* s_group, const uint8_t* Wq,
                                    const float* w_scale, int M, int N, int K, int g,
-                                   uint16_t* Y, hipStream_t stream);
+                                   uint16_t* Y, float out_scale, hipStream_t stream);
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 

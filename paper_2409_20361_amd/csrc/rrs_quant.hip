@@ -56,7 +56,7 @@ __device__ __forceinline__ void load_row_or_zero(const uint16_t* __restrict__ X,
 // ---------------------------------------------------------------------------
 // 1. rotate + per-workgroup group maxima
 // ---------------------------------------------------------------------------
-template <int K>
+template <int K, bool kRot>
 __global__ __launch_bounds__(Teams<K>::threads) void rot_max_kernel(
     const uint16_t* __restrict__ X, int M, int g, int rows_per_wg,
     const int32_t* __restrict__ perm, float* __restrict__ gpart) {
@@ -85,7 +85,7 @@ __global__ __launch_bounds__(Teams<K>::threads) void rot_max_kernel(
 #pragma unroll
     for (int e = 0; e < E; ++e) v[e] = vn[e];
     if (it + 1 < iters) load_row_or_zero<K>(X, r0 + (it + 1) * kTeams + team, r1, t, vn);
-    fwht_row<K>(v, slot, t);  // v[e] = y[t + 256 e]
+    fwht_row<K, kRot>(v, slot, t);  // v[e] = y[t + 256 e]
 #pragma unroll
     for (int e = 0; e < E; ++e) cm[e] = fmaxf(cm[e], fabsf(v[e]));
   }
@@ -131,7 +131,7 @@ __global__ __launch_bounds__(Teams<K>::threads) void rot_max_kernel(
 // ---------------------------------------------------------------------------
 // 2. group scales, per-token scale, codes
 // ---------------------------------------------------------------------------
-template <int K>
+template <int K, bool kRot, bool kSmooth>
 __global__ __launch_bounds__(Teams<K>::threads) void quant_kernel(
     const uint16_t* __restrict__ X, int M, int g, int rows_per_wg, int nparts,
     const int32_t* __restrict__ perm, const float* __restrict__ gpart,
@@ -159,9 +159,16 @@ __global__ __launch_bounds__(Teams<K>::threads) void quant_kernel(
   float vn[E];  // next row, loaded while the current one is processed
   load_row_or_zero<K>(X, r0 + team, r1, t, vn);
 
-  // s_b = max over the partial rows; threads split (group, row slice) and
-  // issue their loads eight at a time so the latencies overlap.
-  {
+  if constexpr (!kSmooth) {
+    // Ablation without smoothing: every scale is 1 (rotation + per-token only).
+    if (tid < G) {
+      rg[tid] = 1.0f;
+      if (blockIdx.x == 0) s_group[tid] = 1.0f;
+    }
+    __syncthreads();
+  } else {
+    // s_b = max over the partial rows; threads split (group, row slice) and
+    // issue their loads eight at a time so the latencies overlap.
     const int nsl = kThreads / G;  // G <= 256 <= kThreads
     const int b = tid % G;
     const int sl = tid / G;
@@ -199,7 +206,7 @@ __global__ __launch_bounds__(Teams<K>::threads) void quant_kernel(
 #pragma unroll
     for (int e = 0; e < E; ++e) v[e] = vn[e];
     if (it + 1 < iters) load_row_or_zero<K>(X, r0 + (it + 1) * kTeams + team, r1, t, vn);
-    fwht_row<K>(v, slot, t);
+    fwht_row<K, kRot>(v, slot, t);
     // back to natural order through LDS, with the static reorder applied
     __syncthreads();
 #pragma unroll
@@ -243,7 +250,7 @@ int num_cus() {
 }
 
 template <int K>
-hipError_t launch_k(const uint16_t* X, int M, int g, const int32_t* perm, uint8_t* Xq,
+hipError_t launch_k(const uint16_t* X, int M, int g, const int32_t* perm, int flags, uint8_t* Xq,
                     float* a_scale, float* s_group, void* workspace, hipStream_t stream) {
   constexpr int kTeams = Teams<K>::n;
   // Pass 1 writes one partial row per workgroup: at most 256 of them, so the
@@ -259,9 +266,22 @@ hipError_t launch_k(const uint16_t* X, int M, int g, const int32_t* perm, uint8_
   const int wgs1 = split(kMaxPartialRows, &rpw1);
   const int wgs2 = split(4 * num_cus(), &rpw2);
   float* gpart = static_cast<float*>(workspace);
-  rot_max_kernel<K><<<wgs1, Teams<K>::threads, 0, stream>>>(X, M, g, rpw1, perm, gpart);
-  quant_kernel<K><<<wgs2, Teams<K>::threads, 0, stream>>>(X, M, g, rpw2, wgs1, perm, gpart, Xq,
-                                                          a_scale, s_group);
+  const bool rot = !(flags & kSkipRotation);
+  const bool smooth = !(flags & kSkipSmoothing);
+#define RRS_QUANT(R_, S_)                                                                   \
+  quant_kernel<K, R_, S_><<<wgs2, Teams<K>::threads, 0, stream>>>(X, M, g, rpw2, wgs1, perm, \
+                                                                  gpart, Xq, a_scale, s_group)
+  if (smooth) {
+    if (rot)
+      rot_max_kernel<K, true><<<wgs1, Teams<K>::threads, 0, stream>>>(X, M, g, rpw1, perm, gpart);
+    else
+      rot_max_kernel<K, false><<<wgs1, Teams<K>::threads, 0, stream>>>(X, M, g, rpw1, perm, gpart);
+  }
+  if (rot && smooth) RRS_QUANT(true, true);
+  else if (rot) RRS_QUANT(true, false);
+  else if (smooth) RRS_QUANT(false, true);
+  else RRS_QUANT(false, false);
+#undef RRS_QUANT
   return hipGetLastError();
 }
 
@@ -276,19 +296,20 @@ size_t quant_workspace_bytes(int M, int K) {
 }
 
 hipError_t launch_rotate_smooth_quant(const uint16_t* X, int M, int K, int g,
-                                      const int32_t* perm, uint8_t* Xq, float* a_scale,
-                                      float* s_group, void* workspace, hipStream_t stream) {
+                                      const int32_t* perm, int flags, uint8_t* Xq,
+                                      float* a_scale, float* s_group, void* workspace,
+                                      hipStream_t stream) {
   // One wave per row wins at K = 4096, and at K = 2048 once there are enough
   // rows; elsewhere the team kernels below are faster (measured).
   if (K == 4096 || (K == 2048 && M >= 512))
-    return launch_rotate_smooth_quant_wave(X, M, K, g, perm, Xq, a_scale, s_group, workspace,
-                                           kMaxPartialRows, 2 * num_cus(), stream);
+    return launch_rotate_smooth_quant_wave(X, M, K, g, perm, flags, Xq, a_scale, s_group,
+                                           workspace, kMaxPartialRows, 2 * num_cus(), stream);
   switch (K) {
-    case 512: return launch_k<512>(X, M, g, perm, Xq, a_scale, s_group, workspace, stream);
-    case 1024: return launch_k<1024>(X, M, g, perm, Xq, a_scale, s_group, workspace, stream);
-    case 2048: return launch_k<2048>(X, M, g, perm, Xq, a_scale, s_group, workspace, stream);
-    case 8192: return launch_k<8192>(X, M, g, perm, Xq, a_scale, s_group, workspace, stream);
-    case 16384: return launch_k<16384>(X, M, g, perm, Xq, a_scale, s_group, workspace, stream);
+    case 512: return launch_k<512>(X, M, g, perm, flags, Xq, a_scale, s_group, workspace, stream);
+    case 1024: return launch_k<1024>(X, M, g, perm, flags, Xq, a_scale, s_group, workspace, stream);
+    case 2048: return launch_k<2048>(X, M, g, perm, flags, Xq, a_scale, s_group, workspace, stream);
+    case 8192: return launch_k<8192>(X, M, g, perm, flags, Xq, a_scale, s_group, workspace, stream);
+    case 16384: return launch_k<16384>(X, M, g, perm, flags, Xq, a_scale, s_group, workspace, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -64,18 +64,20 @@ __device__ __forceinline__ void raw_to_float(const uint4 (&raw)[8], float (&v)[6
 }
 
 // Rotate one row held in layout 1 (v[e] = x[64 l + e]); on exit layout 2
-// (v[e] = y[l + R e]). `row` is this row's LDS region (wave-private).
-template <int K>
+// (v[e] = y[l + R e]; y = x when kRot is false: the same data movement without
+// the butterflies, for the ablation without rotation). `row` is this row's LDS
+// region (wave-private).
+template <int K, bool kRot>
 __device__ __forceinline__ void fwht_wave_row(float (&v)[64], float* row, int l) {
   using S = WaveRow<K>;
-  fwht_stages<64, 0, 6>(v);
+  if constexpr (kRot) fwht_stages<64, 0, 6>(v);
 #pragma unroll
   for (int m = 0; m < 16; ++m)
     *reinterpret_cast<float4*>(row + lds_a(64 * l + 4 * m)) =
         make_float4(v[4 * m], v[4 * m + 1], v[4 * m + 2], v[4 * m + 3]);
 #pragma unroll
   for (int e = 0; e < 64; ++e) v[e] = row[lds_a(l + S::R * e)];
-  fwht_stages<64, 6 - S::LR, 6>(v);
+  if constexpr (kRot) fwht_stages<64, 6 - S::LR, 6>(v);
 }
 
 // Max over the R lanes of each row of the wave (aligned groups of R lanes).
@@ -91,7 +93,7 @@ __device__ __forceinline__ float row_max(float x) {
 // ---------------------------------------------------------------------------
 constexpr int kRotWaves = 8;
 
-template <int K>
+template <int K, bool kRot>
 __global__ __launch_bounds__(kRotWaves * 64) void rot_max_wave_kernel(
     const uint16_t* __restrict__ X, int M, int g, int rows_per_wg,
     const int32_t* __restrict__ perm, float* __restrict__ gpart) {
@@ -129,7 +131,7 @@ __global__ __launch_bounds__(kRotWaves * 64) void rot_max_wave_kernel(
       const int r = row_of(p + 1);
       load_raw64(X + (size_t)min(r, M - 1) * K + 64 * l, r < r1, raw);
     }
-    fwht_wave_row<K>(v, row, l);  // v[e] = y[l + R e]
+    fwht_wave_row<K, kRot>(v, row, l);  // v[e] = y[l + R e]
 #pragma unroll
     for (int e = 0; e < 64; ++e) cm[e] = fmaxf(cm[e], fabsf(v[e]));
   }
@@ -176,7 +178,7 @@ __global__ __launch_bounds__(kRotWaves * 64) void rot_max_wave_kernel(
 // ---------------------------------------------------------------------------
 constexpr int kQuantWaves = 4;
 
-template <int K>
+template <int K, bool kRot, bool kSmooth>
 __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
     const uint16_t* __restrict__ X, int M, int g, int rows_per_wg, int nparts,
     const int32_t* __restrict__ perm, const float* __restrict__ gpart,
@@ -209,34 +211,43 @@ __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
     load_raw64(X + (size_t)min(r, M - 1) * K + 64 * l, r < r1, raw);
   }
 
-  // s_b = max over the partial rows. Thread t takes group b = t % GMAX and
-  // rows t / GMAX + k NS (NS = 256 / GMAX slices) with a fixed number of
-  // unconditional loads (row indices clamped to the last row, entries for
-  // b >= G read neighbouring rows and are ignored: every index stays inside
-  // the 256 x K/64 workspace), then the slices are combined through LDS.
-  {
-    constexpr int NS = NT / GMAX;
-    constexpr int NL = (256 + NS - 1) / NS;  // loads per thread for up to 256 rows
-    const int b = tid % GMAX;
-    const int sl = tid / GMAX;
-    float x[NL];
-#pragma unroll
-    for (int k = 0; k < NL; ++k) {
-      const int i = min(sl + k * NS, nparts - 1);
-      x[k] = gpart[(size_t)i * G + b];
-    }
-    float m = 0.0f;
-#pragma unroll
-    for (int k = 0; k < NL; ++k) m = fmaxf(m, x[k]);
-    red[tid] = m;
-    __syncthreads();
+  if constexpr (!kSmooth) {
+    // Ablation without smoothing: every scale is 1 (rotation + per-token only).
     if (tid < G) {
-      float sv = red[tid];
-      for (int q = 1; q < NS; ++q) sv = fmaxf(sv, red[q * GMAX + tid]);
-      rg[tid] = (sv == 0.0f) ? 0.0f : __fdiv_rn(1.0f, sv);
-      if (blockIdx.x == 0) s_group[tid] = sv;
+      rg[tid] = 1.0f;
+      if (blockIdx.x == 0) s_group[tid] = 1.0f;
     }
     __syncthreads();
+  } else {
+    // s_b = max over the partial rows. Thread t takes group b = t % GMAX and
+    // rows t / GMAX + k NS (NS = 256 / GMAX slices) with a fixed number of
+    // unconditional loads (row indices clamped to the last row, entries for
+    // b >= G read neighbouring rows and are ignored: every index stays inside
+    // the 256 x K/64 workspace), then the slices are combined through LDS.
+    {
+      constexpr int NS = NT / GMAX;
+      constexpr int NL = (256 + NS - 1) / NS;  // loads per thread for up to 256 rows
+      const int b = tid % GMAX;
+      const int sl = tid / GMAX;
+      float x[NL];
+#pragma unroll
+      for (int k = 0; k < NL; ++k) {
+        const int i = min(sl + k * NS, nparts - 1);
+        x[k] = gpart[(size_t)i * G + b];
+      }
+      float m = 0.0f;
+#pragma unroll
+      for (int k = 0; k < NL; ++k) m = fmaxf(m, x[k]);
+      red[tid] = m;
+      __syncthreads();
+      if (tid < G) {
+        float sv = red[tid];
+        for (int q = 1; q < NS; ++q) sv = fmaxf(sv, red[q * GMAX + tid]);
+        rg[tid] = (sv == 0.0f) ? 0.0f : __fdiv_rn(1.0f, sv);
+        if (blockIdx.x == 0) s_group[tid] = sv;
+      }
+      __syncthreads();
+    }
   }
   // Positions 64 l .. 64 l + 63 of a row lie in one group (g >= 64).
   const float rb = rg[(64 * l) / g];
@@ -250,7 +261,7 @@ __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
       const int rn = row_of(p + 1);
       load_raw64(X + (size_t)min(rn, M - 1) * K + 64 * l, rn < r1, raw);
     }
-    fwht_wave_row<K>(v, row, l);  // v[e] = y[l + R e]
+    fwht_wave_row<K, kRot>(v, row, l);  // v[e] = y[l + R e]
     // back to layout 1 through LDS, with the static reorder applied
 #pragma unroll
     for (int e = 0; e < 64; ++e) row[lds_a(l + S::R * e)] = v[e];
@@ -291,7 +302,7 @@ __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
 }
 
 template <int K>
-hipError_t launch_wave(const uint16_t* X, int M, int g, const int32_t* perm, uint8_t* Xq,
+hipError_t launch_wave(const uint16_t* X, int M, int g, const int32_t* perm, int flags, uint8_t* Xq,
                        float* a_scale, float* s_group, void* workspace, int max_partials,
                        int max_quant_wgs, hipStream_t stream) {
   using S = WaveRow<K>;
@@ -308,23 +319,37 @@ hipError_t launch_wave(const uint16_t* X, int M, int g, const int32_t* perm, uin
   const int rpw2 = (M + wgs2 - 1) / wgs2;
   wgs2 = (M + rpw2 - 1) / rpw2;
   float* gpart = static_cast<float*>(workspace);
-  rot_max_wave_kernel<K><<<wgs1, kRotWaves * 64, 0, stream>>>(X, M, g, rpw1, perm, gpart);
-  quant_wave_kernel<K><<<wgs2, kQuantWaves * 64, 0, stream>>>(X, M, g, rpw2, wgs1, perm, gpart,
-                                                               Xq, a_scale, s_group);
+  const bool rot = !(flags & kSkipRotation);
+  const bool smooth = !(flags & kSkipSmoothing);
+#define RRS_QUANT(R_, S_)                                                                 \
+  quant_wave_kernel<K, R_, S_><<<wgs2, kQuantWaves * 64, 0, stream>>>(                    \
+      X, M, g, rpw2, wgs1, perm, gpart, Xq, a_scale, s_group)
+  if (smooth) {
+    if (rot)
+      rot_max_wave_kernel<K, true><<<wgs1, kRotWaves * 64, 0, stream>>>(X, M, g, rpw1, perm, gpart);
+    else
+      rot_max_wave_kernel<K, false><<<wgs1, kRotWaves * 64, 0, stream>>>(X, M, g, rpw1, perm, gpart);
+  }
+  if (rot && smooth) RRS_QUANT(true, true);
+  else if (rot) RRS_QUANT(true, false);
+  else if (smooth) RRS_QUANT(false, true);
+  else RRS_QUANT(false, false);
+#undef RRS_QUANT
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_rotate_smooth_quant_wave(const uint16_t* X, int M, int K, int g,
-                                           const int32_t* perm, uint8_t* Xq, float* a_scale,
-                                           float* s_group, void* workspace, int max_partials,
-                                           int max_quant_wgs, hipStream_t stream) {
+                                           const int32_t* perm, int flags, uint8_t* Xq,
+                                           float* a_scale, float* s_group, void* workspace,
+                                           int max_partials, int max_quant_wgs,
+                                           hipStream_t stream) {
   switch (K) {
-    case 512: return launch_wave<512>(X, M, g, perm, Xq, a_scale, s_group, workspace, max_partials, max_quant_wgs, stream);
-    case 1024: return launch_wave<1024>(X, M, g, perm, Xq, a_scale, s_group, workspace, max_partials, max_quant_wgs, stream);
-    case 2048: return launch_wave<2048>(X, M, g, perm, Xq, a_scale, s_group, workspace, max_partials, max_quant_wgs, stream);
-    case 4096: return launch_wave<4096>(X, M, g, perm, Xq, a_scale, s_group, workspace, max_partials, max_quant_wgs, stream);
+    case 512: return launch_wave<512>(X, M, g, perm, flags, Xq, a_scale, s_group, workspace, max_partials, max_quant_wgs, stream);
+    case 1024: return launch_wave<1024>(X, M, g, perm, flags, Xq, a_scale, s_group, workspace, max_partials, max_quant_wgs, stream);
+    case 2048: return launch_wave<2048>(X, M, g, perm, flags, Xq, a_scale, s_group, workspace, max_partials, max_quant_wgs, stream);
+    case 4096: return launch_wave<4096>(X, M, g, perm, flags, Xq, a_scale, s_group, workspace, max_partials, max_quant_wgs, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -2,7 +2,8 @@
 // quantized per output channel; round-to-nearest stands in for GPTQ).
 //
 // For each output channel n (a column of W, K x N row-major):
-//   u = H_K W[:, n]                 (same FWHT and stage order as activations)
+//   u = H_K W[:, n]                 (same FWHT and stage order as activations;
+//                                    u = W[:, n] for the ablation without rotation)
 //   u'_j = u_{perm[j]}              (optional static reorder, Fig. 4 step (1))
 //   b_n = max_j |u_j|, winv = fl(7 / b_n), beta_n = fl(b_n / 7)
 //   code_j = clamp(rint(fl(u'_j * winv)), -7, 7), packed into Wq[n][j / 2].
@@ -14,7 +15,7 @@
 namespace rrs {
 namespace {
 
-template <int K>
+template <int K, bool kRot>
 __global__ __launch_bounds__(kRowThreads) void prep_weight_kernel(
     const uint16_t* __restrict__ W, int N, const int32_t* __restrict__ perm,
     uint8_t* __restrict__ Wq, float* __restrict__ w_scale) {
@@ -48,7 +49,7 @@ __global__ __launch_bounds__(kRowThreads) void prep_weight_kernel(
     float v[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) v[e] = col[lds_pad(t * E + e)];
-    fwht_row<K>(v, col, t);
+    fwht_row<K, kRot>(v, col, t);
     float lm = 0.0f;
 #pragma unroll
     for (int e = 0; e < E; ++e) lm = fmaxf(lm, fabsf(v[e]));
@@ -68,25 +69,28 @@ __global__ __launch_bounds__(kRowThreads) void prep_weight_kernel(
 }
 
 template <int K>
-hipError_t launch_k(const uint16_t* W, int N, const int32_t* perm, uint8_t* Wq,
+hipError_t launch_k(const uint16_t* W, int N, const int32_t* perm, bool rotate, uint8_t* Wq,
                     float* w_scale, hipStream_t stream) {
   constexpr int C = 32768 / K;
   const int grid = (N + C - 1) / C;
-  prep_weight_kernel<K><<<grid, kRowThreads, 0, stream>>>(W, N, perm, Wq, w_scale);
+  if (rotate)
+    prep_weight_kernel<K, true><<<grid, kRowThreads, 0, stream>>>(W, N, perm, Wq, w_scale);
+  else
+    prep_weight_kernel<K, false><<<grid, kRowThreads, 0, stream>>>(W, N, perm, Wq, w_scale);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_prepare_weight(const uint16_t* W, int K, int N, const int32_t* perm,
-                                 uint8_t* Wq, float* w_scale, hipStream_t stream) {
+                                 bool rotate, uint8_t* Wq, float* w_scale, hipStream_t stream) {
   switch (K) {
-    case 512: return launch_k<512>(W, N, perm, Wq, w_scale, stream);
-    case 1024: return launch_k<1024>(W, N, perm, Wq, w_scale, stream);
-    case 2048: return launch_k<2048>(W, N, perm, Wq, w_scale, stream);
-    case 4096: return launch_k<4096>(W, N, perm, Wq, w_scale, stream);
-    case 8192: return launch_k<8192>(W, N, perm, Wq, w_scale, stream);
-    case 16384: return launch_k<16384>(W, N, perm, Wq, w_scale, stream);
+    case 512: return launch_k<512>(W, N, perm, rotate, Wq, w_scale, stream);
+    case 1024: return launch_k<1024>(W, N, perm, rotate, Wq, w_scale, stream);
+    case 2048: return launch_k<2048>(W, N, perm, rotate, Wq, w_scale, stream);
+    case 4096: return launch_k<4096>(W, N, perm, rotate, Wq, w_scale, stream);
+    case 8192: return launch_k<8192>(W, N, perm, rotate, Wq, w_scale, stream);
+    case 16384: return launch_k<16384>(W, N, perm, rotate, Wq, w_scale, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -395,24 +395,49 @@ def test_diagnostics():
     assert O.victim_measure(np.ones(8)) == pytest.approx(1.0)
 
 
-def test_method_ordering_report():
-    # Report only (parity unpinned): quantization error vs the fp64 product
-    # for QuaRot-style rotation, Runtime Smooth and RRS on outlier-laden data.
-    w = synth.custom("t", 64, 1024, 64, 128, 25, n_chan=10, chan_factor=(20, 100),
-                     n_spike=6, spike_mag=(100, 500))
+def _variant_errors(w):
+    # Relative Frobenius error of each variant's output against the fp64
+    # product X W, all four variants quantizing the same inputs.
     X = synth.activations(w)
     W = synth.weights(w)
     ref = O.fp64_reference(X, W)
-    K = X.shape[1]
     out = {}
-    for name, rot, sm in (("quarot", True, False), ("rs", False, True), ("rrs", True, True)):
-        act = O.rotate_smooth_quant(X, 128, rotate=rot, smooth=sm)
+    for name, rot, sm in (("rrs", True, True), ("rs", False, True),
+                          ("quarot", True, False), ("none", False, False)):
+        act = O.rotate_smooth_quant(X, w.g, rotate=rot, smooth=sm)
         wq = O.prepare_weight(W, rotate=rot)
-        P = O.group_partials(act.q, wq.q, 128)
-        Y = O.output(P, act.s, act.alpha, wq.beta, norm=K if rot else 1)
+        P = O.group_partials(act.q, wq.q, w.g)
+        Y = O.output(P, act.s, act.alpha, wq.beta, norm=w.K if rot else 1)
         out[name] = float(np.linalg.norm(Y - ref) / np.linalg.norm(ref))
-    print("relative error vs fp64 XW:", out)
-    assert out["rrs"] < 0.5
+    return out
+
+
+@pytest.mark.parametrize("seed", [11, 12, 13])
+def test_ablation_ordering_spikes(seed):
+    # Section 3.2 and the ablation of Section 4: Runtime Smooth alone is hurt by
+    # a few huge spike tokens (they inflate the channel maxima, which then
+    # crush every other token's values), while the rotation spreads each spike
+    # over all channels. On spike data both rotated variants must clearly beat
+    # both unrotated ones, and Runtime Smooth alone must be the worst.
+    w = synth.custom("s", 128, 2048, 128, 128, seed, n_chan=0, n_spike=20,
+                     spike_mag=(100, 500))
+    e = _variant_errors(w)
+    assert e["rs"] > 1.5 * e["rrs"], e
+    assert e["none"] > 1.1 * e["quarot"], e
+    assert e["rs"] > e["none"], e
+    assert e["rrs"] < 1.05 * e["quarot"], e
+
+
+@pytest.mark.parametrize("seed", [11, 12, 13])
+def test_ablation_ordering_channels_and_spikes(seed):
+    # Channel-wise outliers plus spikes (the mix Section 3 describes): RRS must
+    # beat both Runtime Smooth alone and no treatment at all.
+    w = synth.custom("b", 128, 2048, 128, 128, seed, n_chan=20, chan_factor=(20, 100),
+                     n_spike=20, spike_mag=(100, 500))
+    e = _variant_errors(w)
+    assert e["rrs"] < 0.8 * e["rs"], e
+    assert e["rrs"] < 0.85 * e["none"], e
+    assert e["rrs"] < 1.05 * e["quarot"], e
 
 
 def test_fwht_fp32_canonical_stage_order():

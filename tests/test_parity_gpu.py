@@ -339,3 +339,66 @@ def test_gemm_deterministic():
     y1 = rrs.w4a4_gemm(Xq, a, s, Wq, beta, w.g)
     y2 = rrs.w4a4_gemm(Xq, a, s, Wq, beta, w.g)
     assert torch.equal(y1, y2)
+
+
+# ------------------------------------------------------------------ ablation switches
+
+ABLATIONS = [(1, "no-rotation"), (2, "no-smoothing"), (3, "neither")]
+
+
+def _ablation_case(w, flags, perm=None, label=""):
+    """The _ex entry points with RRS_SKIP_* flags against the oracle's
+    rotate / smooth switches (the paper's Runtime-Smooth-only and QuaRot-style
+    baselines): codes, scales and packed weights bit for bit, Y within the
+    tolerance (normalization 1 without rotation)."""
+    rrs = _rrs()
+    rot = not flags & rrs.SKIP_ROTATION
+    smooth = not flags & rrs.SKIP_SMOOTHING
+    print(f"[case] ablation {label} flags={flags} M={w.M} K={w.K} N={w.N} g={w.g} "
+          f"perm={perm is not None}", flush=True)
+    X = synth.activations(w)
+    W = synth.weights(w)
+    Xg = to_gpu(X)
+    pg = None if perm is None else to_gpu(perm)
+    Wq, beta = rrs.prepare_weight(to_gpu(W), pg, flags=flags & rrs.SKIP_ROTATION)
+    Xq, a, s = rrs.rotate_smooth_quant(Xg, w.g, perm=pg, flags=flags)
+    Y = rrs.w4a4_gemm(Xq, a, s, Wq, beta, w.g, flags=flags)
+    Y2 = rrs.linear(Xg, Wq, beta, w.g, perm=pg, flags=flags)
+    assert torch.equal(Y, Y2), f"{label}: rrs_linear_ex differs from quant + gemm"
+
+    act = O.rotate_smooth_quant(X, w.g, perm=perm, rotate=rot, smooth=smooth)
+    wq = O.prepare_weight(W, perm=perm, rotate=rot)
+    np.testing.assert_array_equal(to_np(a), act.alpha)
+    np.testing.assert_array_equal(to_np(s), act.s)
+    if not smooth:
+        assert np.all(to_np(s) == 1.0)
+    check_codes(to_np(Xq), act, label)
+    np.testing.assert_array_equal(to_np(beta), wq.beta)
+    np.testing.assert_array_equal(to_np(Wq), wq.packed)
+    P = O.group_partials(act.q, wq.q, w.g)
+    norm = w.K if rot else 1
+    y_ref = O.output(P, act.s, act.alpha, wq.beta, norm=norm)
+    nw = check_y(to_np(Y).astype(np.float32), y_ref, P, act.s, act.alpha, wq.beta, norm, label)
+    print(f"{label}: normwise |dY|/|Y| = {nw:.3e}")
+
+
+@pytest.mark.parametrize("flags,name", ABLATIONS)
+@pytest.mark.parametrize("M,K,N,g", [
+    (16, 512, 512, 128),     # team quant kernels, few-token GEMM
+    (77, 4096, 272, 128),    # one-wave-per-row quant, main GEMM
+    (8, 8192, 144, 128),     # team quant (K = 8192), few-token GEMM
+    (130, 2048, 400, 512),   # team quant (K = 2048, few rows), main GEMM, g = 512
+    (600, 2048, 96, 64),     # one-wave-per-row quant (K = 2048, many rows), g = 64
+])
+def test_ablation_variants(flags, name, M, K, N, g):
+    w = synth.custom("a", M, K, N, g, M + N + K + flags, n_chan=max(1, K // 100),
+                     chan_factor=(20, 100), n_spike=max(1, M * K // 10000),
+                     spike_mag=(100, 500))
+    _ablation_case(w, flags, label=f"{name} {M}x{K}x{N}/g{g}")
+
+
+@pytest.mark.parametrize("flags,name", ABLATIONS)
+def test_ablation_variants_with_perm(flags, name):
+    w = synth.custom("a", 40, 4096, 160, 128, 77, n_chan=40, chan_factor=(20, 100),
+                     n_spike=20, spike_mag=(100, 500))
+    _ablation_case(w, flags, perm=synth.permutation(w.K, 5), label=f"{name} perm")
