@@ -119,20 +119,10 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
     pb[j] = Wq + (size_t)(n + c) * krow + q * (g / 8);
   }
 
-  // Wave-private copy of this wave's K quarter of Xq: row r < M at
+  // Wave-private LDS copy of this wave's K quarter of Xq: row r < M at
   // r * a_row_bytes(K); lanes then read their row min(c, M - 1).
   uint8_t* aq = lds + kq * kMaxLdsA;
   const int arb = a_row_bytes(K, g);
-  if constexpr (kLdsA) {
-    const int qb = max(nb, 0) * (g / 2);  // bytes of this wave's groups in a row
-    const uint8_t* src = Xq + (size_t)b0 * (g / 2);
-    for (int e = lane * 16; e < M * qb; e += 64 * 16) {
-      const int r = e / qb;
-      const int o = e - r * qb;
-      *reinterpret_cast<uint4*>(aq + r * arb + o) =
-          *reinterpret_cast<const uint4*>(src + (size_t)r * krow + o);
-    }
-  }
   const uint8_t* pal = aq + min(c, M - 1) * arb + q * (g / 8);
 
   uint32_t wa[D][NW], wb[D][kBlocks][NW];
@@ -184,8 +174,21 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
     }
   };
 
+  // The first groups' weight loads are issued before the token copy, so the
+  // weight stream starts at once instead of after the copy's load latency.
 #pragma unroll
   for (int d = 0; d < D; ++d) load(d, d);
+  // Wave-private copy of this wave's K quarter of Xq (see aq above).
+  if constexpr (kLdsA) {
+    const int qb = max(nb, 0) * (g / 2);  // bytes of this wave's groups in a row
+    const uint8_t* src = Xq + (size_t)b0 * (g / 2);
+    for (int e = lane * 16; e < M * qb; e += 64 * 16) {
+      const int r = e / qb;
+      const int o = e - r * qb;
+      *reinterpret_cast<uint4*>(aq + r * arb + o) =
+          *reinterpret_cast<const uint4*>(src + (size_t)r * krow + o);
+    }
+  }
   int i = 0;
   for (; i < steps - D; i += D) {
 #pragma unroll
