@@ -53,6 +53,58 @@ __device__ __forceinline__ void load_row_or_zero(const uint16_t* __restrict__ X,
   }
 }
 
+// Per-channel maxima cm (this thread's E channels t + 256 e) of every team
+// combined in LDS, then maxima over each group of g (reordered) positions.
+// Returns, for threads tid < K / g, the maximum of group tid; 0 elsewhere.
+// Must be called by all threads of the workgroup; cbuf holds >= K floats.
+template <int K>
+__device__ __forceinline__ float group_maxima(const float (&cm)[FwhtShape<K>::E], float* cbuf,
+                                              int g, const int32_t* __restrict__ perm) {
+  constexpr int E = FwhtShape<K>::E;
+  constexpr int kTeams = Teams<K>::n;
+  constexpr int kThreads = Teams<K>::threads;
+  const int tid = threadIdx.x;
+  const int team = tid >> 8;
+  const int t = tid & (kRowThreads - 1);
+  __syncthreads();
+  if (team == 0) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) cbuf[t + e * kRowThreads] = cm[e];
+  }
+  __syncthreads();
+  for (int tm = 1; tm < kTeams; ++tm) {
+    if (team == tm) {
+#pragma unroll
+      for (int e = 0; e < E; ++e)
+        cbuf[t + e * kRowThreads] = fmaxf(cbuf[t + e * kRowThreads], cm[e]);
+    }
+    __syncthreads();
+  }
+  // The first NA threads cover P consecutive positions each, all inside one
+  // group (P <= 64 <= g).
+  constexpr int NA = K < kThreads ? K : kThreads;
+  constexpr int P = K / NA;
+  float pm = 0.0f;
+  if (tid < NA) {
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      const int j = tid * P + q;
+      pm = fmaxf(pm, cbuf[perm ? perm[j] : j]);
+    }
+  }
+  __syncthreads();
+  cbuf[tid] = pm;  // tid < kThreads <= slot_floats
+  __syncthreads();
+  const int G = K / g;
+  float s = 0.0f;
+  if (tid < G) {
+    const int per = g / P;  // threads per group
+    for (int u = 0; u < per; ++u) s = fmaxf(s, cbuf[tid * per + u]);
+  }
+  __syncthreads();  // cbuf may be reused by the caller
+  return s;
+}
+
 // ---------------------------------------------------------------------------
 // 1. rotate + per-workgroup group maxima
 // ---------------------------------------------------------------------------
@@ -89,43 +141,8 @@ __global__ __launch_bounds__(Teams<K>::threads) void rot_max_kernel(
 #pragma unroll
     for (int e = 0; e < E; ++e) cm[e] = fmaxf(cm[e], fabsf(v[e]));
   }
-  // Per-channel maxima of the workgroup: teams combined in LDS.
-  __syncthreads();
-  if (team == 0) {
-#pragma unroll
-    for (int e = 0; e < E; ++e) cbuf[t + e * kRowThreads] = cm[e];
-  }
-  __syncthreads();
-  for (int tm = 1; tm < kTeams; ++tm) {
-    if (team == tm) {
-#pragma unroll
-      for (int e = 0; e < E; ++e)
-        cbuf[t + e * kRowThreads] = fmaxf(cbuf[t + e * kRowThreads], cm[e]);
-    }
-    __syncthreads();
-  }
-  // Group maxima over the (reordered) positions. The first NA threads cover
-  // P consecutive positions each, all inside one group (P <= 64 <= g).
-  constexpr int NA = K < kThreads ? K : kThreads;
-  constexpr int P = K / NA;
-  float pm = 0.0f;
-  if (tid < NA) {
-#pragma unroll
-    for (int q = 0; q < P; ++q) {
-      const int j = tid * P + q;
-      pm = fmaxf(pm, cbuf[perm ? perm[j] : j]);
-    }
-  }
-  __syncthreads();
-  cbuf[tid] = pm;  // tid < kThreads <= slot_floats
-  __syncthreads();
-  const int G = K / g;
-  if (tid < G) {
-    const int per = g / P;  // threads per group
-    float s = 0.0f;
-    for (int u = 0; u < per; ++u) s = fmaxf(s, cbuf[tid * per + u]);
-    gpart[(size_t)blockIdx.x * G + tid] = s;
-  }
+  const float s = group_maxima<K>(cm, cbuf, g, perm);
+  if (tid < K / g) gpart[(size_t)blockIdx.x * (K / g) + tid] = s;
 }
 
 // ---------------------------------------------------------------------------

@@ -74,6 +74,30 @@ def test_quant_with_perm(K, g):
     _quant_case(synth.activations(w), g, perm=synth.permutation(K, K), label=f"perm K={K}")
 
 
+@pytest.mark.parametrize("M", [15, 16, 17])
+@pytest.mark.parametrize("K,g", [(4096, 128), (8192, 128), (1024, 64)])
+def test_quant_few_tokens_boundary(M, K, g):
+    # around the few-token size, where the partial-row split changes
+    w = synth.custom("f", M, K, 16, g, 11 + M + K, n_chan=max(1, K // 100), n_spike=2,
+                     spike_mag=(100, 500))
+    _quant_case(synth.activations(w), g, label=f"few {M}x{K}/g{g}")
+
+
+@pytest.mark.parametrize("flags", [1, 0])
+def test_quant_few_tokens_perm_and_no_rotation(flags):
+    rrs = _rrs()
+    K, g, M = 2048, 128, 9
+    w = synth.custom("fp", M, K, 16, g, 5, n_chan=8, n_spike=3)
+    X = synth.activations(w)
+    perm = synth.permutation(K, K + 1)
+    print(f"[case] few-token quant flags={flags} M={M} K={K}", flush=True)
+    act = O.rotate_smooth_quant(X, g, perm=perm, rotate=not (flags & 1))
+    Xq, a, s = rrs.rotate_smooth_quant(to_gpu(X), g, perm=to_gpu(perm), flags=flags)
+    np.testing.assert_array_equal(to_np(s), act.s)
+    np.testing.assert_array_equal(to_np(a), act.alpha)
+    check_codes(to_np(Xq), act, "few-token perm")
+
+
 def test_quant_degenerate_rows_and_groups():
     # an all-zero token (alpha = 0, codes 0) and all-ones tokens, which rotate
     # to [K, 0, ..., 0]: every group but the first has s_b = 0 (codes 0).
