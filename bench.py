@@ -60,6 +60,10 @@ def parse():
     ap.add_argument("--decode-only", action="store_true",
                     help="only the decode measurement (for per-kernel profiles)")
     ap.add_argument("--decode-steps", type=int, default=100)
+    ap.add_argument("--no-schemes", action="store_true",
+                    help="skip the per-channel / Runtime Smooth / sub-channel kernel comparison")
+    ap.add_argument("--schemes-only", action="store_true",
+                    help="only the kernel comparison of the three scale schemes")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run 5 plain 256 MiB device copies, the reference kernel "
                          "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE counters")
@@ -180,6 +184,62 @@ def decode_bench(args, torch, rrs, synth):
     }
 
 
+def scheme_bench(torch, rrs, reps=30):
+    """Kernel comparison of Section 4.5 (Fig. 6): per-channel, Runtime Smooth and
+    sub-channel A4W4 on the shared 128 x 128 skeleton, plus the tuned Runtime Smooth
+    kernel, at LLaMA-7B shapes (hidden 4096, sequence length 1024, 1/2/4 sequences).
+    The GEMMs only read codes and scales, so they run on random packed codes and
+    positive scales generated on the GPU."""
+    dev = torch.device("cuda:0")
+    g = 128
+    K = 4096
+    G = K // g
+    gen = torch.Generator(device=dev).manual_seed(7)
+    rows = []
+    for N, proj in ((4096, "o_proj"), (12288, "qkv_proj"), (22016, "gate_up_proj")):
+        Wq = torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device=dev, generator=gen)
+        wN = torch.rand((N,), device=dev, generator=gen) + 0.5
+        wGN = torch.rand((G, N), device=dev, generator=gen) + 0.5
+        for M in (1024, 2048, 4096):
+            Xq = torch.randint(0, 256, (M, K // 2), dtype=torch.uint8, device=dev, generator=gen)
+            aM = torch.rand((M,), device=dev, generator=gen) + 0.5
+            aGM = torch.rand((G, M), device=dev, generator=gen) + 0.5
+            s = torch.rand((G,), device=dev, generator=gen) + 0.5
+            Y = torch.empty((M, N), dtype=torch.float16, device=dev)
+            calls = {
+                "per_channel": lambda: rrs.w4a4_gemm_scheme(rrs.SCHEME_PER_CHANNEL, Xq, aM, None,
+                                                            Wq, wN, g, out=Y),
+                "runtime_smooth": lambda: rrs.w4a4_gemm_scheme(rrs.SCHEME_RUNTIME_SMOOTH, Xq, aM,
+                                                               s, Wq, wN, g, out=Y),
+                "sub_channel": lambda: rrs.w4a4_gemm_scheme(rrs.SCHEME_SUB_CHANNEL, Xq, aGM,
+                                                            None, Wq, wGN, g, out=Y),
+                "rrs_tuned": lambda: rrs.w4a4_gemm(Xq, aM, s, Wq, wN, g, out=Y),
+                "per_channel_tuned": lambda: rrs.w4a4_gemm_per_channel(Xq, aM, Wq, wN, out=Y),
+            }
+            row = {"proj": proj, "M": M, "N": N, "K": K}
+            for name, fn in calls.items():
+                for _ in range(5):
+                    fn()
+                torch.cuda.synchronize()
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(reps):
+                    fn()
+                e1.record()
+                torch.cuda.synchronize()
+                row[name + "_us"] = round(e0.elapsed_time(e1) * 1e3 / reps, 2)
+            pc = row["per_channel_us"]
+            row["rs_overhead"] = round(row["runtime_smooth_us"] / pc - 1.0, 4)
+            row["sub_channel_overhead"] = round(row["sub_channel_us"] / pc - 1.0, 4)
+            row["tuned_rs_overhead"] = round(row["rrs_tuned_us"] / row["per_channel_tuned_us"]
+                                             - 1.0, 4)
+            rows.append(row)
+    return {"skeleton": "128x128 tiles, i8 MFMA (per_channel, runtime_smooth, sub_channel); "
+                        "tuned: the 256x128 main kernel (rrs_tuned, per_channel_tuned)",
+            "group_size": g, "rows": rows}
+
+
 def cpu_baseline(synth):
     """The CPU oracle as it stands, on a bounded sample of the same workload."""
     import numpy as np
@@ -232,6 +292,10 @@ def main():
     rrs.lib()
     if args.copy_calibration:
         copy_calibration(torch)
+    if args.schemes_only:
+        print(json.dumps({"metric": METRIC, "scheme_comparison": scheme_bench(torch, rrs)}),
+              flush=True)
+        return
     if args.decode_only:
         print(json.dumps({"metric": METRIC, "decode": decode_bench(args, torch, rrs, synth)}),
               flush=True)
@@ -273,6 +337,9 @@ def main():
     }
     if not args.no_decode:
         out["decode"] = decode_bench(args, torch, rrs, synth)
+    if not args.no_schemes:
+        log("kernel comparison of the scale schemes")
+        out["scheme_comparison"] = scheme_bench(torch, rrs)
     if not args.no_cpu:
         log("timing the CPU oracle baseline")
         out["cpu_baseline"] = cpu_baseline(synth)

@@ -198,6 +198,78 @@ rrs_status rrs_linear_ex(const void* X, const void* Wq, const float* w_scale, in
 rrs_status rrs_w4a4_gemm_partials(const void* Xq, const void* Wq, int M, int N, int K,
                                   int group_size, int32_t* P, void* stream);
 
+/*
+ * ------------------------------------------------------------------------
+ * Baselines of the kernel-efficiency comparison (Section 4.5, Fig. 6).
+ * Per-channel A4W4 (one scale per token and per output channel, the setting
+ * of QuaRot and SpinQuant), Runtime Smooth A4W4 (the same plus one smoothing
+ * scale per group) and sub-channel A4W4 (one scale per (token, group) and per
+ * (output channel, group)) run on one shared GEMM skeleton (128 x 128 tiles)
+ * that differs between the three only in how scales are applied, so their
+ * times compare the schemes, not the kernels. rrs_w4a4_gemm is the tuned
+ * Runtime Smooth kernel and is not part of this comparison.
+ * ------------------------------------------------------------------------
+ */
+enum {
+  RRS_SCHEME_PER_CHANNEL = 0,
+  RRS_SCHEME_RUNTIME_SMOOTH = 1,
+  RRS_SCHEME_SUB_CHANNEL = 2
+};
+
+/*
+ * Sub-channel quantization of activations: y = x H_K (x itself with
+ * RRS_SKIP_ROTATION); for token i and group b of g channels,
+ * m = max_j |y_ij|, inv = fl(7/m) (0 if m = 0), q = clamp(rint(fl(y inv)), -7, 7).
+ *   X in      : M x K float16, row-major.
+ *   Xq out    : M x K/2 bytes, packed as for rrs_rotate_smooth_quant.
+ *   a_sub out : L x M float32, a_sub[b * M + i] = fl(m / 7), L = K / g (group-major).
+ * One launch; no workspace. Shapes and errors as rrs_rotate_smooth_quant
+ * (flags: only RRS_SKIP_ROTATION).
+ */
+rrs_status rrs_quantize_sub_channel(const void* X, int M, int K, int group_size, int flags,
+                                    void* Xq, float* a_sub, void* stream);
+
+/*
+ * Sub-channel weight preparation: u = H_K W (W with RRS_SKIP_ROTATION), then
+ * for output channel n and group b the same RTN as above.
+ *   W in      : K x N float16, row-major.
+ *   Wq out    : N x K/2 bytes, as rrs_prepare_weight.
+ *   w_sub out : L x N float32, w_sub[b * N + n] (group-major).
+ */
+rrs_status rrs_prepare_weight_sub_channel(const void* W, int K, int N, int group_size,
+                                          int flags, void* Wq, float* w_sub, void* stream);
+
+/*
+ * GEMM of one scheme on the comparison skeleton; Y out M x N float16. With
+ * norm = K (1 with RRS_SKIP_ROTATION):
+ *   RRS_SCHEME_PER_CHANNEL   : Y = x_scale[i] w_scale[n] / norm * sum_j q_x q_w
+ *                              (x_scale M, w_scale N; s_group unused, may be NULL;
+ *                              inputs from rrs_rotate_smooth_quant_ex with
+ *                              RRS_SKIP_SMOOTHING and rrs_prepare_weight_ex);
+ *   RRS_SCHEME_RUNTIME_SMOOTH: Y as rrs_w4a4_gemm (x_scale M, s_group L, w_scale N);
+ *   RRS_SCHEME_SUB_CHANNEL   : Y = 1 / norm * sum_b fl(x_scale[b M + i] w_scale[b N + n]) P_b
+ *                              (x_scale L x M, w_scale L x N; s_group unused).
+ * group_size is ignored by RRS_SCHEME_PER_CHANNEL (pass any valid one).
+ * Errors as rrs_w4a4_gemm_ex; an unknown scheme is RRS_ERR_FLAGS.
+ */
+rrs_status rrs_w4a4_gemm_scheme(int scheme, const void* Xq, const float* x_scale,
+                                const float* s_group, const void* Wq, const float* w_scale,
+                                int M, int N, int K, int group_size, int flags, void* Y,
+                                void* stream);
+
+/*
+ * Per-channel A4W4 GEMM (one scale per token and per output channel, no
+ * smoothing; the setting of QuaRot and SpinQuant, Section 2.1) on the same
+ * tuned main loop as rrs_w4a4_gemm, without its per-group rescale:
+ *   Y[i, n] = fp16( a_scale[i] * w_scale[n] / norm * sum_j q_x[i, j] q_w[j, n] ),
+ * norm = K (1 with RRS_SKIP_ROTATION). Inputs from rrs_rotate_smooth_quant_ex
+ * with RRS_SKIP_SMOOTHING (its s_group is all ones and unused here) and
+ * rrs_prepare_weight_ex. Shapes, alignment and errors as rrs_w4a4_gemm_ex.
+ */
+rrs_status rrs_w4a4_gemm_per_channel(const void* Xq, const float* a_scale, const void* Wq,
+                                     const float* w_scale, int M, int N, int K, int flags,
+                                     void* Y, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

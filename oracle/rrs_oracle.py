@@ -320,6 +320,90 @@ def linear(X: np.ndarray, W: np.ndarray, g: int, perm: Optional[np.ndarray] = No
 
 
 # --------------------------------------------------------------------------
+# Baselines of the kernel-efficiency comparison (Section 4.5, Fig. 6)
+# --------------------------------------------------------------------------
+#
+# Per-channel A4W4 (the setting of Section 2.1 and of QuaRot/SpinQuant): one
+# scale per token and one per output channel, no smoothing. Its quantizer is
+# rotate_smooth_quant(..., smooth=False) with prepare_weight, and its output is
+# output(P, ones, alpha, beta, norm): sum_b 1 * P_b is the plain integer dot
+# product.
+#
+# Sub-channel A4W4 (Section 2.1 "sub-channel"): every row is split into groups
+# of g channels, each (token, group) and each (output channel, group) has its
+# own scale (shapes [M, L] and [N, L], L = K / g, Section 4.5), so the output
+# multiplies every group partial by a matrix of scales instead of a scalar.
+
+@dataclass
+class SubChannelQuant:
+    """Sub-channel quantization of the rows of a matrix (tokens, or weight
+    columns seen as rows)."""
+    y: np.ndarray        # rotated (or not) values, rows x K
+    m: np.ndarray        # per (row, group) maxima, rows x G
+    inv: np.ndarray      # fl(7 / m), 0 where m = 0
+    scale: np.ndarray    # fl(m / 7), rows x G
+    q: np.ndarray        # codes, rows x K int8
+    v: np.ndarray        # pre-rounding values, rows x K
+    packed: np.ndarray   # rows x K/2 uint8
+
+
+def _sub_channel_rows(y: np.ndarray, g: int, mode: str) -> SubChannelQuant:
+    """Symmetric RTN of every (row, group) block with its own absmax (Section 2.1)."""
+    dt = _dt(mode)
+    R, K = y.shape
+    if K % g:
+        raise ValueError("group size must divide K")
+    G = K // g
+    blocks = y.reshape(R, G, g)
+    m = np.abs(blocks).max(axis=2).astype(dt)
+    inv = np.zeros_like(m)
+    nz = m != 0
+    inv[nz] = dt(QMAX) / m[nz]
+    v = (blocks * inv[:, :, None]).astype(dt).reshape(R, K)
+    q = np.clip(np.rint(v), -QMAX, QMAX).astype(np.int8)
+    scale = (m / dt(QMAX)).astype(dt)
+    return SubChannelQuant(y, m, inv, scale, q, v, pack_int4(q))
+
+
+def sub_channel_quant(X: np.ndarray, g: int, mode: str = "fp32",
+                      rotate: bool = True) -> SubChannelQuant:
+    """Activations: y = x H_K (or x), then one scale per (token, group)."""
+    dt = _dt(mode)
+    y = fwht(X, mode) if rotate else np.array(X, dtype=dt)
+    return _sub_channel_rows(y, g, mode)
+
+
+def sub_channel_weight(W: np.ndarray, g: int, mode: str = "fp32",
+                       rotate: bool = True) -> SubChannelQuant:
+    """Weights: u = H_K W (or W); output channel n is row n of u^T, one scale per
+    (output channel, group). The packed result is N x K/2 like prepare_weight's."""
+    dt = _dt(mode)
+    u = fwht(W, mode, axis=0) if rotate else np.array(W, dtype=dt)
+    return _sub_channel_rows(np.ascontiguousarray(u.T), g, mode)
+
+
+def output_sub_channel(P: np.ndarray, a_sub: np.ndarray, b_sub: np.ndarray, norm: int
+                       ) -> np.ndarray:
+    """Y = fl32((1/norm) * sum_b a_ib b_nb P_b[i, n]), in binary64 before the cast.
+
+    a_sub: M x G token-group scales, b_sub: N x G channel-group scales.
+    """
+    a = np.asarray(a_sub, np.float64)
+    b = np.asarray(b_sub, np.float64)
+    acc = np.einsum("ib,nb,bin->in", a, b, P.astype(np.float64))
+    return (acc / norm).astype(np.float32)
+
+
+def output_sub_channel_abs_terms(P: np.ndarray, a_sub: np.ndarray, b_sub: np.ndarray,
+                                 norm: int) -> np.ndarray:
+    """T = (1/norm) sum_b |a_ib b_nb P_b[i, n]|, the magnitude bounding the
+    rounding of any binary32 order of the sub-channel sum."""
+    a = np.abs(np.asarray(a_sub, np.float64))
+    b = np.abs(np.asarray(b_sub, np.float64))
+    return np.einsum("ib,nb,bin->in", a, b, np.abs(P).astype(np.float64)) / norm
+
+
+# --------------------------------------------------------------------------
 # Diagnostics (Section 2.3, Appendix A.1, A.2): smoothness and victim measures
 # --------------------------------------------------------------------------
 

@@ -13,6 +13,9 @@ INT4 inference" (arXiv 2409.20361), Sections 3.1-3.3.
 from __future__ import annotations
 
 from ._binding import (  # noqa: F401
+    SCHEME_PER_CHANNEL,
+    SCHEME_RUNTIME_SMOOTH,
+    SCHEME_SUB_CHANNEL,
     SKIP_ROTATION,
     SKIP_SMOOTHING,
     RRSError,
@@ -21,16 +24,22 @@ from ._binding import (  # noqa: F401
     linear,
     linear_workspace_bytes,
     prepare_weight,
+    prepare_weight_sub_channel,
+    quantize_sub_channel,
     rotate_smooth_quant,
     status_string,
     version,
     w4a4_gemm,
     w4a4_gemm_partials,
+    w4a4_gemm_per_channel,
+    w4a4_gemm_scheme,
     workspace_bytes,
 )
 
 __all__ = [
-    "SKIP_ROTATION", "SKIP_SMOOTHING", "RRSError", "lib", "lib_path", "linear",
-    "linear_workspace_bytes", "prepare_weight", "rotate_smooth_quant", "status_string",
-    "version", "w4a4_gemm", "w4a4_gemm_partials", "workspace_bytes",
+    "SCHEME_PER_CHANNEL", "SCHEME_RUNTIME_SMOOTH", "SCHEME_SUB_CHANNEL", "SKIP_ROTATION",
+    "SKIP_SMOOTHING", "RRSError", "lib", "lib_path", "linear", "linear_workspace_bytes",
+    "prepare_weight", "prepare_weight_sub_channel", "quantize_sub_channel",
+    "rotate_smooth_quant", "status_string", "version", "w4a4_gemm", "w4a4_gemm_partials",
+    "w4a4_gemm_per_channel", "w4a4_gemm_scheme", "workspace_bytes",
 ]

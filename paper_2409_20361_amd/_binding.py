@@ -33,7 +33,18 @@ _SIGNATURES = {
                          [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp]),
     "rrs_linear_ex": (ctypes.c_int32,
                       [_vp, _vp, _vp, _i, _i, _i, _i, _vp, _i, _vp, _vp, _sz, _vp]),
+    "rrs_quantize_sub_channel": (ctypes.c_int32, [_vp, _i, _i, _i, _i, _vp, _vp, _vp]),
+    "rrs_prepare_weight_sub_channel": (ctypes.c_int32, [_vp, _i, _i, _i, _i, _vp, _vp, _vp]),
+    "rrs_w4a4_gemm_per_channel": (ctypes.c_int32,
+                                  [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp]),
+    "rrs_w4a4_gemm_scheme": (ctypes.c_int32,
+                             [_i, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp]),
 }
+
+# Scale schemes of the kernel comparison (include/rrs.h, RRS_SCHEME_*).
+SCHEME_PER_CHANNEL = 0
+SCHEME_RUNTIME_SMOOTH = 1
+SCHEME_SUB_CHANNEL = 2
 
 # Ablation switches (include/rrs.h): 0 is RRS itself.
 SKIP_ROTATION = 1    # plain Runtime Smooth: no Hadamard rotation
@@ -193,3 +204,78 @@ def w4a4_gemm_partials(Xq: torch.Tensor, Wq: torch.Tensor, g: int) -> torch.Tens
     _check(lib().rrs_w4a4_gemm_partials(xp, wp, M, N, K, g, P.data_ptr(), _stream(Xq.device)),
            "rrs_w4a4_gemm_partials")
     return P
+
+
+def quantize_sub_channel(X: torch.Tensor, g: int, flags: int = 0
+                         ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """X: M x K fp16 -> (Xq M x K/2 uint8, a_sub K/g x M f32), one scale per (token, group)."""
+    M, K = X.shape
+    xp = _dev(X, "X", torch.float16, (M, K))
+    Xq = torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
+    a = torch.empty((K // g, M), dtype=torch.float32, device=X.device)
+    _check(lib().rrs_quantize_sub_channel(xp, M, K, g, flags, Xq.data_ptr(), a.data_ptr(),
+                                          _stream(X.device)), "rrs_quantize_sub_channel")
+    return Xq, a
+
+
+def prepare_weight_sub_channel(W: torch.Tensor, g: int, flags: int = 0
+                               ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """W: K x N fp16 -> (Wq N x K/2 uint8, w_sub K/g x N f32), one scale per (channel, group)."""
+    K, N = W.shape
+    wp = _dev(W, "W", torch.float16, (K, N))
+    Wq = torch.empty((N, K // 2), dtype=torch.uint8, device=W.device)
+    ws = torch.empty((K // g, N), dtype=torch.float32, device=W.device)
+    _check(lib().rrs_prepare_weight_sub_channel(wp, K, N, g, flags, Wq.data_ptr(), ws.data_ptr(),
+                                                _stream(W.device)),
+           "rrs_prepare_weight_sub_channel")
+    return Wq, ws
+
+
+def w4a4_gemm_scheme(scheme: int, Xq: torch.Tensor, x_scale: torch.Tensor,
+                     s_group: Optional[torch.Tensor], Wq: torch.Tensor, w_scale: torch.Tensor,
+                     g: int, flags: int = 0, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """One scale scheme on the comparison skeleton -> Y M x N fp16.
+
+    per-channel: x_scale (M,), w_scale (N,); Runtime Smooth: x_scale (M,), s_group (K/g,),
+    w_scale (N,); sub-channel: x_scale (K/g, M), w_scale (K/g, N).
+    """
+    M, Kh = Xq.shape
+    N = Wq.shape[0]
+    K = 2 * Kh
+    G = K // g
+    xq = _dev(Xq, "Xq", torch.uint8, (M, Kh))
+    wq = _dev(Wq, "Wq", torch.uint8, (N, Kh))
+    if scheme == SCHEME_SUB_CHANNEL:
+        xs = _dev(x_scale, "x_scale", torch.float32, (G, M))
+        ws = _dev(w_scale, "w_scale", torch.float32, (G, N))
+    else:
+        xs = _dev(x_scale, "x_scale", torch.float32, (M,))
+        ws = _dev(w_scale, "w_scale", torch.float32, (N,))
+    sp = None
+    if scheme == SCHEME_RUNTIME_SMOOTH:
+        sp = _dev(s_group, "s_group", torch.float32, (G,))
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float16, device=Xq.device)
+    yp = _dev(out, "Y", torch.float16, (M, N))
+    _check(lib().rrs_w4a4_gemm_scheme(scheme, xq, xs, sp, wq, ws, M, N, K, g, flags, yp,
+                                      _stream(Xq.device)), "rrs_w4a4_gemm_scheme")
+    return out
+
+
+def w4a4_gemm_per_channel(Xq: torch.Tensor, a_scale: torch.Tensor, Wq: torch.Tensor,
+                          w_scale: torch.Tensor, flags: int = 0,
+                          out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Per-channel A4W4 on the tuned main loop: Y = fp16(a_i w_n / K * sum_j q q)."""
+    M, Kh = Xq.shape
+    N = Wq.shape[0]
+    K = 2 * Kh
+    xq = _dev(Xq, "Xq", torch.uint8, (M, Kh))
+    ap = _dev(a_scale, "a_scale", torch.float32, (M,))
+    wq = _dev(Wq, "Wq", torch.uint8, (N, Kh))
+    wp = _dev(w_scale, "w_scale", torch.float32, (N,))
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float16, device=Xq.device)
+    yp = _dev(out, "Y", torch.float16, (M, N))
+    _check(lib().rrs_w4a4_gemm_per_channel(xq, ap, wq, wp, M, N, K, flags, yp,
+                                           _stream(Xq.device)), "rrs_w4a4_gemm_per_channel")
+    return out

@@ -14,7 +14,7 @@
 
 namespace {
 
-constexpr int kVersion = 200;  // 0.2.0: ablation (_ex) entry points
+constexpr int kVersion = 300;  // 0.3.0: per-channel / sub-channel comparison baselines
 constexpr int kMaxDevices = 64;
 
 bool is_aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -238,6 +238,83 @@ rrs_status rrs_linear(const void* X, const void* Wq, const float* w_scale, int M
                       size_t workspace_bytes, void* stream) {
   return rrs_linear_ex(X, Wq, w_scale, M, N, K, group_size, perm, 0, Y, workspace,
                        workspace_bytes, stream);
+}
+
+rrs_status rrs_quantize_sub_channel(const void* X, int M, int K, int group_size, int flags,
+                                    void* Xq, float* a_sub, void* stream) {
+  if (debug_enabled())
+    std::fprintf(stderr, "[rrs] quantize_sub_channel X=%p M=%d K=%d g=%d flags=%d Xq=%p a=%p\n",
+                 X, M, K, group_size, flags, Xq, (void*)a_sub);
+  if (!X || !Xq || !a_sub) return RRS_ERR_NULL;
+  if (!valid_m(M) || !valid_k(K)) return RRS_ERR_SHAPE;
+  if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
+  if (!valid_flags(flags, RRS_SKIP_ROTATION)) return RRS_ERR_FLAGS;
+  if (!is_aligned(X) || !is_aligned(Xq) || !is_aligned(a_sub)) return RRS_ERR_ALIGN;
+  if (rrs_status s = check_device()) return s;
+  return from_hip(rrs::launch_quantize_sub_channel(
+      static_cast<const uint16_t*>(X), M, K, group_size, flags, static_cast<uint8_t*>(Xq), a_sub,
+      static_cast<hipStream_t>(stream)));
+}
+
+rrs_status rrs_prepare_weight_sub_channel(const void* W, int K, int N, int group_size,
+                                          int flags, void* Wq, float* w_sub, void* stream) {
+  if (debug_enabled())
+    std::fprintf(stderr, "[rrs] prepare_weight_sub_channel W=%p K=%d N=%d g=%d flags=%d\n", W, K,
+                 N, group_size, flags);
+  if (!W || !Wq || !w_sub) return RRS_ERR_NULL;
+  if (!valid_k(K) || !valid_n(N)) return RRS_ERR_SHAPE;
+  if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
+  if (!valid_flags(flags, RRS_SKIP_ROTATION)) return RRS_ERR_FLAGS;
+  if (!is_aligned(W) || !is_aligned(Wq) || !is_aligned(w_sub)) return RRS_ERR_ALIGN;
+  if (rrs_status s = check_device()) return s;
+  return from_hip(rrs::launch_prepare_weight_sub_channel(
+      static_cast<const uint16_t*>(W), K, N, group_size, !(flags & RRS_SKIP_ROTATION),
+      static_cast<uint8_t*>(Wq), w_sub, static_cast<hipStream_t>(stream)));
+}
+
+rrs_status rrs_w4a4_gemm_scheme(int scheme, const void* Xq, const float* x_scale,
+                                const float* s_group, const void* Wq, const float* w_scale,
+                                int M, int N, int K, int group_size, int flags, void* Y,
+                                void* stream) {
+  if (debug_enabled())
+    std::fprintf(stderr, "[rrs] w4a4_gemm_scheme %d M=%d N=%d K=%d g=%d flags=%d\n", scheme, M,
+                 N, K, group_size, flags);
+  if (scheme != RRS_SCHEME_PER_CHANNEL && scheme != RRS_SCHEME_RUNTIME_SMOOTH &&
+      scheme != RRS_SCHEME_SUB_CHANNEL)
+    return RRS_ERR_FLAGS;
+  const bool need_s = scheme == RRS_SCHEME_RUNTIME_SMOOTH;
+  if (!Xq || !x_scale || !Wq || !w_scale || !Y || (need_s && !s_group)) return RRS_ERR_NULL;
+  if (!valid_m(M) || !valid_n(N) || !valid_k(K)) return RRS_ERR_SHAPE;
+  if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
+  if (!valid_flags(flags, kAllFlags)) return RRS_ERR_FLAGS;
+  if (!is_aligned(Xq) || !is_aligned(x_scale) || (need_s && !is_aligned(s_group)) ||
+      !is_aligned(Wq) || !is_aligned(w_scale) || !is_aligned(Y))
+    return RRS_ERR_ALIGN;
+  if (rrs_status s = check_device()) return s;
+  const int internal = scheme == RRS_SCHEME_PER_CHANNEL ? 1
+                       : scheme == RRS_SCHEME_SUB_CHANNEL ? 2
+                                                          : 0;
+  return from_hip(rrs::launch_w4a4_gemm_scheme(
+      internal, static_cast<const uint8_t*>(Xq), x_scale, s_group,
+      static_cast<const uint8_t*>(Wq), w_scale, M, N, K, group_size, static_cast<uint16_t*>(Y),
+      out_scale(K, flags), static_cast<hipStream_t>(stream)));
+}
+
+rrs_status rrs_w4a4_gemm_per_channel(const void* Xq, const float* a_scale, const void* Wq,
+                                     const float* w_scale, int M, int N, int K, int flags,
+                                     void* Y, void* stream) {
+  if (debug_enabled())
+    std::fprintf(stderr, "[rrs] w4a4_gemm_per_channel M=%d N=%d K=%d flags=%d\n", M, N, K, flags);
+  if (!Xq || !a_scale || !Wq || !w_scale || !Y) return RRS_ERR_NULL;
+  if (!valid_m(M) || !valid_n(N) || !valid_k(K)) return RRS_ERR_SHAPE;
+  if (!valid_flags(flags, kAllFlags)) return RRS_ERR_FLAGS;
+  if (!is_aligned(Xq) || !is_aligned(a_scale) || !is_aligned(Wq) || !is_aligned(w_scale) ||
+      !is_aligned(Y))
+    return RRS_ERR_ALIGN;
+  if (rrs_status s = check_device()) return s;
+  return from_hip(rrs::launch_w4a4_gemm_per_channel(
+      static_cast<const uint8_t*>(Xq), a_scale, static_cast<const uint8_t*>(Wq), w_scale, M, N, K,
+      static_cast<uint16_t*>(Y), out_scale(K, flags), static_cast<hipStream_t>(stream)));
 }
 
 rrs_status rrs_w4a4_gemm_partials(const void* Xq, const void* Wq, int M, int N, int K,

@@ -153,6 +153,28 @@ __device__ __forceinline__ float block_max256(float x, float* red) {
   return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
 }
 
+// Sub-channel quantization helper. On entry each of the 256 threads of a row
+// team holds E consecutive channels [t E, t E + E) of the row, all inside one
+// group of g (E <= 64 <= g), and lm = their largest |value|. Returns the
+// largest |value| of this thread's group. `red` is 256 floats and `gm` K / g
+// floats of LDS private to the team; contains workgroup barriers, so every
+// thread of the workgroup must call it.
+__device__ __forceinline__ float row_group_max(float lm, float* red, float* gm, int t, int E,
+                                               int g, int G) {
+  red[t] = lm;
+  __syncthreads();
+  const int per = g / E;  // threads per group
+  if (t < G) {
+    float m = 0.0f;
+    for (int u = 0; u < per; ++u) m = fmaxf(m, red[t * per + u]);
+    gm[t] = m;
+  }
+  __syncthreads();
+  const float r = gm[(t * E) / g];
+  __syncthreads();  // red and gm may be rewritten for the next row
+  return r;
+}
+
 // Symmetric INT4 code of v: clamp(rint(v), -7, 7) as a 4-bit two's complement nibble.
 __device__ __forceinline__ uint32_t int4_nibble(float v) {
   const float q = fminf(fmaxf(__builtin_rintf(v), -7.0f), 7.0f);

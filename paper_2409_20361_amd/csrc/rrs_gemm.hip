@@ -100,8 +100,11 @@ __device__ __forceinline__ int acc_col(int n0, int wn, int j, int lane) {
   return n0 + wn * 64 + j * 32 + (lane & 31);
 }
 
-// GS = g / 32 MFMA k-steps per smoothing group.
-template <int GS, bool kPartials>
+// GS = g / 32 MFMA k-steps per smoothing group. kPerChannel: the per-channel
+// A4W4 baseline of the paper's kernel comparison (Section 4.5) on this same
+// main loop: no smoothing, so no per-group rescale; the int32 accumulators run
+// over all of K (|256 P| <= 256 * 49 * 16384 < 2^31) and are converted once.
+template <int GS, bool kPartials, bool kPerChannel = false>
 __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
@@ -183,7 +186,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        acc[h][j][r] = (kPartials || GS > 8) ? 0 : 0x4B400000;
+        acc[h][j][r] = (kPartials || kPerChannel || GS > 8) ? 0 : 0x4B400000;
         f[h][j][r] = 0.0f;
       }
 
@@ -200,7 +203,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
 
   // Rescale one slice of half h's accumulators: elements [q0, q0 + CONV) of 32.
   auto rescale = [&](int h, int q0, float s, int grp) {
-    if constexpr (!kPartials) {
+    if constexpr (kPerChannel) {
+      return;
+    } else if constexpr (!kPartials) {
 #pragma unroll
       for (int q = 0; q < CONV; ++q) {
         const int e = q0 + q;
@@ -258,7 +263,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
       const bool g_last = ((c0 + PH) % GS) == 0;  // chunk closes a group
       const bool tile_end = ks0 + PH == 4;
       float s_cur = 0.0f, s_prev = 0.0f;
-      if constexpr (!kPartials) {
+      if constexpr (!kPartials && !kPerChannel) {
         if (g_last) s_cur = s_group[grp];
         if (g_first) s_prev = grp > 0 ? s_group[grp - 1] : 0.0f;
       }
@@ -270,7 +275,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
       // next tile is unpacked into the other LDS stage.
 #pragma unroll
       for (int s = 0; s < PH; ++s) {
-        const bool fresh = g_first && s == 0;
+        const bool fresh = !kPerChannel && g_first && s == 0;
         acc[0][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa0[s], fb[s][0], fresh ? ((kPartials || GS > 8) ? zero : magic) : acc[0][0], 0, 0, 0);
         acc[0][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa0[s], fb[s][1], fresh ? ((kPartials || GS > 8) ? zero : magic) : acc[0][1], 0, 0, 0);
         fa1[s] = afrag(stage, 1, ks0 + s);
@@ -303,7 +308,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
       // if this chunk closed it.
 #pragma unroll
       for (int s = 0; s < PH; ++s) {
-        const bool fresh = g_first && s == 0;
+        const bool fresh = !kPerChannel && g_first && s == 0;
         acc[1][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa1[s], fb[s][0], fresh ? ((kPartials || GS > 8) ? zero : magic) : acc[1][0], 0, 0, 0);
         acc[1][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa1[s], fb[s][1], fresh ? ((kPartials || GS > 8) ? zero : magic) : acc[1][1], 0, 0, 0);
         fb[s][0] = bfrag(nstage, 0, nks0 + s);
@@ -314,8 +319,14 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
       }
     }
   }
-  // H1's last group.
-  {
+  if constexpr (kPerChannel) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) f[h][j][r] = (float)acc[h][j][r];
+  } else {  // H1's last group.
     const int G = nsteps / GS;
     const float s_last = kPartials ? 0.0f : s_group[G - 1];
 #pragma unroll
@@ -407,6 +418,20 @@ hipError_t launch_w4a4_gemm(const uint8_t* Xq, const float* a_scale, const float
                                   stream);
   return launch_main<false>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, nullptr,
                             out_scale, stream);
+}
+
+hipError_t launch_w4a4_gemm_per_channel(const uint8_t* Xq, const float* a_scale,
+                                       const uint8_t* Wq, const float* w_scale, int M, int N,
+                                       int K, uint16_t* Y, float out_scale, hipStream_t stream) {
+  if (!main_kernel_fits(K, 128))
+    return launch_w4a4_gemm_scheme(1, Xq, a_scale, nullptr, Wq, w_scale, M, N, K, K, Y,
+                                   out_scale, stream);
+  const int tm = (M + BM - 1) / BM;
+  const int tn = (N + BN - 1) / BN;
+  const int grid = 8 * ((tm * tn + 7) / 8);
+  gemm_main_kernel<4, false, true><<<grid, kThreads, 0, stream>>>(
+      Xq, a_scale, nullptr, Wq, w_scale, M, N, K, Y, nullptr, out_scale);
+  return hipGetLastError();
 }
 
 hipError_t launch_w4a4_gemm_partials(const uint8_t* Xq, const uint8_t* Wq, int M, int N,

@@ -18,6 +18,15 @@
 //
 // At the end of each smoothing group the int32 accumulators are converted
 // and added into fp32 accumulators with one FMA by s_b, then restart at 0.
+//
+// The same skeleton also runs the two baselines of the paper's kernel
+// comparison (Section 4.5, Fig. 6), so that the three scale schemes differ in
+// nothing else:
+//   per-channel A4W4: no per-group work; the int32 accumulators run over all
+//     of K (|256 P| <= 256 * 49 * 16384 < 2^31) and are converted once;
+//   sub-channel A4W4: at the end of group b every accumulator is scaled by
+//     fl(a[b][i] * w[b][n]) (scales of shape L x M and L x N, group-major),
+//     loaded at the group's first tile.
 #include "rrs_internal.h"
 
 namespace rrs {
@@ -45,7 +54,11 @@ __device__ __forceinline__ uint16_t float_to_half_bits(float x) {
   return __builtin_bit_cast(uint16_t, (_Float16)x);
 }
 
-template <bool kPartials>
+enum Scheme { kRuntimeSmooth = 0, kPerChannel = 1, kSubChannel = 2 };
+
+// kScheme kSubChannel: a_scale is L x M, w_scale is L x N (s_group unused);
+// kPerChannel: s_group unused.
+template <bool kPartials, int kScheme = kRuntimeSmooth>
 __global__ __launch_bounds__(256) void gemm_small_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
@@ -96,8 +109,26 @@ __global__ __launch_bounds__(256) void gemm_small_kernel(
   if (a_ok) ra = *reinterpret_cast<const uint4*>(gA);
   if (b_ok) rb = *reinterpret_cast<const uint4*>(gB);
 
+  // Sub-channel scales of the current group: this lane's 32 rows and 2 columns.
+  float sa[2][16], sb[2];
   for (int kt = 0; kt < nkt; ++kt) {
     const int st = kt & 1;
+    if constexpr (kScheme == kSubChannel && !kPartials) {
+      if (kt % tiles_per_group == 0) {
+        const int grp = kt / tiles_per_group;
+        const float* ag = a_scale + (size_t)grp * M;
+        const float* wg = w_scale + (size_t)grp * N;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            sa[i][r] = ag[min(row, M - 1)];
+          }
+#pragma unroll
+        for (int j = 0; j < 2; ++j) sb[j] = wg[min(n0 + wn * 64 + j * 32 + (lane & 31), N - 1)];
+      }
+    }
     *reinterpret_cast<uint4*>(&sA[st][st_off]) = unpack_lo(ra);
     *reinterpret_cast<uint4*>(&sA[st][st_off + 16]) = unpack_hi(ra);
     *reinterpret_cast<uint4*>(&sB[st][st_off]) = unpack_lo(rb);
@@ -124,6 +155,7 @@ __global__ __launch_bounds__(256) void gemm_small_kernel(
         for (int j = 0; j < 2; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[i], b[j], acc[i][j], 0, 0, 0);
     }
+    if constexpr (kScheme == kPerChannel && !kPartials) continue;
     if ((kt + 1) % tiles_per_group == 0) {
       const int grp = kt / tiles_per_group;
       if constexpr (kPartials) {
@@ -138,6 +170,14 @@ __global__ __launch_bounds__(256) void gemm_small_kernel(
               const int col = n0 + wn * 64 + j * 32 + (lane & 31);
               if (row < M && col < N) Pg[(size_t)row * N + col] = acc[i][j][r] >> 8;
             }
+      } else if constexpr (kScheme == kSubChannel) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              f[i][j][r] = __builtin_fmaf(sa[i][r] * sb[j], (float)acc[i][j][r], f[i][j][r]);
       } else {
         const float s = s_group[grp];
 #pragma unroll
@@ -157,7 +197,29 @@ __global__ __launch_bounds__(256) void gemm_small_kernel(
     }
   }
 
-  if constexpr (!kPartials) {
+  if constexpr (kScheme == kPerChannel && !kPartials) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) f[i][j][r] = (float)acc[i][j][r];
+  }
+  if constexpr (kScheme == kSubChannel && !kPartials) {
+    const float inv = out_scale;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int col = n0 + wn * 64 + j * 32 + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (row < M && col < N)
+            Y[(size_t)row * N + col] = float_to_half_bits(f[i][j][r] * inv);
+        }
+      }
+  } else if constexpr (!kPartials) {
     // 2^-8 undoes the 16x16 of the unpacked operands, 1/K the unnormalized rotation.
     const float inv = out_scale;  // 2^-8 / K (2^-8 without rotation), exact
 #pragma unroll
@@ -186,6 +248,29 @@ hipError_t launch_w4a4_gemm_small(const uint8_t* Xq, const float* a_scale, const
   dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
   gemm_small_kernel<false><<<grid, 256, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale, M, N, K,
                                                      g, Y, nullptr, out_scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_w4a4_gemm_scheme(int scheme, const uint8_t* Xq, const float* x_scale,
+                                   const float* s_group, const uint8_t* Wq, const float* w_scale,
+                                   int M, int N, int K, int g, uint16_t* Y, float out_scale,
+                                   hipStream_t stream) {
+  dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
+  switch (scheme) {
+    case kRuntimeSmooth:
+      gemm_small_kernel<false, kRuntimeSmooth><<<grid, 256, 0, stream>>>(
+          Xq, x_scale, s_group, Wq, w_scale, M, N, K, g, Y, nullptr, out_scale);
+      break;
+    case kPerChannel:
+      gemm_small_kernel<false, kPerChannel><<<grid, 256, 0, stream>>>(
+          Xq, x_scale, nullptr, Wq, w_scale, M, N, K, K, Y, nullptr, out_scale);
+      break;
+    case kSubChannel:
+      gemm_small_kernel<false, kSubChannel><<<grid, 256, 0, stream>>>(
+          Xq, x_scale, nullptr, Wq, w_scale, M, N, K, g, Y, nullptr, out_scale);
+      break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

@@ -58,6 +58,22 @@ hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
                                    const float* w_scale, int M, int N, int K, int g,
                                    uint16_t* Y, float out_scale, hipStream_t stream);
 
+// Baselines of the kernel comparison (per-channel / sub-channel A4W4).
+hipError_t launch_quantize_sub_channel(const uint16_t* X, int M, int K, int g, int flags,
+                                       uint8_t* Xq, float* a_sub, hipStream_t stream);
+hipError_t launch_prepare_weight_sub_channel(const uint16_t* W, int K, int N, int g, bool rotate,
+                                             uint8_t* Wq, float* w_sub, hipStream_t stream);
+// scheme: 0 Runtime Smooth, 1 per-channel, 2 sub-channel (internal numbering).
+hipError_t launch_w4a4_gemm_scheme(int scheme, const uint8_t* Xq, const float* x_scale,
+                                   const float* s_group, const uint8_t* Wq, const float* w_scale,
+                                   int M, int N, int K, int g, uint16_t* Y, float out_scale,
+                                   hipStream_t stream);
+
+// Per-channel A4W4 on the tuned main loop (no per-group rescale).
+hipError_t launch_w4a4_gemm_per_channel(const uint8_t* Xq, const float* a_scale,
+                                       const uint8_t* Wq, const float* w_scale, int M, int N,
+                                       int K, uint16_t* Y, float out_scale, hipStream_t stream);
+
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 }  // namespace rrs

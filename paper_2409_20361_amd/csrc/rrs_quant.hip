@@ -116,7 +116,6 @@ __global__ __launch_bounds__(Teams<K>::threads) void rot_max_kernel(
   constexpr int E = S::E;
   constexpr int RF = lds_row_floats(K);
   constexpr int kTeams = Teams<K>::n;
-  constexpr int kThreads = Teams<K>::threads;
   __shared__ float slots[slot_floats<K>()];
   float* cbuf = slots;  // reduction scratch once the rows are done
   const int tid = threadIdx.x;
@@ -251,6 +250,81 @@ __global__ __launch_bounds__(Teams<K>::threads) void quant_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Sub-channel baseline (Section 2.1, Section 4.5): every (token, group of g
+// channels) gets its own scale; no smoothing and no cross-token dependency,
+// so one launch. y = x H_K (or x), m = max_{j in group} |y_j|,
+// inv = fl(7 / m) (0 if m = 0), code = clamp(rint(fl(y * inv)), -7, 7),
+// a_sub[b * M + i] = fl(m / 7) (group-major, L x M).
+// ---------------------------------------------------------------------------
+template <int K, bool kRot>
+__global__ __launch_bounds__(Teams<K>::threads) void subchan_quant_kernel(
+    const uint16_t* __restrict__ X, int M, int g, int rows_per_wg, uint8_t* __restrict__ Xq,
+    float* __restrict__ a_sub) {
+  using S = FwhtShape<K>;
+  constexpr int E = S::E;
+  constexpr int RF = lds_row_floats(K);
+  constexpr int kTeams = Teams<K>::n;
+  __shared__ float slots[slot_floats<K>()];
+  __shared__ float red[kTeams][256];
+  __shared__ float gm[kTeams][256];
+  const int tid = threadIdx.x;
+  const int team = tid >> 8;
+  const int t = tid & (kRowThreads - 1);
+  const int G = K / g;
+  float* slot = slots + team * RF;
+  const int iters = (rows_per_wg + kTeams - 1) / kTeams;
+  const int r0 = blockIdx.x * rows_per_wg;
+  const int r1 = min(M, r0 + rows_per_wg);
+  float vn[E];
+  load_row_or_zero<K>(X, r0 + team, r1, t, vn);
+  for (int it = 0; it < iters; ++it) {
+    const int r = r0 + it * kTeams + team;
+    float v[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) v[e] = vn[e];
+    if (it + 1 < iters) load_row_or_zero<K>(X, r0 + (it + 1) * kTeams + team, r1, t, vn);
+    fwht_row<K, kRot>(v, slot, t);
+    // back to natural order: thread t takes channels [t E, t E + E)
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < E; ++e) slot[lds_pad(t + e * kRowThreads)] = v[e];
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < E; ++e) v[e] = slot[lds_pad(t * E + e)];
+    float lm = 0.0f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) lm = fmaxf(lm, fabsf(v[e]));
+    const float m = row_group_max(lm, red[team], gm[team], t, E, g, G);
+    const float inv = (m == 0.0f) ? 0.0f : __fdiv_rn(7.0f, m);
+    if (r < r1) {
+      uint32_t nib[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) nib[e] = int4_nibble(v[e] * inv);
+      store_nibbles<E>(Xq + (size_t)r * (K / 2) + (size_t)t * (E / 2), nib);
+      if ((t * E) % g == 0) a_sub[(size_t)((t * E) / g) * M + r] = __fdiv_rn(m, 7.0f);
+    }
+  }
+}
+
+int num_cus();
+inline int num_cus_sub() { return num_cus(); }
+
+template <int K>
+hipError_t launch_sub_k(const uint16_t* X, int M, int g, bool rot, uint8_t* Xq, float* a_sub,
+                        hipStream_t stream) {
+  constexpr int kTeams = Teams<K>::n;
+  int wgs = (M + kTeams - 1) / kTeams;
+  wgs = wgs < 4 * num_cus_sub() ? wgs : 4 * num_cus_sub();
+  const int rpw = (M + wgs - 1) / wgs;
+  wgs = (M + rpw - 1) / rpw;
+  if (rot)
+    subchan_quant_kernel<K, true><<<wgs, Teams<K>::threads, 0, stream>>>(X, M, g, rpw, Xq, a_sub);
+  else
+    subchan_quant_kernel<K, false><<<wgs, Teams<K>::threads, 0, stream>>>(X, M, g, rpw, Xq, a_sub);
+  return hipGetLastError();
+}
+
 int g_num_cus = 0;
 
 int num_cus() {
@@ -303,6 +377,20 @@ hipError_t launch_k(const uint16_t* X, int M, int g, const int32_t* perm, int fl
 }
 
 }  // namespace
+
+hipError_t launch_quantize_sub_channel(const uint16_t* X, int M, int K, int g, int flags,
+                                       uint8_t* Xq, float* a_sub, hipStream_t stream) {
+  const bool rot = !(flags & kSkipRotation);
+  switch (K) {
+    case 512: return launch_sub_k<512>(X, M, g, rot, Xq, a_sub, stream);
+    case 1024: return launch_sub_k<1024>(X, M, g, rot, Xq, a_sub, stream);
+    case 2048: return launch_sub_k<2048>(X, M, g, rot, Xq, a_sub, stream);
+    case 4096: return launch_sub_k<4096>(X, M, g, rot, Xq, a_sub, stream);
+    case 8192: return launch_sub_k<8192>(X, M, g, rot, Xq, a_sub, stream);
+    case 16384: return launch_sub_k<16384>(X, M, g, rot, Xq, a_sub, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
 
 int quant_partial_rows(int M) { return M < kMaxPartialRows ? M : kMaxPartialRows; }
 

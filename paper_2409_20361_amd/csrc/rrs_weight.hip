@@ -15,16 +15,20 @@
 namespace rrs {
 namespace {
 
-template <int K, bool kRot>
+// kSub: the sub-channel baseline of Section 4.5: one scale per (output
+// channel, group of g), w_scale[b * N + n] = fl(m_b / 7) (group-major, L x N);
+// no reorder.
+template <int K, bool kRot, bool kSub = false>
 __global__ __launch_bounds__(kRowThreads) void prep_weight_kernel(
     const uint16_t* __restrict__ W, int N, const int32_t* __restrict__ perm,
-    uint8_t* __restrict__ Wq, float* __restrict__ w_scale) {
+    uint8_t* __restrict__ Wq, float* __restrict__ w_scale, int g) {
   using S = FwhtShape<K>;
   constexpr int E = S::E;
   constexpr int C = 32768 / K;
   constexpr int kCol = lds_row_floats(K);
   __shared__ float lds[C * kCol];
-  __shared__ float red[4];
+  __shared__ float red[kSub ? 256 : 4];
+  __shared__ float gm[kSub ? 256 : 1];
   const int t = threadIdx.x;
   const int n0 = blockIdx.x * C;
 
@@ -53,31 +57,57 @@ __global__ __launch_bounds__(kRowThreads) void prep_weight_kernel(
     float lm = 0.0f;
 #pragma unroll
     for (int e = 0; e < E; ++e) lm = fmaxf(lm, fabsf(v[e]));
-    const float b = block_max256(lm, red);  // contains barriers
+    float b = 0.0f;
+    if constexpr (!kSub) b = block_max256(lm, red);  // contains barriers
 #pragma unroll
     for (int e = 0; e < E; ++e) col[lds_pad(t + e * kRowThreads)] = v[e];
     __syncthreads();
 #pragma unroll
     for (int e = 0; e < E; ++e) v[e] = col[lds_pad(src[e])];
+    if constexpr (kSub) {
+      // this thread's channels [t E, t E + E) lie in one group
+      lm = 0.0f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) lm = fmaxf(lm, fabsf(v[e]));
+      b = row_group_max(lm, red, gm, t, E, g, K / g);
+    }
     const float winv = (b == 0.0f) ? 0.0f : __fdiv_rn(7.0f, b);
     uint32_t nib[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) nib[e] = int4_nibble(v[e] * winv);
     store_nibbles<E>(Wq + (size_t)n * (K / 2) + (size_t)t * (E / 2), nib);
-    if (t == 0) w_scale[n] = __fdiv_rn(b, 7.0f);
+    if constexpr (kSub) {
+      if ((t * E) % g == 0) w_scale[(size_t)((t * E) / g) * N + n] = __fdiv_rn(b, 7.0f);
+    } else {
+      if (t == 0) w_scale[n] = __fdiv_rn(b, 7.0f);
+    }
   }
 }
 
 template <int K>
 hipError_t launch_k(const uint16_t* W, int N, const int32_t* perm, bool rotate, uint8_t* Wq,
-                    float* w_scale, hipStream_t stream) {
+                    float* w_scale, int g_sub, hipStream_t stream) {
   constexpr int C = 32768 / K;
   const int grid = (N + C - 1) / C;
-  if (rotate)
-    prep_weight_kernel<K, true><<<grid, kRowThreads, 0, stream>>>(W, N, perm, Wq, w_scale);
-  else
-    prep_weight_kernel<K, false><<<grid, kRowThreads, 0, stream>>>(W, N, perm, Wq, w_scale);
+  if (g_sub > 0) {
+    if (rotate)
+      prep_weight_kernel<K, true, true><<<grid, kRowThreads, 0, stream>>>(W, N, nullptr, Wq,
+                                                                          w_scale, g_sub);
+    else
+      prep_weight_kernel<K, false, true><<<grid, kRowThreads, 0, stream>>>(W, N, nullptr, Wq,
+                                                                           w_scale, g_sub);
+  } else if (rotate) {
+    prep_weight_kernel<K, true><<<grid, kRowThreads, 0, stream>>>(W, N, perm, Wq, w_scale, 0);
+  } else {
+    prep_weight_kernel<K, false><<<grid, kRowThreads, 0, stream>>>(W, N, perm, Wq, w_scale, 0);
+  }
   return hipGetLastError();
+}
+
+template <int K>
+hipError_t launch_k(const uint16_t* W, int N, const int32_t* perm, bool rotate, uint8_t* Wq,
+                    float* w_scale, hipStream_t stream) {
+  return launch_k<K>(W, N, perm, rotate, Wq, w_scale, 0, stream);
 }
 
 }  // namespace
@@ -91,6 +121,19 @@ hipError_t launch_prepare_weight(const uint16_t* W, int K, int N, const int32_t*
     case 4096: return launch_k<4096>(W, N, perm, rotate, Wq, w_scale, stream);
     case 8192: return launch_k<8192>(W, N, perm, rotate, Wq, w_scale, stream);
     case 16384: return launch_k<16384>(W, N, perm, rotate, Wq, w_scale, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_prepare_weight_sub_channel(const uint16_t* W, int K, int N, int g, bool rotate,
+                                             uint8_t* Wq, float* w_sub, hipStream_t stream) {
+  switch (K) {
+    case 512: return launch_k<512>(W, N, nullptr, rotate, Wq, w_sub, g, stream);
+    case 1024: return launch_k<1024>(W, N, nullptr, rotate, Wq, w_sub, g, stream);
+    case 2048: return launch_k<2048>(W, N, nullptr, rotate, Wq, w_sub, g, stream);
+    case 4096: return launch_k<4096>(W, N, nullptr, rotate, Wq, w_sub, g, stream);
+    case 8192: return launch_k<8192>(W, N, nullptr, rotate, Wq, w_sub, g, stream);
+    case 16384: return launch_k<16384>(W, N, nullptr, rotate, Wq, w_sub, g, stream);
     default: return hipErrorInvalidValue;
   }
 }

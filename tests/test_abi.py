@@ -260,3 +260,78 @@ def test_no_device():
         assert _gemm_ex(flags=f) == NODEV
         assert _lin_ex(flags=f) == NODEV
     assert _prep_ex(flags=1) == NODEV
+
+
+# ------------------------------------------- kernel-comparison baselines (Section 4.5)
+
+def _squant(**kw):
+    a = dict(X=P, M=16, K=512, g=128, flags=0, Xq=P, a=P)
+    a.update(kw)
+    return rrs.lib().rrs_quantize_sub_channel(a["X"], a["M"], a["K"], a["g"], a["flags"],
+                                              a["Xq"], a["a"], None)
+
+
+def _sprep(**kw):
+    a = dict(W=P, K=512, N=512, g=128, flags=0, Wq=P, w=P)
+    a.update(kw)
+    return rrs.lib().rrs_prepare_weight_sub_channel(a["W"], a["K"], a["N"], a["g"], a["flags"],
+                                                    a["Wq"], a["w"], None)
+
+
+def _scheme(**kw):
+    a = dict(scheme=rrs.SCHEME_SUB_CHANNEL, Xq=P, x=P, s=None, Wq=P, w=P, M=16, N=512, K=512,
+             g=128, flags=0, Y=P)
+    a.update(kw)
+    return rrs.lib().rrs_w4a4_gemm_scheme(a["scheme"], a["Xq"], a["x"], a["s"], a["Wq"], a["w"],
+                                          a["M"], a["N"], a["K"], a["g"], a["flags"], a["Y"],
+                                          None)
+
+
+@pytest.mark.parametrize("fn,key", [
+    (_squant, "X"), (_squant, "Xq"), (_squant, "a"),
+    (_sprep, "W"), (_sprep, "Wq"), (_sprep, "w"),
+    (_scheme, "Xq"), (_scheme, "x"), (_scheme, "Wq"), (_scheme, "w"), (_scheme, "Y"),
+])
+def test_baseline_null_pointers(fn, key):
+    assert fn(**{key: None}) == NULL
+
+
+def test_baseline_scheme_checks():
+    # s_group is needed only by the Runtime Smooth scheme
+    assert _scheme(scheme=rrs.SCHEME_RUNTIME_SMOOTH, s=None) == NULL
+    assert _scheme(scheme=rrs.SCHEME_RUNTIME_SMOOTH, s=MIS) == ALIGN
+    assert _scheme(scheme=7) == FLAGS
+    assert _scheme(scheme=-1) == FLAGS
+    assert _scheme(flags=4) == FLAGS
+    assert _scheme(N=20) == SHAPE
+    assert _scheme(K=768) == SHAPE
+    assert _scheme(g=96) == GROUP
+    assert _scheme(x=MIS) == ALIGN
+    assert _squant(flags=rrs.SKIP_SMOOTHING) == FLAGS   # only the rotation switch applies
+    assert _squant(M=0) == SHAPE
+    assert _squant(g=1024) == GROUP
+    assert _squant(a=MIS) == ALIGN
+    assert _sprep(flags=rrs.SKIP_SMOOTHING) == FLAGS
+    assert _sprep(N=8) == SHAPE
+    assert _sprep(g=32) == GROUP
+    assert _sprep(Wq=MIS) == ALIGN
+
+
+def _pc(**kw):
+    a = dict(Xq=P, a=P, Wq=P, w=P, M=16, N=512, K=512, flags=0, Y=P)
+    a.update(kw)
+    return rrs.lib().rrs_w4a4_gemm_per_channel(a["Xq"], a["a"], a["Wq"], a["w"], a["M"], a["N"],
+                                               a["K"], a["flags"], a["Y"], None)
+
+
+@pytest.mark.parametrize("key", ["Xq", "a", "Wq", "w", "Y"])
+def test_per_channel_null(key):
+    assert _pc(**{key: None}) == NULL
+
+
+def test_per_channel_checks():
+    assert _pc(M=0) == SHAPE
+    assert _pc(N=24) == SHAPE
+    assert _pc(K=1000) == SHAPE
+    assert _pc(flags=8) == FLAGS
+    assert _pc(Y=MIS) == ALIGN

@@ -462,3 +462,85 @@ def test_fwht_fp32_canonical_stage_order():
     rev = scalar_fwht([1 << i for i in reversed(range(6))])
     assert not np.array_equal(fwd, rev)
     np.testing.assert_array_equal(O.fwht(x[None, :], "fp32")[0], fwd)
+
+
+# ---------------------------------------------------------------- efficiency baselines
+# (per-channel and sub-channel A4W4 of Section 4.5, Fig. 6)
+
+def _rtn_row_fp32(row, qmax=7):
+    """Textbook symmetric RTN of one block in binary32 scalar steps."""
+    m = np.float32(0)
+    for x in row:
+        m = max(m, np.float32(abs(np.float32(x))))
+    inv = np.float32(0) if m == 0 else np.float32(np.float32(qmax) / m)
+    codes = [int(np.clip(np.rint(np.float32(np.float32(x) * inv)), -qmax, qmax)) for x in row]
+    return m, codes
+
+
+def test_sub_channel_brute_force_tiny():
+    rng = np.random.default_rng(3)
+    X = (rng.standard_normal((3, 16)) * 4).astype(np.float16)
+    X[1, 5] = 0  # exercise a zero code
+    X[2, 8:12] = 0  # an all-zero group: scale 0, codes 0
+    q = O.sub_channel_quant(X, 4, rotate=False)
+    for i in range(3):
+        for b in range(4):
+            m, codes = _rtn_row_fp32(X[i, 4 * b:4 * b + 4])
+            assert q.m[i, b] == m
+            assert q.scale[i, b] == np.float32(m / np.float32(7))
+            assert list(q.q[i, 4 * b:4 * b + 4]) == codes
+
+
+def test_sub_channel_one_group_is_per_token_rtn():
+    # g = K leaves one group per row: the same codes and scales as per-token
+    # quantization without smoothing (the per-channel A4W4 activation quantizer)
+    w = synth.custom("sc", 5, 512, 16, 128, 21, n_chan=4, n_spike=2)
+    X = synth.activations(w)
+    sub = O.sub_channel_quant(X, 512)
+    per = O.rotate_smooth_quant(X, 128, smooth=False)
+    np.testing.assert_array_equal(sub.q, per.q)
+    np.testing.assert_array_equal(sub.scale[:, 0], per.alpha)
+
+
+def test_sub_channel_block_extremes_and_reconstruction():
+    w = synth.custom("sc", 7, 1024, 16, 64, 22, n_chan=10, n_spike=5)
+    q = O.sub_channel_quant(synth.activations(w), 64)
+    blocks = q.q.reshape(7, 16, 64).astype(np.int32)
+    assert np.abs(blocks).max() <= 7
+    ymax = np.abs(q.y.reshape(7, 16, 64)).argmax(axis=2)
+    hit = np.take_along_axis(np.abs(blocks), ymax[:, :, None], axis=2)[:, :, 0]
+    assert np.all(hit[q.m > 0] == 7)
+    recon = blocks * q.scale[:, :, None].astype(np.float64)
+    err = np.abs(recon - q.y.reshape(7, 16, 64).astype(np.float64))
+    assert np.all(err <= q.scale[:, :, None] * (0.5 + 1e-5) + 1e-30)
+
+
+def test_sub_channel_weight_matches_columns():
+    # weights are quantized per output channel and group: column n of W is
+    # sub-channel quantized like a token row of its transpose
+    rng = np.random.default_rng(9)
+    W = (rng.standard_normal((256, 6)) * 0.02).astype(np.float16)
+    wq = O.sub_channel_weight(W, 64)
+    ref = O.sub_channel_quant(np.ascontiguousarray(W.T), 64)
+    np.testing.assert_array_equal(wq.q, ref.q)
+    np.testing.assert_array_equal(wq.scale, ref.scale)
+    assert wq.packed.shape == (6, 128)
+
+
+def test_output_sub_channel_brute_force_and_reduction():
+    rng = np.random.default_rng(4)
+    M, N, G = 3, 5, 4
+    P = rng.integers(-3000, 3000, size=(G, M, N))
+    a = rng.uniform(0.1, 2, (M, G)).astype(np.float32)
+    b = rng.uniform(0.1, 2, (N, G)).astype(np.float32)
+    Y = O.output_sub_channel(P, a, b, norm=8)
+    for i in range(M):
+        for n in range(N):
+            ref = sum(float(a[i, k]) * float(b[n, k]) * int(P[k, i, n]) for k in range(G)) / 8
+            assert Y[i, n] == np.float32(ref)
+    # equal scales across groups: the per-channel output with s = 1
+    alpha = rng.uniform(0.1, 2, M).astype(np.float32)
+    beta = rng.uniform(0.1, 2, N).astype(np.float32)
+    Ysub = O.output_sub_channel(P, np.repeat(alpha[:, None], G, 1), np.repeat(beta[:, None], G, 1), 8)
+    Yper = O.output(P, np.ones(G, np.float32), alpha, beta, 8)
+    np.testing.assert_array_equal(Ysub, Yper)
