@@ -320,6 +320,61 @@ def linear(X: np.ndarray, W: np.ndarray, g: int, perm: Optional[np.ndarray] = No
 
 
 # --------------------------------------------------------------------------
+# Runtime channel reorder (Fig. 4 step (1), Section 3.2)
+# --------------------------------------------------------------------------
+#
+# Fig. 4 step (1) reorders the channels by their channel-wise maxima before
+# the grouping, so that channels of similar size share a smoothing scale.
+# Taken at run time the order comes from this call's maxima c_j (Eq. 1, over
+# the rotated activations of Section 3.3). Readings: channels move in blocks
+# of `block` consecutive channels (block = 1 is a sort of single channels);
+# a block's key is its largest c_j; keys are sorted largest first and equal
+# keys keep increasing block index. The weight rows move with their channels,
+# which leaves every product x_j w_j, and so the layer, unchanged up to the
+# new grouping.
+
+def runtime_block_order(c: np.ndarray, block: int) -> np.ndarray:
+    """Block order of Fig. 4 step (1): position p takes block order[p]."""
+    K = c.shape[0]
+    if block < 1 or K % block:
+        raise ValueError("block must divide K")
+    nb = K // block
+    key = c.reshape(nb, block).max(axis=1)
+    return np.array(sorted(range(nb), key=lambda B: (-key[B], B)), dtype=np.int64)
+
+
+def block_order_to_perm(order: np.ndarray, block: int) -> np.ndarray:
+    """Channel permutation of a block order: position j takes channel perm[j]."""
+    order = np.asarray(order, dtype=np.int64)
+    return (order[:, None] * block + np.arange(block)[None, :]).reshape(-1)
+
+
+def rotate_smooth_quant_reorder(X: np.ndarray, g: int, block: int = 32, mode: str = "fp32",
+                                rotate: bool = True):
+    """Rotate, reorder by this call's channel maxima, smooth and quantize.
+
+    Returns (ActQuant, order, perm); the ActQuant holds the reordered
+    activations, as rotate_smooth_quant with that perm.
+    """
+    dt = _dt(mode)
+    y = fwht(X, mode) if rotate else np.array(X, dtype=dt)
+    order = runtime_block_order(channel_max(y), block)
+    perm = block_order_to_perm(order, block)
+    return rotate_smooth_quant(X, g, perm, mode, rotate), order, perm
+
+
+def linear_reorder(X: np.ndarray, W: np.ndarray, g: int, block: int = 32, mode: str = "fp32",
+                   rotate: bool = True):
+    """RRS linear layer with the runtime reorder: returns (Y, act, wq, P, order)."""
+    K = X.shape[1]
+    act, order, perm = rotate_smooth_quant_reorder(X, g, block, mode, rotate)
+    wq = prepare_weight(W, perm, mode, rotate)
+    P = group_partials(act.q, wq.q, g)
+    Y = output(P, act.s, act.alpha, wq.beta, norm=K if rotate else 1)
+    return Y, act, wq, P, order
+
+
+# --------------------------------------------------------------------------
 # Baselines of the kernel-efficiency comparison (Section 4.5, Fig. 6)
 # --------------------------------------------------------------------------
 #

@@ -544,3 +544,163 @@ def test_output_sub_channel_brute_force_and_reduction():
     Ysub = O.output_sub_channel(P, np.repeat(alpha[:, None], G, 1), np.repeat(beta[:, None], G, 1), 8)
     Yper = O.output(P, np.ones(G, np.float32), alpha, beta, 8)
     np.testing.assert_array_equal(Ysub, Yper)
+
+
+# ---------------------------------------------------------------- runtime reorder
+
+def test_reorder_golden():
+    gold = _load("reorder_worked.json")
+    for case in gold["cases"]:
+        X = np.array(case["X"], dtype=np.float16)
+        g, block, rot = case["g"], case["block"], case["rotate"]
+        act, order, perm = O.rotate_smooth_quant_reorder(X, g, block, rotate=rot)
+        np.testing.assert_array_equal(order, case["order"])
+        if "perm" in case:
+            np.testing.assert_array_equal(perm, case["perm"])
+        if "y" in case:
+            np.testing.assert_array_equal(act.y, np.array(case["y"], np.float32))
+        np.testing.assert_array_equal(act.s, np.array(case["s"], np.float32))
+        np.testing.assert_array_equal(act.q, np.array(case["codes_x"], np.int8))
+        num, den = case["alpha_fraction"]
+        assert np.all(act.alpha == np.float32(num) / np.float32(den))
+        if "W" in case:
+            W = np.array(case["W"], dtype=np.float16)
+            Y, act2, wq, P, order2 = O.linear_reorder(X, W, g, block, rotate=rot)
+            np.testing.assert_array_equal(order2, case["order"])
+            np.testing.assert_array_equal(wq.q, np.array(case["codes_w"], np.int8))
+            np.testing.assert_array_equal(P, np.array(case["P"], np.int64))
+            sP = np.array(case["sum_sP"], np.float64)
+            expect = (sP * act2.alpha.astype(np.float64)[:, None]
+                      * wq.beta.astype(np.float64)[None, :] / case["K"]).astype(np.float32)
+            np.testing.assert_array_equal(Y, expect)
+
+
+@pytest.mark.parametrize("block", [1, 32])
+def test_reorder_sorted_and_largest_first(block):
+    # After the reorder the block keys never increase along K, so the first
+    # group holds the largest channel maximum and the group scales never
+    # increase; the reordered columns are the original ones moved.
+    w = synth.custom("r", 64, 1024, 8, 128, 31, n_chan=12, chan_factor=(5, 60), n_spike=3)
+    X = synth.activations(w)
+    act, order, perm = O.rotate_smooth_quant_reorder(X, 128, block)
+    y = O.fwht(X)
+    c = O.channel_max(y)
+    np.testing.assert_array_equal(np.sort(perm), np.arange(1024))
+    np.testing.assert_array_equal(act.y, y[:, perm])
+    keys = act.c.reshape(-1, block).max(axis=1)
+    assert np.all(np.diff(keys) <= 0)
+    assert act.s[0] == c.max()
+    assert np.all(np.diff(act.s) <= 0)
+
+
+def test_reorder_sum_of_scales_is_minimal_brute_force():
+    # Cutting the sorted blocks into consecutive groups minimises the sum of
+    # the group maxima over every assignment of blocks to positions: checked
+    # against all 8! orders of a tiny case (no rotation, 16 channels in blocks
+    # of 2, groups of g = 4 channels = 2 blocks, so 4 groups).
+    import itertools
+    rng = np.random.default_rng(5)
+    X = rng.uniform(-4, 4, size=(3, 16)).astype(np.float16)
+    block, g = 2, 4
+    act, order, perm = O.rotate_smooth_quant_reorder(X, g, block, rotate=False)
+    c = O.channel_max(np.array(X, np.float32))
+    keys = c.reshape(8, 2).max(axis=1)
+    best = min(sum(max(keys[p[2 * b]], keys[p[2 * b + 1]]) for b in range(4))
+               for p in itertools.permutations(range(8)))
+    assert float(act.s.sum()) == pytest.approx(float(best), rel=0, abs=0)
+
+
+def test_reorder_ties_keep_index_order():
+    # Zero input: every key is 0, so the order is the identity. Duplicated
+    # blocks (no rotation): equal keys stay in increasing block index.
+    X = np.zeros((4, 512), np.float16)
+    _, order, _ = O.rotate_smooth_quant_reorder(X, 128, 32)
+    np.testing.assert_array_equal(order, np.arange(16))
+    rng = np.random.default_rng(9)
+    base = rng.uniform(-1, 1, size=(5, 32)).astype(np.float16)
+    scale = np.array([1, 3, 1, 2, 3, 1, 2, 2, 1, 3, 3, 1, 2, 1, 2, 3], np.float16)
+    X = np.concatenate([base * s for s in scale], axis=1)
+    _, order, _ = O.rotate_smooth_quant_reorder(X, 128, 32, rotate=False)
+    expect = sorted(range(16), key=lambda B: (-float(scale[B]), B))
+    np.testing.assert_array_equal(order, expect)
+
+
+def test_reorder_invariant_to_input_block_order():
+    # Without rotation, moving X's column blocks around gives the same sorted
+    # operand: codes and scales are identical, only the reported order moves.
+    rng = np.random.default_rng(2)
+    # block B scaled by 1.25^B: keys far apart, so no two are equal
+    X = (rng.normal(0, 1, size=(32, 1024))
+         * np.repeat(1.25 ** rng.permutation(32), 32)[None, :]).astype(np.float16)
+    Q = rng.permutation(32)
+    Xq = X[:, O.block_order_to_perm(Q, 32)]
+    a0, o0, _ = O.rotate_smooth_quant_reorder(X, 128, 32, rotate=False)
+    a1, o1, _ = O.rotate_smooth_quant_reorder(Xq, 128, 32, rotate=False)
+    keys = O.channel_max(np.array(X, np.float32)).reshape(32, 32).max(axis=1)
+    assert len(np.unique(keys)) == 32  # distinct keys: the sorted operand is unique
+    np.testing.assert_array_equal(a1.q, a0.q)
+    np.testing.assert_array_equal(a1.s, a0.s)
+    np.testing.assert_array_equal(a1.alpha, a0.alpha)
+    np.testing.assert_array_equal(Q[o1], o0)
+
+
+def test_reorder_one_group_changes_nothing():
+    # With one group over all of K the grouping cannot change: the output is
+    # bit-identical to the layer without reorder (the integer sum is the same
+    # set of products).
+    w = synth.custom("o", 16, 512, 24, 512, 43, n_chan=6, n_spike=2)
+    X, W = synth.activations(w), synth.weights(w)
+    Y0, *_ = O.linear(X, W, 512)
+    Y1, *_ = O.linear_reorder(X, W, 512, 32)
+    np.testing.assert_array_equal(Y1, Y0)
+
+
+def test_reorder_block_equal_to_group_moves_whole_groups():
+    # Blocks as large as a group move whole groups: the same scales, the same
+    # partials, summed in another order.
+    w = synth.custom("q", 16, 1024, 24, 128, 44, n_chan=6, n_spike=2)
+    X, W = synth.activations(w), synth.weights(w)
+    Y0, a0, _, P0 = O.linear(X, W, 128)
+    Y1, a1, _, P1, order = O.linear_reorder(X, W, 128, 128)
+    np.testing.assert_array_equal(a1.s, a0.s[order])
+    np.testing.assert_array_equal(P1, P0[order])
+    np.testing.assert_allclose(Y1, Y0, rtol=1e-6, atol=0)
+
+
+def test_reorder_weight_rows_move_with_channels():
+    # Per-output-channel weight scales do not depend on the row order, so the
+    # reordered weight codes are the unreordered codes with rows moved: the
+    # GEMM may gather rows of weights prepared once, without the reorder.
+    w = synth.custom("w", 4, 1024, 40, 128, 45)
+    W = synth.weights(w)
+    perm = O.block_order_to_perm(np.random.default_rng(3).permutation(32), 32)
+    w0 = O.prepare_weight(W)
+    w1 = O.prepare_weight(W, perm)
+    np.testing.assert_array_equal(w1.q, w0.q[perm])
+    np.testing.assert_array_equal(w1.beta, w0.beta)
+
+
+def test_reorder_groups_outlier_channels_together():
+    # What Fig. 4 step (1) is for: outlier channels scattered over every group
+    # inflate every group's scale; after the reorder they share one group and
+    # the other channels keep small scales, which lowers the error of
+    # Runtime Smooth (no rotation) on this channel-outlier input.
+    rng = np.random.default_rng(7)
+    M, K, N, g = 64, 512, 32, 128
+    X = rng.normal(0, 1, size=(M, K))
+    X[:, [5, 133, 261, 389]] *= 80.0  # one outlier channel in each group
+    X = X.astype(np.float16)
+    W = rng.normal(0, 1, size=(K, N))
+    W[[5, 133, 261, 389], :] /= 80.0  # outliers do not dominate the product
+    W = W.astype(np.float16)
+    ref = O.fp64_reference(X, W)
+
+    def err(Y):
+        return float(np.linalg.norm(Y - ref) / np.linalg.norm(ref))
+
+    act = O.rotate_smooth_quant(X, g, rotate=False)
+    wq = O.prepare_weight(W, rotate=False)
+    Y0 = O.output(O.group_partials(act.q, wq.q, g), act.s, act.alpha, wq.beta, 1)
+    Y1, act1, *_ = O.linear_reorder(X, W, g, 1, rotate=False)
+    assert act1.s[1] < act.s.min() / 10
+    assert err(Y1) < 0.7 * err(Y0), (err(Y1), err(Y0))
