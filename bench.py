@@ -60,6 +60,10 @@ def parse():
     ap.add_argument("--decode-only", action="store_true",
                     help="only the decode measurement (for per-kernel profiles)")
     ap.add_argument("--decode-steps", type=int, default=100)
+    ap.add_argument("--no-reorder", action="store_true",
+                    help="skip the runtime-reorder comparison")
+    ap.add_argument("--reorder-only", action="store_true",
+                    help="only the runtime-reorder comparison")
     ap.add_argument("--no-schemes", action="store_true",
                     help="skip the per-channel / Runtime Smooth / sub-channel kernel comparison")
     ap.add_argument("--schemes-only", action="store_true",
@@ -240,6 +244,65 @@ def scheme_bench(torch, rrs, reps=30):
             "group_size": g, "rows": rows}
 
 
+def reorder_bench(torch, rrs, synth, reps=50):
+    """Runtime channel reorder (Fig. 4 step (1) at run time) against the same
+    layer without it, at the prefill (qkv) and decode shapes: quantizer,
+    GEMM and the whole layer, each timed alone with HIP events. The decode
+    GEMMs cycle through 4 weight copies, as in decode_bench."""
+    dev = torch.device("cuda:0")
+    out = {"block": rrs.REORDER_BLOCK}
+    for name in ("qkv", "decode"):
+        w = synth.WORKLOADS[name]
+        log(f"reorder: {name} M={w.M} K={w.K} N={w.N}")
+        X = torch.from_numpy(synth.activations(w)).to(dev)
+        Wq0, beta = rrs.prepare_weight(torch.from_numpy(synth.weights(w)).to(dev))
+        copies = [Wq0] + ([Wq0.clone() for _ in range(3)] if name == "decode" else [])
+        nc = len(copies)
+        Xq = torch.empty((w.M, w.K // 2), dtype=torch.uint8, device=dev)
+        a = torch.empty((w.M,), dtype=torch.float32, device=dev)
+        s = torch.empty((w.G,), dtype=torch.float32, device=dev)
+        Xq2, a2, s2 = torch.empty_like(Xq), torch.empty_like(a), torch.empty_like(s)
+        bo = torch.empty((w.K // rrs.REORDER_BLOCK,), dtype=torch.int32, device=dev)
+        Y = torch.empty((w.M, w.N), dtype=torch.float16, device=dev)
+        qws = torch.empty((rrs.workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8, device=dev)
+        rws = torch.empty((rrs.reorder_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
+                          device=dev)
+        lws = torch.empty((rrs.linear_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
+                          device=dev)
+        lrws = torch.empty((rrs.linear_reorder_workspace_bytes(w.M, w.K, w.g),),
+                           dtype=torch.uint8, device=dev)
+        rrs.rotate_smooth_quant(X, w.g, workspace=qws, out=(Xq, a, s))
+        rrs.rotate_smooth_quant_reorder(X, w.g, workspace=rws, out=(Xq2, a2, s2, bo))
+        calls = {
+            "quant": lambda i: rrs.rotate_smooth_quant(X, w.g, workspace=qws, out=(Xq, a, s)),
+            "quant_reorder": lambda i: rrs.rotate_smooth_quant_reorder(
+                X, w.g, workspace=rws, out=(Xq2, a2, s2, bo)),
+            "gemm": lambda i: rrs.w4a4_gemm(Xq, a, s, copies[i % nc], beta, w.g, out=Y),
+            "gemm_reorder": lambda i: rrs.w4a4_gemm_reorder(Xq2, a2, s2, copies[i % nc], beta,
+                                                            bo, w.g, out=Y),
+            "linear": lambda i: rrs.linear(X, copies[i % nc], beta, w.g, workspace=lws, out=Y),
+            "linear_reorder": lambda i: rrs.linear_reorder(X, copies[i % nc], beta, w.g,
+                                                           workspace=lrws, out=Y),
+        }
+        row = {"M": w.M, "K": w.K, "N": w.N, "group_size": w.g}
+        for key, fn in calls.items():
+            it = iter(range(1 << 30))
+            prewarm(torch, lambda: fn(next(it)), seconds=0.2)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for i in range(reps):
+                fn(i)
+            e1.record()
+            torch.cuda.synchronize()
+            row[key + "_us"] = round(e0.elapsed_time(e1) * 1e3 / reps, 2)
+        for key in ("quant", "gemm", "linear"):
+            row[key + "_overhead"] = round(row[key + "_reorder_us"] / row[key + "_us"] - 1.0, 4)
+        out[name] = row
+        del X, Wq0, copies
+    return out
+
+
 def cpu_baseline(synth):
     """The CPU oracle as it stands, on a bounded sample of the same workload."""
     import numpy as np
@@ -296,6 +359,10 @@ def main():
         print(json.dumps({"metric": METRIC, "scheme_comparison": scheme_bench(torch, rrs)}),
               flush=True)
         return
+    if args.reorder_only:
+        print(json.dumps({"metric": METRIC, "reorder": reorder_bench(torch, rrs, synth)}),
+              flush=True)
+        return
     if args.decode_only:
         print(json.dumps({"metric": METRIC, "decode": decode_bench(args, torch, rrs, synth)}),
               flush=True)
@@ -337,6 +404,8 @@ def main():
     }
     if not args.no_decode:
         out["decode"] = decode_bench(args, torch, rrs, synth)
+    if not args.no_reorder:
+        out["reorder"] = reorder_bench(torch, rrs, synth)
     if not args.no_schemes:
         log("kernel comparison of the scale schemes")
         out["scheme_comparison"] = scheme_bench(torch, rrs)

@@ -270,6 +270,78 @@ rrs_status rrs_w4a4_gemm_per_channel(const void* Xq, const float* a_scale, const
                                      const float* w_scale, int M, int N, int K, int flags,
                                      void* Y, void* stream);
 
+/*
+ * ------------------------------------------------------------------------
+ * Runtime channel reorder (Fig. 4 step (1) taken at run time, Section 3.2):
+ * before the grouping, the rotated channels are sorted by this call's
+ * channel-wise maxima c_j = max_i |y_ij| (Eq. 1), so that channels of similar
+ * size share a smoothing scale. Channels move in blocks of 32 consecutive
+ * channels (RRS_REORDER_BLOCK): a block's key is its largest c_j, keys are
+ * sorted largest first, equal keys keep increasing block index, and group b
+ * takes the sorted blocks [b g/32, (b+1) g/32). The weights are prepared once
+ * in natural order (rrs_prepare_weight with perm = NULL); the GEMM fetches
+ * the weight block that belongs to each position.
+ * ------------------------------------------------------------------------
+ */
+enum { RRS_REORDER_BLOCK = 32 };
+
+/*
+ * Bytes of device workspace rrs_rotate_smooth_quant_reorder needs (0 for
+ * invalid arguments). It holds up to 256 rows of K/32 block maxima, the
+ * sorted group maxima and the channel permutation.
+ */
+size_t rrs_reorder_workspace_bytes(int M, int K, int group_size);
+
+/*
+ * rrs_rotate_smooth_quant with the runtime reorder:
+ *   X in            : M x K float16.
+ *   Xq out          : M x K/2 bytes; position j of a row holds rotated channel
+ *                     32 block_order[j / 32] + j % 32.
+ *   a_scale out     : M float32; s_group out: K/g float32, over the reordered
+ *                     positions (so s_group never increases with b).
+ *   block_order out : K/32 int32, a permutation of 0..K/32-1.
+ *   workspace       : at least rrs_reorder_workspace_bytes(M, K, g) bytes.
+ * flags: RRS_SKIP_ROTATION (reorder the unrotated channels: Runtime Smooth
+ * with its reorder step); RRS_SKIP_SMOOTHING -> RRS_ERR_FLAGS (without
+ * smoothing the order changes nothing). Three launches.
+ */
+rrs_status rrs_rotate_smooth_quant_reorder(const void* X, int M, int K, int group_size,
+                                           int flags, void* Xq, float* a_scale,
+                                           float* s_group, int32_t* block_order,
+                                           void* workspace, size_t workspace_bytes,
+                                           void* stream);
+
+/*
+ * rrs_w4a4_gemm whose position block p of Xq (channels [32 p, 32 p + 32))
+ * pairs with block block_order[p] of every Wq row:
+ *   Y[i, n] = fp16( alpha_i beta_n / norm * sum_b s_b sum_{j in group b}
+ *                   q_x[i, j] q_w[32 block_order[j / 32] + j % 32, n] ),
+ * norm = K (1 with RRS_SKIP_ROTATION). Wq, w_scale from rrs_prepare_weight
+ * without perm; Xq, a_scale, s_group, block_order from
+ * rrs_rotate_smooth_quant_reorder. block_order is read on the device and each
+ * entry is reduced modulo K/32 (loads stay in bounds for any table; a table
+ * that is not a permutation gives meaningless results). flags: only
+ * RRS_SKIP_ROTATION. Other errors as rrs_w4a4_gemm_ex.
+ */
+rrs_status rrs_w4a4_gemm_reorder(const void* Xq, const float* a_scale, const float* s_group,
+                                 const void* Wq, const float* w_scale,
+                                 const int32_t* block_order, int M, int N, int K,
+                                 int group_size, int flags, void* Y, void* stream);
+
+/* Workspace of rrs_linear_reorder: the quantizer's workspace plus Xq,
+ * a_scale, s_group and block_order (0 for invalid arguments). */
+size_t rrs_linear_reorder_workspace_bytes(int M, int K, int group_size);
+
+/*
+ * One RRS linear layer with the runtime reorder:
+ * rrs_rotate_smooth_quant_reorder followed by rrs_w4a4_gemm_reorder, the
+ * intermediates kept in the workspace. W prepared by rrs_prepare_weight
+ * (perm = NULL, same RRS_SKIP_ROTATION bit). Errors as the two calls.
+ */
+rrs_status rrs_linear_reorder(const void* X, const void* Wq, const float* w_scale, int M,
+                              int N, int K, int group_size, int flags, void* Y, void* workspace,
+                              size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -13,6 +13,7 @@ INT4 inference" (arXiv 2409.20361), Sections 3.1-3.3.
 from __future__ import annotations
 
 from ._binding import (  # noqa: F401
+    REORDER_BLOCK,
     SCHEME_PER_CHANNEL,
     SCHEME_RUNTIME_SMOOTH,
     SCHEME_SUB_CHANNEL,
@@ -22,24 +23,31 @@ from ._binding import (  # noqa: F401
     lib,
     lib_path,
     linear,
+    linear_reorder,
+    linear_reorder_workspace_bytes,
     linear_workspace_bytes,
     prepare_weight,
     prepare_weight_sub_channel,
     quantize_sub_channel,
     rotate_smooth_quant,
+    rotate_smooth_quant_reorder,
+    reorder_workspace_bytes,
     status_string,
     version,
     w4a4_gemm,
     w4a4_gemm_partials,
     w4a4_gemm_per_channel,
+    w4a4_gemm_reorder,
     w4a4_gemm_scheme,
     workspace_bytes,
 )
 
 __all__ = [
-    "SCHEME_PER_CHANNEL", "SCHEME_RUNTIME_SMOOTH", "SCHEME_SUB_CHANNEL", "SKIP_ROTATION",
-    "SKIP_SMOOTHING", "RRSError", "lib", "lib_path", "linear", "linear_workspace_bytes",
+    "REORDER_BLOCK", "SCHEME_PER_CHANNEL", "SCHEME_RUNTIME_SMOOTH", "SCHEME_SUB_CHANNEL",
+    "SKIP_ROTATION", "SKIP_SMOOTHING", "RRSError", "lib", "lib_path", "linear", "linear_reorder",
+    "linear_reorder_workspace_bytes", "linear_workspace_bytes",
     "prepare_weight", "prepare_weight_sub_channel", "quantize_sub_channel",
-    "rotate_smooth_quant", "status_string", "version", "w4a4_gemm", "w4a4_gemm_partials",
-    "w4a4_gemm_per_channel", "w4a4_gemm_scheme", "workspace_bytes",
+    "reorder_workspace_bytes", "rotate_smooth_quant", "rotate_smooth_quant_reorder",
+    "status_string", "version", "w4a4_gemm", "w4a4_gemm_partials",
+    "w4a4_gemm_per_channel", "w4a4_gemm_reorder", "w4a4_gemm_scheme", "workspace_bytes",
 ]

@@ -39,7 +39,19 @@ _SIGNATURES = {
                                   [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp]),
     "rrs_w4a4_gemm_scheme": (ctypes.c_int32,
                              [_i, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp]),
+    "rrs_reorder_workspace_bytes": (_sz, [_i, _i, _i]),
+    "rrs_linear_reorder_workspace_bytes": (_sz, [_i, _i, _i]),
+    "rrs_rotate_smooth_quant_reorder": (ctypes.c_int32,
+                                        [_vp, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _sz,
+                                         _vp]),
+    "rrs_w4a4_gemm_reorder": (ctypes.c_int32,
+                              [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp]),
+    "rrs_linear_reorder": (ctypes.c_int32,
+                           [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp, _sz, _vp]),
 }
+
+# Channels per block of the runtime reorder (include/rrs.h, RRS_REORDER_BLOCK).
+REORDER_BLOCK = 32
 
 # Scale schemes of the kernel comparison (include/rrs.h, RRS_SCHEME_*).
 SCHEME_PER_CHANNEL = 0
@@ -279,3 +291,71 @@ def w4a4_gemm_per_channel(Xq: torch.Tensor, a_scale: torch.Tensor, Wq: torch.Ten
     _check(lib().rrs_w4a4_gemm_per_channel(xq, ap, wq, wp, M, N, K, flags, yp,
                                            _stream(Xq.device)), "rrs_w4a4_gemm_per_channel")
     return out
+
+
+def reorder_workspace_bytes(M: int, K: int, g: int) -> int:
+    return lib().rrs_reorder_workspace_bytes(M, K, g)
+
+
+def linear_reorder_workspace_bytes(M: int, K: int, g: int) -> int:
+    return lib().rrs_linear_reorder_workspace_bytes(M, K, g)
+
+
+def rotate_smooth_quant_reorder(X: torch.Tensor, g: int, workspace: Optional[torch.Tensor] = None,
+                                out=None, flags: int = 0):
+    """Runtime reorder variant: X M x K fp16 -> (Xq, a_scale, s_group, block_order K/32 int32)."""
+    M, K = X.shape
+    xp = _dev(X, "X", torch.float16, (M, K))
+    if out is None:
+        Xq = torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
+        a = torch.empty((M,), dtype=torch.float32, device=X.device)
+        s = torch.empty((max(K // g, 1),), dtype=torch.float32, device=X.device)
+        order = torch.empty((max(K // REORDER_BLOCK, 1),), dtype=torch.int32, device=X.device)
+    else:
+        Xq, a, s, order = out
+    nbytes = reorder_workspace_bytes(M, K, g)
+    if workspace is None:
+        workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=X.device)
+    _check(lib().rrs_rotate_smooth_quant_reorder(
+        xp, M, K, g, flags, Xq.data_ptr(), a.data_ptr(), s.data_ptr(), order.data_ptr(),
+        workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(X.device)),
+        "rrs_rotate_smooth_quant_reorder")
+    return Xq, a, s, order
+
+
+def w4a4_gemm_reorder(Xq: torch.Tensor, a_scale: torch.Tensor, s_group: torch.Tensor,
+                      Wq: torch.Tensor, w_scale: torch.Tensor, block_order: torch.Tensor, g: int,
+                      out: Optional[torch.Tensor] = None, flags: int = 0) -> torch.Tensor:
+    """GEMM pairing position block p of Xq with block block_order[p] of every Wq row."""
+    M, Kh = Xq.shape
+    K = 2 * Kh
+    N = Wq.shape[0]
+    args = (_dev(Xq, "Xq", torch.uint8, (M, Kh)), _dev(a_scale, "a_scale", torch.float32, (M,)),
+            _dev(s_group, "s_group", torch.float32, (K // g,)),
+            _dev(Wq, "Wq", torch.uint8, (N, Kh)), _dev(w_scale, "w_scale", torch.float32, (N,)),
+            _dev(block_order, "block_order", torch.int32, (K // REORDER_BLOCK,)))
+    Y = out if out is not None else torch.empty((M, N), dtype=torch.float16, device=Xq.device)
+    yp = _dev(Y, "Y", torch.float16, (M, N))
+    _check(lib().rrs_w4a4_gemm_reorder(*args, M, N, K, g, flags, yp, _stream(Xq.device)),
+           "rrs_w4a4_gemm_reorder")
+    return Y
+
+
+def linear_reorder(X: torch.Tensor, Wq: torch.Tensor, w_scale: torch.Tensor, g: int,
+                   workspace: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                   flags: int = 0) -> torch.Tensor:
+    """One RRS linear layer with the runtime reorder: X M x K fp16 -> Y M x N fp16."""
+    M, K = X.shape
+    N = Wq.shape[0]
+    xp = _dev(X, "X", torch.float16, (M, K))
+    wqp = _dev(Wq, "Wq", torch.uint8, (N, K // 2))
+    wsp = _dev(w_scale, "w_scale", torch.float32, (N,))
+    nbytes = linear_reorder_workspace_bytes(M, K, g)
+    if workspace is None:
+        workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=X.device)
+    Y = out if out is not None else torch.empty((M, N), dtype=torch.float16, device=X.device)
+    yp = _dev(Y, "Y", torch.float16, (M, N))
+    _check(lib().rrs_linear_reorder(xp, wqp, wsp, M, N, K, g, flags, yp, workspace.data_ptr(),
+                                    workspace.numel() * workspace.element_size(),
+                                    _stream(X.device)), "rrs_linear_reorder")
+    return Y

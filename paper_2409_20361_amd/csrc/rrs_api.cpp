@@ -14,7 +14,7 @@
 
 namespace {
 
-constexpr int kVersion = 300;  // 0.3.0: per-channel / sub-channel comparison baselines
+constexpr int kVersion = 400;  // 0.4.0: runtime channel reorder
 constexpr int kMaxDevices = 64;
 
 bool is_aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -77,6 +77,14 @@ rrs_status from_hip(hipError_t e) { return e == hipSuccess ? RRS_OK : RRS_ERR_HI
 size_t linear_ws_bytes(int M, int K, int g) {
   return rrs::quant_workspace_bytes(M, K) + rrs::align256((size_t)M * (K / 2)) +
          rrs::align256((size_t)M * 4) + rrs::align256((size_t)(K / g) * 4);
+}
+
+static_assert(RRS_REORDER_BLOCK == rrs::kReorderBlock, "public and internal block sizes agree");
+
+size_t linear_reorder_ws_bytes(int M, int K, int g) {
+  return rrs::reorder_workspace_bytes(K) + rrs::align256((size_t)M * (K / 2)) +
+         rrs::align256((size_t)M * 4) + rrs::align256((size_t)(K / g) * 4) +
+         rrs::align256((size_t)(K / RRS_REORDER_BLOCK) * 4);
 }
 
 }  // namespace
@@ -315,6 +323,102 @@ rrs_status rrs_w4a4_gemm_per_channel(const void* Xq, const float* a_scale, const
   return from_hip(rrs::launch_w4a4_gemm_per_channel(
       static_cast<const uint8_t*>(Xq), a_scale, static_cast<const uint8_t*>(Wq), w_scale, M, N, K,
       static_cast<uint16_t*>(Y), out_scale(K, flags), static_cast<hipStream_t>(stream)));
+}
+
+size_t rrs_reorder_workspace_bytes(int M, int K, int group_size) {
+  if (!valid_m(M) || !valid_k(K) || !valid_group(K, group_size)) return 0;
+  return rrs::reorder_workspace_bytes(K);
+}
+
+size_t rrs_linear_reorder_workspace_bytes(int M, int K, int group_size) {
+  if (!valid_m(M) || !valid_k(K) || !valid_group(K, group_size)) return 0;
+  return linear_reorder_ws_bytes(M, K, group_size);
+}
+
+rrs_status rrs_rotate_smooth_quant_reorder(const void* X, int M, int K, int group_size,
+                                           int flags, void* Xq, float* a_scale,
+                                           float* s_group, int32_t* block_order,
+                                           void* workspace, size_t workspace_bytes,
+                                           void* stream) {
+  if (debug_enabled())
+    std::fprintf(stderr,
+                 "[rrs] rotate_smooth_quant_reorder X=%p M=%d K=%d g=%d flags=%d Xq=%p a=%p "
+                 "s=%p order=%p ws=%p (%zu B)\n",
+                 X, M, K, group_size, flags, Xq, (void*)a_scale, (void*)s_group,
+                 (void*)block_order, workspace, workspace_bytes);
+  if (!X || !Xq || !a_scale || !s_group || !block_order || !workspace) return RRS_ERR_NULL;
+  if (!valid_m(M) || !valid_k(K)) return RRS_ERR_SHAPE;
+  if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
+  if (!valid_flags(flags, RRS_SKIP_ROTATION)) return RRS_ERR_FLAGS;
+  if (!is_aligned(X) || !is_aligned(Xq) || !is_aligned(a_scale) || !is_aligned(s_group) ||
+      !is_aligned(block_order) || !is_aligned(workspace))
+    return RRS_ERR_ALIGN;
+  if (workspace_bytes < rrs::reorder_workspace_bytes(K)) return RRS_ERR_WORKSPACE;
+  if (rrs_status s = check_device()) return s;
+  return from_hip(rrs::launch_rotate_smooth_quant_reorder(
+      static_cast<const uint16_t*>(X), M, K, group_size, flags, static_cast<uint8_t*>(Xq),
+      a_scale, s_group, block_order, workspace, static_cast<hipStream_t>(stream)));
+}
+
+rrs_status rrs_w4a4_gemm_reorder(const void* Xq, const float* a_scale, const float* s_group,
+                                 const void* Wq, const float* w_scale,
+                                 const int32_t* block_order, int M, int N, int K,
+                                 int group_size, int flags, void* Y, void* stream) {
+  if (debug_enabled())
+    std::fprintf(stderr, "[rrs] w4a4_gemm_reorder M=%d N=%d K=%d g=%d flags=%d order=%p\n", M,
+                 N, K, group_size, flags, (const void*)block_order);
+  if (!Xq || !a_scale || !s_group || !Wq || !w_scale || !block_order || !Y) return RRS_ERR_NULL;
+  if (!valid_m(M) || !valid_n(N) || !valid_k(K)) return RRS_ERR_SHAPE;
+  if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
+  if (!valid_flags(flags, RRS_SKIP_ROTATION)) return RRS_ERR_FLAGS;
+  if (!is_aligned(Xq) || !is_aligned(a_scale) || !is_aligned(s_group) || !is_aligned(Wq) ||
+      !is_aligned(w_scale) || !is_aligned(block_order) || !is_aligned(Y))
+    return RRS_ERR_ALIGN;
+  if (rrs_status s = check_device()) return s;
+  return from_hip(rrs::launch_w4a4_gemm_reorder(
+      static_cast<const uint8_t*>(Xq), a_scale, s_group, static_cast<const uint8_t*>(Wq),
+      w_scale, block_order, M, N, K, group_size, static_cast<uint16_t*>(Y), out_scale(K, flags),
+      static_cast<hipStream_t>(stream)));
+}
+
+rrs_status rrs_linear_reorder(const void* X, const void* Wq, const float* w_scale, int M,
+                              int N, int K, int group_size, int flags, void* Y, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  if (debug_enabled())
+    std::fprintf(stderr,
+                 "[rrs] linear_reorder X=%p Wq=%p w=%p M=%d N=%d K=%d g=%d flags=%d Y=%p ws=%p "
+                 "(%zu B)\n",
+                 X, Wq, (const void*)w_scale, M, N, K, group_size, flags, Y, workspace,
+                 workspace_bytes);
+  if (!X || !Wq || !w_scale || !Y || !workspace) return RRS_ERR_NULL;
+  if (!valid_m(M) || !valid_n(N) || !valid_k(K)) return RRS_ERR_SHAPE;
+  if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
+  if (!valid_flags(flags, RRS_SKIP_ROTATION)) return RRS_ERR_FLAGS;
+  if (!is_aligned(X) || !is_aligned(Wq) || !is_aligned(w_scale) || !is_aligned(Y) ||
+      !is_aligned(workspace))
+    return RRS_ERR_ALIGN;
+  if (workspace_bytes < linear_reorder_ws_bytes(M, K, group_size)) return RRS_ERR_WORKSPACE;
+  if (rrs_status s = check_device()) return s;
+
+  char* ws = static_cast<char*>(workspace);
+  void* qws = ws;
+  ws += rrs::reorder_workspace_bytes(K);
+  uint8_t* xq = reinterpret_cast<uint8_t*>(ws);
+  ws += rrs::align256((size_t)M * (K / 2));
+  float* a = reinterpret_cast<float*>(ws);
+  ws += rrs::align256((size_t)M * 4);
+  float* s = reinterpret_cast<float*>(ws);
+  ws += rrs::align256((size_t)(K / group_size) * 4);
+  int32_t* order = reinterpret_cast<int32_t*>(ws);
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = rrs::launch_rotate_smooth_quant_reorder(
+      static_cast<const uint16_t*>(X), M, K, group_size, flags, xq, a, s, order, qws, st);
+  if (e != hipSuccess) return RRS_ERR_HIP;
+  return from_hip(rrs::launch_w4a4_gemm_reorder(xq, a, s, static_cast<const uint8_t*>(Wq),
+                                                w_scale, order, M, N, K, group_size,
+                                                static_cast<uint16_t*>(Y), out_scale(K, flags),
+                                                st));
 }
 
 rrs_status rrs_w4a4_gemm_partials(const void* Xq, const void* Wq, int M, int N, int K,

@@ -104,14 +104,18 @@ __device__ __forceinline__ int acc_col(int n0, int wn, int j, int lane) {
 // A4W4 baseline of the paper's kernel comparison (Section 4.5) on this same
 // main loop: no smoothing, so no per-group rescale; the int32 accumulators run
 // over all of K (|256 P| <= 256 * 49 * 16384 < 2^31) and are converted once.
-template <int GS, bool kPartials, bool kPerChannel = false>
+// kGather (runtime channel reorder): position block p (32 channels, 16 bytes
+// of a packed row) of Xq pairs with block border[p] of every Wq row; the
+// table is kept in LDS and each B slot reads its entry one tile ahead.
+template <int GS, bool kPartials, bool kPerChannel = false, bool kGather = false>
 __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
     const float* __restrict__ w_scale, int M, int N, int K, uint16_t* __restrict__ Y,
-    int32_t* __restrict__ P, float out_scale) {
+    int32_t* __restrict__ P, float out_scale, const int32_t* __restrict__ border) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[2 * STAGE];
   __shared__ float scale_tab[BM + BN];  // alpha of the tile's rows, then beta of its columns
+  __shared__ int btab[kGather ? 16384 / kReorderBlock : 1];
 
   const TileMap tile = map_tile(M, N);
   if (!tile.valid) return;
@@ -133,7 +137,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
   const int brow = t >> 2;
   const int bq = t & 3;
   const uint8_t* ga = Xq + (size_t)min(m0 + arow, M - 1) * krow + ahalf * 32;
-  const uint8_t* gb = Wq + (size_t)min(n0 + brow, N - 1) * krow + bq * 16;
+  const uint8_t* gb = Wq + (size_t)min(n0 + brow, N - 1) * krow + (kGather ? 0 : bq * 16);
   const int a_st = arow * ROWP + ahalf * 64;
   const int b_st = A_BYTES + brow * ROWP + bq * 32;
 
@@ -145,11 +149,18 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
 
   // Packed tiles in flight: two register sets, tile kt lives in set kt & 1.
   uint4 ra0[2], ra1[2], rb0[2];
-  auto gload = [&](int set, int kt) {
+  // Byte offset in the Wq row of this thread's B slot of tile kt.
+  auto boff = [&](int kt) -> uint32_t {
+    if constexpr (kGather)
+      return (uint32_t)btab[kt * 4 + bq] * 16u;
+    else
+      return (uint32_t)kt * (BK / 2);
+  };
+  auto gload = [&](int set, int kt, uint32_t bo) {
     const uint4* p = reinterpret_cast<const uint4*>(ga + (size_t)kt * (BK / 2));
     ra0[set] = p[0];
     ra1[set] = p[1];
-    rb0[set] = *reinterpret_cast<const uint4*>(gb + (size_t)kt * (BK / 2));
+    rb0[set] = *reinterpret_cast<const uint4*>(gb + bo);
   };
   auto lstore = [&](int set, int stage) {
     uint8_t* s = lds + stage * STAGE;
@@ -239,12 +250,19 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
     else if (t < BM + BN)
       scale_tab[t] = w_scale[min(n0 + t - BM, N - 1)];
   }
-  gload(0, 0);
+  if constexpr (kGather) {
+    // Entries are masked into range, so any table keeps every load in bounds.
+    for (int i = t; i < K / kReorderBlock; i += kThreads)
+      btab[i] = border[i] & (K / kReorderBlock - 1);
+    __syncthreads();
+  }
+  gload(0, 0, boff(0));
   lstore(0, 0);
-  gload(1, min(1, ntiles - 1));
-  gload(0, min(2, ntiles - 1));
+  gload(1, min(1, ntiles - 1), boff(min(1, ntiles - 1)));
+  gload(0, min(2, ntiles - 1), boff(min(2, ntiles - 1)));
   __syncthreads();
   v4i fb[PH][2], fa0[PH], fa1[PH];
+  uint32_t bnext = 0;  // gather only
 #pragma unroll
   for (int s = 0; s < PH; ++s) {
     fb[s][0] = bfrag(0, 0, s);
@@ -286,6 +304,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
           const int kt = j0 >> 2;
 #pragma unroll
           for (int i = s * 6 / PH; i < (s + 1) * 6 / PH; ++i) lpiece((kt + 1) & 1, stage ^ 1, i);
+          // Gather: the B offset of the tile fetched after the barrier below,
+          // read here so that the barrier's wait covers the LDS read.
+          if (s == PH - 1) bnext = boff(min(kt + 3, ntiles - 1));
         }
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -296,8 +317,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
       // this stages a duplicate that is never read.)
       if (tile_end) {
         const int kt = j0 >> 2;
+        const int kn = min(kt + 3, ntiles - 1);
         __syncthreads();
-        gload((kt + 1) & 1, min(kt + 3, ntiles - 1));
+        gload((kt + 1) & 1, kn, kGather ? bnext : boff(kn));
       }
       const int nstage = tile_end ? stage ^ 1 : stage;
       const int nks0 = (ks0 + PH) & 3;
@@ -375,10 +397,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
   }
 }
 
-template <bool kPartials>
+template <bool kPartials, bool kGather = false>
 hipError_t launch_main(const uint8_t* Xq, const float* a_scale, const float* s_group,
                        const uint8_t* Wq, const float* w_scale, int M, int N, int K, int g,
-                       uint16_t* Y, int32_t* P, float out_scale, hipStream_t stream) {
+                       uint16_t* Y, int32_t* P, float out_scale, hipStream_t stream,
+                       const int32_t* border = nullptr) {
   const int tm = (M + BM - 1) / BM;
   const int tn = (N + BN - 1) / BN;
   const int T = tm * tn;
@@ -386,8 +409,8 @@ hipError_t launch_main(const uint8_t* Xq, const float* a_scale, const float* s_g
   switch (g) {
 #define RRS_CASE(G_)                                                                       \
   case G_:                                                                                 \
-    gemm_main_kernel<G_ / 32, kPartials><<<grid, kThreads, 0, stream>>>(                   \
-        Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, P, out_scale);                      \
+    gemm_main_kernel<G_ / 32, kPartials, false, kGather><<<grid, kThreads, 0, stream>>>(   \
+        Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, P, out_scale, border);              \
     break;
     RRS_CASE(64)
     RRS_CASE(128)
@@ -430,8 +453,23 @@ hipError_t launch_w4a4_gemm_per_channel(const uint8_t* Xq, const float* a_scale,
   const int tn = (N + BN - 1) / BN;
   const int grid = 8 * ((tm * tn + 7) / 8);
   gemm_main_kernel<4, false, true><<<grid, kThreads, 0, stream>>>(
-      Xq, a_scale, nullptr, Wq, w_scale, M, N, K, Y, nullptr, out_scale);
+      Xq, a_scale, nullptr, Wq, w_scale, M, N, K, Y, nullptr, out_scale, nullptr);
   return hipGetLastError();
+}
+
+hipError_t launch_w4a4_gemm_reorder(const uint8_t* Xq, const float* a_scale,
+                                    const float* s_group, const uint8_t* Wq,
+                                    const float* w_scale, const int32_t* border, int M, int N,
+                                    int K, int g, uint16_t* Y, float out_scale,
+                                    hipStream_t stream) {
+  if (decode_kernel_fits(M))
+    return launch_w4a4_gemm_decode(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, out_scale,
+                                   stream, border);
+  // Every shape the ABI accepts fits the main kernel (K / 32 >= 16 is a power
+  // of two); the fallback kernel has no gather.
+  if (!main_kernel_fits(K, g)) return hipErrorInvalidValue;
+  return launch_main<false, true>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, nullptr,
+                                  out_scale, stream, border);
 }
 
 hipError_t launch_w4a4_gemm_partials(const uint8_t* Xq, const uint8_t* Wq, int M, int N,

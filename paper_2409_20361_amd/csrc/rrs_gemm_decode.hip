@@ -77,18 +77,22 @@ constexpr int kPartBytes = 4 * kBlocks * 64 * 16;
 
 // GS = g / 64 MFMA k-steps per group. kLdsA: each wave first copies its K
 // quarter of Xq into LDS (when it fits), so the token fragments are LDS reads
-// instead of vector-memory loads queued behind the weight stream.
-template <int GS, bool kLdsA>
+// instead of vector-memory loads queued behind the weight stream. kGather
+// (runtime channel reorder): position block p (32 channels, 16 bytes of a
+// packed row) of Xq pairs with block border[p] of every Wq row; the table is
+// staged in LDS before the first weight load.
+template <int GS, bool kLdsA, bool kGather = false>
 __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
     const float* __restrict__ w_scale, int M, int N, int K, uint16_t* __restrict__ Y,
-    float out_scale) {
+    float out_scale, const int32_t* __restrict__ border) {
   constexpr int g = GS * 64;
   constexpr int NW = g / 32;                  // words per lane per group and block
   constexpr int D = NW >= 16 ? 1 : (NW >= 8 ? 2 : 4);  // groups in flight
   // Token slices during the loop; the partial sums reuse the space after it.
   __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsA ? 4 * kMaxLdsA : kPartBytes];
+  __shared__ int btab[kGather ? 16384 / kReorderBlock : 1];
   v4f(*part)[kBlocks][64] = reinterpret_cast<v4f(*)[kBlocks][64]>(lds);
 
   const int t = threadIdx.x;
@@ -112,11 +116,18 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
   // output rows that are never stored. Column blocks past N load block 0 and
   // are never stored.
   const uint8_t* pa = Xq + (size_t)min(c, M - 1) * krow + q * (g / 8);
+  // Gather: row starts only; the offset inside the row comes from the table.
   const uint8_t* pb[kBlocks];
 #pragma unroll
   for (int j = 0; j < kBlocks; ++j) {
     const int n = n0 + j * kCols < N ? n0 + j * kCols : 0;
-    pb[j] = Wq + (size_t)(n + c) * krow + q * (g / 8);
+    pb[j] = Wq + (size_t)(n + c) * krow + (kGather ? 0 : q * (g / 8));
+  }
+  if constexpr (kGather) {
+    // Entries are masked into range, so any table keeps every load in bounds.
+    for (int i = t; i < K / kReorderBlock; i += kThreads)
+      btab[i] = border[i] & (K / kReorderBlock - 1);
+    __syncthreads();
   }
 
   // Wave-private LDS copy of this wave's K quarter of Xq: row r < M at
@@ -127,10 +138,36 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
 
   uint32_t wa[D][NW], wb[D][kBlocks][NW];
   auto load = [&](int d, int i) {
-    const size_t off = (size_t)min(b0 + i, G - 1) * (g / 2);
+    const int gi = min(b0 + i, G - 1);
+    const size_t off = (size_t)gi * (g / 2);
     if constexpr (!kLdsA) load_words<NW>(pa + off, wa[d]);
+    if constexpr (kGather) {
+      // This lane's g/8 bytes of group gi cover position blocks starting at
+      // gi g/32 + q g/128 (half of block gi * 2 + q / 2 when g = 64).
+      if constexpr (NW == 2) {
+        const uint32_t o = (uint32_t)btab[gi * 2 + (q >> 1)] * 16u + (q & 1) * 8u;
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) load_words<NW>(pb[j] + off, wb[d][j]);
+        for (int j = 0; j < kBlocks; ++j) load_words<2>(pb[j] + o, wb[d][j]);
+      } else {
+        uint32_t o[NW / 4];
+#pragma unroll
+        for (int cc = 0; cc < NW / 4; ++cc)
+          o[cc] = (uint32_t)btab[gi * NW + q * (NW / 4) + cc] * 16u;
+#pragma unroll
+        for (int j = 0; j < kBlocks; ++j)
+#pragma unroll
+          for (int cc = 0; cc < NW / 4; ++cc) {
+            const uint4 v = *reinterpret_cast<const uint4*>(pb[j] + o[cc]);
+            wb[d][j][4 * cc] = v.x;
+            wb[d][j][4 * cc + 1] = v.y;
+            wb[d][j][4 * cc + 2] = v.z;
+            wb[d][j][4 * cc + 3] = v.w;
+          }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < kBlocks; ++j) load_words<NW>(pb[j] + off, wb[d][j]);
+    }
   };
   // Token words from LDS, read just before use (the quarter starts at group b0;
   // padded steps past this wave's groups reread its last group).
@@ -238,17 +275,20 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
 
 bool decode_kernel_fits(int M) { return M >= 1 && M <= kCols; }
 
-hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
-                                   const float* s_group, const uint8_t* Wq,
-                                   const float* w_scale, int M, int N, int K, int g,
-                                   uint16_t* Y, float out_scale, hipStream_t stream) {
+namespace {
+
+template <bool kGather>
+hipError_t launch_decode(const uint8_t* Xq, const float* a_scale, const float* s_group,
+                         const uint8_t* Wq, const float* w_scale, int M, int N, int K, int g,
+                         uint16_t* Y, float out_scale, hipStream_t stream,
+                         const int32_t* border) {
   const int grid = (N / kCols + kBlocks - 1) / kBlocks;  // N % 16 == 0 (API precondition)
   const bool lds_a = (size_t)M * a_row_bytes(K, g) <= (size_t)kMaxLdsA;
-#define RRS_DECODE(GS_)                                                                  \
-  (lds_a ? (gemm_decode_kernel<GS_, true><<<grid, kThreads, 0, stream>>>(                 \
-               Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale), 0)             \
-         : (gemm_decode_kernel<GS_, false><<<grid, kThreads, 0, stream>>>(                \
-               Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale), 0))
+#define RRS_DECODE(GS_)                                                                      \
+  (lds_a ? (gemm_decode_kernel<GS_, true, kGather><<<grid, kThreads, 0, stream>>>(            \
+               Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale, border), 0)         \
+         : (gemm_decode_kernel<GS_, false, kGather><<<grid, kThreads, 0, stream>>>(           \
+               Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale, border), 0))
   switch (g) {
     case 64: RRS_DECODE(1); break;
     case 128: RRS_DECODE(2); break;
@@ -258,6 +298,20 @@ hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
   }
 #undef RRS_DECODE
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
+                                   const float* s_group, const uint8_t* Wq,
+                                   const float* w_scale, int M, int N, int K, int g,
+                                   uint16_t* Y, float out_scale, hipStream_t stream,
+                                   const int32_t* border) {
+  if (border)
+    return launch_decode<true>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, out_scale,
+                               stream, border);
+  return launch_decode<false>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, out_scale,
+                              stream, nullptr);
 }
 
 }  // namespace rrs

@@ -17,6 +17,10 @@ size_t quant_workspace_bytes(int M, int K);
 constexpr int kSkipRotation = 1;
 constexpr int kSkipSmoothing = 2;
 
+// Channels per block of the runtime reorder: one MFMA k-step of 32 INT4
+// codes, 16 bytes of a packed row.
+constexpr int kReorderBlock = 32;
+
 hipError_t launch_rotate_smooth_quant(const uint16_t* X, int M, int K, int g,
                                       const int32_t* perm, int flags, uint8_t* Xq,
                                       float* a_scale, float* s_group, void* workspace,
@@ -42,7 +46,8 @@ hipError_t launch_w4a4_gemm_partials(const uint8_t* Xq, const uint8_t* Wq, int M
                                      int K, int g, int32_t* P, hipStream_t stream);
 
 // Simple 128 x 128 tile kernel: the fallback for shapes the main kernel's
-// unrolling does not cover (K / 32 not a multiple of max(8, g / 16)).
+// unrolling does not cover (K / 32 not a multiple of max(8, g / 32); no shape
+// the ABI accepts today).
 hipError_t launch_w4a4_gemm_small(const uint8_t* Xq, const float* a_scale,
                                   const float* s_group, const uint8_t* Wq,
                                   const float* w_scale, int M, int N, int K, int g,
@@ -56,7 +61,8 @@ bool decode_kernel_fits(int M);
 hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
                                    const float* s_group, const uint8_t* Wq,
                                    const float* w_scale, int M, int N, int K, int g,
-                                   uint16_t* Y, float out_scale, hipStream_t stream);
+                                   uint16_t* Y, float out_scale, hipStream_t stream,
+                                   const int32_t* border = nullptr);
 
 // Baselines of the kernel comparison (per-channel / sub-channel A4W4).
 hipError_t launch_quantize_sub_channel(const uint16_t* X, int M, int K, int g, int flags,
@@ -73,6 +79,35 @@ hipError_t launch_w4a4_gemm_scheme(int scheme, const uint8_t* Xq, const float* x
 hipError_t launch_w4a4_gemm_per_channel(const uint8_t* Xq, const float* a_scale,
                                        const uint8_t* Wq, const float* w_scale, int M, int N,
                                        int K, uint16_t* Y, float out_scale, hipStream_t stream);
+
+// Runtime channel reorder (Fig. 4 step (1) at run time). Pass 1: rows of
+// K / 32 block maxima (at most block_maxima_rows() rows); pass 2: the
+// quantizer's second pass with a given permutation and one row of group
+// maxima (K / g used, max(K / 64, 64) readable).
+int block_maxima_rows();
+hipError_t launch_block_maxima(const uint16_t* X, int M, int K, bool rotate, float* part,
+                               int* nrows, hipStream_t stream);
+hipError_t launch_block_maxima_wave(const uint16_t* X, int M, int K, bool rotate, float* part,
+                                    int max_partials, int* nrows, hipStream_t stream);
+hipError_t launch_quantize_given_maxima(const uint16_t* X, int M, int K, int g,
+                                        const int32_t* perm, bool rotate, const float* gmax,
+                                        uint8_t* Xq, float* a_scale, float* s_group,
+                                        hipStream_t stream);
+hipError_t launch_quantize_given_wave(const uint16_t* X, int M, int K, int g,
+                                      const int32_t* perm, bool rotate, const float* gmax,
+                                      int max_quant_wgs, uint8_t* Xq, float* a_scale,
+                                      float* s_group, hipStream_t stream);
+size_t reorder_workspace_bytes(int K);
+hipError_t launch_rotate_smooth_quant_reorder(const uint16_t* X, int M, int K, int g, int flags,
+                                              uint8_t* Xq, float* a_scale, float* s_group,
+                                              int32_t* block_order, void* workspace,
+                                              hipStream_t stream);
+// GEMM whose Xq position block p pairs with Wq block border[p].
+hipError_t launch_w4a4_gemm_reorder(const uint8_t* Xq, const float* a_scale,
+                                    const float* s_group, const uint8_t* Wq,
+                                    const float* w_scale, const int32_t* border, int M, int N,
+                                    int K, int g, uint16_t* Y, float out_scale,
+                                    hipStream_t stream);
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 

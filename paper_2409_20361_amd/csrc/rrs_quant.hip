@@ -54,15 +54,12 @@ __device__ __forceinline__ void load_row_or_zero(const uint16_t* __restrict__ X,
 }
 
 // Per-channel maxima cm (this thread's E channels t + 256 e) of every team
-// combined in LDS, then maxima over each group of g (reordered) positions.
-// Returns, for threads tid < K / g, the maximum of group tid; 0 elsewhere.
-// Must be called by all threads of the workgroup; cbuf holds >= K floats.
+// combined into cbuf[0, K). Must be called by all threads of the workgroup;
+// cbuf holds >= K floats.
 template <int K>
-__device__ __forceinline__ float group_maxima(const float (&cm)[FwhtShape<K>::E], float* cbuf,
-                                              int g, const int32_t* __restrict__ perm) {
+__device__ __forceinline__ void combine_teams(const float (&cm)[FwhtShape<K>::E], float* cbuf) {
   constexpr int E = FwhtShape<K>::E;
   constexpr int kTeams = Teams<K>::n;
-  constexpr int kThreads = Teams<K>::threads;
   const int tid = threadIdx.x;
   const int team = tid >> 8;
   const int t = tid & (kRowThreads - 1);
@@ -80,6 +77,18 @@ __device__ __forceinline__ float group_maxima(const float (&cm)[FwhtShape<K>::E]
     }
     __syncthreads();
   }
+}
+
+// Per-channel maxima of every team combined (combine_teams), then maxima over
+// each group of g (reordered) positions. Returns, for threads tid < K / g, the
+// maximum of group tid; 0 elsewhere. Must be called by all threads of the
+// workgroup; cbuf holds >= K floats.
+template <int K>
+__device__ __forceinline__ float group_maxima(const float (&cm)[FwhtShape<K>::E], float* cbuf,
+                                              int g, const int32_t* __restrict__ perm) {
+  constexpr int kThreads = Teams<K>::threads;
+  const int tid = threadIdx.x;
+  combine_teams<K>(cm, cbuf);
   // The first NA threads cover P consecutive positions each, all inside one
   // group (P <= 64 <= g).
   constexpr int NA = K < kThreads ? K : kThreads;
@@ -108,7 +117,10 @@ __device__ __forceinline__ float group_maxima(const float (&cm)[FwhtShape<K>::E]
 // ---------------------------------------------------------------------------
 // 1. rotate + per-workgroup group maxima
 // ---------------------------------------------------------------------------
-template <int K, bool kRot>
+// kBlocks (runtime reorder): the row written holds instead the maxima of the
+// K / 32 blocks of 32 consecutive channels, in natural order (g and perm are
+// not used).
+template <int K, bool kRot, bool kBlocks = false>
 __global__ __launch_bounds__(Teams<K>::threads) void rot_max_kernel(
     const uint16_t* __restrict__ X, int M, int g, int rows_per_wg,
     const int32_t* __restrict__ perm, float* __restrict__ gpart) {
@@ -140,8 +152,19 @@ __global__ __launch_bounds__(Teams<K>::threads) void rot_max_kernel(
 #pragma unroll
     for (int e = 0; e < E; ++e) cm[e] = fmaxf(cm[e], fabsf(v[e]));
   }
-  const float s = group_maxima<K>(cm, cbuf, g, perm);
-  if (tid < K / g) gpart[(size_t)blockIdx.x * (K / g) + tid] = s;
+  if constexpr (kBlocks) {
+    combine_teams<K>(cm, cbuf);
+    float* out = gpart + (size_t)blockIdx.x * (K / 32);
+    for (int B = tid; B < K / 32; B += Teams<K>::threads) {
+      float m = 0.0f;
+      // start at a different channel per thread: fewer LDS bank conflicts
+      for (int q = 0; q < 32; ++q) m = fmaxf(m, cbuf[B * 32 + ((q + B) & 31)]);
+      out[B] = m;
+    }
+  } else {
+    const float s = group_maxima<K>(cm, cbuf, g, perm);
+    if (tid < K / g) gpart[(size_t)blockIdx.x * (K / g) + tid] = s;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -340,22 +363,26 @@ int num_cus() {
   return g_num_cus;
 }
 
+// Rows of M per workgroup for a grid of at most `cap` workgroups of kTeams
+// teams (one row per team where the cap allows); returns the grid size.
+// Pass 1 writes one partial row per workgroup: at most kMaxPartialRows of
+// them, so the reduction every pass-2 workgroup repeats stays small. Pass 2
+// has no such limit: up to 4 workgroups per CU.
+template <int K>
+int split_rows(int M, int cap, int* rows_per_wg) {
+  constexpr int kTeams = Teams<K>::n;
+  int wgs = (M + kTeams - 1) / kTeams;
+  wgs = wgs < cap ? wgs : cap;
+  *rows_per_wg = (M + wgs - 1) / wgs;
+  return (M + *rows_per_wg - 1) / *rows_per_wg;
+}
+
 template <int K>
 hipError_t launch_k(const uint16_t* X, int M, int g, const int32_t* perm, int flags, uint8_t* Xq,
                     float* a_scale, float* s_group, void* workspace, hipStream_t stream) {
-  constexpr int kTeams = Teams<K>::n;
-  // Pass 1 writes one partial row per workgroup: at most 256 of them, so the
-  // reduction every pass-2 workgroup repeats stays small. Pass 2 has no such
-  // limit: up to 4 workgroups per CU, one row per team where possible.
-  auto split = [&](int cap, int* rows_per_wg) {
-    int wgs = (M + kTeams - 1) / kTeams;
-    wgs = wgs < cap ? wgs : cap;
-    *rows_per_wg = (M + wgs - 1) / wgs;
-    return (M + *rows_per_wg - 1) / *rows_per_wg;
-  };
   int rpw1 = 0, rpw2 = 0;
-  const int wgs1 = split(kMaxPartialRows, &rpw1);
-  const int wgs2 = split(4 * num_cus(), &rpw2);
+  const int wgs1 = split_rows<K>(M, kMaxPartialRows, &rpw1);
+  const int wgs2 = split_rows<K>(M, 4 * num_cus(), &rpw2);
   float* gpart = static_cast<float*>(workspace);
   const bool rot = !(flags & kSkipRotation);
   const bool smooth = !(flags & kSkipSmoothing);
@@ -376,7 +403,76 @@ hipError_t launch_k(const uint16_t* X, int M, int g, const int32_t* perm, int fl
   return hipGetLastError();
 }
 
+// Runtime reorder, pass 1: block maxima rows (see rot_max_kernel's kBlocks).
+template <int K>
+hipError_t launch_block_max_k(const uint16_t* X, int M, bool rot, float* part, int* nrows,
+                              hipStream_t stream) {
+  int rpw = 0;
+  const int wgs = split_rows<K>(M, kMaxPartialRows, &rpw);
+  if (rot)
+    rot_max_kernel<K, true, true><<<wgs, Teams<K>::threads, 0, stream>>>(X, M, 32, rpw, nullptr,
+                                                                          part);
+  else
+    rot_max_kernel<K, false, true><<<wgs, Teams<K>::threads, 0, stream>>>(X, M, 32, rpw, nullptr,
+                                                                           part);
+  *nrows = wgs;
+  return hipGetLastError();
+}
+
+// Runtime reorder, pass 2: quant with one given row of group maxima.
+template <int K>
+hipError_t launch_given_k(const uint16_t* X, int M, int g, const int32_t* perm, bool rot,
+                          const float* gmax, uint8_t* Xq, float* a_scale, float* s_group,
+                          hipStream_t stream) {
+  int rpw = 0;
+  const int wgs = split_rows<K>(M, 4 * num_cus(), &rpw);
+  if (rot)
+    quant_kernel<K, true, true><<<wgs, Teams<K>::threads, 0, stream>>>(
+        X, M, g, rpw, 1, perm, gmax, Xq, a_scale, s_group);
+  else
+    quant_kernel<K, false, true><<<wgs, Teams<K>::threads, 0, stream>>>(
+        X, M, g, rpw, 1, perm, gmax, Xq, a_scale, s_group);
+  return hipGetLastError();
+}
+
+// One wave per row wins at K = 4096, and at K = 2048 once there are enough
+// rows; elsewhere the team kernels are faster (measured).
+bool use_wave_kernels(int M, int K) { return K == 4096 || (K == 2048 && M >= 512); }
+
 }  // namespace
+
+hipError_t launch_block_maxima(const uint16_t* X, int M, int K, bool rotate, float* part,
+                               int* nrows, hipStream_t stream) {
+  if (use_wave_kernels(M, K))
+    return launch_block_maxima_wave(X, M, K, rotate, part, kMaxPartialRows, nrows, stream);
+  switch (K) {
+    case 512: return launch_block_max_k<512>(X, M, rotate, part, nrows, stream);
+    case 1024: return launch_block_max_k<1024>(X, M, rotate, part, nrows, stream);
+    case 2048: return launch_block_max_k<2048>(X, M, rotate, part, nrows, stream);
+    case 8192: return launch_block_max_k<8192>(X, M, rotate, part, nrows, stream);
+    case 16384: return launch_block_max_k<16384>(X, M, rotate, part, nrows, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_quantize_given_maxima(const uint16_t* X, int M, int K, int g,
+                                        const int32_t* perm, bool rotate, const float* gmax,
+                                        uint8_t* Xq, float* a_scale, float* s_group,
+                                        hipStream_t stream) {
+  if (use_wave_kernels(M, K))
+    return launch_quantize_given_wave(X, M, K, g, perm, rotate, gmax, 2 * num_cus(), Xq,
+                                      a_scale, s_group, stream);
+  switch (K) {
+    case 512: return launch_given_k<512>(X, M, g, perm, rotate, gmax, Xq, a_scale, s_group, stream);
+    case 1024: return launch_given_k<1024>(X, M, g, perm, rotate, gmax, Xq, a_scale, s_group, stream);
+    case 2048: return launch_given_k<2048>(X, M, g, perm, rotate, gmax, Xq, a_scale, s_group, stream);
+    case 8192: return launch_given_k<8192>(X, M, g, perm, rotate, gmax, Xq, a_scale, s_group, stream);
+    case 16384: return launch_given_k<16384>(X, M, g, perm, rotate, gmax, Xq, a_scale, s_group, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+int block_maxima_rows() { return kMaxPartialRows; }
 
 hipError_t launch_quantize_sub_channel(const uint16_t* X, int M, int K, int g, int flags,
                                        uint8_t* Xq, float* a_sub, hipStream_t stream) {
@@ -404,9 +500,7 @@ hipError_t launch_rotate_smooth_quant(const uint16_t* X, int M, int K, int g,
                                       const int32_t* perm, int flags, uint8_t* Xq,
                                       float* a_scale, float* s_group, void* workspace,
                                       hipStream_t stream) {
-  // One wave per row wins at K = 4096, and at K = 2048 once there are enough
-  // rows; elsewhere the team kernels below are faster (measured).
-  if (K == 4096 || (K == 2048 && M >= 512))
+  if (use_wave_kernels(M, K))
     return launch_rotate_smooth_quant_wave(X, M, K, g, perm, flags, Xq, a_scale, s_group,
                                            workspace, kMaxPartialRows, 2 * num_cus(), stream);
   switch (K) {

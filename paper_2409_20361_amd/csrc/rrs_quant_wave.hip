@@ -301,23 +301,26 @@ __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
   }
 }
 
+// Rows of M per workgroup of `waves` waves, one row per wave where a grid of
+// at most `cap` workgroups allows it; returns the grid size.
+template <int K>
+int wave_split(int M, int waves, int cap, int* rows_per_wg) {
+  const int rows_wg_min = waves * WaveRow<K>::RW;
+  int wgs = (M + rows_wg_min - 1) / rows_wg_min;
+  wgs = wgs < cap ? wgs : cap;
+  *rows_per_wg = (M + wgs - 1) / wgs;
+  return (M + *rows_per_wg - 1) / *rows_per_wg;
+}
+
 template <int K>
 hipError_t launch_wave(const uint16_t* X, int M, int g, const int32_t* perm, int flags, uint8_t* Xq,
                        float* a_scale, float* s_group, void* workspace, int max_partials,
                        int max_quant_wgs, hipStream_t stream) {
-  using S = WaveRow<K>;
   // rot_max: at most max_partials workgroups (one partial row each).
-  const int rows_wg_min1 = kRotWaves * S::RW;
-  int wgs1 = (M + rows_wg_min1 - 1) / rows_wg_min1;
-  wgs1 = wgs1 < max_partials ? wgs1 : max_partials;
-  const int rpw1 = (M + wgs1 - 1) / wgs1;
-  wgs1 = (M + rpw1 - 1) / rpw1;
+  int rpw1 = 0, rpw2 = 0;
+  const int wgs1 = wave_split<K>(M, kRotWaves, max_partials, &rpw1);
   // quant: one row per wave where the grid allows it.
-  const int rows_wg_min2 = kQuantWaves * S::RW;
-  int wgs2 = (M + rows_wg_min2 - 1) / rows_wg_min2;
-  wgs2 = wgs2 < max_quant_wgs ? wgs2 : max_quant_wgs;
-  const int rpw2 = (M + wgs2 - 1) / wgs2;
-  wgs2 = (M + rpw2 - 1) / rpw2;
+  const int wgs2 = wave_split<K>(M, kQuantWaves, max_quant_wgs, &rpw2);
   float* gpart = static_cast<float*>(workspace);
   const bool rot = !(flags & kSkipRotation);
   const bool smooth = !(flags & kSkipSmoothing);
@@ -338,7 +341,65 @@ hipError_t launch_wave(const uint16_t* X, int M, int g, const int32_t* perm, int
   return hipGetLastError();
 }
 
+// Runtime reorder, pass 1: rot_max with groups of 32 natural-order channels
+// writes the K / 32 block maxima per workgroup (P = K / 512 <= 8 positions per
+// thread, 32 / P threads per block, K / 32 <= 128 blocks).
+template <int K>
+hipError_t launch_block_max_wave(const uint16_t* X, int M, bool rot, float* part,
+                                 int max_partials, int* nrows, hipStream_t stream) {
+  int rpw = 0;
+  const int wgs = wave_split<K>(M, kRotWaves, max_partials, &rpw);
+  if (rot)
+    rot_max_wave_kernel<K, true><<<wgs, kRotWaves * 64, 0, stream>>>(X, M, 32, rpw, nullptr, part);
+  else
+    rot_max_wave_kernel<K, false><<<wgs, kRotWaves * 64, 0, stream>>>(X, M, 32, rpw, nullptr,
+                                                                       part);
+  *nrows = wgs;
+  return hipGetLastError();
+}
+
+// Runtime reorder, pass 2: quant with one given row of group maxima. The
+// kernel reads K / 64 entries of that row (those past K / g are ignored).
+template <int K>
+hipError_t launch_given_wave(const uint16_t* X, int M, int g, const int32_t* perm, bool rot,
+                             const float* gmax, int max_quant_wgs, uint8_t* Xq, float* a_scale,
+                             float* s_group, hipStream_t stream) {
+  int rpw = 0;
+  const int wgs = wave_split<K>(M, kQuantWaves, max_quant_wgs, &rpw);
+  if (rot)
+    quant_wave_kernel<K, true, true><<<wgs, kQuantWaves * 64, 0, stream>>>(
+        X, M, g, rpw, 1, perm, gmax, Xq, a_scale, s_group);
+  else
+    quant_wave_kernel<K, false, true><<<wgs, kQuantWaves * 64, 0, stream>>>(
+        X, M, g, rpw, 1, perm, gmax, Xq, a_scale, s_group);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_block_maxima_wave(const uint16_t* X, int M, int K, bool rotate, float* part,
+                                    int max_partials, int* nrows, hipStream_t stream) {
+  switch (K) {
+    case 512: return launch_block_max_wave<512>(X, M, rotate, part, max_partials, nrows, stream);
+    case 1024: return launch_block_max_wave<1024>(X, M, rotate, part, max_partials, nrows, stream);
+    case 2048: return launch_block_max_wave<2048>(X, M, rotate, part, max_partials, nrows, stream);
+    case 4096: return launch_block_max_wave<4096>(X, M, rotate, part, max_partials, nrows, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_quantize_given_wave(const uint16_t* X, int M, int K, int g,
+                                      const int32_t* perm, bool rotate, const float* gmax,
+                                      int max_quant_wgs, uint8_t* Xq, float* a_scale,
+                                      float* s_group, hipStream_t stream) {
+  switch (K) {
+    case 512: return launch_given_wave<512>(X, M, g, perm, rotate, gmax, max_quant_wgs, Xq, a_scale, s_group, stream);
+    case 1024: return launch_given_wave<1024>(X, M, g, perm, rotate, gmax, max_quant_wgs, Xq, a_scale, s_group, stream);
+    case 2048: return launch_given_wave<2048>(X, M, g, perm, rotate, gmax, max_quant_wgs, Xq, a_scale, s_group, stream);
+    case 4096: return launch_given_wave<4096>(X, M, g, perm, rotate, gmax, max_quant_wgs, Xq, a_scale, s_group, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
 
 hipError_t launch_rotate_smooth_quant_wave(const uint16_t* X, int M, int K, int g,
                                            const int32_t* perm, int flags, uint8_t* Xq,

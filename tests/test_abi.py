@@ -335,3 +335,82 @@ def test_per_channel_checks():
     assert _pc(K=1000) == SHAPE
     assert _pc(flags=8) == FLAGS
     assert _pc(Y=MIS) == ALIGN
+
+
+# ------------------------------------------- runtime channel reorder (Fig. 4 step (1))
+
+def _rq(**kw):
+    a = dict(X=P, M=16, K=512, g=128, flags=0, Xq=P, a=P, s=P, order=P, ws=P, wsb=1 << 30)
+    a.update(kw)
+    return rrs.lib().rrs_rotate_smooth_quant_reorder(a["X"], a["M"], a["K"], a["g"], a["flags"],
+                                                     a["Xq"], a["a"], a["s"], a["order"],
+                                                     a["ws"], a["wsb"], None)
+
+
+def _rg(**kw):
+    a = dict(Xq=P, a=P, s=P, Wq=P, w=P, order=P, M=16, N=512, K=512, g=128, flags=0, Y=P)
+    a.update(kw)
+    return rrs.lib().rrs_w4a4_gemm_reorder(a["Xq"], a["a"], a["s"], a["Wq"], a["w"], a["order"],
+                                           a["M"], a["N"], a["K"], a["g"], a["flags"], a["Y"],
+                                           None)
+
+
+def _rl(**kw):
+    a = dict(X=P, Wq=P, w=P, M=16, N=512, K=512, g=128, flags=0, Y=P, ws=P, wsb=1 << 30)
+    a.update(kw)
+    return rrs.lib().rrs_linear_reorder(a["X"], a["Wq"], a["w"], a["M"], a["N"], a["K"], a["g"],
+                                        a["flags"], a["Y"], a["ws"], a["wsb"], None)
+
+
+def test_reorder_workspace_queries():
+    lib = rrs.lib()
+    a256 = lambda x: (x + 255) // 256 * 256  # noqa: E731
+    for M, K, g in ((16, 512, 128), (2048, 4096, 128), (8, 8192, 64), (3, 16384, 512)):
+        q = lib.rrs_reorder_workspace_bytes(M, K, g)
+        # 256 rows of K/32 block maxima, max(K/64, 64) group maxima, K permutation entries
+        assert q == a256(256 * (K // 32) * 4) + a256(4 * max(K // 64, 64)) + a256(4 * K)
+        lw = lib.rrs_linear_reorder_workspace_bytes(M, K, g)
+        assert lw == q + a256(M * K // 2) + a256(4 * M) + a256(4 * (K // g)) + a256(4 * (K // 32))
+    for bad in ((0, 512, 128), (16, 500, 128), (16, 512, 32), (16, 512, 1024)):
+        assert lib.rrs_reorder_workspace_bytes(*bad) == 0
+        assert lib.rrs_linear_reorder_workspace_bytes(*bad) == 0
+
+
+@pytest.mark.parametrize("fn,key", [
+    (_rq, "X"), (_rq, "Xq"), (_rq, "a"), (_rq, "s"), (_rq, "order"), (_rq, "ws"),
+    (_rg, "Xq"), (_rg, "a"), (_rg, "s"), (_rg, "Wq"), (_rg, "w"), (_rg, "order"), (_rg, "Y"),
+    (_rl, "X"), (_rl, "Wq"), (_rl, "w"), (_rl, "Y"), (_rl, "ws"),
+])
+def test_reorder_null_pointers(fn, key):
+    assert fn(**{key: None}) == NULL
+
+
+@pytest.mark.parametrize("fn", [_rq, _rg, _rl])
+def test_reorder_checks(fn):
+    assert fn(M=0) == SHAPE
+    assert fn(K=768) == SHAPE
+    assert fn(g=32) == GROUP
+    assert fn(g=1024) == GROUP
+    # only the rotation switch applies: without smoothing the order changes nothing
+    assert fn(flags=rrs.SKIP_SMOOTHING) == FLAGS
+    assert fn(flags=4) == FLAGS
+    key = {_rq: "Xq", _rg: "order", _rl: "Y"}[fn]
+    assert fn(**{key: MIS}) == ALIGN
+    if fn is not _rq:
+        assert fn(N=24) == SHAPE
+
+
+def test_reorder_workspace_too_small():
+    need = rrs.reorder_workspace_bytes(16, 512, 128)
+    assert _rq(wsb=need - 1) == WS
+    need_l = rrs.linear_reorder_workspace_bytes(16, 512, 128)
+    assert _rl(wsb=need_l - 1) == WS
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="reaches the device check; only meaningful "
+                    "(and only safe with fake pointers) where no GPU is visible")
+def test_reorder_no_device():
+    for f in (0, rrs.SKIP_ROTATION):
+        assert _rq(flags=f) == NODEV
+        assert _rg(flags=f) == NODEV
+        assert _rl(flags=f) == NODEV

@@ -187,7 +187,7 @@ def _partials_case(qx, qw, g, label):
 @pytest.mark.parametrize("M,K,N,g", [
     (16, 512, 512, 128), (1, 512, 16, 64), (7, 1024, 144, 256), (129, 2048, 272, 512),
     (200, 4096, 128, 128), (3, 8192, 48, 64),
-    (5, 512, 32, 512),   # K = g = 512: the 128 x 128 fallback kernel
+    (5, 512, 32, 512),   # K = g = 512: one group, a single trip of the main loop
 ])
 def test_partials_random_codes(M, K, N, g):
     rng = np.random.default_rng(M * 7 + N)
@@ -246,7 +246,7 @@ def test_linear_tiny_seeds(seed):
 @pytest.mark.parametrize("M,K,N,g", [
     (1, 512, 16, 64), (5, 1024, 48, 256), (130, 2048, 400, 512), (77, 4096, 272, 128),
     (300, 512, 1040, 64), (9, 16384, 64, 128),
-    (33, 512, 96, 512),   # K = g = 512: the 128 x 128 fallback kernel
+    (33, 512, 96, 512),   # K = g = 512: one group, a single trip of the main loop
 ])
 def test_linear_ragged(M, K, N, g):
     w = synth.custom("l", M, K, N, g, M + N + K, n_chan=max(1, K // 100),
