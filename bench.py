@@ -33,7 +33,7 @@ METRIC = "effective W4A4 TOPS at M=2048,K=4096,N=12288; HBM GB/s at M=8 decode"
 # --pmc runs (FETCH_SIZE, WRITE_SIZE) scaled by a 256 MiB copy-kernel
 # calibration (profiles/gemm_main_kernel_qkv.md), keyed by the sha1 prefix of
 # the kernel source they were measured on. Any other source reports null.
-GEMM_TRAFFIC_BYTES = {"7d0b3751debd": 158.87e6}
+GEMM_TRAFFIC_BYTES = {"ad8a469e2cca": 159.56e6}
 INT8_MFMA_PEAK_TOPS = 5000.0   # MI355X dense int8 MFMA, 5.0 POP/s
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 
@@ -388,7 +388,7 @@ def main():
                    "step": "rrs_rotate_smooth_quant + rrs_w4a4_gemm"},
         "roofline": {
             "bound": "mfma",
-            "kernel": "gemm_main_kernel<4,false> (rrs_w4a4_gemm)",
+            "kernel": "gemm_main_kernel<4,false,false,false> (rrs_w4a4_gemm)",
             "achieved": round(gemm_tops, 2),
             "peak": INT8_MFMA_PEAK_TOPS,
             "unit": "TOP/s",
