@@ -188,6 +188,54 @@ def decode_bench(args, torch, rrs, synth):
     }
 
 
+def few_token_bench(torch, rrs, synth, reps=50):
+    """Few-token layers at the decode shape (K=8192, N=28672, g=128) for
+    M = 1, 2, 4, 8, 16: quantizer, GEMM and the whole layer, each timed alone
+    with HIP events, weights cycling through 4 copies. Up to M = 4 at this K
+    the quantizer is the one-launch kernel."""
+    dev = torch.device("cuda:0")
+    base = synth.WORKLOADS["decode"]
+    W = torch.from_numpy(synth.weights(base)).to(dev)
+    Wq0, beta = rrs.prepare_weight(W)
+    del W
+    copies = [Wq0] + [Wq0.clone() for _ in range(3)]
+    rows = []
+    for M in (1, 2, 4, 8, 16):
+        w = synth.custom("d", M, base.K, base.N, base.g, 40 + M, n_chan=82, n_spike=2,
+                         spike_mag=(100, 500))
+        X = torch.from_numpy(synth.activations(w)).to(dev)
+        Xq = torch.empty((M, w.K // 2), dtype=torch.uint8, device=dev)
+        a = torch.empty((M,), dtype=torch.float32, device=dev)
+        s = torch.empty((w.G,), dtype=torch.float32, device=dev)
+        Y = torch.empty((M, w.N), dtype=torch.float16, device=dev)
+        qws = torch.empty((rrs.workspace_bytes(M, w.K, w.g),), dtype=torch.uint8, device=dev)
+        lws = torch.empty((rrs.linear_workspace_bytes(M, w.K, w.g),), dtype=torch.uint8,
+                          device=dev)
+        rrs.rotate_smooth_quant(X, w.g, workspace=qws, out=(Xq, a, s))
+        calls = {
+            "quant": lambda i: rrs.rotate_smooth_quant(X, w.g, workspace=qws, out=(Xq, a, s)),
+            "gemm": lambda i: rrs.w4a4_gemm(Xq, a, s, copies[i % 4], beta, w.g, out=Y),
+            "linear": lambda i: rrs.linear(X, copies[i % 4], beta, w.g, workspace=lws, out=Y),
+        }
+        row = {"M": M}
+        for key, fn in calls.items():
+            it = iter(range(1 << 30))
+            prewarm(torch, lambda: fn(next(it)), seconds=0.1)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for i in range(reps):
+                fn(i)
+            e1.record()
+            torch.cuda.synchronize()
+            row[key + "_us"] = round(e0.elapsed_time(e1) * 1e3 / reps, 2)
+        alg = M * w.K // 2 + 4 * M + 4 * w.G + w.N * w.K // 2 + 4 * w.N + 2 * M * w.N
+        row["linear_GBps"] = round(alg / (row["linear_us"] * 1e-6) / 1e9, 1)
+        row["gemm_GBps"] = round(alg / (row["gemm_us"] * 1e-6) / 1e9, 1)
+        rows.append(row)
+    return {"K": base.K, "N": base.N, "group_size": base.g, "weight_copies": 4, "rows": rows}
+
+
 def scheme_bench(torch, rrs, reps=30):
     """Kernel comparison of Section 4.5 (Fig. 6): per-channel, Runtime Smooth and
     sub-channel A4W4 on the shared 128 x 128 skeleton, plus the tuned Runtime Smooth
@@ -364,8 +412,8 @@ def main():
               flush=True)
         return
     if args.decode_only:
-        print(json.dumps({"metric": METRIC, "decode": decode_bench(args, torch, rrs, synth)}),
-              flush=True)
+        print(json.dumps({"metric": METRIC, "decode": decode_bench(args, torch, rrs, synth),
+                          "few_token": few_token_bench(torch, rrs, synth)}), flush=True)
         return
     w, r = qkv_step_bench(args, torch, rrs, synth)
     ops = 2.0 * w.M * w.N * w.K
@@ -404,6 +452,9 @@ def main():
     }
     if not args.no_decode:
         out["decode"] = decode_bench(args, torch, rrs, synth)
+    if not args.no_decode:
+        log("few-token layers at the decode shape")
+        out["few_token"] = few_token_bench(torch, rrs, synth)
     if not args.no_reorder:
         out["reorder"] = reorder_bench(torch, rrs, synth)
     if not args.no_schemes:

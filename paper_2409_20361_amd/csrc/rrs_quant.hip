@@ -56,10 +56,9 @@ __device__ __forceinline__ void load_row_or_zero(const uint16_t* __restrict__ X,
 // Per-channel maxima cm (this thread's E channels t + 256 e) of every team
 // combined into cbuf[0, K). Must be called by all threads of the workgroup;
 // cbuf holds >= K floats.
-template <int K>
+template <int K, int kTeams = Teams<K>::n>
 __device__ __forceinline__ void combine_teams(const float (&cm)[FwhtShape<K>::E], float* cbuf) {
   constexpr int E = FwhtShape<K>::E;
-  constexpr int kTeams = Teams<K>::n;
   const int tid = threadIdx.x;
   const int team = tid >> 8;
   const int t = tid & (kRowThreads - 1);
@@ -83,12 +82,12 @@ __device__ __forceinline__ void combine_teams(const float (&cm)[FwhtShape<K>::E]
 // each group of g (reordered) positions. Returns, for threads tid < K / g, the
 // maximum of group tid; 0 elsewhere. Must be called by all threads of the
 // workgroup; cbuf holds >= K floats.
-template <int K>
+template <int K, int kTeams = Teams<K>::n>
 __device__ __forceinline__ float group_maxima(const float (&cm)[FwhtShape<K>::E], float* cbuf,
                                               int g, const int32_t* __restrict__ perm) {
-  constexpr int kThreads = Teams<K>::threads;
+  constexpr int kThreads = kTeams * kRowThreads;
   const int tid = threadIdx.x;
-  combine_teams<K>(cm, cbuf);
+  combine_teams<K, kTeams>(cm, cbuf);
   // The first NA threads cover P consecutive positions each, all inside one
   // group (P <= 64 <= g).
   constexpr int NA = K < kThreads ? K : kThreads;
@@ -270,6 +269,135 @@ __global__ __launch_bounds__(Teams<K>::threads) void quant_kernel(
       store_nibbles<E>(Xq + (size_t)r * (K / 2) + (size_t)t * (E / 2), nib);
       if (t == 0) a_scale[r] = __fdiv_rn(a, 7.0f);
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Few tokens (M <= 16) in one launch: every workgroup rotates all M rows and
+// takes the channel maxima itself (the same values in every workgroup), so no
+// partial rows go through global memory and the second launch disappears.
+// Team `team` of workgroup w quantizes row w * kTeams + team, which it rotated
+// in iteration w of the first loop and kept in registers.
+// ---------------------------------------------------------------------------
+template <int K>
+struct FewTeams {
+  // four row teams where the registers allow it (a thread keeps three rows'
+  // worth of E values: the row in flight, its channel maxima and its own row)
+  static constexpr int n = K <= 4096 ? 4 : (K == 8192 ? 2 : 1);
+  static constexpr int threads = n * kRowThreads;
+  static constexpr int slot_floats =
+      n * lds_row_floats(K) > 1024 ? n * lds_row_floats(K) : 1024;
+};
+
+// Largest M for which the one-launch kernel beats the two launches. Every
+// workgroup rotates all M rows, ceil(M / teams) of them one after another,
+// while the two-launch path spreads the rows over workgroups but pays a second
+// launch; the crossover was measured on MI355X (events, back to back).
+constexpr int few_max_rows(int K) {
+  return K <= 2048 ? 16 : (K == 4096 ? 8 : (K == 8192 ? 4 : 2));
+}
+
+// Raw fp16 halves of this thread's E elements of row r (zeros past the last row).
+template <int E>
+__device__ __forceinline__ void load_raw_or_zero(const uint16_t* __restrict__ X, int K, int r,
+                                                 int M, int t, uint32_t (&raw)[E / 2]) {
+  if (r < M) {
+    const uint16_t* src = X + (size_t)r * K + (size_t)t * E;
+    if constexpr (E >= 8) {
+#pragma unroll
+      for (int c = 0; c < E / 8; ++c) {
+        const uint4 w = reinterpret_cast<const uint4*>(src)[c];
+        raw[4 * c] = w.x;
+        raw[4 * c + 1] = w.y;
+        raw[4 * c + 2] = w.z;
+        raw[4 * c + 3] = w.w;
+      }
+    } else if constexpr (E == 4) {
+      const uint2 w = *reinterpret_cast<const uint2*>(src);
+      raw[0] = w.x;
+      raw[1] = w.y;
+    } else {
+      raw[0] = *reinterpret_cast<const uint32_t*>(src);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < E / 2; ++i) raw[i] = 0u;
+  }
+}
+
+template <int K, bool kRot>
+__global__ __launch_bounds__(FewTeams<K>::threads) void quant_few_kernel(
+    const uint16_t* __restrict__ X, int M, int g, const int32_t* __restrict__ perm,
+    uint8_t* __restrict__ Xq, float* __restrict__ a_scale, float* __restrict__ s_group) {
+  using S = FwhtShape<K>;
+  constexpr int E = S::E;
+  constexpr int RF = lds_row_floats(K);
+  constexpr int kTeams = FewTeams<K>::n;
+  __shared__ float slots[FewTeams<K>::slot_floats];
+  __shared__ float rg[256];
+  __shared__ float red[4 * kTeams];
+  float* cbuf = slots;  // reduction scratch between the two phases
+  const int tid = threadIdx.x;
+  const int team = tid >> 8;
+  const int t = tid & (kRowThreads - 1);
+  const int G = K / g;
+  float* slot = slots + team * RF;
+  const int iters = (M + kTeams - 1) / kTeams;  // == gridDim.x
+  const int own = blockIdx.x * kTeams + team;
+
+  // 1. every row of the call: rotate, channel maxima; keep this team's own row
+  float cm[E], keep[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) cm[e] = 0.0f;
+  uint32_t raw[E / 2];  // next row, loaded while the current one is transformed
+  load_raw_or_zero<E>(X, K, team, M, t, raw);
+  for (int it = 0; it < iters; ++it) {
+    float v[E];
+#pragma unroll
+    for (int i = 0; i < E / 2; ++i) {
+      v[2 * i] = half_to_float(raw[i] & 0xFFFFu);
+      v[2 * i + 1] = half_to_float(raw[i] >> 16);
+    }
+    if (it + 1 < iters) load_raw_or_zero<E>(X, K, (it + 1) * kTeams + team, M, t, raw);
+    fwht_row<K, kRot>(v, slot, t);  // v[e] = y[t + 256 e]
+#pragma unroll
+    for (int e = 0; e < E; ++e) cm[e] = fmaxf(cm[e], fabsf(v[e]));
+    if (it == (int)blockIdx.x) {  // uniform across the workgroup
+#pragma unroll
+      for (int e = 0; e < E; ++e) keep[e] = v[e];
+    }
+  }
+  const float smax = group_maxima<K, kTeams>(cm, cbuf, g, perm);
+  if (tid < G) {
+    rg[tid] = (smax == 0.0f) ? 0.0f : __fdiv_rn(1.0f, smax);
+    if (blockIdx.x == 0) s_group[tid] = smax;
+  }
+  __syncthreads();
+
+  // 2. this team's own row, exactly as the second pass of the two-launch path
+  const float rb = rg[(t * E) / g];  // this thread's positions lie in one group
+#pragma unroll
+  for (int e = 0; e < E; ++e) slot[lds_pad(t + e * kRowThreads)] = keep[e];
+  __syncthreads();
+  float v[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) v[e] = slot[lds_pad(perm ? perm[t * E + e] : t * E + e)];
+  float lm = 0.0f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) lm = fmaxf(lm, fabsf(v[e]));
+  lm = wave_max(lm * rb);  // fl(M_ib * r_b), max over the wave
+  if ((tid & 63) == 0) red[tid >> 6] = lm;
+  __syncthreads();
+  const float a = fmaxf(fmaxf(red[team * 4], red[team * 4 + 1]),
+                        fmaxf(red[team * 4 + 2], red[team * 4 + 3]));  // 4 waves per team
+  const float inv = (a == 0.0f) ? 0.0f : __fdiv_rn(7.0f, a);
+  const float m = rb * inv;  // fl(r_b * inv_i)
+  if (own < M) {
+    uint32_t nib[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) nib[e] = int4_nibble(v[e] * m);
+    store_nibbles<E>(Xq + (size_t)own * (K / 2) + (size_t)t * (E / 2), nib);
+    if (t == 0) a_scale[own] = __fdiv_rn(a, 7.0f);
   }
 }
 
@@ -496,10 +624,41 @@ size_t quant_workspace_bytes(int M, int K) {
   return align256((size_t)kMaxPartialRows * (K / 64) * 4);
 }
 
+namespace {
+
+template <int K>
+hipError_t launch_few_k(const uint16_t* X, int M, int g, const int32_t* perm, bool rot,
+                        uint8_t* Xq, float* a_scale, float* s_group, hipStream_t stream) {
+  const int grid = (M + FewTeams<K>::n - 1) / FewTeams<K>::n;
+  if (rot)
+    quant_few_kernel<K, true><<<grid, FewTeams<K>::threads, 0, stream>>>(X, M, g, perm, Xq,
+                                                                         a_scale, s_group);
+  else
+    quant_few_kernel<K, false><<<grid, FewTeams<K>::threads, 0, stream>>>(X, M, g, perm, Xq,
+                                                                          a_scale, s_group);
+  return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_rotate_smooth_quant(const uint16_t* X, int M, int K, int g,
                                       const int32_t* perm, int flags, uint8_t* Xq,
                                       float* a_scale, float* s_group, void* workspace,
                                       hipStream_t stream) {
+  // Few tokens with smoothing: one launch (each workgroup takes the channel
+  // maxima of all rows itself).
+  if (M <= few_max_rows(K) && !(flags & kSkipSmoothing)) {
+    const bool rot = !(flags & kSkipRotation);
+    switch (K) {
+      case 512: return launch_few_k<512>(X, M, g, perm, rot, Xq, a_scale, s_group, stream);
+      case 1024: return launch_few_k<1024>(X, M, g, perm, rot, Xq, a_scale, s_group, stream);
+      case 2048: return launch_few_k<2048>(X, M, g, perm, rot, Xq, a_scale, s_group, stream);
+      case 4096: return launch_few_k<4096>(X, M, g, perm, rot, Xq, a_scale, s_group, stream);
+      case 8192: return launch_few_k<8192>(X, M, g, perm, rot, Xq, a_scale, s_group, stream);
+      case 16384: return launch_few_k<16384>(X, M, g, perm, rot, Xq, a_scale, s_group, stream);
+      default: return hipErrorInvalidValue;
+    }
+  }
   if (use_wave_kernels(M, K))
     return launch_rotate_smooth_quant_wave(X, M, K, g, perm, flags, Xq, a_scale, s_group,
                                            workspace, kMaxPartialRows, 2 * num_cus(), stream);

@@ -83,6 +83,37 @@ def test_quant_few_tokens_boundary(M, K, g):
     _quant_case(synth.activations(w), g, label=f"few {M}x{K}/g{g}")
 
 
+# The one-launch few-token quantizer runs for M up to 16 (K <= 2048), 8
+# (K = 4096), 4 (K = 8192) and 2 (K = 16384); these cases sit on both sides
+# of each limit, and cover every row of a workgroup's teams being live or not.
+@pytest.mark.parametrize("K,M", [
+    (512, 1), (512, 5), (512, 16), (512, 17), (1024, 3), (1024, 16), (2048, 2), (2048, 11),
+    (2048, 16), (4096, 1), (4096, 7), (4096, 8), (4096, 9), (8192, 1), (8192, 3), (8192, 4),
+    (8192, 5), (16384, 1), (16384, 2), (16384, 3),
+])
+@pytest.mark.parametrize("g", [64, 512])
+def test_quant_one_launch_few_tokens(K, M, g):
+    w = synth.custom("o", M, K, 16, g, 3 * M + K + g, n_chan=max(1, K // 100), n_spike=2,
+                     spike_mag=(100, 500))
+    _quant_case(synth.activations(w), g, label=f"one-launch {M}x{K}/g{g}")
+
+
+@pytest.mark.parametrize("K,M", [(1024, 6), (4096, 5), (8192, 2), (16384, 1)])
+@pytest.mark.parametrize("flags", [1, 0])
+def test_quant_one_launch_perm_and_no_rotation(K, M, flags):
+    rrs = _rrs()
+    g = 128
+    w = synth.custom("op", M, K, 16, g, 7 + K + M, n_chan=8, n_spike=3)
+    X = synth.activations(w)
+    perm = synth.permutation(K, K + M)
+    print(f"[case] one-launch quant flags={flags} M={M} K={K}", flush=True)
+    act = O.rotate_smooth_quant(X, g, perm=perm, rotate=not (flags & 1))
+    Xq, a, s = rrs.rotate_smooth_quant(to_gpu(X), g, perm=to_gpu(perm), flags=flags)
+    np.testing.assert_array_equal(to_np(s), act.s)
+    np.testing.assert_array_equal(to_np(a), act.alpha)
+    check_codes(to_np(Xq), act, "one-launch perm")
+
+
 @pytest.mark.parametrize("flags", [1, 0])
 def test_quant_few_tokens_perm_and_no_rotation(flags):
     rrs = _rrs()
