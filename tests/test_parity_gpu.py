@@ -364,10 +364,13 @@ def test_gemm_few_tokens_extreme(M, g):
 @pytest.mark.parametrize("M,K,N,g", [
     (1, 512, 16, 512), (2, 512, 48, 64), (3, 1024, 272, 128), (8, 8192, 144, 128),
     (13, 4096, 64, 256), (16, 16384, 32, 64), (16, 2048, 1040, 512), (17, 2048, 80, 128),
+    (16, 8192, 96, 128), (8, 16384, 32, 128), (12, 8192, 48, 256),
 ])
 def test_gemm_few_tokens_random(M, K, N, g):
     # M <= 16 runs the few-token kernel (M = 17 the main kernel): every K
-    # split, group size and ragged column count, against the oracle.
+    # split, group size and ragged column count, against the oracle; the token
+    # slice in LDS (up to 10 KB per wave) or from global memory (16x8192,
+    # 8x16384, 12x8192, 16x16384).
     rng = np.random.default_rng(M * 31 + K + N)
     qx = rng.integers(-7, 8, size=(M, K)).astype(np.int8)
     qw = rng.integers(-7, 8, size=(K, N)).astype(np.int8)
