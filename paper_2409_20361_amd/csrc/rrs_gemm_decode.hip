@@ -77,22 +77,18 @@ constexpr int kPartBytes = 4 * kBlocks * 64 * 16;
 
 // GS = g / 64 MFMA k-steps per group. kLdsA: each wave first copies its K
 // quarter of Xq into LDS (when it fits), so the token fragments are LDS reads
-// instead of vector-memory loads queued behind the weight stream. kGather
-// (runtime channel reorder): position block p (32 channels, 16 bytes of a
-// packed row) of Xq pairs with block border[p] of every Wq row; the table is
-// staged in LDS before the first weight load.
-template <int GS, bool kLdsA, bool kGather = false>
+// instead of vector-memory loads queued behind the weight stream.
+template <int GS, bool kLdsA>
 __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
     const float* __restrict__ w_scale, int M, int N, int K, uint16_t* __restrict__ Y,
-    float out_scale, const int32_t* __restrict__ border) {
+    float out_scale) {
   constexpr int g = GS * 64;
   constexpr int NW = g / 32;                  // words per lane per group and block
   constexpr int D = NW >= 16 ? 1 : (NW >= 8 ? 2 : 4);  // groups in flight
   // Token slices during the loop; the partial sums reuse the space after it.
   __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsA ? 4 * kMaxLdsA : kPartBytes];
-  __shared__ int btab[kGather ? 16384 / kReorderBlock : 1];
   v4f(*part)[kBlocks][64] = reinterpret_cast<v4f(*)[kBlocks][64]>(lds);
 
   const int t = threadIdx.x;
@@ -116,18 +112,11 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
   // output rows that are never stored. Column blocks past N load block 0 and
   // are never stored.
   const uint8_t* pa = Xq + (size_t)min(c, M - 1) * krow + q * (g / 8);
-  // Gather: row starts only; the offset inside the row comes from the table.
   const uint8_t* pb[kBlocks];
 #pragma unroll
   for (int j = 0; j < kBlocks; ++j) {
     const int n = n0 + j * kCols < N ? n0 + j * kCols : 0;
-    pb[j] = Wq + (size_t)(n + c) * krow + (kGather ? 0 : q * (g / 8));
-  }
-  if constexpr (kGather) {
-    // Entries are masked into range, so any table keeps every load in bounds.
-    for (int i = t; i < K / kReorderBlock; i += kThreads)
-      btab[i] = border[i] & (K / kReorderBlock - 1);
-    __syncthreads();
+    pb[j] = Wq + (size_t)(n + c) * krow + q * (g / 8);
   }
 
   // Wave-private LDS copy of this wave's K quarter of Xq: row r < M at
@@ -138,36 +127,10 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
 
   uint32_t wa[D][NW], wb[D][kBlocks][NW];
   auto load = [&](int d, int i) {
-    const int gi = min(b0 + i, G - 1);
-    const size_t off = (size_t)gi * (g / 2);
+    const size_t off = (size_t)min(b0 + i, G - 1) * (g / 2);
     if constexpr (!kLdsA) load_words<NW>(pa + off, wa[d]);
-    if constexpr (kGather) {
-      // This lane's g/8 bytes of group gi cover position blocks starting at
-      // gi g/32 + q g/128 (half of block gi * 2 + q / 2 when g = 64).
-      if constexpr (NW == 2) {
-        const uint32_t o = (uint32_t)btab[gi * 2 + (q >> 1)] * 16u + (q & 1) * 8u;
 #pragma unroll
-        for (int j = 0; j < kBlocks; ++j) load_words<2>(pb[j] + o, wb[d][j]);
-      } else {
-        uint32_t o[NW / 4];
-#pragma unroll
-        for (int cc = 0; cc < NW / 4; ++cc)
-          o[cc] = (uint32_t)btab[gi * NW + q * (NW / 4) + cc] * 16u;
-#pragma unroll
-        for (int j = 0; j < kBlocks; ++j)
-#pragma unroll
-          for (int cc = 0; cc < NW / 4; ++cc) {
-            const uint4 v = *reinterpret_cast<const uint4*>(pb[j] + o[cc]);
-            wb[d][j][4 * cc] = v.x;
-            wb[d][j][4 * cc + 1] = v.y;
-            wb[d][j][4 * cc + 2] = v.z;
-            wb[d][j][4 * cc + 3] = v.w;
-          }
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < kBlocks; ++j) load_words<NW>(pb[j] + off, wb[d][j]);
-    }
+    for (int j = 0; j < kBlocks; ++j) load_words<NW>(pb[j] + off, wb[d][j]);
   };
   // Token words from LDS, read just before use (the quarter starts at group b0;
   // padded steps past this wave's groups reread its last group).
@@ -271,24 +234,209 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Runtime channel reorder: position block p (32 channels, 16 bytes of a packed
+// row) of Xq pairs with natural block border[p] of every Wq row.
+//
+// The weights still stream in natural order: a sorted-order walk over the
+// weight rows would use the eight 16-byte blocks of each 128-byte line at
+// different times, and this streaming kernel would fetch most lines several
+// times. Instead the (small, cache-resident) token codes are gathered. Wave kq
+// walks its K quarter in quads of four natural blocks 4m .. 4m + 3: lane (c, q)
+// loads block 4m + q of weight row n0 + 16 j + c (the four lanes of a row read
+// 64 contiguous bytes) and position block inv[4m + q] of token row c. A 4 x 4
+// dword transpose through a wave-private LDS region then gives lane group q
+// dword q of each of the four blocks, so that one v_mfma_i32_16x16x32_i8 per
+// block and column block (lane group q holds channels 8q .. 8q + 7 of the block
+// after the unpack, the same for both operands) yields the block's exact
+// partial sum. It is rescaled by the scale of the group its position falls in,
+// s_{inv[B] / (g/32)}: the sum over a group's blocks is taken in fp32 (K/32
+// rescaled terms per output instead of K/g).
+// ---------------------------------------------------------------------------
+constexpr int kGatherAhead = 2;  // quads in flight per wave
+constexpr int kTrStride = 20;    // dwords per row of the transpose region (conflict-free)
+
+__device__ __forceinline__ long unpack_dword(uint32_t w) {
+  const uint32_t lo = (w << 4) & 0xF0F0F0F0u;
+  const uint32_t hi = w & 0xF0F0F0F0u;
+  return (long)(((unsigned long)hi << 32) | lo);
+}
+
+__global__ __launch_bounds__(kThreads) void gemm_decode_gather_kernel(
+    const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
+    const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
+    const float* __restrict__ w_scale, const int32_t* __restrict__ border, int M, int N,
+    int K, int g, uint16_t* __restrict__ Y, float out_scale) {
+  constexpr int kMaxBlocks = 16384 / kReorderBlock;
+  constexpr int kArrays = 1 + kBlocks;  // token codes and the column blocks' weights
+  __shared__ int inv[kMaxBlocks];      // natural block -> byte offset of its position block
+  __shared__ float sblk[kMaxBlocks];   // natural block -> scale of its position's group
+  __shared__ __attribute__((aligned(16))) uint32_t tr[4][kArrays][kCols * kTrStride];
+  __shared__ __attribute__((aligned(16))) v4f part[4][kBlocks][64];
+
+  const int t = threadIdx.x;
+  const int lane = t & 63;
+  const int kq = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int c = lane & 15;
+  const int q = lane >> 4;
+  const int n0 = blockIdx.x * (kBlocks * kCols);
+  const size_t krow = (size_t)K / 2;
+  const int NB = K / kReorderBlock;
+  const int quads = NB / 16;     // quads per wave (K >= 512: at least 1)
+  const int b0 = kq * (NB / 4);  // first natural block of this wave
+  const int steps = (quads + kGatherAhead - 1) / kGatherAhead * kGatherAhead;
+
+  // Tables. Entries are reduced modulo K/32, so any table keeps every load in
+  // bounds; a table that is not a permutation leaves some blocks at scale 0.
+  for (int i = t; i < NB; i += kThreads) {
+    inv[i] = 0;
+    sblk[i] = 0.0f;
+  }
+  __syncthreads();
+  for (int p = t; p < NB; p += kThreads) {
+    const int B = border[p] & (NB - 1);
+    inv[B] = p * 16;
+    sblk[B] = s_group[p / (g / kReorderBlock)];
+  }
+  __syncthreads();
+
+  // Token rows >= M read row M - 1 and column blocks past N read block 0: their
+  // results are never stored.
+  const uint8_t* pa = Xq + (size_t)min(c, M - 1) * krow;
+  const uint8_t* pb[kBlocks];
+#pragma unroll
+  for (int j = 0; j < kBlocks; ++j) {
+    const int n = n0 + j * kCols < N ? n0 + j * kCols : 0;
+    pb[j] = Wq + (size_t)(n + c) * krow + q * 16;
+  }
+  uint32_t* trw = &tr[kq][0][0];
+
+  uint4 ld[kGatherAhead][kArrays];
+  // Steps past this wave's quads reload its last quad and add it with scale 0.
+  auto load = [&](int d, int i) {
+    const int B0 = b0 + 4 * min(i, quads - 1);
+    ld[d][0] = *reinterpret_cast<const uint4*>(pa + inv[B0 + q]);
+#pragma unroll
+    for (int j = 0; j < kBlocks; ++j)
+      ld[d][1 + j] = *reinterpret_cast<const uint4*>(pb[j] + (size_t)B0 * 16);
+  };
+
+  constexpr int kMagic = 0x4B400000;  // bits of 1.5 * 2^23
+  const v4i seed = {kMagic, kMagic, kMagic, kMagic};
+  float f[kBlocks][4];
+#pragma unroll
+  for (int j = 0; j < kBlocks; ++j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) f[j][r] = 0.0f;
+
+  // 4 x 4 transpose, first half: lane (c, q) holds dwords 0..3 of block q of
+  // the quad and writes them to row c of the wave's region; the registers are
+  // then free for the next loads.
+  auto stash = [&](int d) {
+#pragma unroll
+    for (int a = 0; a < kArrays; ++a) {
+      uint32_t* base = trw + a * (kCols * kTrStride) + c * kTrStride + q;
+      base[0] = ld[d][a].x;
+      base[4] = ld[d][a].y;
+      base[8] = ld[d][a].z;
+      base[12] = ld[d][a].w;
+    }
+  };
+  // Second half: take back dword q of blocks 0..3, then one MFMA per block.
+  auto consume = [&](int i) {
+    uint4 tv[kArrays];
+#pragma unroll
+    for (int a = 0; a < kArrays; ++a)
+      tv[a] = *reinterpret_cast<const uint4*>(trw + a * (kCols * kTrStride) + c * kTrStride +
+                                              4 * q);
+    const int B0 = b0 + 4 * min(i, quads - 1);
+    const uint32_t av[4] = {tv[0].x, tv[0].y, tv[0].z, tv[0].w};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float s = i < quads ? sblk[B0 + u] : 0.0f;
+      const long a = unpack_dword(av[u]);
+#pragma unroll
+      for (int j = 0; j < kBlocks; ++j) {
+        const uint32_t bw = u == 0 ? tv[1 + j].x : u == 1 ? tv[1 + j].y
+                          : u == 2 ? tv[1 + j].z : tv[1 + j].w;
+        // |256 P_B| <= 256 * 49 * 32 < 2^22: the magic-seeded result read as
+        // a float is exactly 1.5 * 2^23 + 256 P_B.
+        const v4i acc = __builtin_amdgcn_mfma_i32_16x16x32_i8(a, unpack_dword(bw), seed, 0, 0, 0);
+        const v4f accf = __builtin_bit_cast(v4f, acc);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) f[j][r] = __builtin_fmaf(s, accf[r] - 12582912.0f, f[j][r]);
+      }
+    }
+  };
+
+#pragma unroll
+  for (int d = 0; d < kGatherAhead; ++d) load(d, d);
+  int i = 0;
+  for (; i < steps - kGatherAhead; i += kGatherAhead) {
+#pragma unroll
+    for (int d = 0; d < kGatherAhead; ++d) {
+      stash(d);
+      load(d, i + d + kGatherAhead);
+      consume(i + d);
+    }
+  }
+#pragma unroll
+  for (int d = 0; d < kGatherAhead; ++d) {
+    stash(d);
+    consume(i + d);
+  }
+
+  // Partial sums of the four K quarters, added in a fixed order (as above).
+#pragma unroll
+  for (int j = 0; j < kBlocks; ++j) part[kq][j][lane] = v4f{f[j][0], f[j][1], f[j][2], f[j][3]};
+  __syncthreads();
+  const int w = t >> 6;
+  if (w < kBlocks && n0 + w * kCols < N) {
+    v4f sum = part[0][w][lane];
+#pragma unroll
+    for (int p = 1; p < 4; ++p) {
+      const v4f x = part[p][w][lane];
+      sum.x += x.x;
+      sum.y += x.y;
+      sum.z += x.z;
+      sum.w += x.w;
+    }
+    const float inv_s = out_scale;
+    const int col = n0 + w * kCols + c;
+    const float bcol = w_scale[col];
+    const float sv[4] = {sum.x, sum.y, sum.z, sum.w};
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = 4 * q + r;
+      if (row < M) {
+        const float sc = a_scale[row] * inv_s;
+        Y[(size_t)row * N + col] = __builtin_bit_cast(uint16_t, (_Float16)((sv[r] * sc) * bcol));
+      }
+    }
+  }
+}
+
 }  // namespace
 
 bool decode_kernel_fits(int M) { return M >= 1 && M <= kCols; }
 
-namespace {
-
-template <bool kGather>
-hipError_t launch_decode(const uint8_t* Xq, const float* a_scale, const float* s_group,
-                         const uint8_t* Wq, const float* w_scale, int M, int N, int K, int g,
-                         uint16_t* Y, float out_scale, hipStream_t stream,
-                         const int32_t* border) {
+hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
+                                   const float* s_group, const uint8_t* Wq,
+                                   const float* w_scale, int M, int N, int K, int g,
+                                   uint16_t* Y, float out_scale, hipStream_t stream,
+                                   const int32_t* border) {
   const int grid = (N / kCols + kBlocks - 1) / kBlocks;  // N % 16 == 0 (API precondition)
+  if (border) {
+    gemm_decode_gather_kernel<<<grid, kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale,
+                                                            border, M, N, K, g, Y, out_scale);
+    return hipGetLastError();
+  }
   const bool lds_a = (size_t)M * a_row_bytes(K, g) <= (size_t)kMaxLdsA;
-#define RRS_DECODE(GS_)                                                                      \
-  (lds_a ? (gemm_decode_kernel<GS_, true, kGather><<<grid, kThreads, 0, stream>>>(            \
-               Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale, border), 0)         \
-         : (gemm_decode_kernel<GS_, false, kGather><<<grid, kThreads, 0, stream>>>(           \
-               Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale, border), 0))
+#define RRS_DECODE(GS_)                                                                  \
+  (lds_a ? (gemm_decode_kernel<GS_, true><<<grid, kThreads, 0, stream>>>(                 \
+               Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale), 0)             \
+         : (gemm_decode_kernel<GS_, false><<<grid, kThreads, 0, stream>>>(                \
+               Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale), 0))
   switch (g) {
     case 64: RRS_DECODE(1); break;
     case 128: RRS_DECODE(2); break;
@@ -298,20 +446,6 @@ hipError_t launch_decode(const uint8_t* Xq, const float* a_scale, const float* s
   }
 #undef RRS_DECODE
   return hipGetLastError();
-}
-
-}  // namespace
-
-hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
-                                   const float* s_group, const uint8_t* Wq,
-                                   const float* w_scale, int M, int N, int K, int g,
-                                   uint16_t* Y, float out_scale, hipStream_t stream,
-                                   const int32_t* border) {
-  if (border)
-    return launch_decode<true>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, out_scale,
-                               stream, border);
-  return launch_decode<false>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, out_scale,
-                              stream, nullptr);
 }
 
 }  // namespace rrs
