@@ -211,6 +211,38 @@ __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
     load_raw64(X + (size_t)min(r, M - 1) * K + 64 * l, r < r1, raw);
   }
 
+  // s_b = max over the partial rows. Thread t takes group b = t % GMAX and
+  // rows t / GMAX + k NS (NS = 256 / GMAX slices) with a fixed number of
+  // unconditional loads (row indices clamped to the last row, entries for
+  // b >= G read neighbouring rows and are ignored: every index stays inside
+  // the 256 x K/64 workspace). The loads are issued here and reduced after
+  // the first row's rotation, which does not need the scales and hides their
+  // latency.
+  constexpr int NS = NT / GMAX;
+  constexpr int NL = (256 + NS - 1) / NS;  // loads per thread for up to 256 rows
+  float x[kSmooth ? NL : 1];
+  if constexpr (kSmooth) {
+    const int b = tid % GMAX;
+    const int sl = tid / GMAX;
+#pragma unroll
+    for (int k = 0; k < NL; ++k) {
+      const int i = min(sl + k * NS, nparts - 1);
+      x[k] = gpart[(size_t)i * G + b];
+    }
+  }
+
+  // Rotate row p into v (layout 2), prefetching row p + 1.
+  float v[64];
+  auto rotate = [&](int p) {
+    raw_to_float(raw, v);
+    if (p + 1 < passes) {
+      const int rn = row_of(p + 1);
+      load_raw64(X + (size_t)min(rn, M - 1) * K + 64 * l, rn < r1, raw);
+    }
+    fwht_wave_row<K, kRot>(v, row, l);  // v[e] = y[l + R e]
+  };
+  rotate(0);
+
   if constexpr (!kSmooth) {
     // Ablation without smoothing: every scale is 1 (rotation + per-token only).
     if (tid < G) {
@@ -219,35 +251,18 @@ __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
     }
     __syncthreads();
   } else {
-    // s_b = max over the partial rows. Thread t takes group b = t % GMAX and
-    // rows t / GMAX + k NS (NS = 256 / GMAX slices) with a fixed number of
-    // unconditional loads (row indices clamped to the last row, entries for
-    // b >= G read neighbouring rows and are ignored: every index stays inside
-    // the 256 x K/64 workspace), then the slices are combined through LDS.
-    {
-      constexpr int NS = NT / GMAX;
-      constexpr int NL = (256 + NS - 1) / NS;  // loads per thread for up to 256 rows
-      const int b = tid % GMAX;
-      const int sl = tid / GMAX;
-      float x[NL];
+    float m = 0.0f;
 #pragma unroll
-      for (int k = 0; k < NL; ++k) {
-        const int i = min(sl + k * NS, nparts - 1);
-        x[k] = gpart[(size_t)i * G + b];
-      }
-      float m = 0.0f;
-#pragma unroll
-      for (int k = 0; k < NL; ++k) m = fmaxf(m, x[k]);
-      red[tid] = m;
-      __syncthreads();
-      if (tid < G) {
-        float sv = red[tid];
-        for (int q = 1; q < NS; ++q) sv = fmaxf(sv, red[q * GMAX + tid]);
-        rg[tid] = (sv == 0.0f) ? 0.0f : __fdiv_rn(1.0f, sv);
-        if (blockIdx.x == 0) s_group[tid] = sv;
-      }
-      __syncthreads();
+    for (int k = 0; k < NL; ++k) m = fmaxf(m, x[k]);
+    red[tid] = m;
+    __syncthreads();
+    if (tid < G) {
+      float sv = red[tid];
+      for (int q = 1; q < NS; ++q) sv = fmaxf(sv, red[q * GMAX + tid]);
+      rg[tid] = (sv == 0.0f) ? 0.0f : __fdiv_rn(1.0f, sv);
+      if (blockIdx.x == 0) s_group[tid] = sv;
     }
+    __syncthreads();
   }
   // Positions 64 l .. 64 l + 63 of a row lie in one group (g >= 64).
   const float rb = rg[(64 * l) / g];
@@ -255,13 +270,7 @@ __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
   for (int p = 0; p < passes; ++p) {
     const int r = row_of(p);
     const bool live = r < r1;
-    float v[64];
-    raw_to_float(raw, v);
-    if (p + 1 < passes) {
-      const int rn = row_of(p + 1);
-      load_raw64(X + (size_t)min(rn, M - 1) * K + 64 * l, rn < r1, raw);
-    }
-    fwht_wave_row<K, kRot>(v, row, l);  // v[e] = y[l + R e]
+    if (p > 0) rotate(p);
     // back to layout 1 through LDS, with the static reorder applied
 #pragma unroll
     for (int e = 0; e < 64; ++e) row[lds_a(l + S::R * e)] = v[e];
