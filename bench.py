@@ -15,6 +15,10 @@ duration is taken from HIP events recorded around it on the launch stream.
 A decode-shaped measurement (M=8, K=8192, N=28672) reports HBM GB/s of the
 GEMM over algorithmic bytes, cycling through 4 weight copies (470 MB, more
 than the 256 MB Infinity Cache) so that every call streams its weight from HBM.
+Further objects on the same line: few-token layers at the decode shape
+(M = 1..16), the gate/up and large prefill configurations against their own
+rooflines, the runtime-reorder comparison, the kernel comparison of the three
+scale schemes, and the CPU oracle baseline.
 
 Prints one JSON line.
 """
@@ -60,6 +64,10 @@ def parse():
     ap.add_argument("--decode-only", action="store_true",
                     help="only the decode measurement (for per-kernel profiles)")
     ap.add_argument("--decode-steps", type=int, default=100)
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the gate/up and large prefill configurations")
+    ap.add_argument("--configs-only", action="store_true",
+                    help="only the gate/up and large prefill configurations")
     ap.add_argument("--no-reorder", action="store_true",
                     help="skip the runtime-reorder comparison")
     ap.add_argument("--reorder-only", action="store_true",
@@ -140,7 +148,9 @@ def qkv_step_bench(args, torch, rrs, synth):
     step_ms = evs[0][0].elapsed_time(evs[-1][2]) / args.steps
     return w, dict(step_ms=step_ms, wall_ms=wall * 1e3 / args.steps,
                    quant_ms=sum(quant_ms) / len(quant_ms), gemm_ms=sum(gemm_ms) / len(gemm_ms),
-                   gemm_ms_min=min(gemm_ms), quant_ms_min=min(quant_ms))
+                   gemm_ms_min=min(gemm_ms), quant_ms_min=min(quant_ms),
+                   gemm_ms_med=sorted(gemm_ms)[len(gemm_ms) // 2],
+                   quant_ms_med=sorted(quant_ms)[len(quant_ms) // 2])
 
 
 def decode_bench(args, torch, rrs, synth):
@@ -186,6 +196,62 @@ def decode_bench(args, torch, rrs, synth):
         "linear_GBps": round(alg / (lm * 1e-3) / 1e9, 1),
         "weight_copies": 4,
     }
+
+
+def quant_bytes(w):
+    """Algorithmic HBM bytes of rrs_rotate_smooth_quant: read X, write Xq, alpha, s."""
+    return 2 * w.M * w.K + w.M * w.K // 2 + 4 * w.M + 4 * w.G
+
+
+def config_bench(torch, rrs, synth, names=("gateup", "large"), reps=10):
+    """The other prefill configurations, each against its own roofline: the GEMM
+    (int8 MFMA peak) and the quantizer (HBM) timed alone with HIP events, and
+    the whole layer."""
+    dev = torch.device("cuda:0")
+    out = {}
+    for name in names:
+        w = synth.WORKLOADS[name]
+        log(f"config {name} M={w.M} K={w.K} N={w.N} g={w.g}")
+        X = torch.from_numpy(synth.activations(w)).to(dev)
+        W = torch.from_numpy(synth.weights(w)).to(dev)
+        Wq, beta = rrs.prepare_weight(W)
+        del W
+        Xq = torch.empty((w.M, w.K // 2), dtype=torch.uint8, device=dev)
+        a = torch.empty((w.M,), dtype=torch.float32, device=dev)
+        s = torch.empty((w.G,), dtype=torch.float32, device=dev)
+        Y = torch.empty((w.M, w.N), dtype=torch.float16, device=dev)
+        qws = torch.empty((rrs.workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8, device=dev)
+        lws = torch.empty((rrs.linear_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
+                          device=dev)
+        rrs.rotate_smooth_quant(X, w.g, workspace=qws, out=(Xq, a, s))
+        calls = {
+            "quant": lambda: rrs.rotate_smooth_quant(X, w.g, workspace=qws, out=(Xq, a, s)),
+            "gemm": lambda: rrs.w4a4_gemm(Xq, a, s, Wq, beta, w.g, out=Y),
+            "linear": lambda: rrs.linear(X, Wq, beta, w.g, workspace=lws, out=Y),
+        }
+        row = {"M": w.M, "K": w.K, "N": w.N, "group_size": w.g}
+        for key, fn in calls.items():
+            prewarm(torch, fn, seconds=0.2)
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+            ev[0].record()
+            for i in range(reps):
+                fn()
+                ev[i + 1].record()
+            torch.cuda.synchronize()
+            t = sorted(ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(reps))
+            row[key + "_us"] = round(sum(t) / reps, 2)
+            row[key + "_us_median"] = round(t[reps // 2], 2)
+        ops = 2.0 * w.M * w.N * w.K
+        row["gemm_TOPS"] = round(ops / (row["gemm_us"] * 1e-6) / 1e12, 1)
+        row["gemm_frac_int8_peak"] = round(row["gemm_TOPS"] / INT8_MFMA_PEAK_TOPS, 4)
+        row["linear_TOPS"] = round(ops / (row["linear_us"] * 1e-6) / 1e12, 1)
+        qb = quant_bytes(w)
+        row["quant_GBps"] = round(qb / (row["quant_us"] * 1e-6) / 1e9, 1)
+        row["quant_frac_hbm"] = round(row["quant_GBps"] / HBM_PEAK_GBS, 4)
+        out[name] = row
+        del X, Wq, Y, Xq, lws
+        torch.cuda.empty_cache()
+    return out
 
 
 def few_token_bench(torch, rrs, synth, reps=50):
@@ -365,14 +431,18 @@ def cpu_baseline(synth):
     W = synth.weights(w)
     wq = O.prepare_weight(W)          # offline, not timed
     chunk = 256
-    times = []
+    times, tq, tg = [], [], []
     for rep in range(3):
         t0 = time.perf_counter()
         act = O.rotate_smooth_quant(X, w.g)
+        t1 = time.perf_counter()
         for r0 in range(0, w.M, chunk):
             P = O.group_partials(act.q[r0:r0 + chunk], wq.q, w.g)
             O.output(P, act.s, act.alpha[r0:r0 + chunk], wq.beta, norm=w.K)
-        times.append(time.perf_counter() - t0)
+        t2 = time.perf_counter()
+        times.append(t2 - t0)
+        tq.append(t1 - t0)
+        tg.append(t2 - t1)
         if sum(times) > 20.0:
             break
     t_step = sorted(times)[len(times) // 2]
@@ -382,6 +452,8 @@ def cpu_baseline(synth):
         "unit": "TOPS",
         "cores": int(cores),
         "kind": "oracle",
+        "quant_s": round(sorted(tq)[len(tq) // 2], 3),
+        "gemm_s": round(sorted(tg)[len(tg) // 2], 3),
         "sample": (f"the whole step on the qkv workload (all {w.M} tokens x {w.N} outputs; "
                    f"GEMM and epilogue in {chunk}-token chunks), median of {len(times)} "
                    f"run(s): {t_step:.2f} s per step; weight preparation excluded"),
@@ -405,6 +477,10 @@ def main():
         copy_calibration(torch)
     if args.schemes_only:
         print(json.dumps({"metric": METRIC, "scheme_comparison": scheme_bench(torch, rrs)}),
+              flush=True)
+        return
+    if args.configs_only:
+        print(json.dumps({"metric": METRIC, "configs": config_bench(torch, rrs, synth)}),
               flush=True)
         return
     if args.reorder_only:
@@ -447,6 +523,12 @@ def main():
             "quant_us": round(r["quant_ms"] * 1e3, 2),
             "gemm_us": round(r["gemm_ms"] * 1e3, 2),
             "gemm_us_min": round(r["gemm_ms_min"] * 1e3, 2),
+            "gemm_us_median": round(r["gemm_ms_med"] * 1e3, 2),
+            "quant_us_median": round(r["quant_ms_med"] * 1e3, 2),
+            "quant_bytes": quant_bytes(w),
+            "quant_GBps": round(quant_bytes(w) / (r["quant_ms"] * 1e-3) / 1e9, 1),
+            "quant_frac_hbm": round(quant_bytes(w) / (r["quant_ms"] * 1e-3) / 1e9
+                                    / HBM_PEAK_GBS, 4),
             "wall_ms_per_step": round(r["wall_ms"], 5),
         },
     }
@@ -455,6 +537,8 @@ def main():
     if not args.no_decode:
         log("few-token layers at the decode shape")
         out["few_token"] = few_token_bench(torch, rrs, synth)
+    if not args.no_configs:
+        out["configs"] = config_bench(torch, rrs, synth)
     if not args.no_reorder:
         out["reorder"] = reorder_bench(torch, rrs, synth)
     if not args.no_schemes:
