@@ -64,6 +64,10 @@ def parse():
     ap.add_argument("--decode-only", action="store_true",
                     help="only the decode measurement (for per-kernel profiles)")
     ap.add_argument("--decode-steps", type=int, default=100)
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the HIP-graph replay timings")
+    ap.add_argument("--graph-only", action="store_true",
+                    help="only the HIP-graph replay timings")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the gate/up and large prefill configurations")
     ap.add_argument("--configs-only", action="store_true",
@@ -196,6 +200,80 @@ def decode_bench(args, torch, rrs, synth):
         "linear_GBps": round(alg / (lm * 1e-3) / 1e9, 1),
         "weight_copies": 4,
     }
+
+
+def graph_bench(torch, rrs, synth, reps=50):
+    """The same calls replayed from a HIP graph (torch.cuda.CUDAGraph on the
+    library's launches): the qkv step (quantizer + GEMM) and the decode GEMM
+    and layer (4 weight copies, one captured call per copy). Replays remove
+    the host launch cost and the gaps between back-to-back launches; the
+    kernels and their work are unchanged."""
+    dev = torch.device("cuda:0")
+    out = {}
+
+    def timed(fn_capture, per_replay):
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn_capture()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            fn_capture()
+        prewarm(torch, graph.replay, seconds=0.2)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / (reps * per_replay)
+
+    w = synth.WORKLOADS["qkv"]
+    X = torch.from_numpy(synth.activations(w)).to(dev)
+    Wq, beta = rrs.prepare_weight(torch.from_numpy(synth.weights(w)).to(dev))
+    Xq = torch.empty((w.M, w.K // 2), dtype=torch.uint8, device=dev)
+    a = torch.empty((w.M,), dtype=torch.float32, device=dev)
+    s = torch.empty((w.G,), dtype=torch.float32, device=dev)
+    Y = torch.empty((w.M, w.N), dtype=torch.float16, device=dev)
+    ws = torch.empty((rrs.workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8, device=dev)
+
+    def step():
+        rrs.rotate_smooth_quant(X, w.g, workspace=ws, out=(Xq, a, s))
+        rrs.w4a4_gemm(Xq, a, s, Wq, beta, w.g, out=Y)
+    step_us = timed(step, 1)
+    ops = 2.0 * w.M * w.N * w.K
+    out["qkv"] = {"step_us": round(step_us, 2),
+                  "TOPS": round(ops / (step_us * 1e-6) / 1e12, 1)}
+    del X, Wq, Xq, Y
+
+    w = synth.WORKLOADS["decode"]
+    X = torch.from_numpy(synth.activations(w)).to(dev)
+    Wq0, beta = rrs.prepare_weight(torch.from_numpy(synth.weights(w)).to(dev))
+    copies = [Wq0] + [Wq0.clone() for _ in range(3)]
+    Xq, a, s = rrs.rotate_smooth_quant(X, w.g)
+    Y = torch.empty((w.M, w.N), dtype=torch.float16, device=dev)
+    lws = torch.empty((rrs.linear_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
+                      device=dev)
+
+    def gemms():
+        for c in copies:
+            rrs.w4a4_gemm(Xq, a, s, c, beta, w.g, out=Y)
+
+    def linears():
+        for c in copies:
+            rrs.linear(X, c, beta, w.g, workspace=lws, out=Y)
+    alg = (w.M * w.K // 2 + 4 * w.M + 4 * w.G + w.N * w.K // 2 + 4 * w.N + 2 * w.M * w.N)
+    g_us = timed(gemms, len(copies))
+    l_us = timed(linears, len(copies))
+    out["decode"] = {"gemm_us": round(g_us, 2),
+                     "gemm_GBps": round(alg / (g_us * 1e-6) / 1e9, 1),
+                     "gemm_frac_hbm": round(alg / (g_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                     "linear_us": round(l_us, 2),
+                     "linear_GBps": round(alg / (l_us * 1e-6) / 1e9, 1)}
+    return out
 
 
 def quant_bytes(w):
@@ -479,6 +557,10 @@ def main():
         print(json.dumps({"metric": METRIC, "scheme_comparison": scheme_bench(torch, rrs)}),
               flush=True)
         return
+    if args.graph_only:
+        print(json.dumps({"metric": METRIC, "graph": graph_bench(torch, rrs, synth)}),
+              flush=True)
+        return
     if args.configs_only:
         print(json.dumps({"metric": METRIC, "configs": config_bench(torch, rrs, synth)}),
               flush=True)
@@ -534,6 +616,9 @@ def main():
     }
     if not args.no_decode:
         out["decode"] = decode_bench(args, torch, rrs, synth)
+    if not args.no_graph:
+        log("the same calls replayed from HIP graphs")
+        out["graph"] = graph_bench(torch, rrs, synth)
     if not args.no_decode:
         log("few-token layers at the decode shape")
         out["few_token"] = few_token_bench(torch, rrs, synth)
