@@ -36,9 +36,19 @@
  * Data layouts (fixed by this library; the paper does not specify them):
  *  - X:  M x K float16, row-major.
  *  - W:  K x N float16, row-major (the transpose of nn.Linear's weight).
- *  - Xq: M x K/2 bytes, row-major; Wq: N x K/2 bytes, one row per output
- *    channel. Codes are INT4 two's complement in [-7, 7], two per byte, the
- *    low nibble holding the even channel index.
+ *  - Xq: M x K/2 bytes, row-major. Codes are INT4 two's complement in
+ *    [-7, 7], two per byte, the low nibble holding the even channel index.
+ *  - Wq: N x K/2 bytes of the same packed codes (row n = output channel n),
+ *    tiled: rows in blocks of 16, each block stored as its K/128 tiles of
+ *    16 rows x 64 bytes (1 KB) one after another, and inside a tile the
+ *    four 16-byte quarters of the 16 rows quarter by quarter. Packed byte j
+ *    of row n sits at byte
+ *      (n / 16) * 8K + (j / 64) * 1024 + ((j % 64) / 16) * 256
+ *        + (n % 16) * 16 + j % 16.
+ *    A wave's load of one K tile of 16 channels is then one contiguous 1 KB
+ *    run, which the few-token GEMM streams at close to copy speed. Every
+ *    entry point that takes Wq expects this layout, as written by
+ *    rrs_prepare_weight / rrs_prepare_weight_sub_channel.
  *  - a_scale: M float32 (per token); w_scale: N float32 (per output channel);
  *    s_group: K/g float32 (one smoothing scale per channel group).
  *  - Y:  M x N float16, row-major.
@@ -109,7 +119,8 @@ size_t rrs_workspace_bytes(int M, int K, int group_size);
  *                weight becomes row perm[j]'s rotation (the static channel
  *                reorder of Fig. 4 step (1)); pass the same perm to
  *                rrs_rotate_smooth_quant / rrs_linear.
- *   Wq      out: N x K/2 bytes, packed INT4 codes of u = H_K W per column.
+ *   Wq      out: N x K/2 bytes, packed INT4 codes of u = H_K W per column,
+ *                in the tiled layout above.
  *   w_scale out: N float32, beta_n = max_k |u_kn| / 7.
  * Not on the timed path.
  */

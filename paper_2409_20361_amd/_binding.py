@@ -137,7 +137,10 @@ def _perm_ptr(perm: Optional[torch.Tensor], K: int) -> Optional[int]:
 
 def prepare_weight(W: torch.Tensor, perm: Optional[torch.Tensor] = None, flags: int = 0
                    ) -> Tuple[torch.Tensor, torch.Tensor]:
-    """W: K x N fp16 (the transpose of nn.Linear's weight) -> (Wq N x K/2 uint8, w_scale N f32)."""
+    """W: K x N fp16 (the transpose of nn.Linear's weight) -> (Wq N x K/2 uint8, w_scale N f32).
+
+    Wq holds the packed codes in the tiled layout of include/rrs.h (16-row
+    blocks of 1 KB tiles), which every GEMM entry point expects."""
     K, N = W.shape
     wp = _dev(W, "W", torch.float16, (K, N))
     Wq = torch.empty((N, K // 2), dtype=torch.uint8, device=W.device)

@@ -7,8 +7,9 @@
 // each wave 64 x 64 as 2 x 2 blocks of v_mfma_i32_32x32x32_i8. K advances in
 // tiles of 128 (four MFMA k-steps of 32).
 //
-// Data path: packed INT4 (Xq: M x K/2, Wq: N x K/2, K contiguous) is loaded
-// from HBM into registers two tiles ahead, unpacked to int8 and stored in a
+// Data path: packed INT4 (Xq: M x K/2, K contiguous; Wq tiled, see wq_piece:
+// one wave's slot of a K tile, 16 rows x 64 bytes, is one contiguous 1 KB
+// tile) is loaded from HBM into registers two tiles ahead, unpacked to int8 and stored in a
 // double-buffered LDS stage whose rows are padded to 144 bytes (conflict-free
 // 128-bit fragment reads at immediate offsets). The unpack and the LDS stores
 // of the next tile are spread over the MFMAs of the current tile's H0 phase
@@ -137,7 +138,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
   const int brow = t >> 2;
   const int bq = t & 3;
   const uint8_t* ga = Xq + (size_t)min(m0 + arow, M - 1) * krow + ahalf * 32;
-  const uint8_t* gb = Wq + (size_t)min(n0 + brow, N - 1) * krow + (kGather ? 0 : bq * 16);
+  const int bn = min(n0 + brow, N - 1);
+  const uint8_t* gb = Wq + wq_piece(bn, 0, K) + (kGather ? 0 : bq * 256);
   const int a_st = arow * ROWP + ahalf * 64;
   const int b_st = A_BYTES + brow * ROWP + bq * 32;
 
@@ -149,12 +151,15 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
 
   // Packed tiles in flight: two register sets, tile kt lives in set kt & 1.
   uint4 ra0[2], ra1[2], rb0[2];
-  // Byte offset in the Wq row of this thread's B slot of tile kt.
+  // Byte offset from gb of this thread's B slot of tile kt: piece 4 kt + bq of
+  // its row, or piece btab[4 kt + bq] with the runtime reorder.
   auto boff = [&](int kt) -> uint32_t {
-    if constexpr (kGather)
-      return (uint32_t)btab[kt * 4 + bq] * 16u;
-    else
-      return (uint32_t)kt * (BK / 2);
+    if constexpr (kGather) {
+      const uint32_t p = (uint32_t)btab[kt * 4 + bq];
+      return (p >> 2) * 1024u + (p & 3u) * 256u;
+    } else {
+      return (uint32_t)kt * 1024u;
+    }
   };
   auto gload = [&](int set, int kt, uint32_t bo) {
     const uint4* p = reinterpret_cast<const uint4*>(ga + (size_t)kt * (BK / 2));

@@ -10,12 +10,16 @@
 //     waves split K into quarters (whole smoothing groups each) and add their
 //     fp32 partial sums in a fixed order at the end (deterministic); each
 //     wave unpacks its token codes once for both blocks;
-//   - per group, lane (c, q) (c = lane % 16, q = lane / 16) loads the g/8
-//     contiguous bytes [q g/8, (q+1) g/8) of the group in Wq row n0 + c, and
-//     the same bytes of Xq row c (zero for c >= M). MFMA k-step s of the group
-//     (v_mfma_i32_16x16x64_i8, 64 codes) takes bytes [8 s, 8 s + 8) of every
-//     lane, so each k-step stays inside one group and A and B pair the same
-//     codes;
+//   - per group, lane (c, q) (c = lane % 16, q = lane / 16) takes g/8 bytes
+//     of Wq row n0 + c and the same bytes of Xq row c (zero for c >= M): for
+//     g = 64 bytes [8 q, 8 q + 8) of the group, for g >= 128 bytes
+//     [64 h + 16 q, +16) of each 64-byte piece h of it. In the tiled Wq
+//     (wq_piece) these are bytes [16 lane, +16) of the group's 1 KB tiles, so
+//     every weight load instruction of a wave reads one contiguous tile
+//     (512 contiguous bytes for g = 64). MFMA k-step s of the group
+//     (v_mfma_i32_16x16x64_i8, 64 codes) takes the lane's bytes [8 s, 8 s + 8)
+//     in that order, so each k-step stays inside one group and A and B pair
+//     the same codes;
 //   - loads run several groups ahead of the MFMAs (about 48 bytes of Wq per
 //     lane in flight, tens of KB per CU), with no branch between a load and
 //     its use, so each wait is for exactly the group about to be used.
@@ -45,9 +49,11 @@ __device__ __forceinline__ v4i unpack_pair(uint32_t w0, uint32_t w1) {
   return r;
 }
 
-// NW = g / 32 words (g / 8 bytes) per lane per group, read from p.
+// NW = g / 32 words (g / 8 bytes) per lane per group: one 8-byte piece at p
+// (g = 64) or NW / 4 pieces of 16 bytes at p, p + stride, ...
 template <int NW>
-__device__ __forceinline__ void load_words(const uint8_t* __restrict__ p, uint32_t (&w)[NW]) {
+__device__ __forceinline__ void load_words(const uint8_t* __restrict__ p, int stride,
+                                           uint32_t (&w)[NW]) {
   if constexpr (NW == 2) {
     const uint2 v = *reinterpret_cast<const uint2*>(p);
     w[0] = v.x;
@@ -55,7 +61,7 @@ __device__ __forceinline__ void load_words(const uint8_t* __restrict__ p, uint32
   } else {
 #pragma unroll
     for (int c = 0; c < NW / 4; ++c) {
-      const uint4 v = reinterpret_cast<const uint4*>(p)[c];
+      const uint4 v = *reinterpret_cast<const uint4*>(p + (size_t)c * stride);
       w[4 * c] = v.x;
       w[4 * c + 1] = v.y;
       w[4 * c + 2] = v.z;
@@ -111,32 +117,36 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
   // partial sums are finite). Token rows >= M load row M - 1; they only feed
   // output rows that are never stored. Column blocks past N load block 0 and
   // are never stored.
-  const uint8_t* pa = Xq + (size_t)min(c, M - 1) * krow + q * (g / 8);
+  // Byte offsets of this lane's codes inside a group: in a packed Xq row, and
+  // in the group's region of the column block's tiled rows (8 g bytes).
+  const int xo = g == 64 ? q * 8 : q * 16;
+  const int wo = g == 64 ? (q >> 1) * 256 + c * 16 + (q & 1) * 8 : lane * 16;
+  const uint8_t* pa = Xq + (size_t)min(c, M - 1) * krow + xo;
   const uint8_t* pb[kBlocks];
 #pragma unroll
   for (int j = 0; j < kBlocks; ++j) {
     const int n = n0 + j * kCols < N ? n0 + j * kCols : 0;
-    pb[j] = Wq + (size_t)(n + c) * krow + q * (g / 8);
+    pb[j] = Wq + wq_piece(n, 0, K) + wo;
   }
 
   // Wave-private LDS copy of this wave's K quarter of Xq: row r < M at
   // r * a_row_bytes(K); lanes then read their row min(c, M - 1).
   uint8_t* aq = lds + kq * kMaxLdsA;
   const int arb = a_row_bytes(K, g);
-  const uint8_t* pal = aq + min(c, M - 1) * arb + q * (g / 8);
+  const uint8_t* pal = aq + min(c, M - 1) * arb + xo;
 
   uint32_t wa[D][NW], wb[D][kBlocks][NW];
   auto load = [&](int d, int i) {
-    const size_t off = (size_t)min(b0 + i, G - 1) * (g / 2);
-    if constexpr (!kLdsA) load_words<NW>(pa + off, wa[d]);
+    const int b = min(b0 + i, G - 1);
+    if constexpr (!kLdsA) load_words<NW>(pa + (size_t)b * (g / 2), 64, wa[d]);
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) load_words<NW>(pb[j] + off, wb[d][j]);
+    for (int j = 0; j < kBlocks; ++j) load_words<NW>(pb[j] + (size_t)b * (8 * g), 1024, wb[d][j]);
   };
   // Token words from LDS, read just before use (the quarter starts at group b0;
   // padded steps past this wave's groups reread its last group).
   auto read_a = [&](int d, int i) {
     const int li = min(i, max(nb, 1) - 1);
-    load_words<NW>(pal + li * (g / 2), wa[d]);
+    load_words<NW>(pal + li * (g / 2), 64, wa[d]);
   };
 
   constexpr int kMagic = 0x4B400000;  // bits of 1.5 * 2^23
@@ -243,8 +253,8 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
 // different times, and this streaming kernel would fetch most lines several
 // times. Instead the (small, cache-resident) token codes are gathered. Wave kq
 // walks its K quarter in quads of four natural blocks 4m .. 4m + 3: lane (c, q)
-// loads block 4m + q of weight row n0 + 16 j + c (the four lanes of a row read
-// 64 contiguous bytes) and position block inv[4m + q] of token row c. A 4 x 4
+// loads block 4m + q of weight row n0 + 16 j + c (the wave reads tile m of the
+// column block, 1 KB contiguous) and position block inv[4m + q] of token row c. A 4 x 4
 // dword transpose through a wave-private LDS region then gives lane group q
 // dword q of each of the four blocks, so that one v_mfma_i32_16x16x32_i8 per
 // block and column block (lane group q holds channels 8q .. 8q + 7 of the block
@@ -307,7 +317,7 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_gather_kernel(
 #pragma unroll
   for (int j = 0; j < kBlocks; ++j) {
     const int n = n0 + j * kCols < N ? n0 + j * kCols : 0;
-    pb[j] = Wq + (size_t)(n + c) * krow + q * 16;
+    pb[j] = Wq + wq_piece(n, 0, K) + lane * 16;  // quad m is tile m of the block
   }
   uint32_t* trw = &tr[kq][0][0];
 
@@ -318,7 +328,7 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_gather_kernel(
     ld[d][0] = *reinterpret_cast<const uint4*>(pa + inv[B0 + q]);
 #pragma unroll
     for (int j = 0; j < kBlocks; ++j)
-      ld[d][1 + j] = *reinterpret_cast<const uint4*>(pb[j] + (size_t)B0 * 16);
+      ld[d][1 + j] = *reinterpret_cast<const uint4*>(pb[j] + (size_t)B0 * 256);
   };
 
   constexpr int kMagic = 0x4B400000;  // bits of 1.5 * 2^23

@@ -3,7 +3,8 @@
 //   Y[i, n] = fp16( alpha_i * beta_n / K * sum_b s_b * P_b[i, n] )
 //   P_b[i, n] = sum_{j in group b} qx[i, j] * qw[j, n]   (exact int32)
 //
-// Both operands are K-contiguous packed INT4 (Xq: M x K/2, Wq: N x K/2).
+// Packed INT4 operands: Xq M x K/2, K contiguous; Wq in the tiled layout of
+// wq_piece() (a row's K tile of 32 bytes is pieces 2 kt and 2 kt + 1).
 // Fallback kernel for shapes outside the main kernel's unrolling (rrs_gemm.hip).
 // Tile 128 x 128 per 256-thread workgroup, four waves of 64 x 64, K step 64.
 // Global -> registers (16 B per thread per operand) -> unpacked to int8 ->
@@ -82,7 +83,8 @@ __global__ __launch_bounds__(256) void gemm_small_kernel(
   const bool a_ok = (m0 + lrow) < M;
   const bool b_ok = (n0 + lrow) < N;
   const uint8_t* gA = Xq + (size_t)(a_ok ? m0 + lrow : 0) * kbytes_row + lhalf * 16;
-  const uint8_t* gB = Wq + (size_t)(b_ok ? n0 + lrow : 0) * kbytes_row + lhalf * 16;
+  // Tiled Wq: piece 2 kt + lhalf of the row lies 512 kt bytes after piece lhalf.
+  const uint8_t* gB = Wq + wq_piece(b_ok ? n0 + lrow : 0, lhalf, K);
   const int st_off = lrow * LROW + lhalf * 32;
 
   uint4 ra = make_uint4(0, 0, 0, 0);
@@ -136,7 +138,7 @@ __global__ __launch_bounds__(256) void gemm_small_kernel(
     __syncthreads();
     if (kt + 1 < nkt) {
       if (a_ok) ra = *reinterpret_cast<const uint4*>(gA + (size_t)(kt + 1) * KBYTES);
-      if (b_ok) rb = *reinterpret_cast<const uint4*>(gB + (size_t)(kt + 1) * KBYTES);
+      if (b_ok) rb = *reinterpret_cast<const uint4*>(gB + (size_t)(kt + 1) * 512);
     }
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {

@@ -21,6 +21,16 @@ constexpr int kSkipSmoothing = 2;
 // codes, 16 bytes of a packed row.
 constexpr int kReorderBlock = 32;
 
+// Tiled Wq (the layout rrs_prepare_weight writes): rows in blocks of 16, each
+// block's K/128 tiles of 1 KB stored one after another; inside a tile, byte
+// (q * 16 + r) * 16 + e is packed byte 64 c + 16 q + e of row 16 nb + r for
+// tile c of block nb. A 16-row block spans 16 * K/2 = 8 K bytes.
+// Byte offset of piece p (packed bytes [16 p, 16 p + 16)) of row n.
+__host__ __device__ inline size_t wq_piece(int n, int p, int K) {
+  return (size_t)(n >> 4) * ((size_t)8 * K) + (size_t)(p >> 2) * 1024 + (p & 3) * 256 +
+         (n & 15) * 16;
+}
+
 hipError_t launch_rotate_smooth_quant(const uint16_t* X, int M, int K, int g,
                                       const int32_t* perm, int flags, uint8_t* Xq,
                                       float* a_scale, float* s_group, void* workspace,

@@ -6,7 +6,8 @@
 //                                    u = W[:, n] for the ablation without rotation)
 //   u'_j = u_{perm[j]}              (optional static reorder, Fig. 4 step (1))
 //   b_n = max_j |u_j|, winv = fl(7 / b_n), beta_n = fl(b_n / 7)
-//   code_j = clamp(rint(fl(u'_j * winv)), -7, 7), packed into Wq[n][j / 2].
+//   code_j = clamp(rint(fl(u'_j * winv)), -7, 7), packed as byte j / 2 of row
+//   n (low nibble even j) in the tiled layout of wq_piece().
 // A workgroup stages C = 32768 / K whole columns in LDS (139 KB), then
 // transforms and quantizes them one after another.
 #include "rrs_device.h"
@@ -18,6 +19,24 @@ namespace {
 // kSub: the sub-channel baseline of Section 4.5: one scale per (output
 // channel, group of g), w_scale[b * N + n] = fl(m_b / 7) (group-major, L x N);
 // no reorder.
+// Stores this thread's E codes, packed bytes [j0, j0 + E/2) of row n: one
+// store inside a 16-byte piece (E <= 32), else one per piece.
+template <int E>
+__device__ __forceinline__ void store_wq(uint8_t* __restrict__ Wq, int n, int j0, int K,
+                                         const uint32_t (&nib)[E]) {
+  if constexpr (E <= 32) {
+    store_nibbles<E>(Wq + wq_piece(n, j0 >> 4, K) + (j0 & 15), nib);
+  } else {
+#pragma unroll
+    for (int c = 0; c < E / 32; ++c) {
+      uint32_t part[32];
+#pragma unroll
+      for (int e = 0; e < 32; ++e) part[e] = nib[32 * c + e];
+      store_nibbles<32>(Wq + wq_piece(n, (j0 >> 4) + c, K), part);
+    }
+  }
+}
+
 template <int K, bool kRot, bool kSub = false>
 __global__ __launch_bounds__(kRowThreads) void prep_weight_kernel(
     const uint16_t* __restrict__ W, int N, const int32_t* __restrict__ perm,
@@ -75,7 +94,7 @@ __global__ __launch_bounds__(kRowThreads) void prep_weight_kernel(
     uint32_t nib[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) nib[e] = int4_nibble(v[e] * winv);
-    store_nibbles<E>(Wq + (size_t)n * (K / 2) + (size_t)t * (E / 2), nib);
+    store_wq<E>(Wq, n, t * (E / 2), K, nib);
     if constexpr (kSub) {
       if ((t * E) % g == 0) w_scale[(size_t)((t * E) / g) * N + n] = __fdiv_rn(b, 7.0f);
     } else {

@@ -18,6 +18,27 @@ def to_np(t):
     return t.detach().cpu().numpy()
 
 
+def tile_wq(rows):
+    """Row-major packed weights (N x K/2 bytes) -> the tiled layout that
+    rrs_prepare_weight writes (include/rrs.h): 16-row blocks, each a run of K/128
+    tiles of 1 KB; inside tile c of block nb, byte (q * 16 + r) * 16 + e holds
+    packed byte 64 c + 16 q + e of row 16 nb + r. Returned as an N x K/2 array."""
+    rows = np.ascontiguousarray(rows, dtype=np.uint8)
+    N, Kh = rows.shape
+    assert N % 16 == 0 and Kh % 64 == 0
+    t = rows.reshape(N // 16, 16, Kh // 64, 4, 16).transpose(0, 2, 3, 1, 4)
+    return np.ascontiguousarray(t).reshape(N, Kh)
+
+
+def untile_wq(tiled):
+    """Inverse of tile_wq: tiled weight bytes -> N x K/2 row-major packed rows."""
+    tiled = np.ascontiguousarray(tiled, dtype=np.uint8)
+    N, Kh = tiled.shape
+    assert N % 16 == 0 and Kh % 64 == 0
+    t = tiled.reshape(N // 16, Kh // 64, 4, 16, 16).transpose(0, 3, 1, 2, 4)
+    return np.ascontiguousarray(t).reshape(N, Kh)
+
+
 def near_half_integer(v, rel=1e-6):
     """Pre-rounding values within rel*|v| of a rounding boundary (k + 1/2)."""
     v = np.asarray(v, np.float64)

@@ -414,3 +414,27 @@ def test_reorder_no_device():
         assert _rq(flags=f) == NODEV
         assert _rg(flags=f) == NODEV
         assert _rl(flags=f) == NODEV
+
+
+# ------------------------------------------------------------------ tiled Wq
+
+@pytest.mark.parametrize("N,K", [(16, 512), (48, 1024), (32, 4096)])
+def test_wq_tiling_helpers_follow_the_documented_layout(N, K):
+    # include/rrs.h: packed byte j of row n sits at
+    # (n/16) * 8K + (j/64) * 1024 + ((j%64)/16) * 256 + (n%16) * 16 + j%16.
+    import numpy as np
+    from tests._gpu_util import tile_wq, untile_wq
+    rows = np.random.default_rng(N + K).integers(0, 256, (N, K // 2), dtype=np.uint8)
+    flat = tile_wq(rows).reshape(-1)
+    assert flat.size == N * K // 2
+    for n in range(N):
+        for j in range(K // 2):
+            off = (n // 16) * 8 * K + (j // 64) * 1024 + ((j % 64) // 16) * 256 + (n % 16) * 16 \
+                + j % 16
+            assert flat[off] == rows[n, j]
+    np.testing.assert_array_equal(untile_wq(tile_wq(rows)), rows)
+    # a wave-sized slot (16 rows x 64 bytes of one K tile) is one contiguous 1 KB run
+    slot = rows[16:32, 64:128] if N >= 32 and K >= 256 else rows[:16, :64]
+    nb, c = (1, 1) if N >= 32 and K >= 256 else (0, 0)
+    run = flat[nb * 8 * K + c * 1024: nb * 8 * K + c * 1024 + 1024]
+    assert sorted(run.tolist()) == sorted(slot.reshape(-1).tolist())
