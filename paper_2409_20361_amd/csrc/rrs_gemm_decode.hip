@@ -73,18 +73,10 @@ __device__ __forceinline__ void load_words(const uint8_t* __restrict__ p, int st
 // Groups per wave: whole groups, K split in quarters (one group each when K
 // has fewer than four groups; waves past the last group get none).
 __host__ __device__ inline int groups_per_wave(int K, int g) { return K / g >= 4 ? K / g / 4 : 1; }
-// LDS bytes per row of one wave's slice of Xq: its groups, padded by 16 bytes
-// so the 16 rows a lane quarter reads start in different banks.
-__host__ __device__ inline int a_row_bytes(int K, int g) {
-  return groups_per_wave(K, g) * (g / 2) + 16;
-}
-constexpr int kMaxLdsA = 10240;  // per wave; four workgroups per CU fit in LDS
 constexpr int kPartBytes = 4 * kBlocks * 64 * 16;
 
-// GS = g / 64 MFMA k-steps per group. kLdsA: each wave first copies its K
-// quarter of Xq into LDS (when it fits), so the token fragments are LDS reads
-// instead of vector-memory loads queued behind the weight stream.
-template <int GS, bool kLdsA>
+// GS = g / 64 MFMA k-steps per group.
+template <int GS>
 __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
@@ -93,8 +85,8 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
   constexpr int g = GS * 64;
   constexpr int NW = g / 32;                  // words per lane per group and block
   constexpr int D = NW >= 16 ? 1 : (NW >= 8 ? 2 : 4);  // groups in flight
-  // Token slices during the loop; the partial sums reuse the space after it.
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsA ? 4 * kMaxLdsA : kPartBytes];
+  // The four waves' fp32 partial sums, added at the end.
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kPartBytes];
   v4f(*part)[kBlocks][64] = reinterpret_cast<v4f(*)[kBlocks][64]>(lds);
 
   const int t = threadIdx.x;
@@ -129,24 +121,13 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
     pb[j] = Wq + wq_piece(n, 0, K) + wo;
   }
 
-  // Wave-private LDS copy of this wave's K quarter of Xq: row r < M at
-  // r * a_row_bytes(K); lanes then read their row min(c, M - 1).
-  uint8_t* aq = lds + kq * kMaxLdsA;
-  const int arb = a_row_bytes(K, g);
-  const uint8_t* pal = aq + min(c, M - 1) * arb + xo;
 
   uint32_t wa[D][NW], wb[D][kBlocks][NW];
   auto load = [&](int d, int i) {
     const int b = min(b0 + i, G - 1);
-    if constexpr (!kLdsA) load_words<NW>(pa + (size_t)b * (g / 2), 64, wa[d]);
+    load_words<NW>(pa + (size_t)b * (g / 2), 64, wa[d]);
 #pragma unroll
     for (int j = 0; j < kBlocks; ++j) load_words<NW>(pb[j] + (size_t)b * (8 * g), 1024, wb[d][j]);
-  };
-  // Token words from LDS, read just before use (the quarter starts at group b0;
-  // padded steps past this wave's groups reread its last group).
-  auto read_a = [&](int d, int i) {
-    const int li = min(i, max(nb, 1) - 1);
-    load_words<NW>(pal + li * (g / 2), 64, wa[d]);
   };
 
   constexpr int kMagic = 0x4B400000;  // bits of 1.5 * 2^23
@@ -158,7 +139,6 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
     for (int r = 0; r < 4; ++r) f[j][r] = 0.0f;
 
   auto consume = [&](int d, int i) {
-    if constexpr (kLdsA) read_a(d, i);
     const float s = i < nb ? s_group[min(b0 + i, G - 1)] : 0.0f;
     v4i acc[kBlocks];
 #pragma unroll
@@ -184,21 +164,8 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
     }
   };
 
-  // The first groups' weight loads are issued before the token copy, so the
-  // weight stream starts at once instead of after the copy's load latency.
 #pragma unroll
   for (int d = 0; d < D; ++d) load(d, d);
-  // Wave-private copy of this wave's K quarter of Xq (see aq above).
-  if constexpr (kLdsA) {
-    const int qb = max(nb, 0) * (g / 2);  // bytes of this wave's groups in a row
-    const uint8_t* src = Xq + (size_t)b0 * (g / 2);
-    for (int e = lane * 16; e < M * qb; e += 64 * 16) {
-      const int r = e / qb;
-      const int o = e - r * qb;
-      *reinterpret_cast<uint4*>(aq + r * arb + o) =
-          *reinterpret_cast<const uint4*>(src + (size_t)r * krow + o);
-    }
-  }
   int i = 0;
   for (; i < steps - D; i += D) {
 #pragma unroll
@@ -211,7 +178,6 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
   for (int d = 0; d < D; ++d) consume(d, i + d);
 
   // Partial sums of the four K quarters, added in a fixed order.
-  if constexpr (kLdsA) __syncthreads();  // every wave is done with its token slice
 #pragma unroll
   for (int j = 0; j < kBlocks; ++j) part[kq][j][lane] = v4f{f[j][0], f[j][1], f[j][2], f[j][3]};
   __syncthreads();
@@ -441,12 +407,9 @@ hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
                                                             border, M, N, K, g, Y, out_scale);
     return hipGetLastError();
   }
-  const bool lds_a = (size_t)M * a_row_bytes(K, g) <= (size_t)kMaxLdsA;
-#define RRS_DECODE(GS_)                                                                  \
-  (lds_a ? (gemm_decode_kernel<GS_, true><<<grid, kThreads, 0, stream>>>(                 \
-               Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale), 0)             \
-         : (gemm_decode_kernel<GS_, false><<<grid, kThreads, 0, stream>>>(                \
-               Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale), 0))
+#define RRS_DECODE(GS_)                                                              \
+  gemm_decode_kernel<GS_><<<grid, kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale, M, \
+                                                         N, K, Y, out_scale)
   switch (g) {
     case 64: RRS_DECODE(1); break;
     case 128: RRS_DECODE(2); break;
