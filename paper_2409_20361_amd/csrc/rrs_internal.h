@@ -121,4 +121,13 @@ hipError_t launch_w4a4_gemm_reorder(const uint8_t* Xq, const float* a_scale,
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+// rotate + smooth + quant with one workgroup per row for M <= 16 tokens, no
+// static reorder, smoothing on (rrs_quant_rows.hip); the workspace holds
+// quant_rows_workspace_bytes(K, g) bytes of any content (set up by the call).
+bool quant_rows_fits(int M);
+size_t quant_rows_workspace_bytes(int K, int g);
+hipError_t launch_quant_rows(const uint16_t* X, int M, int K, int g, bool rotate, uint8_t* Xq,
+                             float* a_scale, float* s_group, void* workspace,
+                             hipStream_t stream);
+
 }  // namespace rrs
