@@ -467,7 +467,7 @@ hipError_t launch_w4a4_gemm_reorder(const uint8_t* Xq, const float* a_scale,
                                     const float* w_scale, const int32_t* border, int M, int N,
                                     int K, int g, uint16_t* Y, float out_scale,
                                     hipStream_t stream) {
-  if (decode_kernel_fits(M))
+  if (decode_gather_fits(M))
     return launch_w4a4_gemm_decode(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, out_scale,
                                    stream, border);
   // Every shape the ABI accepts fits the main kernel (K / 32 >= 16 is a power

@@ -1,4 +1,4 @@
-// W4A4 GEMM with Runtime Smooth for few tokens (decode: M <= 16), the same
+// W4A4 GEMM with Runtime Smooth for few tokens (decode: M <= 64), the same
 // product as the main kernel (Section 3.2, Eq. 3, Fig. 4 step (3)):
 //   Y[i, n] = fp16( alpha_i * beta_n / K * sum_b s_b * P_b[i, n] )
 //   P_b[i, n] = sum_{j in group b} qx[i, j] * qw[j, n]   (exact int32)
@@ -10,6 +10,10 @@
 //     waves split K into quarters (whole smoothing groups each) and add their
 //     fp32 partial sums in a fixed order at the end (deterministic); each
 //     wave unpacks its token codes once for both blocks;
+//   - tokens come in up to four blocks of 16 (TB), every block multiplied
+//     with the same weight words, so the weights still stream once for up to
+//     64 tokens (the 256-row tiles of the main kernel would leave most of
+//     their MFMA work idle at such M);
 //   - per group, lane (c, q) (c = lane % 16, q = lane / 16) takes g/8 bytes
 //     of Wq row n0 + c and the same bytes of Xq row c (zero for c >= M): for
 //     g = 64 bytes [8 q, 8 q + 8) of the group, for g >= 128 bytes
@@ -73,10 +77,11 @@ __device__ __forceinline__ void load_words(const uint8_t* __restrict__ p, int st
 // Groups per wave: whole groups, K split in quarters (one group each when K
 // has fewer than four groups; waves past the last group get none).
 __host__ __device__ inline int groups_per_wave(int K, int g) { return K / g >= 4 ? K / g / 4 : 1; }
-constexpr int kPartBytes = 4 * kBlocks * 64 * 16;
+constexpr int kMaxTokenBlocks = 4;  // up to 64 tokens
 
-// GS = g / 64 MFMA k-steps per group.
-template <int GS>
+// GS = g / 64 MFMA k-steps per group; TB token blocks of 16 rows (tokens
+// 16 tb .. 16 tb + 15 in block tb), all multiplied with the same weight words.
+template <int GS, int TB>
 __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
@@ -84,10 +89,11 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
     float out_scale) {
   constexpr int g = GS * 64;
   constexpr int NW = g / 32;                  // words per lane per group and block
-  constexpr int D = NW >= 16 ? 1 : (NW >= 8 ? 2 : 4);  // groups in flight
+  constexpr int D0 = NW >= 16 ? 1 : (NW >= 8 ? 2 : 4);
+  constexpr int D = TB >= 4 && D0 > 1 ? D0 / 2 : D0;  // groups in flight
   // The four waves' fp32 partial sums, added at the end.
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kPartBytes];
-  v4f(*part)[kBlocks][64] = reinterpret_cast<v4f(*)[kBlocks][64]>(lds);
+  __shared__ __attribute__((aligned(16))) uint8_t lds[4 * TB * kBlocks * 64 * 16];
+  v4f(*part)[TB][kBlocks][64] = reinterpret_cast<v4f(*)[TB][kBlocks][64]>(lds);
 
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -113,7 +119,9 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
   // in the group's region of the column block's tiled rows (8 g bytes).
   const int xo = g == 64 ? q * 8 : q * 16;
   const int wo = g == 64 ? (q >> 1) * 256 + c * 16 + (q & 1) * 8 : lane * 16;
-  const uint8_t* pa = Xq + (size_t)min(c, M - 1) * krow + xo;
+  const uint8_t* pa[TB];
+#pragma unroll
+  for (int tb = 0; tb < TB; ++tb) pa[tb] = Xq + (size_t)min(16 * tb + c, M - 1) * krow + xo;
   const uint8_t* pb[kBlocks];
 #pragma unroll
   for (int j = 0; j < kBlocks; ++j) {
@@ -121,47 +129,58 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
     pb[j] = Wq + wq_piece(n, 0, K) + wo;
   }
 
-
-  uint32_t wa[D][NW], wb[D][kBlocks][NW];
+  uint32_t wa[D][TB][NW], wb[D][kBlocks][NW];
   auto load = [&](int d, int i) {
     const int b = min(b0 + i, G - 1);
-    load_words<NW>(pa + (size_t)b * (g / 2), 64, wa[d]);
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) load_words<NW>(pa[tb] + (size_t)b * (g / 2), 64, wa[d][tb]);
 #pragma unroll
     for (int j = 0; j < kBlocks; ++j) load_words<NW>(pb[j] + (size_t)b * (8 * g), 1024, wb[d][j]);
   };
 
   constexpr int kMagic = 0x4B400000;  // bits of 1.5 * 2^23
   const v4i seed = GS > 4 ? v4i{0, 0, 0, 0} : v4i{kMagic, kMagic, kMagic, kMagic};
-  float f[kBlocks][4];
+  float f[TB][kBlocks][4];
 #pragma unroll
-  for (int j = 0; j < kBlocks; ++j)
+  for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) f[j][r] = 0.0f;
+    for (int j = 0; j < kBlocks; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) f[tb][j][r] = 0.0f;
 
   auto consume = [&](int d, int i) {
     const float s = i < nb ? s_group[min(b0 + i, G - 1)] : 0.0f;
-    v4i acc[kBlocks];
+    v4i acc[TB][kBlocks];
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) acc[j] = seed;
+    for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+      for (int j = 0; j < kBlocks; ++j) acc[tb][j] = seed;
 #pragma unroll
     for (int st = 0; st < GS; ++st) {
-      const v4i a = unpack_pair(wa[d][2 * st], wa[d][2 * st + 1]);
+      v4i bv[kBlocks];
 #pragma unroll
-      for (int j = 0; j < kBlocks; ++j)
-        acc[j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(
-            a, unpack_pair(wb[d][j][2 * st], wb[d][j][2 * st + 1]), acc[j], 0, 0, 0);
-    }
+      for (int j = 0; j < kBlocks; ++j) bv[j] = unpack_pair(wb[d][j][2 * st], wb[d][j][2 * st + 1]);
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) {
-      // Bit-cast the whole vector, then index: bit-casting a single element
-      // of an ext_vector is miscompiled (every element reads element 0).
-      const v4f accf = __builtin_bit_cast(v4f, acc[j]);
+      for (int tb = 0; tb < TB; ++tb) {
+        const v4i a = unpack_pair(wa[d][tb][2 * st], wa[d][tb][2 * st + 1]);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float pv = GS > 4 ? (float)acc[j][r] : accf[r] - 12582912.0f;
-        f[j][r] = __builtin_fmaf(s, pv, f[j][r]);
+        for (int j = 0; j < kBlocks; ++j)
+          acc[tb][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, bv[j], acc[tb][j], 0, 0, 0);
       }
     }
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+      for (int j = 0; j < kBlocks; ++j) {
+        // Bit-cast the whole vector, then index: bit-casting a single element
+        // of an ext_vector is miscompiled (every element reads element 0).
+        const v4f accf = __builtin_bit_cast(v4f, acc[tb][j]);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float pv = GS > 4 ? (float)acc[tb][j][r] : accf[r] - 12582912.0f;
+          f[tb][j][r] = __builtin_fmaf(s, pv, f[tb][j][r]);
+        }
+      }
   };
 
 #pragma unroll
@@ -179,32 +198,39 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
 
   // Partial sums of the four K quarters, added in a fixed order.
 #pragma unroll
-  for (int j = 0; j < kBlocks; ++j) part[kq][j][lane] = v4f{f[j][0], f[j][1], f[j][2], f[j][3]};
+  for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+    for (int j = 0; j < kBlocks; ++j)
+      part[kq][tb][j][lane] = v4f{f[tb][j][0], f[tb][j][1], f[tb][j][2], f[tb][j][3]};
   __syncthreads();
   // Wave w stores column block w (if any): sums in the order kq = 0, 1, 2, 3.
   const int w = t >> 6;
   if (w < kBlocks && n0 + w * kCols < N) {
-    v4f sum = part[0][w][lane];
-#pragma unroll
-    for (int p = 1; p < 4; ++p) {
-      const v4f x = part[p][w][lane];
-      sum.x += x.x;
-      sum.y += x.y;
-      sum.z += x.z;
-      sum.w += x.w;
-    }
     // out_scale = 2^-8 (undoes the 16 x 16 of the unpacked operands) / K (the
     // unnormalized rotation; 1 without rotation), an exact power of two.
     const float inv = out_scale;
     const int col = n0 + w * kCols + c;
     const float bcol = w_scale[col];
-    const float sv[4] = {sum.x, sum.y, sum.z, sum.w};
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = 4 * q + r;  // output row of accumulator r of this lane
-      if (row < M) {
-        const float sc = a_scale[row] * inv;
-        Y[(size_t)row * N + col] = __builtin_bit_cast(uint16_t, (_Float16)((sv[r] * sc) * bcol));
+    for (int tb = 0; tb < TB; ++tb) {
+      v4f sum = part[0][tb][w][lane];
+#pragma unroll
+      for (int p = 1; p < 4; ++p) {
+        const v4f x = part[p][tb][w][lane];
+        sum.x += x.x;
+        sum.y += x.y;
+        sum.z += x.z;
+        sum.w += x.w;
+      }
+      const float sv[4] = {sum.x, sum.y, sum.z, sum.w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * tb + 4 * q + r;  // output row of accumulator r of this lane
+        if (row < M) {
+          const float sc = a_scale[row] * inv;
+          Y[(size_t)row * N + col] =
+              __builtin_bit_cast(uint16_t, (_Float16)((sv[r] * sc) * bcol));
+        }
       }
     }
   }
@@ -394,7 +420,8 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_gather_kernel(
 
 }  // namespace
 
-bool decode_kernel_fits(int M) { return M >= 1 && M <= kCols; }
+bool decode_kernel_fits(int M) { return M >= 1 && M <= kCols * kMaxTokenBlocks; }
+bool decode_gather_fits(int M) { return M >= 1 && M <= kCols; }
 
 hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
                                    const float* s_group, const uint8_t* Wq,
@@ -403,20 +430,27 @@ hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
                                    const int32_t* border) {
   const int grid = (N / kCols + kBlocks - 1) / kBlocks;  // N % 16 == 0 (API precondition)
   if (border) {
+    if (M > kCols) return hipErrorInvalidValue;  // the gather kernel takes one token block
     gemm_decode_gather_kernel<<<grid, kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale,
                                                             border, M, N, K, g, Y, out_scale);
     return hipGetLastError();
   }
-#define RRS_DECODE(GS_)                                                              \
-  gemm_decode_kernel<GS_><<<grid, kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale, M, \
-                                                         N, K, Y, out_scale)
+  const int tbs = M <= kCols ? 1 : (M <= 2 * kCols ? 2 : 4);
+#define RRS_DECODE(GS_, TB_)                                                             \
+  gemm_decode_kernel<GS_, TB_><<<grid, kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq, \
+                                                              w_scale, M, N, K, Y, out_scale)
+#define RRS_DECODE_TB(GS_)                      \
+  if (tbs == 1) RRS_DECODE(GS_, 1);             \
+  else if (tbs == 2) RRS_DECODE(GS_, 2);        \
+  else RRS_DECODE(GS_, 4);
   switch (g) {
-    case 64: RRS_DECODE(1); break;
-    case 128: RRS_DECODE(2); break;
-    case 256: RRS_DECODE(4); break;
-    case 512: RRS_DECODE(8); break;
+    case 64: RRS_DECODE_TB(1) break;
+    case 128: RRS_DECODE_TB(2) break;
+    case 256: RRS_DECODE_TB(4) break;
+    case 512: RRS_DECODE_TB(8) break;
     default: return hipErrorInvalidValue;
   }
+#undef RRS_DECODE_TB
 #undef RRS_DECODE
   return hipGetLastError();
 }

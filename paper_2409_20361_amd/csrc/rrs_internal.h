@@ -66,8 +66,10 @@ hipError_t launch_w4a4_gemm_partials_small(const uint8_t* Xq, const uint8_t* Wq,
                                            int N, int K, int g, int32_t* P,
                                            hipStream_t stream);
 
-// Few-token kernel (decode): streams Wq once, for M <= 16.
+// Few-token kernel (decode): streams Wq once, for M <= 64 (up to four blocks
+// of 16 tokens); its runtime-reorder variant takes M <= 16.
 bool decode_kernel_fits(int M);
+bool decode_gather_fits(int M);
 hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
                                    const float* s_group, const uint8_t* Wq,
                                    const float* w_scale, int M, int N, int K, int g,

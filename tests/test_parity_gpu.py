@@ -347,7 +347,7 @@ def _gemm_codes_case(qx, qw, g, seed, label):
     return P
 
 
-@pytest.mark.parametrize("M", [1, 8, 16])
+@pytest.mark.parametrize("M", [1, 8, 16, 17, 40, 64])
 @pytest.mark.parametrize("g", [64, 128, 256, 512])
 def test_gemm_few_tokens_extreme(M, g):
     # Few-token (decode) kernel with every code +-7: |P_b| = 49 g.
@@ -365,12 +365,13 @@ def test_gemm_few_tokens_extreme(M, g):
     (1, 512, 16, 512), (2, 512, 48, 64), (3, 1024, 272, 128), (8, 8192, 144, 128),
     (13, 4096, 64, 256), (16, 16384, 32, 64), (16, 2048, 1040, 512), (17, 2048, 80, 128),
     (16, 8192, 96, 128), (8, 16384, 32, 128), (12, 8192, 48, 256),
+    (24, 1024, 48, 64), (32, 4096, 144, 128), (33, 512, 16, 512), (48, 8192, 80, 256),
+    (64, 2048, 272, 64), (64, 16384, 32, 128), (65, 2048, 48, 128),
 ])
 def test_gemm_few_tokens_random(M, K, N, g):
-    # M <= 16 runs the few-token kernel (M = 17 the main kernel): every K
-    # split, group size and ragged column count, against the oracle; the token
-    # slice in LDS (up to 10 KB per wave) or from global memory (16x8192,
-    # 8x16384, 12x8192, 16x16384).
+    # M <= 64 runs the few-token kernel (one, two or four blocks of 16 tokens;
+    # M = 65 the main kernel): every K split, group size, ragged token and
+    # column count, against the oracle.
     rng = np.random.default_rng(M * 31 + K + N)
     qx = rng.integers(-7, 8, size=(M, K)).astype(np.int8)
     qw = rng.integers(-7, 8, size=(K, N)).astype(np.int8)
