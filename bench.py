@@ -16,7 +16,7 @@ A decode-shaped measurement (M=8, K=8192, N=28672) reports HBM GB/s of the
 GEMM over algorithmic bytes, cycling through 4 weight copies (470 MB, more
 than the 256 MB Infinity Cache) so that every call streams its weight from HBM.
 Further objects on the same line: few-token layers at the decode shape
-(M = 1..16), the gate/up and large prefill configurations against their own
+(M = 1..64), the gate/up and large prefill configurations against their own
 rooflines, the runtime-reorder comparison, the kernel comparison of the three
 scale schemes, and the CPU oracle baseline.
 
@@ -334,9 +334,10 @@ def config_bench(torch, rrs, synth, names=("gateup", "large"), reps=10):
 
 def few_token_bench(torch, rrs, synth, reps=50):
     """Few-token layers at the decode shape (K=8192, N=28672, g=128) for
-    M = 1, 2, 4, 8, 16: quantizer, GEMM and the whole layer, each timed alone
-    with HIP events, weights cycling through 4 copies. Up to M = 4 at this K
-    the quantizer is the one-launch kernel."""
+    M = 1, 2, 4, 8, 16, 32, 64: quantizer, GEMM and the whole layer, each timed
+    with HIP events around 50 back-to-back calls, weights cycling through 4
+    copies. Up to M = 16 the quantizer is one launch with one workgroup per
+    row; up to M = 64 the GEMM is the few-token kernel."""
     dev = torch.device("cuda:0")
     base = synth.WORKLOADS["decode"]
     W = torch.from_numpy(synth.weights(base)).to(dev)
@@ -344,7 +345,7 @@ def few_token_bench(torch, rrs, synth, reps=50):
     del W
     copies = [Wq0] + [Wq0.clone() for _ in range(3)]
     rows = []
-    for M in (1, 2, 4, 8, 16):
+    for M in (1, 2, 4, 8, 16, 32, 64):
         w = synth.custom("d", M, base.K, base.N, base.g, 40 + M, n_chan=82, n_spike=2,
                          spike_mag=(100, 500))
         X = torch.from_numpy(synth.activations(w)).to(dev)
