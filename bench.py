@@ -37,7 +37,7 @@ METRIC = "effective W4A4 TOPS at M=2048,K=4096,N=12288; HBM GB/s at M=8 decode"
 # --pmc runs (FETCH_SIZE, WRITE_SIZE) scaled by a 256 MiB copy-kernel
 # calibration (profiles/gemm_main_kernel_qkv.md), keyed by the sha1 prefix of
 # the kernel source they were measured on. Any other source reports null.
-GEMM_TRAFFIC_BYTES = {"4c9b40f16dc8": 159.66e6}
+GEMM_TRAFFIC_BYTES = {}
 INT8_MFMA_PEAK_TOPS = 5000.0   # MI355X dense int8 MFMA, 5.0 POP/s
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 
@@ -64,6 +64,8 @@ def parse():
     ap.add_argument("--decode-only", action="store_true",
                     help="only the decode measurement (for per-kernel profiles)")
     ap.add_argument("--decode-steps", type=int, default=100)
+    ap.add_argument("--no-tiled", action="store_true",
+                    help="decode measurement on the row-major weights only")
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the HIP-graph replay timings")
     ap.add_argument("--graph-only", action="store_true",
@@ -162,44 +164,52 @@ def decode_bench(args, torch, rrs, synth):
     dev = torch.device("cuda:0")
     log(f"decode M={w.M} K={w.K} N={w.N}: generating inputs")
     X = torch.from_numpy(synth.activations(w)).to(dev)
-    Wq0, beta = rrs.prepare_weight(torch.from_numpy(synth.weights(w)).to(dev))
-    copies = [Wq0] + [Wq0.clone() for _ in range(3)]   # 4 x 117 MB > 256 MB MALL
+    W = torch.from_numpy(synth.weights(w)).to(dev)
     Xq, a, s = rrs.rotate_smooth_quant(X, w.g)
     Y = torch.empty((w.M, w.N), dtype=torch.float16, device=dev)
     lws = torch.empty((rrs.linear_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
                       device=dev)
-    it = iter(range(1 << 30))
-    prewarm(torch, lambda: rrs.w4a4_gemm(Xq, a, s, copies[next(it) % 4], beta, w.g, out=Y))
-    torch.cuda.synchronize()
-    n = args.decode_steps
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
-    ev[0].record()
-    for i in range(n):
-        rrs.w4a4_gemm(Xq, a, s, copies[i % 4], beta, w.g, out=Y)
-        ev[i + 1].record()
-    torch.cuda.synchronize()
-    g_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(n)]
-    ev2 = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
-    ev2[0].record()
-    for i in range(n):
-        rrs.linear(X, copies[i % 4], beta, w.g, workspace=lws, out=Y)
-        ev2[i + 1].record()
-    torch.cuda.synchronize()
-    l_ms = [ev2[i].elapsed_time(ev2[i + 1]) for i in range(n)]
     alg = (w.M * w.K // 2 + 4 * w.M + 4 * w.G + w.N * w.K // 2 + 4 * w.N + 2 * w.M * w.N)
-    gm = sum(g_ms) / n
-    lm = sum(l_ms) / n
-    return {
-        "config": {"workload": "decode", "M": w.M, "K": w.K, "N": w.N, "group_size": w.g},
-        "algorithmic_bytes": alg,
-        "gemm_us": round(gm * 1e3, 3),
-        "gemm_us_min": round(min(g_ms) * 1e3, 3),
-        "gemm_GBps": round(alg / (gm * 1e-3) / 1e9, 1),
-        "gemm_frac_hbm": round(alg / (gm * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-        "linear_us": round(lm * 1e3, 3),
-        "linear_GBps": round(alg / (lm * 1e-3) / 1e9, 1),
-        "weight_copies": 4,
-    }
+    n = args.decode_steps
+
+    def measure(flags):
+        Wq0, beta = rrs.prepare_weight(W, flags=flags)
+        copies = [Wq0] + [Wq0.clone() for _ in range(3)]   # 4 x 117 MB > 256 MB MALL
+        it = iter(range(1 << 30))
+        prewarm(torch, lambda: rrs.w4a4_gemm(Xq, a, s, copies[next(it) % 4], beta, w.g, out=Y,
+                                             flags=flags))
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        ev[0].record()
+        for i in range(n):
+            rrs.w4a4_gemm(Xq, a, s, copies[i % 4], beta, w.g, out=Y, flags=flags)
+            ev[i + 1].record()
+        torch.cuda.synchronize()
+        g_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(n)]
+        ev2 = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        ev2[0].record()
+        for i in range(n):
+            rrs.linear(X, copies[i % 4], beta, w.g, workspace=lws, out=Y, flags=flags)
+            ev2[i + 1].record()
+        torch.cuda.synchronize()
+        l_ms = [ev2[i].elapsed_time(ev2[i + 1]) for i in range(n)]
+        gm = sum(g_ms) / n
+        lm = sum(l_ms) / n
+        return {
+            "gemm_us": round(gm * 1e3, 3),
+            "gemm_us_min": round(min(g_ms) * 1e3, 3),
+            "gemm_GBps": round(alg / (gm * 1e-3) / 1e9, 1),
+            "gemm_frac_hbm": round(alg / (gm * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "linear_us": round(lm * 1e3, 3),
+            "linear_GBps": round(alg / (lm * 1e-3) / 1e9, 1),
+        }
+
+    out = {"config": {"workload": "decode", "M": w.M, "K": w.K, "N": w.N, "group_size": w.g},
+           "algorithmic_bytes": alg, "weight_copies": 4, "weight_layout": "row-major"}
+    out.update(measure(0))
+    if not args.no_tiled:
+        out["tiled"] = measure(rrs.WEIGHT_TILED)
+    return out
 
 
 def graph_bench(torch, rrs, synth, reps=50):
@@ -337,13 +347,17 @@ def few_token_bench(torch, rrs, synth, reps=50):
     M = 1, 2, 4, 8, 16, 32, 64: quantizer, GEMM and the whole layer, each timed
     with HIP events around 50 back-to-back calls, weights cycling through 4
     copies. Up to M = 16 the quantizer is one launch with one workgroup per
-    row; up to M = 64 the GEMM is the few-token kernel."""
+    row; up to M = 64 the GEMM is the few-token kernel. The *_tiled entries
+    run the same calls on the tiled weight layout."""
     dev = torch.device("cuda:0")
     base = synth.WORKLOADS["decode"]
     W = torch.from_numpy(synth.weights(base)).to(dev)
     Wq0, beta = rrs.prepare_weight(W)
+    Wt0, _ = rrs.prepare_weight(W, flags=rrs.WEIGHT_TILED)
     del W
     copies = [Wq0] + [Wq0.clone() for _ in range(3)]
+    tiled = [Wt0] + [Wt0.clone() for _ in range(3)]
+    T = rrs.WEIGHT_TILED
     rows = []
     for M in (1, 2, 4, 8, 16, 32, 64):
         w = synth.custom("d", M, base.K, base.N, base.g, 40 + M, n_chan=82, n_spike=2,
@@ -361,6 +375,10 @@ def few_token_bench(torch, rrs, synth, reps=50):
             "quant": lambda i: rrs.rotate_smooth_quant(X, w.g, workspace=qws, out=(Xq, a, s)),
             "gemm": lambda i: rrs.w4a4_gemm(Xq, a, s, copies[i % 4], beta, w.g, out=Y),
             "linear": lambda i: rrs.linear(X, copies[i % 4], beta, w.g, workspace=lws, out=Y),
+            "gemm_tiled": lambda i: rrs.w4a4_gemm(Xq, a, s, tiled[i % 4], beta, w.g, out=Y,
+                                                  flags=T),
+            "linear_tiled": lambda i: rrs.linear(X, tiled[i % 4], beta, w.g, workspace=lws,
+                                                 out=Y, flags=T),
         }
         row = {"M": M}
         for key, fn in calls.items():
@@ -377,6 +395,7 @@ def few_token_bench(torch, rrs, synth, reps=50):
         alg = M * w.K // 2 + 4 * M + 4 * w.G + w.N * w.K // 2 + 4 * w.N + 2 * M * w.N
         row["linear_GBps"] = round(alg / (row["linear_us"] * 1e-6) / 1e9, 1)
         row["gemm_GBps"] = round(alg / (row["gemm_us"] * 1e-6) / 1e9, 1)
+        row["gemm_tiled_GBps"] = round(alg / (row["gemm_tiled_us"] * 1e-6) / 1e9, 1)
         rows.append(row)
     return {"K": base.K, "N": base.N, "group_size": base.g, "weight_copies": 4, "rows": rows}
 

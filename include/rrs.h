@@ -38,17 +38,20 @@
  *  - W:  K x N float16, row-major (the transpose of nn.Linear's weight).
  *  - Xq: M x K/2 bytes, row-major. Codes are INT4 two's complement in
  *    [-7, 7], two per byte, the low nibble holding the even channel index.
- *  - Wq: N x K/2 bytes of the same packed codes (row n = output channel n),
- *    tiled: rows in blocks of 16, each block stored as its K/128 tiles of
- *    16 rows x 64 bytes (1 KB) one after another, and inside a tile the
- *    four 16-byte quarters of the 16 rows quarter by quarter. Packed byte j
- *    of row n sits at byte
+ *  - Wq: N x K/2 bytes of the same packed codes, row-major (row n = output
+ *    channel n, K contiguous): packed byte j of row n at n * K/2 + j.
+ *    Optional tiled layout (flag RRS_WEIGHT_TILED of the _ex functions):
+ *    rows in blocks of 16, each block stored as its K/128 tiles of 16 rows x
+ *    64 bytes (1 KB) one after another, and inside a tile the four 16-byte
+ *    quarters of the 16 rows quarter by quarter, so packed byte j of row n
+ *    sits at
  *      (n / 16) * 8K + (j / 64) * 1024 + ((j % 64) / 16) * 256
  *        + (n % 16) * 16 + j % 16.
- *    A wave's load of one K tile of 16 channels is then one contiguous 1 KB
- *    run, which the few-token GEMM streams at close to copy speed. Every
- *    entry point that takes Wq expects this layout, as written by
- *    rrs_prepare_weight / rrs_prepare_weight_sub_channel.
+ *    There a wave's load of one K tile of 16 channels is one contiguous 1 KB
+ *    run, which the few-token GEMM (M <= 64) streams about 10 % faster than
+ *    the row-major rows. Results are bit-identical in both layouts; a weight
+ *    prepared with the flag must be multiplied with it, and one prepared
+ *    without it without it.
  *  - a_scale: M float32 (per token); w_scale: N float32 (per output channel);
  *    s_group: K/g float32 (one smoothing scale per channel group).
  *  - Y:  M x N float16, row-major.
@@ -95,8 +98,13 @@ enum {
  * of one layer (weight preparation and the GEMM take only RRS_SKIP_ROTATION
  * into account; RRS_SKIP_SMOOTHING is accepted and has no effect there, except
  * that rrs_prepare_weight_ex rejects it: weights are never smoothed).
+ *
+ * Layout switch (not an ablation): RRS_WEIGHT_TILED selects the tiled Wq
+ * layout above for every call that writes or reads Wq. Every _ex function
+ * accepts it; the ones that do not touch Wq ignore it, so one flags value
+ * can serve all calls of a layer.
  */
-enum { RRS_SKIP_ROTATION = 1, RRS_SKIP_SMOOTHING = 2 };
+enum { RRS_SKIP_ROTATION = 1, RRS_SKIP_SMOOTHING = 2, RRS_WEIGHT_TILED = 4 };
 
 /* Human-readable name of a status code (static storage; never NULL). */
 const char* rrs_status_string(rrs_status status);
@@ -120,7 +128,7 @@ size_t rrs_workspace_bytes(int M, int K, int group_size);
  *                reorder of Fig. 4 step (1)); pass the same perm to
  *                rrs_rotate_smooth_quant / rrs_linear.
  *   Wq      out: N x K/2 bytes, packed INT4 codes of u = H_K W per column,
- *                in the tiled layout above.
+ *                row-major (tiled with RRS_WEIGHT_TILED in the _ex call).
  *   w_scale out: N float32, beta_n = max_k |u_kn| / 7.
  * Not on the timed path.
  */
@@ -128,7 +136,8 @@ rrs_status rrs_prepare_weight(const void* W, int K, int N, const int32_t* perm,
                               void* Wq, float* w_scale, void* stream);
 
 /* rrs_prepare_weight with flags: RRS_SKIP_ROTATION quantizes W itself
- * (u = W) for the ablation without rotation; any other bit -> RRS_ERR_FLAGS. */
+ * (u = W) for the ablation without rotation; RRS_WEIGHT_TILED writes the
+ * tiled layout; any other bit -> RRS_ERR_FLAGS. */
 rrs_status rrs_prepare_weight_ex(const void* W, int K, int N, const int32_t* perm, int flags,
                                  void* Wq, float* w_scale, void* stream);
 
@@ -196,7 +205,7 @@ rrs_status rrs_linear(const void* X, const void* Wq, const float* w_scale, int M
 
 /* rrs_linear with ablation flags (quantization and GEMM as in their _ex
  * forms); Wq and w_scale must come from rrs_prepare_weight_ex with the same
- * RRS_SKIP_ROTATION bit. */
+ * RRS_SKIP_ROTATION and RRS_WEIGHT_TILED bits. */
 rrs_status rrs_linear_ex(const void* X, const void* Wq, const float* w_scale, int M, int N,
                          int K, int group_size, const int32_t* perm, int flags, void* Y,
                          void* workspace, size_t workspace_bytes, void* stream);
@@ -204,7 +213,8 @@ rrs_status rrs_linear_ex(const void* X, const void* Wq, const float* w_scale, in
 /*
  * Test hook: the exact int32 group partials P[b][i][n] (b < K/g, i < M,
  * n < N; G x M x N int32, row-major) from the same GEMM main loop as
- * rrs_w4a4_gemm, before any scaling (Eq. 3's inner sums per block).
+ * rrs_w4a4_gemm, before any scaling (Eq. 3's inner sums per block). Wq
+ * row-major.
  */
 rrs_status rrs_w4a4_gemm_partials(const void* Xq, const void* Wq, int M, int N, int K,
                                   int group_size, int32_t* P, void* stream);
@@ -235,7 +245,7 @@ enum {
  *   Xq out    : M x K/2 bytes, packed as for rrs_rotate_smooth_quant.
  *   a_sub out : L x M float32, a_sub[b * M + i] = fl(m / 7), L = K / g (group-major).
  * One launch; no workspace. Shapes and errors as rrs_rotate_smooth_quant
- * (flags: only RRS_SKIP_ROTATION).
+ * (flags: RRS_SKIP_ROTATION; RRS_WEIGHT_TILED is accepted and ignored).
  */
 rrs_status rrs_quantize_sub_channel(const void* X, int M, int K, int group_size, int flags,
                                     void* Xq, float* a_sub, void* stream);
@@ -244,7 +254,8 @@ rrs_status rrs_quantize_sub_channel(const void* X, int M, int K, int group_size,
  * Sub-channel weight preparation: u = H_K W (W with RRS_SKIP_ROTATION), then
  * for output channel n and group b the same RTN as above.
  *   W in      : K x N float16, row-major.
- *   Wq out    : N x K/2 bytes, as rrs_prepare_weight.
+ *   Wq out    : N x K/2 bytes, as rrs_prepare_weight_ex (RRS_WEIGHT_TILED
+ *               for the tiled layout).
  *   w_sub out : L x N float32, w_sub[b * N + n] (group-major).
  */
 rrs_status rrs_prepare_weight_sub_channel(const void* W, int K, int N, int group_size,
@@ -314,7 +325,8 @@ size_t rrs_reorder_workspace_bytes(int M, int K, int group_size);
  *   workspace       : at least rrs_reorder_workspace_bytes(M, K, g) bytes.
  * flags: RRS_SKIP_ROTATION (reorder the unrotated channels: Runtime Smooth
  * with its reorder step); RRS_SKIP_SMOOTHING -> RRS_ERR_FLAGS (without
- * smoothing the order changes nothing). Three launches.
+ * smoothing the order changes nothing); RRS_WEIGHT_TILED is accepted and
+ * ignored. Three launches.
  */
 rrs_status rrs_rotate_smooth_quant_reorder(const void* X, int M, int K, int group_size,
                                            int flags, void* Xq, float* a_scale,
@@ -331,8 +343,8 @@ rrs_status rrs_rotate_smooth_quant_reorder(const void* X, int M, int K, int grou
  * without perm; Xq, a_scale, s_group, block_order from
  * rrs_rotate_smooth_quant_reorder. block_order is read on the device and each
  * entry is reduced modulo K/32 (loads stay in bounds for any table; a table
- * that is not a permutation gives meaningless results). flags: only
- * RRS_SKIP_ROTATION. Other errors as rrs_w4a4_gemm_ex.
+ * that is not a permutation gives meaningless results). flags:
+ * RRS_SKIP_ROTATION, RRS_WEIGHT_TILED. Other errors as rrs_w4a4_gemm_ex.
  */
 rrs_status rrs_w4a4_gemm_reorder(const void* Xq, const float* a_scale, const float* s_group,
                                  const void* Wq, const float* w_scale,
@@ -347,7 +359,8 @@ size_t rrs_linear_reorder_workspace_bytes(int M, int K, int group_size);
  * One RRS linear layer with the runtime reorder:
  * rrs_rotate_smooth_quant_reorder followed by rrs_w4a4_gemm_reorder, the
  * intermediates kept in the workspace. W prepared by rrs_prepare_weight
- * (perm = NULL, same RRS_SKIP_ROTATION bit). Errors as the two calls.
+ * (perm = NULL, same RRS_SKIP_ROTATION and RRS_WEIGHT_TILED bits). Errors as
+ * the two calls.
  */
 rrs_status rrs_linear_reorder(const void* X, const void* Wq, const float* w_scale, int M,
                               int N, int K, int group_size, int flags, void* Y, void* workspace,

@@ -19,6 +19,7 @@ from ._binding import (  # noqa: F401
     SCHEME_SUB_CHANNEL,
     SKIP_ROTATION,
     SKIP_SMOOTHING,
+    WEIGHT_TILED,
     RRSError,
     lib,
     lib_path,
@@ -44,7 +45,7 @@ from ._binding import (  # noqa: F401
 
 __all__ = [
     "REORDER_BLOCK", "SCHEME_PER_CHANNEL", "SCHEME_RUNTIME_SMOOTH", "SCHEME_SUB_CHANNEL",
-    "SKIP_ROTATION", "SKIP_SMOOTHING", "RRSError", "lib", "lib_path", "linear", "linear_reorder",
+    "SKIP_ROTATION", "SKIP_SMOOTHING", "WEIGHT_TILED", "RRSError", "lib", "lib_path", "linear", "linear_reorder",
     "linear_reorder_workspace_bytes", "linear_workspace_bytes",
     "prepare_weight", "prepare_weight_sub_channel", "quantize_sub_channel",
     "reorder_workspace_bytes", "rotate_smooth_quant", "rotate_smooth_quant_reorder",

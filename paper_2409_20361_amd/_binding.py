@@ -61,6 +61,7 @@ SCHEME_SUB_CHANNEL = 2
 # Ablation switches (include/rrs.h): 0 is RRS itself.
 SKIP_ROTATION = 1    # plain Runtime Smooth: no Hadamard rotation
 SKIP_SMOOTHING = 2   # rotation + per-token quantization only (smoothing scales all 1)
+WEIGHT_TILED = 4     # Wq in 16-row blocks of 1 KB tiles (layout switch, not an ablation)
 
 
 class RRSError(RuntimeError):
@@ -139,8 +140,9 @@ def prepare_weight(W: torch.Tensor, perm: Optional[torch.Tensor] = None, flags: 
                    ) -> Tuple[torch.Tensor, torch.Tensor]:
     """W: K x N fp16 (the transpose of nn.Linear's weight) -> (Wq N x K/2 uint8, w_scale N f32).
 
-    Wq holds the packed codes in the tiled layout of include/rrs.h (16-row
-    blocks of 1 KB tiles), which every GEMM entry point expects."""
+    Wq holds the packed codes row-major; with flags | WEIGHT_TILED in the tiled
+    layout of include/rrs.h (16-row blocks of 1 KB tiles), which the GEMM calls
+    then need the same flag for."""
     K, N = W.shape
     wp = _dev(W, "W", torch.float16, (K, N))
     Wq = torch.empty((N, K // 2), dtype=torch.uint8, device=W.device)

@@ -14,7 +14,7 @@
 
 namespace {
 
-constexpr int kVersion = 400;  // 0.4.0: runtime channel reorder
+constexpr int kVersion = 500;  // 0.5.0: row-major Wq by default, RRS_WEIGHT_TILED option
 constexpr int kMaxDevices = 64;
 
 bool is_aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -26,9 +26,15 @@ bool valid_group(int K, int g) {
   return (g == 64 || g == 128 || g == 256 || g == 512) && K % g == 0;
 }
 bool valid_flags(int flags, int allowed) { return (flags & ~allowed) == 0; }
-constexpr int kAllFlags = RRS_SKIP_ROTATION | RRS_SKIP_SMOOTHING;
+// Every _ex function accepts RRS_WEIGHT_TILED, so that one flags value can
+// serve all calls of a layer; only the calls that read or write Wq use it.
+constexpr int kQuantFlags = RRS_SKIP_ROTATION | RRS_SKIP_SMOOTHING;
+constexpr int kAllFlags = kQuantFlags | RRS_WEIGHT_TILED;
+constexpr int kRotationFlags = RRS_SKIP_ROTATION | RRS_WEIGHT_TILED;
 static_assert(RRS_SKIP_ROTATION == rrs::kSkipRotation && RRS_SKIP_SMOOTHING == rrs::kSkipSmoothing,
               "public and internal flag values agree");
+
+rrs::WqLayout layout(int flags) { return rrs::WqLayout{(flags & RRS_WEIGHT_TILED) != 0}; }
 
 // Output scale of the GEMM: 2^-8 undoes the 16 x 16 of the unpacked int8
 // operands, 1/K the unnormalized rotation (absent without rotation).
@@ -129,13 +135,13 @@ rrs_status rrs_prepare_weight_ex(const void* W, int K, int N, const int32_t* per
                  K, N, (const void*)perm, flags, Wq, (void*)w_scale);
   if (!W || !Wq || !w_scale) return RRS_ERR_NULL;
   if (!valid_k(K) || !valid_n(N)) return RRS_ERR_SHAPE;
-  if (!valid_flags(flags, RRS_SKIP_ROTATION)) return RRS_ERR_FLAGS;
+  if (!valid_flags(flags, kRotationFlags)) return RRS_ERR_FLAGS;
   if (!is_aligned(W) || !is_aligned(Wq) || !is_aligned(w_scale) || (perm && !is_aligned(perm)))
     return RRS_ERR_ALIGN;
   if (rrs_status s = check_device()) return s;
   return from_hip(rrs::launch_prepare_weight(
       static_cast<const uint16_t*>(W), K, N, perm, !(flags & RRS_SKIP_ROTATION),
-      static_cast<uint8_t*>(Wq), w_scale, static_cast<hipStream_t>(stream)));
+      static_cast<uint8_t*>(Wq), w_scale, static_cast<hipStream_t>(stream), layout(flags)));
 }
 
 rrs_status rrs_prepare_weight(const void* W, int K, int N, const int32_t* perm, void* Wq,
@@ -163,8 +169,8 @@ rrs_status rrs_rotate_smooth_quant_ex(const void* X, int M, int K, int group_siz
   if (workspace_bytes < rrs::quant_workspace_bytes(M, K)) return RRS_ERR_WORKSPACE;
   if (rrs_status s = check_device()) return s;
   return from_hip(rrs::launch_rotate_smooth_quant(
-      static_cast<const uint16_t*>(X), M, K, group_size, perm, flags, static_cast<uint8_t*>(Xq),
-      a_scale, s_group, workspace, static_cast<hipStream_t>(stream)));
+      static_cast<const uint16_t*>(X), M, K, group_size, perm, flags & kQuantFlags,
+      static_cast<uint8_t*>(Xq), a_scale, s_group, workspace, static_cast<hipStream_t>(stream)));
 }
 
 rrs_status rrs_rotate_smooth_quant(const void* X, int M, int K, int group_size,
@@ -195,7 +201,7 @@ rrs_status rrs_w4a4_gemm_ex(const void* Xq, const float* a_scale, const float* s
   return from_hip(rrs::launch_w4a4_gemm(
       static_cast<const uint8_t*>(Xq), a_scale, s_group, static_cast<const uint8_t*>(Wq),
       w_scale, M, N, K, group_size, static_cast<uint16_t*>(Y), out_scale(K, flags),
-      static_cast<hipStream_t>(stream)));
+      static_cast<hipStream_t>(stream), layout(flags)));
 }
 
 rrs_status rrs_w4a4_gemm(const void* Xq, const float* a_scale, const float* s_group,
@@ -234,11 +240,12 @@ rrs_status rrs_linear_ex(const void* X, const void* Wq, const float* w_scale, in
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = rrs::launch_rotate_smooth_quant(static_cast<const uint16_t*>(X), M, K,
-                                                 group_size, perm, flags, xq, a, s, qws, st);
+                                                 group_size, perm, flags & kQuantFlags, xq, a,
+                                                 s, qws, st);
   if (e != hipSuccess) return RRS_ERR_HIP;
   return from_hip(rrs::launch_w4a4_gemm(xq, a, s, static_cast<const uint8_t*>(Wq), w_scale, M,
                                         N, K, group_size, static_cast<uint16_t*>(Y),
-                                        out_scale(K, flags), st));
+                                        out_scale(K, flags), st, layout(flags)));
 }
 
 rrs_status rrs_linear(const void* X, const void* Wq, const float* w_scale, int M, int N,
@@ -256,11 +263,12 @@ rrs_status rrs_quantize_sub_channel(const void* X, int M, int K, int group_size,
   if (!X || !Xq || !a_sub) return RRS_ERR_NULL;
   if (!valid_m(M) || !valid_k(K)) return RRS_ERR_SHAPE;
   if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
-  if (!valid_flags(flags, RRS_SKIP_ROTATION)) return RRS_ERR_FLAGS;
+  if (!valid_flags(flags, kRotationFlags)) return RRS_ERR_FLAGS;
   if (!is_aligned(X) || !is_aligned(Xq) || !is_aligned(a_sub)) return RRS_ERR_ALIGN;
   if (rrs_status s = check_device()) return s;
   return from_hip(rrs::launch_quantize_sub_channel(
-      static_cast<const uint16_t*>(X), M, K, group_size, flags, static_cast<uint8_t*>(Xq), a_sub,
+      static_cast<const uint16_t*>(X), M, K, group_size, flags & RRS_SKIP_ROTATION,
+      static_cast<uint8_t*>(Xq), a_sub,
       static_cast<hipStream_t>(stream)));
 }
 
@@ -272,12 +280,12 @@ rrs_status rrs_prepare_weight_sub_channel(const void* W, int K, int N, int group
   if (!W || !Wq || !w_sub) return RRS_ERR_NULL;
   if (!valid_k(K) || !valid_n(N)) return RRS_ERR_SHAPE;
   if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
-  if (!valid_flags(flags, RRS_SKIP_ROTATION)) return RRS_ERR_FLAGS;
+  if (!valid_flags(flags, kRotationFlags)) return RRS_ERR_FLAGS;
   if (!is_aligned(W) || !is_aligned(Wq) || !is_aligned(w_sub)) return RRS_ERR_ALIGN;
   if (rrs_status s = check_device()) return s;
   return from_hip(rrs::launch_prepare_weight_sub_channel(
       static_cast<const uint16_t*>(W), K, N, group_size, !(flags & RRS_SKIP_ROTATION),
-      static_cast<uint8_t*>(Wq), w_sub, static_cast<hipStream_t>(stream)));
+      static_cast<uint8_t*>(Wq), w_sub, static_cast<hipStream_t>(stream), layout(flags)));
 }
 
 rrs_status rrs_w4a4_gemm_scheme(int scheme, const void* Xq, const float* x_scale,
@@ -305,7 +313,7 @@ rrs_status rrs_w4a4_gemm_scheme(int scheme, const void* Xq, const float* x_scale
   return from_hip(rrs::launch_w4a4_gemm_scheme(
       internal, static_cast<const uint8_t*>(Xq), x_scale, s_group,
       static_cast<const uint8_t*>(Wq), w_scale, M, N, K, group_size, static_cast<uint16_t*>(Y),
-      out_scale(K, flags), static_cast<hipStream_t>(stream)));
+      out_scale(K, flags), static_cast<hipStream_t>(stream), layout(flags)));
 }
 
 rrs_status rrs_w4a4_gemm_per_channel(const void* Xq, const float* a_scale, const void* Wq,
@@ -322,7 +330,8 @@ rrs_status rrs_w4a4_gemm_per_channel(const void* Xq, const float* a_scale, const
   if (rrs_status s = check_device()) return s;
   return from_hip(rrs::launch_w4a4_gemm_per_channel(
       static_cast<const uint8_t*>(Xq), a_scale, static_cast<const uint8_t*>(Wq), w_scale, M, N, K,
-      static_cast<uint16_t*>(Y), out_scale(K, flags), static_cast<hipStream_t>(stream)));
+      static_cast<uint16_t*>(Y), out_scale(K, flags), static_cast<hipStream_t>(stream),
+      layout(flags)));
 }
 
 size_t rrs_reorder_workspace_bytes(int M, int K, int group_size) {
@@ -349,15 +358,16 @@ rrs_status rrs_rotate_smooth_quant_reorder(const void* X, int M, int K, int grou
   if (!X || !Xq || !a_scale || !s_group || !block_order || !workspace) return RRS_ERR_NULL;
   if (!valid_m(M) || !valid_k(K)) return RRS_ERR_SHAPE;
   if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
-  if (!valid_flags(flags, RRS_SKIP_ROTATION)) return RRS_ERR_FLAGS;
+  if (!valid_flags(flags, kRotationFlags)) return RRS_ERR_FLAGS;
   if (!is_aligned(X) || !is_aligned(Xq) || !is_aligned(a_scale) || !is_aligned(s_group) ||
       !is_aligned(block_order) || !is_aligned(workspace))
     return RRS_ERR_ALIGN;
   if (workspace_bytes < rrs::reorder_workspace_bytes(K)) return RRS_ERR_WORKSPACE;
   if (rrs_status s = check_device()) return s;
   return from_hip(rrs::launch_rotate_smooth_quant_reorder(
-      static_cast<const uint16_t*>(X), M, K, group_size, flags, static_cast<uint8_t*>(Xq),
-      a_scale, s_group, block_order, workspace, static_cast<hipStream_t>(stream)));
+      static_cast<const uint16_t*>(X), M, K, group_size, flags & RRS_SKIP_ROTATION,
+      static_cast<uint8_t*>(Xq), a_scale, s_group, block_order, workspace,
+      static_cast<hipStream_t>(stream)));
 }
 
 rrs_status rrs_w4a4_gemm_reorder(const void* Xq, const float* a_scale, const float* s_group,
@@ -370,7 +380,7 @@ rrs_status rrs_w4a4_gemm_reorder(const void* Xq, const float* a_scale, const flo
   if (!Xq || !a_scale || !s_group || !Wq || !w_scale || !block_order || !Y) return RRS_ERR_NULL;
   if (!valid_m(M) || !valid_n(N) || !valid_k(K)) return RRS_ERR_SHAPE;
   if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
-  if (!valid_flags(flags, RRS_SKIP_ROTATION)) return RRS_ERR_FLAGS;
+  if (!valid_flags(flags, kRotationFlags)) return RRS_ERR_FLAGS;
   if (!is_aligned(Xq) || !is_aligned(a_scale) || !is_aligned(s_group) || !is_aligned(Wq) ||
       !is_aligned(w_scale) || !is_aligned(block_order) || !is_aligned(Y))
     return RRS_ERR_ALIGN;
@@ -378,7 +388,7 @@ rrs_status rrs_w4a4_gemm_reorder(const void* Xq, const float* a_scale, const flo
   return from_hip(rrs::launch_w4a4_gemm_reorder(
       static_cast<const uint8_t*>(Xq), a_scale, s_group, static_cast<const uint8_t*>(Wq),
       w_scale, block_order, M, N, K, group_size, static_cast<uint16_t*>(Y), out_scale(K, flags),
-      static_cast<hipStream_t>(stream)));
+      static_cast<hipStream_t>(stream), layout(flags)));
 }
 
 rrs_status rrs_linear_reorder(const void* X, const void* Wq, const float* w_scale, int M,
@@ -393,7 +403,7 @@ rrs_status rrs_linear_reorder(const void* X, const void* Wq, const float* w_scal
   if (!X || !Wq || !w_scale || !Y || !workspace) return RRS_ERR_NULL;
   if (!valid_m(M) || !valid_n(N) || !valid_k(K)) return RRS_ERR_SHAPE;
   if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
-  if (!valid_flags(flags, RRS_SKIP_ROTATION)) return RRS_ERR_FLAGS;
+  if (!valid_flags(flags, kRotationFlags)) return RRS_ERR_FLAGS;
   if (!is_aligned(X) || !is_aligned(Wq) || !is_aligned(w_scale) || !is_aligned(Y) ||
       !is_aligned(workspace))
     return RRS_ERR_ALIGN;
@@ -413,12 +423,13 @@ rrs_status rrs_linear_reorder(const void* X, const void* Wq, const float* w_scal
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = rrs::launch_rotate_smooth_quant_reorder(
-      static_cast<const uint16_t*>(X), M, K, group_size, flags, xq, a, s, order, qws, st);
+      static_cast<const uint16_t*>(X), M, K, group_size, flags & RRS_SKIP_ROTATION, xq, a, s,
+      order, qws, st);
   if (e != hipSuccess) return RRS_ERR_HIP;
   return from_hip(rrs::launch_w4a4_gemm_reorder(xq, a, s, static_cast<const uint8_t*>(Wq),
                                                 w_scale, order, M, N, K, group_size,
                                                 static_cast<uint16_t*>(Y), out_scale(K, flags),
-                                                st));
+                                                st, layout(flags)));
 }
 
 rrs_status rrs_w4a4_gemm_partials(const void* Xq, const void* Wq, int M, int N, int K,

@@ -7,9 +7,10 @@
 // each wave 64 x 64 as 2 x 2 blocks of v_mfma_i32_32x32x32_i8. K advances in
 // tiles of 128 (four MFMA k-steps of 32).
 //
-// Data path: packed INT4 (Xq: M x K/2, K contiguous; Wq tiled, see wq_piece:
-// one wave's slot of a K tile, 16 rows x 64 bytes, is one contiguous 1 KB
-// tile) is loaded from HBM into registers two tiles ahead, unpacked to int8 and stored in a
+// Data path: packed INT4 (Xq: M x K/2, K contiguous; Wq row-major or tiled,
+// see WqLayout: in the tiled layout one wave's slot of a K tile, 16 rows x 64
+// bytes, is one contiguous 1 KB tile) is loaded from HBM into registers two
+// tiles ahead, unpacked to int8 and stored in a
 // double-buffered LDS stage whose rows are padded to 144 bytes (conflict-free
 // 128-bit fragment reads at immediate offsets). The unpack and the LDS stores
 // of the next tile are spread over the MFMAs of the current tile's H0 phase
@@ -108,12 +109,13 @@ __device__ __forceinline__ int acc_col(int n0, int wn, int j, int lane) {
 // kGather (runtime channel reorder): position block p (32 channels, 16 bytes
 // of a packed row) of Xq pairs with block border[p] of every Wq row; the
 // table is kept in LDS and each B slot reads its entry one tile ahead.
-template <int GS, bool kPartials, bool kPerChannel = false, bool kGather = false>
+template <int GS, bool kPartials, bool kPerChannel, bool kGather, bool kTiled>
 __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
     const float* __restrict__ w_scale, int M, int N, int K, uint16_t* __restrict__ Y,
     int32_t* __restrict__ P, float out_scale, const int32_t* __restrict__ border) {
+  constexpr WqLayout lay{kTiled};
   __shared__ __attribute__((aligned(16))) uint8_t lds[2 * STAGE];
   __shared__ float scale_tab[BM + BN];  // alpha of the tile's rows, then beta of its columns
   __shared__ int btab[kGather ? 16384 / kReorderBlock : 1];
@@ -139,7 +141,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
   const int bq = t & 3;
   const uint8_t* ga = Xq + (size_t)min(m0 + arow, M - 1) * krow + ahalf * 32;
   const int bn = min(n0 + brow, N - 1);
-  const uint8_t* gb = Wq + wq_piece(bn, 0, K) + (kGather ? 0 : bq * 256);
+  constexpr uint32_t wts = (uint32_t)lay.tile();     // bytes from one K tile to the next
+  constexpr uint32_t wqs = (uint32_t)lay.quarter();  // bytes from one 16-byte piece to the next
+  const uint8_t* gb = Wq + lay.row(bn, K) + (kGather ? 0u : bq * wqs);
   const int a_st = arow * ROWP + ahalf * 64;
   const int b_st = A_BYTES + brow * ROWP + bq * 32;
 
@@ -156,9 +160,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
   auto boff = [&](int kt) -> uint32_t {
     if constexpr (kGather) {
       const uint32_t p = (uint32_t)btab[kt * 4 + bq];
-      return (p >> 2) * 1024u + (p & 3u) * 256u;
+      return (p >> 2) * wts + (p & 3u) * wqs;
     } else {
-      return (uint32_t)kt * 1024u;
+      return (uint32_t)kt * wts;
     }
   };
   auto gload = [&](int set, int kt, uint32_t bo) {
@@ -406,22 +410,28 @@ template <bool kPartials, bool kGather = false>
 hipError_t launch_main(const uint8_t* Xq, const float* a_scale, const float* s_group,
                        const uint8_t* Wq, const float* w_scale, int M, int N, int K, int g,
                        uint16_t* Y, int32_t* P, float out_scale, hipStream_t stream,
-                       const int32_t* border = nullptr) {
+                       const int32_t* border, WqLayout lay) {
   const int tm = (M + BM - 1) / BM;
   const int tn = (N + BN - 1) / BN;
   const int T = tm * tn;
   const int grid = 8 * ((T + 7) / 8);
   switch (g) {
-#define RRS_CASE(G_)                                                                       \
-  case G_:                                                                                 \
-    gemm_main_kernel<G_ / 32, kPartials, false, kGather><<<grid, kThreads, 0, stream>>>(   \
-        Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, P, out_scale, border);              \
+#define RRS_LAUNCH(G_, T_)                                                                 \
+  gemm_main_kernel<G_ / 32, kPartials, false, kGather, T_><<<grid, kThreads, 0, stream>>>( \
+      Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, P, out_scale, border)
+#define RRS_CASE(G_)          \
+  case G_:                    \
+    if (lay.tiled)            \
+      RRS_LAUNCH(G_, true);   \
+    else                      \
+      RRS_LAUNCH(G_, false);  \
     break;
     RRS_CASE(64)
     RRS_CASE(128)
     RRS_CASE(256)
     RRS_CASE(512)
 #undef RRS_CASE
+#undef RRS_LAUNCH
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -437,28 +447,34 @@ bool main_kernel_fits(int K, int g) {
 
 hipError_t launch_w4a4_gemm(const uint8_t* Xq, const float* a_scale, const float* s_group,
                             const uint8_t* Wq, const float* w_scale, int M, int N, int K,
-                            int g, uint16_t* Y, float out_scale, hipStream_t stream) {
+                            int g, uint16_t* Y, float out_scale, hipStream_t stream,
+                            WqLayout lay) {
   if (decode_kernel_fits(M))
     return launch_w4a4_gemm_decode(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, out_scale,
-                                   stream);
+                                   stream, nullptr, lay);
   if (!main_kernel_fits(K, g))
     return launch_w4a4_gemm_small(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, out_scale,
-                                  stream);
+                                  stream, lay);
   return launch_main<false>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, nullptr,
-                            out_scale, stream);
+                            out_scale, stream, nullptr, lay);
 }
 
 hipError_t launch_w4a4_gemm_per_channel(const uint8_t* Xq, const float* a_scale,
                                        const uint8_t* Wq, const float* w_scale, int M, int N,
-                                       int K, uint16_t* Y, float out_scale, hipStream_t stream) {
+                                       int K, uint16_t* Y, float out_scale, hipStream_t stream,
+                                       WqLayout lay) {
   if (!main_kernel_fits(K, 128))
     return launch_w4a4_gemm_scheme(1, Xq, a_scale, nullptr, Wq, w_scale, M, N, K, K, Y,
-                                   out_scale, stream);
+                                   out_scale, stream, lay);
   const int tm = (M + BM - 1) / BM;
   const int tn = (N + BN - 1) / BN;
   const int grid = 8 * ((tm * tn + 7) / 8);
-  gemm_main_kernel<4, false, true><<<grid, kThreads, 0, stream>>>(
-      Xq, a_scale, nullptr, Wq, w_scale, M, N, K, Y, nullptr, out_scale, nullptr);
+  if (lay.tiled)
+    gemm_main_kernel<4, false, true, false, true><<<grid, kThreads, 0, stream>>>(
+        Xq, a_scale, nullptr, Wq, w_scale, M, N, K, Y, nullptr, out_scale, nullptr);
+  else
+    gemm_main_kernel<4, false, true, false, false><<<grid, kThreads, 0, stream>>>(
+        Xq, a_scale, nullptr, Wq, w_scale, M, N, K, Y, nullptr, out_scale, nullptr);
   return hipGetLastError();
 }
 
@@ -466,23 +482,24 @@ hipError_t launch_w4a4_gemm_reorder(const uint8_t* Xq, const float* a_scale,
                                     const float* s_group, const uint8_t* Wq,
                                     const float* w_scale, const int32_t* border, int M, int N,
                                     int K, int g, uint16_t* Y, float out_scale,
-                                    hipStream_t stream) {
+                                    hipStream_t stream, WqLayout lay) {
   if (decode_gather_fits(M))
     return launch_w4a4_gemm_decode(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, out_scale,
-                                   stream, border);
+                                   stream, border, lay);
   // Every shape the ABI accepts fits the main kernel (K / 32 >= 16 is a power
   // of two); the fallback kernel has no gather.
   if (!main_kernel_fits(K, g)) return hipErrorInvalidValue;
   return launch_main<false, true>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, nullptr,
-                                  out_scale, stream, border);
+                                  out_scale, stream, border, lay);
 }
 
 hipError_t launch_w4a4_gemm_partials(const uint8_t* Xq, const uint8_t* Wq, int M, int N,
-                                     int K, int g, int32_t* P, hipStream_t stream) {
+                                     int K, int g, int32_t* P, hipStream_t stream,
+                                     WqLayout lay) {
   if (!main_kernel_fits(K, g))
-    return launch_w4a4_gemm_partials_small(Xq, Wq, M, N, K, g, P, stream);
+    return launch_w4a4_gemm_partials_small(Xq, Wq, M, N, K, g, P, stream, lay);
   return launch_main<true>(Xq, nullptr, nullptr, Wq, nullptr, M, N, K, g, nullptr, P, 0.0f,
-                           stream);
+                           stream, nullptr, lay);
 }
 
 }  // namespace rrs

@@ -18,9 +18,10 @@
 //     of Wq row n0 + c and the same bytes of Xq row c (zero for c >= M): for
 //     g = 64 bytes [8 q, 8 q + 8) of the group, for g >= 128 bytes
 //     [64 h + 16 q, +16) of each 64-byte piece h of it. In the tiled Wq
-//     (wq_piece) these are bytes [16 lane, +16) of the group's 1 KB tiles, so
+//     (WqLayout) these are bytes [16 lane, +16) of the group's 1 KB tiles, so
 //     every weight load instruction of a wave reads one contiguous tile
-//     (512 contiguous bytes for g = 64). MFMA k-step s of the group
+//     (512 contiguous bytes for g = 64); row-major, 16 rows x 64 bytes.
+//     MFMA k-step s of the group
 //     (v_mfma_i32_16x16x64_i8, 64 codes) takes the lane's bytes [8 s, 8 s + 8)
 //     in that order, so each k-step stays inside one group and A and B pair
 //     the same codes;
@@ -81,12 +82,13 @@ constexpr int kMaxTokenBlocks = 4;  // up to 64 tokens
 
 // GS = g / 64 MFMA k-steps per group; TB token blocks of 16 rows (tokens
 // 16 tb .. 16 tb + 15 in block tb), all multiplied with the same weight words.
-template <int GS, int TB>
+template <int GS, int TB, bool kTiled>
 __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
     const float* __restrict__ w_scale, int M, int N, int K, uint16_t* __restrict__ Y,
     float out_scale) {
+  constexpr WqLayout lay{kTiled};
   constexpr int g = GS * 64;
   constexpr int NW = g / 32;                  // words per lane per group and block
   constexpr int D0 = NW >= 16 ? 1 : (NW >= 8 ? 2 : 4);
@@ -116,9 +118,13 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
   // output rows that are never stored. Column blocks past N load block 0 and
   // are never stored.
   // Byte offsets of this lane's codes inside a group: in a packed Xq row, and
-  // in the group's region of the column block's tiled rows (8 g bytes).
+  // from its Wq row's start (group b starts b gstride later, its pieces h
+  // lie a tile apart).
   const int xo = g == 64 ? q * 8 : q * 16;
-  const int wo = g == 64 ? (q >> 1) * 256 + c * 16 + (q & 1) * 8 : lane * 16;
+  constexpr int wqs = lay.quarter();
+  constexpr int wts = lay.tile();
+  const int wo = g == 64 ? (q >> 1) * wqs + (q & 1) * 8 : q * wqs;
+  constexpr size_t gstride = kTiled ? (size_t)8 * g : (size_t)(g / 2);
   const uint8_t* pa[TB];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb) pa[tb] = Xq + (size_t)min(16 * tb + c, M - 1) * krow + xo;
@@ -126,7 +132,7 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
 #pragma unroll
   for (int j = 0; j < kBlocks; ++j) {
     const int n = n0 + j * kCols < N ? n0 + j * kCols : 0;
-    pb[j] = Wq + wq_piece(n, 0, K) + wo;
+    pb[j] = Wq + lay.row(n + c, K) + wo;
   }
 
   uint32_t wa[D][TB][NW], wb[D][kBlocks][NW];
@@ -135,7 +141,7 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) load_words<NW>(pa[tb] + (size_t)b * (g / 2), 64, wa[d][tb]);
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) load_words<NW>(pb[j] + (size_t)b * (8 * g), 1024, wb[d][j]);
+    for (int j = 0; j < kBlocks; ++j) load_words<NW>(pb[j] + (size_t)b * gstride, wts, wb[d][j]);
   };
 
   constexpr int kMagic = 0x4B400000;  // bits of 1.5 * 2^23
@@ -245,8 +251,9 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
 // different times, and this streaming kernel would fetch most lines several
 // times. Instead the (small, cache-resident) token codes are gathered. Wave kq
 // walks its K quarter in quads of four natural blocks 4m .. 4m + 3: lane (c, q)
-// loads block 4m + q of weight row n0 + 16 j + c (the wave reads tile m of the
-// column block, 1 KB contiguous) and position block inv[4m + q] of token row c. A 4 x 4
+// loads block 4m + q of weight row n0 + 16 j + c (with the tiled Wq the wave
+// reads tile m of the column block, 1 KB contiguous) and position block
+// inv[4m + q] of token row c. A 4 x 4
 // dword transpose through a wave-private LDS region then gives lane group q
 // dword q of each of the four blocks, so that one v_mfma_i32_16x16x32_i8 per
 // block and column block (lane group q holds channels 8q .. 8q + 7 of the block
@@ -264,11 +271,13 @@ __device__ __forceinline__ long unpack_dword(uint32_t w) {
   return (long)(((unsigned long)hi << 32) | lo);
 }
 
+template <bool kTiled>
 __global__ __launch_bounds__(kThreads) void gemm_decode_gather_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
     const float* __restrict__ w_scale, const int32_t* __restrict__ border, int M, int N,
     int K, int g, uint16_t* __restrict__ Y, float out_scale) {
+  constexpr WqLayout lay{kTiled};
   constexpr int kMaxBlocks = 16384 / kReorderBlock;
   constexpr int kArrays = 1 + kBlocks;  // token codes and the column blocks' weights
   __shared__ int inv[kMaxBlocks];      // natural block -> byte offset of its position block
@@ -286,6 +295,7 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_gather_kernel(
   const int NB = K / kReorderBlock;
   const int quads = NB / 16;     // quads per wave (K >= 512: at least 1)
   const int b0 = kq * (NB / 4);  // first natural block of this wave
+  constexpr size_t wts = (size_t)lay.tile();
   const int steps = (quads + kGatherAhead - 1) / kGatherAhead * kGatherAhead;
 
   // Tables. Entries are reduced modulo K/32, so any table keeps every load in
@@ -309,7 +319,7 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_gather_kernel(
 #pragma unroll
   for (int j = 0; j < kBlocks; ++j) {
     const int n = n0 + j * kCols < N ? n0 + j * kCols : 0;
-    pb[j] = Wq + wq_piece(n, 0, K) + lane * 16;  // quad m is tile m of the block
+    pb[j] = Wq + lay.row(n + c, K) + (size_t)q * lay.quarter();  // quad m: m tiles on
   }
   uint32_t* trw = &tr[kq][0][0];
 
@@ -320,7 +330,7 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_gather_kernel(
     ld[d][0] = *reinterpret_cast<const uint4*>(pa + inv[B0 + q]);
 #pragma unroll
     for (int j = 0; j < kBlocks; ++j)
-      ld[d][1 + j] = *reinterpret_cast<const uint4*>(pb[j] + (size_t)B0 * 256);
+      ld[d][1 + j] = *reinterpret_cast<const uint4*>(pb[j] + (size_t)(B0 >> 2) * wts);
   };
 
   constexpr int kMagic = 0x4B400000;  // bits of 1.5 * 2^23
@@ -427,22 +437,34 @@ hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
                                    const float* s_group, const uint8_t* Wq,
                                    const float* w_scale, int M, int N, int K, int g,
                                    uint16_t* Y, float out_scale, hipStream_t stream,
-                                   const int32_t* border) {
+                                   const int32_t* border, WqLayout lay) {
   const int grid = (N / kCols + kBlocks - 1) / kBlocks;  // N % 16 == 0 (API precondition)
   if (border) {
     if (M > kCols) return hipErrorInvalidValue;  // the gather kernel takes one token block
-    gemm_decode_gather_kernel<<<grid, kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale,
-                                                            border, M, N, K, g, Y, out_scale);
+    if (lay.tiled)
+      gemm_decode_gather_kernel<true><<<grid, kThreads, 0, stream>>>(
+          Xq, a_scale, s_group, Wq, w_scale, border, M, N, K, g, Y, out_scale);
+    else
+      gemm_decode_gather_kernel<false><<<grid, kThreads, 0, stream>>>(
+          Xq, a_scale, s_group, Wq, w_scale, border, M, N, K, g, Y, out_scale);
     return hipGetLastError();
   }
   const int tbs = M <= kCols ? 1 : (M <= 2 * kCols ? 2 : 4);
-#define RRS_DECODE(GS_, TB_)                                                             \
-  gemm_decode_kernel<GS_, TB_><<<grid, kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq, \
-                                                              w_scale, M, N, K, Y, out_scale)
-#define RRS_DECODE_TB(GS_)                      \
-  if (tbs == 1) RRS_DECODE(GS_, 1);             \
-  else if (tbs == 2) RRS_DECODE(GS_, 2);        \
-  else RRS_DECODE(GS_, 4);
+#define RRS_DECODE(GS_, TB_)                                             \
+  if (lay.tiled)                                                        \
+    gemm_decode_kernel<GS_, TB_, true><<<grid, kThreads, 0, stream>>>(  \
+        Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale);      \
+  else                                                                  \
+    gemm_decode_kernel<GS_, TB_, false><<<grid, kThreads, 0, stream>>>( \
+        Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale)
+#define RRS_DECODE_TB(GS_) \
+  if (tbs == 1) {          \
+    RRS_DECODE(GS_, 1);    \
+  } else if (tbs == 2) {   \
+    RRS_DECODE(GS_, 2);    \
+  } else {                 \
+    RRS_DECODE(GS_, 4);    \
+  }
   switch (g) {
     case 64: RRS_DECODE_TB(1) break;
     case 128: RRS_DECODE_TB(2) break;

@@ -3,8 +3,8 @@
 //   Y[i, n] = fp16( alpha_i * beta_n / K * sum_b s_b * P_b[i, n] )
 //   P_b[i, n] = sum_{j in group b} qx[i, j] * qw[j, n]   (exact int32)
 //
-// Packed INT4 operands: Xq M x K/2, K contiguous; Wq in the tiled layout of
-// wq_piece() (a row's K tile of 32 bytes is pieces 2 kt and 2 kt + 1).
+// Packed INT4 operands: Xq M x K/2, K contiguous; Wq row-major or tiled
+// (WqLayout; a row's K tile of 32 bytes is pieces 2 kt and 2 kt + 1).
 // Fallback kernel for shapes outside the main kernel's unrolling (rrs_gemm.hip).
 // Tile 128 x 128 per 256-thread workgroup, four waves of 64 x 64, K step 64.
 // Global -> registers (16 B per thread per operand) -> unpacked to int8 ->
@@ -64,7 +64,7 @@ __global__ __launch_bounds__(256) void gemm_small_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
     const float* __restrict__ w_scale, int M, int N, int K, int g,
-    uint16_t* __restrict__ Y, int32_t* __restrict__ P, float out_scale) {
+    uint16_t* __restrict__ Y, int32_t* __restrict__ P, float out_scale, WqLayout lay) {
   __shared__ __attribute__((aligned(16))) uint8_t sA[2][BM * LROW];
   __shared__ __attribute__((aligned(16))) uint8_t sB[2][BN * LROW];
 
@@ -83,8 +83,10 @@ __global__ __launch_bounds__(256) void gemm_small_kernel(
   const bool a_ok = (m0 + lrow) < M;
   const bool b_ok = (n0 + lrow) < N;
   const uint8_t* gA = Xq + (size_t)(a_ok ? m0 + lrow : 0) * kbytes_row + lhalf * 16;
-  // Tiled Wq: piece 2 kt + lhalf of the row lies 512 kt bytes after piece lhalf.
-  const uint8_t* gB = Wq + wq_piece(b_ok ? n0 + lrow : 0, lhalf, K);
+  // Piece 2 kt + lhalf of the row lies (kt / 2) tile + 2 (kt % 2) quarter
+  // bytes after piece lhalf.
+  const uint8_t* gB = Wq + lay.piece(b_ok ? n0 + lrow : 0, lhalf, K);
+  const size_t wts = (size_t)lay.tile(), wqs2 = (size_t)2 * lay.quarter();
   const int st_off = lrow * LROW + lhalf * 32;
 
   uint4 ra = make_uint4(0, 0, 0, 0);
@@ -138,7 +140,9 @@ __global__ __launch_bounds__(256) void gemm_small_kernel(
     __syncthreads();
     if (kt + 1 < nkt) {
       if (a_ok) ra = *reinterpret_cast<const uint4*>(gA + (size_t)(kt + 1) * KBYTES);
-      if (b_ok) rb = *reinterpret_cast<const uint4*>(gB + (size_t)(kt + 1) * 512);
+      if (b_ok)
+        rb = *reinterpret_cast<const uint4*>(gB + (size_t)((kt + 1) >> 1) * wts +
+                                             (size_t)((kt + 1) & 1) * wqs2);
     }
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
@@ -246,30 +250,31 @@ __global__ __launch_bounds__(256) void gemm_small_kernel(
 
 hipError_t launch_w4a4_gemm_small(const uint8_t* Xq, const float* a_scale, const float* s_group,
                             const uint8_t* Wq, const float* w_scale, int M, int N, int K,
-                            int g, uint16_t* Y, float out_scale, hipStream_t stream) {
+                            int g, uint16_t* Y, float out_scale, hipStream_t stream,
+                            WqLayout lay) {
   dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
   gemm_small_kernel<false><<<grid, 256, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale, M, N, K,
-                                                     g, Y, nullptr, out_scale);
+                                                     g, Y, nullptr, out_scale, lay);
   return hipGetLastError();
 }
 
 hipError_t launch_w4a4_gemm_scheme(int scheme, const uint8_t* Xq, const float* x_scale,
                                    const float* s_group, const uint8_t* Wq, const float* w_scale,
                                    int M, int N, int K, int g, uint16_t* Y, float out_scale,
-                                   hipStream_t stream) {
+                                   hipStream_t stream, WqLayout lay) {
   dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
   switch (scheme) {
     case kRuntimeSmooth:
       gemm_small_kernel<false, kRuntimeSmooth><<<grid, 256, 0, stream>>>(
-          Xq, x_scale, s_group, Wq, w_scale, M, N, K, g, Y, nullptr, out_scale);
+          Xq, x_scale, s_group, Wq, w_scale, M, N, K, g, Y, nullptr, out_scale, lay);
       break;
     case kPerChannel:
       gemm_small_kernel<false, kPerChannel><<<grid, 256, 0, stream>>>(
-          Xq, x_scale, nullptr, Wq, w_scale, M, N, K, K, Y, nullptr, out_scale);
+          Xq, x_scale, nullptr, Wq, w_scale, M, N, K, K, Y, nullptr, out_scale, lay);
       break;
     case kSubChannel:
       gemm_small_kernel<false, kSubChannel><<<grid, 256, 0, stream>>>(
-          Xq, x_scale, nullptr, Wq, w_scale, M, N, K, g, Y, nullptr, out_scale);
+          Xq, x_scale, nullptr, Wq, w_scale, M, N, K, g, Y, nullptr, out_scale, lay);
       break;
     default: return hipErrorInvalidValue;
   }
@@ -277,10 +282,11 @@ hipError_t launch_w4a4_gemm_scheme(int scheme, const uint8_t* Xq, const float* x
 }
 
 hipError_t launch_w4a4_gemm_partials_small(const uint8_t* Xq, const uint8_t* Wq, int M, int N,
-                                     int K, int g, int32_t* P, hipStream_t stream) {
+                                     int K, int g, int32_t* P, hipStream_t stream,
+                                     WqLayout lay) {
   dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
   gemm_small_kernel<true><<<grid, 256, 0, stream>>>(Xq, nullptr, nullptr, Wq, nullptr, M, N, K, g,
-                                                    nullptr, P, 0.0f);
+                                                    nullptr, P, 0.0f, lay);
   return hipGetLastError();
 }
 

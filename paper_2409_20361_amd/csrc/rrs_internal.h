@@ -21,15 +21,25 @@ constexpr int kSkipSmoothing = 2;
 // codes, 16 bytes of a packed row.
 constexpr int kReorderBlock = 32;
 
-// Tiled Wq (the layout rrs_prepare_weight writes): rows in blocks of 16, each
-// block's K/128 tiles of 1 KB stored one after another; inside a tile, byte
-// (q * 16 + r) * 16 + e is packed byte 64 c + 16 q + e of row 16 nb + r for
-// tile c of block nb. A 16-row block spans 16 * K/2 = 8 K bytes.
-// Byte offset of piece p (packed bytes [16 p, 16 p + 16)) of row n.
-__host__ __device__ inline size_t wq_piece(int n, int p, int K) {
-  return (size_t)(n >> 4) * ((size_t)8 * K) + (size_t)(p >> 2) * 1024 + (p & 3) * 256 +
-         (n & 15) * 16;
-}
+// Byte layout of Wq. Row-major (the default): row n at n K/2, K contiguous.
+// Tiled (RRS_WEIGHT_TILED): rows in blocks of 16, each block's K/128 tiles of
+// 16 rows x 64 bytes stored one after another, the tile's four 16-byte
+// quarters of the 16 rows quarter by quarter. In both, piece p (packed bytes
+// [16 p, 16 p + 16)) of row n sits at row(n) + (p / 4) tile() + (p % 4) quarter().
+// The hot kernels take the layout as a template argument (a constexpr
+// WqLayout), so that the strides fold into the load instructions' offsets.
+struct WqLayout {
+  bool tiled;
+  constexpr __host__ __device__ size_t row(int n, int K) const {
+    return tiled ? (size_t)(n >> 4) * ((size_t)8 * K) + (size_t)(n & 15) * 16
+                 : (size_t)n * (size_t)(K / 2);
+  }
+  constexpr __host__ __device__ int tile() const { return tiled ? 1024 : 64; }
+  constexpr __host__ __device__ int quarter() const { return tiled ? 256 : 16; }
+  constexpr __host__ __device__ size_t piece(int n, int p, int K) const {
+    return row(n, K) + (size_t)(p >> 2) * tile() + (size_t)(p & 3) * quarter();
+  }
+};
 
 hipError_t launch_rotate_smooth_quant(const uint16_t* X, int M, int K, int g,
                                       const int32_t* perm, int flags, uint8_t* Xq,
@@ -43,17 +53,22 @@ hipError_t launch_rotate_smooth_quant_wave(const uint16_t* X, int M, int K, int 
                                            int max_partials, int max_quant_wgs,
                                            hipStream_t stream);
 
+// Every launcher that writes or reads Wq takes its layout (row-major unless
+// the caller asked for RRS_WEIGHT_TILED).
 hipError_t launch_prepare_weight(const uint16_t* W, int K, int N, const int32_t* perm,
-                                 bool rotate, uint8_t* Wq, float* w_scale, hipStream_t stream);
+                                 bool rotate, uint8_t* Wq, float* w_scale, hipStream_t stream,
+                                 WqLayout lay = {false});
 
 // out_scale multiplies every output with alpha_i beta_n: 2^-8 / K for rotated
 // operands, 2^-8 without rotation (both exact powers of two).
 hipError_t launch_w4a4_gemm(const uint8_t* Xq, const float* a_scale, const float* s_group,
                             const uint8_t* Wq, const float* w_scale, int M, int N, int K,
-                            int g, uint16_t* Y, float out_scale, hipStream_t stream);
+                            int g, uint16_t* Y, float out_scale, hipStream_t stream,
+                            WqLayout lay = {false});
 
 hipError_t launch_w4a4_gemm_partials(const uint8_t* Xq, const uint8_t* Wq, int M, int N,
-                                     int K, int g, int32_t* P, hipStream_t stream);
+                                     int K, int g, int32_t* P, hipStream_t stream,
+                                     WqLayout lay = {false});
 
 // Simple 128 x 128 tile kernel: the fallback for shapes the main kernel's
 // unrolling does not cover (K / 32 not a multiple of max(8, g / 32); no shape
@@ -61,10 +76,11 @@ hipError_t launch_w4a4_gemm_partials(const uint8_t* Xq, const uint8_t* Wq, int M
 hipError_t launch_w4a4_gemm_small(const uint8_t* Xq, const float* a_scale,
                                   const float* s_group, const uint8_t* Wq,
                                   const float* w_scale, int M, int N, int K, int g,
-                                  uint16_t* Y, float out_scale, hipStream_t stream);
+                                  uint16_t* Y, float out_scale, hipStream_t stream,
+                                  WqLayout lay = {false});
 hipError_t launch_w4a4_gemm_partials_small(const uint8_t* Xq, const uint8_t* Wq, int M,
                                            int N, int K, int g, int32_t* P,
-                                           hipStream_t stream);
+                                           hipStream_t stream, WqLayout lay = {false});
 
 // Few-token kernel (decode): streams Wq once, for M <= 64 (up to four blocks
 // of 16 tokens); its runtime-reorder variant takes M <= 16.
@@ -74,23 +90,25 @@ hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
                                    const float* s_group, const uint8_t* Wq,
                                    const float* w_scale, int M, int N, int K, int g,
                                    uint16_t* Y, float out_scale, hipStream_t stream,
-                                   const int32_t* border = nullptr);
+                                   const int32_t* border = nullptr, WqLayout lay = {false});
 
 // Baselines of the kernel comparison (per-channel / sub-channel A4W4).
 hipError_t launch_quantize_sub_channel(const uint16_t* X, int M, int K, int g, int flags,
                                        uint8_t* Xq, float* a_sub, hipStream_t stream);
 hipError_t launch_prepare_weight_sub_channel(const uint16_t* W, int K, int N, int g, bool rotate,
-                                             uint8_t* Wq, float* w_sub, hipStream_t stream);
+                                             uint8_t* Wq, float* w_sub, hipStream_t stream,
+                                             WqLayout lay = {false});
 // scheme: 0 Runtime Smooth, 1 per-channel, 2 sub-channel (internal numbering).
 hipError_t launch_w4a4_gemm_scheme(int scheme, const uint8_t* Xq, const float* x_scale,
                                    const float* s_group, const uint8_t* Wq, const float* w_scale,
                                    int M, int N, int K, int g, uint16_t* Y, float out_scale,
-                                   hipStream_t stream);
+                                   hipStream_t stream, WqLayout lay = {false});
 
 // Per-channel A4W4 on the tuned main loop (no per-group rescale).
 hipError_t launch_w4a4_gemm_per_channel(const uint8_t* Xq, const float* a_scale,
                                        const uint8_t* Wq, const float* w_scale, int M, int N,
-                                       int K, uint16_t* Y, float out_scale, hipStream_t stream);
+                                       int K, uint16_t* Y, float out_scale, hipStream_t stream,
+                                       WqLayout lay = {false});
 
 // Runtime channel reorder (Fig. 4 step (1) at run time). Pass 1: rows of
 // K / 32 block maxima (at most block_maxima_rows() rows); pass 2: the
@@ -119,7 +137,7 @@ hipError_t launch_w4a4_gemm_reorder(const uint8_t* Xq, const float* a_scale,
                                     const float* s_group, const uint8_t* Wq,
                                     const float* w_scale, const int32_t* border, int M, int N,
                                     int K, int g, uint16_t* Y, float out_scale,
-                                    hipStream_t stream);
+                                    hipStream_t stream, WqLayout lay = {false});
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 

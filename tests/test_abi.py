@@ -140,35 +140,37 @@ def test_null_pointers(fn, key):
 
 
 @pytest.mark.parametrize("fn,kw", [
-    (_rsq_ex, dict(flags=4)), (_rsq_ex, dict(flags=-1)), (_rsq_ex, dict(flags=8)),
-    (_gemm_ex, dict(flags=4)), (_gemm_ex, dict(flags=1 << 30)),
-    (_lin_ex, dict(flags=4)), (_lin_ex, dict(flags=7)),
-    (_prep_ex, dict(flags=2)), (_prep_ex, dict(flags=3)), (_prep_ex, dict(flags=4)),
+    (_rsq_ex, dict(flags=8)), (_rsq_ex, dict(flags=-1)), (_rsq_ex, dict(flags=12)),
+    (_gemm_ex, dict(flags=8)), (_gemm_ex, dict(flags=1 << 30)),
+    (_lin_ex, dict(flags=8)), (_lin_ex, dict(flags=15)),
+    (_prep_ex, dict(flags=2)), (_prep_ex, dict(flags=3)), (_prep_ex, dict(flags=6)),
+    (_prep_ex, dict(flags=8)),
 ])
 def test_bad_flags(fn, kw):
     assert fn(**kw) == FLAGS
 
 
-@pytest.mark.parametrize("flags", [0, 1, 2, 3])
+@pytest.mark.parametrize("flags", [0, 1, 2, 3, 4, 5, 6, 7])
 def test_good_flags_pass_the_flag_check(flags):
+    # RRS_WEIGHT_TILED (4) is accepted everywhere, also where it has no effect
     # a valid flag word reaches the next check (alignment, workspace)
     assert _rsq_ex(flags=flags, Xq=MIS) == ALIGN
     assert _rsq_ex(flags=flags, wsb=0) == WS
     assert _gemm_ex(flags=flags, Y=MIS) == ALIGN
     assert _lin_ex(flags=flags, wsb=0) == WS
-    if flags in (0, 1):
+    if flags in (0, 1, 4, 5):
         assert _prep_ex(flags=flags, Wq=MIS) == ALIGN
 
 
 def test_ex_check_order():
     # null beats shape beats group beats flags beats alignment beats workspace
-    assert _rsq_ex(X=None, M=0, g=3, flags=4, Xq=MIS, wsb=0) == NULL
-    assert _rsq_ex(M=0, g=3, flags=4, Xq=MIS, wsb=0) == SHAPE
-    assert _rsq_ex(g=3, flags=4, Xq=MIS, wsb=0) == GROUP
-    assert _rsq_ex(flags=4, Xq=MIS, wsb=0) == FLAGS
+    assert _rsq_ex(X=None, M=0, g=3, flags=8, Xq=MIS, wsb=0) == NULL
+    assert _rsq_ex(M=0, g=3, flags=8, Xq=MIS, wsb=0) == SHAPE
+    assert _rsq_ex(g=3, flags=8, Xq=MIS, wsb=0) == GROUP
+    assert _rsq_ex(flags=8, Xq=MIS, wsb=0) == FLAGS
     assert _rsq_ex(Xq=MIS, wsb=0) == ALIGN
-    assert _gemm_ex(Y=None, flags=4) == NULL
-    assert _gemm_ex(N=8, flags=4) == SHAPE
+    assert _gemm_ex(Y=None, flags=8) == NULL
+    assert _gemm_ex(N=8, flags=8) == SHAPE
     assert _prep_ex(K=1000, flags=2) == SHAPE
     assert _prep_ex(flags=2, W=MIS) == FLAGS
 
@@ -302,7 +304,8 @@ def test_baseline_scheme_checks():
     assert _scheme(scheme=rrs.SCHEME_RUNTIME_SMOOTH, s=MIS) == ALIGN
     assert _scheme(scheme=7) == FLAGS
     assert _scheme(scheme=-1) == FLAGS
-    assert _scheme(flags=4) == FLAGS
+    assert _scheme(flags=8) == FLAGS
+    assert _scheme(flags=4, Y=MIS) == ALIGN
     assert _scheme(N=20) == SHAPE
     assert _scheme(K=768) == SHAPE
     assert _scheme(g=96) == GROUP
@@ -393,7 +396,8 @@ def test_reorder_checks(fn):
     assert fn(g=1024) == GROUP
     # only the rotation switch applies: without smoothing the order changes nothing
     assert fn(flags=rrs.SKIP_SMOOTHING) == FLAGS
-    assert fn(flags=4) == FLAGS
+    assert fn(flags=8) == FLAGS
+    assert fn(flags=rrs.WEIGHT_TILED | rrs.SKIP_SMOOTHING) == FLAGS
     key = {_rq: "Xq", _rg: "order", _rl: "Y"}[fn]
     assert fn(**{key: MIS}) == ALIGN
     if fn is not _rq:

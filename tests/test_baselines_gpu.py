@@ -7,7 +7,7 @@ import pytest
 
 import synth
 from oracle import rrs_oracle as O
-from tests._gpu_util import check_codes, check_y, near_half_integer, to_gpu, to_np, untile_wq
+from tests._gpu_util import check_codes, check_y, near_half_integer, to_gpu, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -64,7 +64,7 @@ def test_prepare_weight_sub_channel(K, N, g, flags):
     ref = O.sub_channel_weight(W, g, rotate=not (flags & rrs.SKIP_ROTATION))
     Wq, ws = rrs.prepare_weight_sub_channel(to_gpu(W), g, flags=flags)
     np.testing.assert_array_equal(to_np(ws), ref.scale.T)
-    _check_sub_codes(untile_wq(to_np(Wq)), ref, "sub-channel weights")
+    _check_sub_codes(to_np(Wq), ref, "sub-channel weights")
 
 
 SHAPES = [(16, 512, 512, 128), (130, 1024, 272, 64), (256, 4096, 384, 128), (33, 2048, 160, 256)]

@@ -10,7 +10,7 @@ import pytest
 
 import synth
 from oracle import rrs_oracle as O
-from tests._gpu_util import check_codes, check_y, tile_wq, to_gpu, to_np, untile_wq
+from tests._gpu_util import check_codes, check_y, to_gpu, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -166,7 +166,7 @@ def _weight_case(w, cols=None, perm=None, label=""):
     print(f"[case] weight {label} K={w.K} N={w.N}", flush=True)
     W = synth.weights(w)
     Wq, beta = rrs.prepare_weight(to_gpu(W), None if perm is None else to_gpu(perm))
-    Wq = untile_wq(to_np(Wq))
+    Wq = to_np(Wq)
     beta = to_np(beta)
     Ws = W if cols is None else W[:, cols]
     ref = O.prepare_weight(Ws, perm=perm)
@@ -211,7 +211,7 @@ def _partials_case(qx, qw, g, label):
     rrs = _rrs()
     print(f"[case] partials {label} M={qx.shape[0]} K={qx.shape[1]} N={qw.shape[1]} g={g}",
           flush=True)
-    Pg = rrs.w4a4_gemm_partials(to_gpu(O.pack_int4(qx)), to_gpu(tile_wq(O.pack_int4(qw.T))), g)
+    Pg = rrs.w4a4_gemm_partials(to_gpu(O.pack_int4(qx)), to_gpu(O.pack_int4(qw.T)), g)
     np.testing.assert_array_equal(to_np(Pg), O.group_partials(qx, qw, g), err_msg=label)
 
 
@@ -322,7 +322,7 @@ def test_gemm_extreme_partials(g):
     s = (rng.random(K // g) * 3 + 0.25).astype(np.float32)
     print(f"[case] extreme partials g={g}", flush=True)
     Y = rrs.w4a4_gemm(to_gpu(O.pack_int4(qx)), to_gpu(alpha), to_gpu(s),
-                      to_gpu(tile_wq(O.pack_int4(qw.T))), to_gpu(beta), g)
+                      to_gpu(O.pack_int4(qw.T)), to_gpu(beta), g)
     P = O.group_partials(qx, qw, g)
     assert np.abs(P).max() == 49 * g
     y_ref = O.output(P, s, alpha, beta, norm=K)
@@ -340,7 +340,7 @@ def _gemm_codes_case(qx, qw, g, seed, label):
     s = (rng.random(K // g) * 3 + 0.25).astype(np.float32)
     print(f"[case] gemm {label} M={M} K={K} N={N} g={g}", flush=True)
     Y = rrs.w4a4_gemm(to_gpu(O.pack_int4(qx)), to_gpu(alpha), to_gpu(s),
-                      to_gpu(tile_wq(O.pack_int4(qw.T))), to_gpu(beta), g)
+                      to_gpu(O.pack_int4(qw.T)), to_gpu(beta), g)
     P = O.group_partials(qx, qw, g)
     y_ref = O.output(P, s, alpha, beta, norm=K)
     check_y(to_np(Y).astype(np.float32), y_ref, P, s, alpha, beta, K, label)
@@ -433,7 +433,7 @@ def _ablation_case(w, flags, perm=None, label=""):
         assert np.all(to_np(s) == 1.0)
     check_codes(to_np(Xq), act, label)
     np.testing.assert_array_equal(to_np(beta), wq.beta)
-    np.testing.assert_array_equal(untile_wq(to_np(Wq)), wq.packed)
+    np.testing.assert_array_equal(to_np(Wq), wq.packed)
     P = O.group_partials(act.q, wq.q, w.g)
     norm = w.K if rot else 1
     y_ref = O.output(P, act.s, act.alpha, wq.beta, norm=norm)

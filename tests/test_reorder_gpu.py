@@ -8,7 +8,7 @@ import pytest
 
 import synth
 from oracle import rrs_oracle as O
-from tests._gpu_util import check_codes, check_y, tile_wq, to_gpu, to_np
+from tests._gpu_util import check_codes, check_y, to_gpu, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -123,7 +123,7 @@ def test_gemm_reorder(M, K, N, g, kind):
     wnat = O.prepare_weight(W)                       # weights prepared once, natural order
     np.testing.assert_array_equal(wq.q, wnat.q[O.block_order_to_perm(order, BLOCK)])
     Y = rrs.w4a4_gemm_reorder(to_gpu(act.packed), to_gpu(act.alpha), to_gpu(act.s),
-                              to_gpu(tile_wq(wnat.packed)), to_gpu(wnat.beta),
+                              to_gpu(wnat.packed), to_gpu(wnat.beta),
                               to_gpu(order.astype(np.int32)), g)
     y_ref = O.output(P, act.s, act.alpha, wq.beta, norm=K)
     Pt, st = _tol_terms(act.q, wq.q, act.s, g, M)
@@ -142,7 +142,7 @@ def test_gemm_reorder_table_entries_masked(M):
     order = np.random.default_rng(3).permutation(K // BLOCK).astype(np.int32)
     act, wq, P = _gemm_ref(X, W, g, order)
     wnat = O.prepare_weight(W)
-    args = (to_gpu(act.packed), to_gpu(act.alpha), to_gpu(act.s), to_gpu(tile_wq(wnat.packed)),
+    args = (to_gpu(act.packed), to_gpu(act.alpha), to_gpu(act.s), to_gpu(wnat.packed),
             to_gpu(wnat.beta))
     Y0 = rrs.w4a4_gemm_reorder(*args, to_gpu(order), g)
     shifted = order + (K // BLOCK) * np.where(np.arange(order.size) % 2 == 0, 3, -1)
