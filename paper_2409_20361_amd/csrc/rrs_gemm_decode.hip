@@ -7,9 +7,11 @@
 // the chip once; the matrix core only has to keep up. The kernel therefore
 // maximizes the weight bytes in flight and never stages them in LDS:
 //   - a workgroup owns two blocks of 16 output columns (rows of Wq); its four
-//     waves split K into quarters (whole smoothing groups each) and add their
-//     fp32 partial sums in a fixed order at the end (deterministic); each
-//     wave unpacks its token codes once for both blocks;
+//     waves take every fourth smoothing group (wave w: groups w, w + 4, ...,
+//     so the four read neighbouring groups of the same rows together) and
+//     add their fp32 partial sums in a fixed order at the end
+//     (deterministic); each wave unpacks its token codes once for both
+//     blocks;
 //   - tokens come in up to four blocks of 16 (TB), every block multiplied
 //     with the same weight words, so the weights still stream once for up to
 //     64 tokens (the 256-row tiles of the main kernel would leave most of
@@ -75,8 +77,8 @@ __device__ __forceinline__ void load_words(const uint8_t* __restrict__ p, int st
   }
 }
 
-// Groups per wave: whole groups, K split in quarters (one group each when K
-// has fewer than four groups; waves past the last group get none).
+// Groups per wave: a quarter of the groups (one each when K has fewer than
+// four groups; waves past the last group get none).
 __host__ __device__ inline int groups_per_wave(int K, int g) { return K / g >= 4 ? K / g / 4 : 1; }
 constexpr int kMaxTokenBlocks = 4;  // up to 64 tokens
 
@@ -106,9 +108,11 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
   const int n0 = blockIdx.x * (kBlocks * kCols);
   const size_t krow = (size_t)K / 2;
   const int G = K / g;
+  // Wave kq takes groups kq, kq + 4, kq + 8, ...: at any time the four waves
+  // read four neighbouring groups of the same rows (in the row-major Wq,
+  // 4 g / 2 contiguous bytes of each row).
   const int per = groups_per_wave(K, g);  // the same for every wave
-  const int b0 = kq * per;
-  const int nb = min(G, b0 + per) - b0;  // groups this wave really has (<= 0 past K)
+  const int nb = G > kq ? (G - kq + 3) / 4 : 0;  // groups this wave really has
   const int steps = (per + D - 1) / D * D;
 
   // The loop is free of branches around loads, so the compiler can count the
@@ -137,7 +141,7 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
 
   uint32_t wa[D][TB][NW], wb[D][kBlocks][NW];
   auto load = [&](int d, int i) {
-    const int b = min(b0 + i, G - 1);
+    const int b = min(kq + 4 * i, G - 1);
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) load_words<NW>(pa[tb] + (size_t)b * (g / 2), 64, wa[d][tb]);
 #pragma unroll
@@ -155,7 +159,7 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
       for (int r = 0; r < 4; ++r) f[tb][j][r] = 0.0f;
 
   auto consume = [&](int d, int i) {
-    const float s = i < nb ? s_group[min(b0 + i, G - 1)] : 0.0f;
+    const float s = i < nb ? s_group[min(kq + 4 * i, G - 1)] : 0.0f;
     v4i acc[TB][kBlocks];
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb)
