@@ -614,7 +614,7 @@ def main():
                    "step": "rrs_rotate_smooth_quant + rrs_w4a4_gemm"},
         "roofline": {
             "bound": "mfma",
-            "kernel": "gemm_main_kernel<4,false,false,false> (rrs_w4a4_gemm)",
+            "kernel": "gemm_main_kernel<4,false,false,false,false> (rrs_w4a4_gemm)",
             "achieved": round(gemm_tops, 2),
             "peak": INT8_MFMA_PEAK_TOPS,
             "unit": "TOP/s",
