@@ -6,7 +6,9 @@
 // With a handful of tokens the work is streaming Wq (N x K/2 bytes) through
 // the chip once; the matrix core only has to keep up. The kernel therefore
 // maximizes the weight bytes in flight and never stages them in LDS:
-//   - a workgroup owns two blocks of 16 output columns (rows of Wq); its four
+//   - a workgroup owns two blocks of 16 output columns (rows of Wq; four
+//     blocks with row-major weights from 8 tokens on and with either layout
+//     above 16 tokens); its four
 //     waves take every fourth smoothing group (wave w: groups w, w + 4, ...,
 //     so the four read neighbouring groups of the same rows together) and
 //     add their fp32 partial sums in a fixed order at the end
@@ -45,7 +47,8 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;  // 4 waves: K quarters of the same columns
 constexpr int kCols = 16;      // columns per MFMA block
-constexpr int kBlocks = 2;     // column blocks per workgroup (they share the A unpack)
+constexpr int kBlocks = 2;     // column blocks per workgroup (they share the A unpack); four
+                               // for larger token counts (launcher)
 
 __device__ __forceinline__ v4i unpack_pair(uint32_t w0, uint32_t w1) {
   v4i r;
@@ -84,7 +87,7 @@ constexpr int kMaxTokenBlocks = 4;  // up to 64 tokens
 
 // GS = g / 64 MFMA k-steps per group; TB token blocks of 16 rows (tokens
 // 16 tb .. 16 tb + 15 in block tb), all multiplied with the same weight words.
-template <int GS, int TB, bool kTiled>
+template <int GS, int TB, bool kTiled, int KB>
 __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
@@ -96,8 +99,8 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
   constexpr int D0 = NW >= 16 ? 1 : (NW >= 8 ? 2 : 4);
   constexpr int D = TB >= 4 && D0 > 1 ? D0 / 2 : D0;  // groups in flight
   // The four waves' fp32 partial sums, added at the end.
-  __shared__ __attribute__((aligned(16))) uint8_t lds[4 * TB * kBlocks * 64 * 16];
-  v4f(*part)[TB][kBlocks][64] = reinterpret_cast<v4f(*)[TB][kBlocks][64]>(lds);
+  __shared__ __attribute__((aligned(16))) uint8_t lds[4 * TB * KB * 64 * 16];
+  v4f(*part)[TB][KB][64] = reinterpret_cast<v4f(*)[TB][KB][64]>(lds);
 
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -105,7 +108,7 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
   const int kq = __builtin_amdgcn_readfirstlane(t >> 6);
   const int c = lane & 15;
   const int q = lane >> 4;
-  const int n0 = blockIdx.x * (kBlocks * kCols);
+  const int n0 = blockIdx.x * (KB * kCols);
   const size_t krow = (size_t)K / 2;
   const int G = K / g;
   // Wave kq takes groups kq, kq + 4, kq + 8, ...: at any time the four waves
@@ -132,56 +135,56 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
   const uint8_t* pa[TB];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb) pa[tb] = Xq + (size_t)min(16 * tb + c, M - 1) * krow + xo;
-  const uint8_t* pb[kBlocks];
+  const uint8_t* pb[KB];
 #pragma unroll
-  for (int j = 0; j < kBlocks; ++j) {
+  for (int j = 0; j < KB; ++j) {
     const int n = n0 + j * kCols < N ? n0 + j * kCols : 0;
     pb[j] = Wq + lay.row(n + c, K) + wo;
   }
 
-  uint32_t wa[D][TB][NW], wb[D][kBlocks][NW];
+  uint32_t wa[D][TB][NW], wb[D][KB][NW];
   auto load = [&](int d, int i) {
     const int b = min(kq + 4 * i, G - 1);
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) load_words<NW>(pa[tb] + (size_t)b * (g / 2), 64, wa[d][tb]);
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) load_words<NW>(pb[j] + (size_t)b * gstride, wts, wb[d][j]);
+    for (int j = 0; j < KB; ++j) load_words<NW>(pb[j] + (size_t)b * gstride, wts, wb[d][j]);
   };
 
   constexpr int kMagic = 0x4B400000;  // bits of 1.5 * 2^23
   const v4i seed = GS > 4 ? v4i{0, 0, 0, 0} : v4i{kMagic, kMagic, kMagic, kMagic};
-  float f[TB][kBlocks][4];
+  float f[TB][KB][4];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j)
+    for (int j = 0; j < KB; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) f[tb][j][r] = 0.0f;
 
   auto consume = [&](int d, int i) {
     const float s = i < nb ? s_group[min(kq + 4 * i, G - 1)] : 0.0f;
-    v4i acc[TB][kBlocks];
+    v4i acc[TB][KB];
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
-      for (int j = 0; j < kBlocks; ++j) acc[tb][j] = seed;
+      for (int j = 0; j < KB; ++j) acc[tb][j] = seed;
 #pragma unroll
     for (int st = 0; st < GS; ++st) {
-      v4i bv[kBlocks];
+      v4i bv[KB];
 #pragma unroll
-      for (int j = 0; j < kBlocks; ++j) bv[j] = unpack_pair(wb[d][j][2 * st], wb[d][j][2 * st + 1]);
+      for (int j = 0; j < KB; ++j) bv[j] = unpack_pair(wb[d][j][2 * st], wb[d][j][2 * st + 1]);
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
         const v4i a = unpack_pair(wa[d][tb][2 * st], wa[d][tb][2 * st + 1]);
 #pragma unroll
-        for (int j = 0; j < kBlocks; ++j)
+        for (int j = 0; j < KB; ++j)
           acc[tb][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, bv[j], acc[tb][j], 0, 0, 0);
       }
     }
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
-      for (int j = 0; j < kBlocks; ++j) {
+      for (int j = 0; j < KB; ++j) {
         // Bit-cast the whole vector, then index: bit-casting a single element
         // of an ext_vector is miscompiled (every element reads element 0).
         const v4f accf = __builtin_bit_cast(v4f, acc[tb][j]);
@@ -210,12 +213,12 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j)
+    for (int j = 0; j < KB; ++j)
       part[kq][tb][j][lane] = v4f{f[tb][j][0], f[tb][j][1], f[tb][j][2], f[tb][j][3]};
   __syncthreads();
   // Wave w stores column block w (if any): sums in the order kq = 0, 1, 2, 3.
   const int w = t >> 6;
-  if (w < kBlocks && n0 + w * kCols < N) {
+  if (w < KB && n0 + w * kCols < N) {
     // out_scale = 2^-8 (undoes the 16 x 16 of the unpacked operands) / K (the
     // unnormalized rotation; 1 without rotation), an exact power of two.
     const float inv = out_scale;
@@ -443,6 +446,11 @@ hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
                                    uint16_t* Y, float out_scale, hipStream_t stream,
                                    const int32_t* border, WqLayout lay) {
   const int grid = (N / kCols + kBlocks - 1) / kBlocks;  // N % 16 == 0 (API precondition)
+  // Four column blocks per workgroup (64 rows of Wq) for row-major weights
+  // from 8 tokens on and for either layout above 16 tokens (at the decode
+  // shape, row-major: 3 % faster at M = 8, 19 % at M = 64).
+  const bool kb4 = lay.tiled ? M > kCols : M >= 8;
+  const int grid4 = (N / kCols + 3) / 4;
   if (border) {
     if (M > kCols) return hipErrorInvalidValue;  // the gather kernel takes one token block
     if (lay.tiled)
@@ -454,12 +462,18 @@ hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
     return hipGetLastError();
   }
   const int tbs = M <= kCols ? 1 : (M <= 2 * kCols ? 2 : 4);
-#define RRS_DECODE(GS_, TB_)                                             \
-  if (lay.tiled)                                                        \
-    gemm_decode_kernel<GS_, TB_, true><<<grid, kThreads, 0, stream>>>(  \
-        Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale);      \
-  else                                                                  \
-    gemm_decode_kernel<GS_, TB_, false><<<grid, kThreads, 0, stream>>>( \
+#define RRS_DECODE(GS_, TB_)                                                    \
+  if (lay.tiled && kb4)                                                        \
+    gemm_decode_kernel<GS_, TB_, true, 4><<<grid4, kThreads, 0, stream>>>(       \
+        Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale);             \
+  else if (lay.tiled)                                                          \
+    gemm_decode_kernel<GS_, TB_, true, kBlocks><<<grid, kThreads, 0, stream>>>(  \
+        Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale);             \
+  else if (kb4)                                                                \
+    gemm_decode_kernel<GS_, TB_, false, 4><<<grid4, kThreads, 0, stream>>>(      \
+        Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale);             \
+  else                                                                         \
+    gemm_decode_kernel<GS_, TB_, false, kBlocks><<<grid, kThreads, 0, stream>>>( \
         Xq, a_scale, s_group, Wq, w_scale, M, N, K, Y, out_scale)
 #define RRS_DECODE_TB(GS_) \
   if (tbs == 1) {          \

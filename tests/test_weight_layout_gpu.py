@@ -71,11 +71,14 @@ def test_tiled_sub_channel_prepare():
     _same(sr, st, "w_sub")
 
 
-# M = 1, 8 and 16 take one block of 16 tokens in the few-token kernel, 24 two
-# and 64 four; 65 and 300 take the main kernel.
+# M = 1, 8 and 16 take one block of 16 tokens in the few-token kernel, 24 and
+# 40 two and 64 four (row-major weights from M = 8 on: four column blocks per
+# workgroup, so N = 208 and 336 leave a partial last workgroup); 65 and 300
+# take the main kernel.
 @pytest.mark.parametrize("M,K,N,g", [
     (1, 8192, 256, 128), (8, 4096, 512, 64), (16, 2048, 128, 512), (24, 4096, 512, 256),
-    (64, 2048, 384, 512), (65, 4096, 512, 128), (300, 1024, 640, 128)])
+    (64, 2048, 384, 512), (65, 4096, 512, 128), (300, 1024, 640, 128),
+    (8, 4096, 208, 128), (40, 2048, 336, 64)])
 def test_gemm_and_linear_agree_across_layouts(M, K, N, g):
     rrs = _rrs()
     print(f"[case] layouts gemm/linear M={M} K={K} N={N} g={g}", flush=True)
