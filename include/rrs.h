@@ -27,9 +27,17 @@
  *  - Shapes: M >= 1; N >= 1 and N % 16 == 0; K a power of two with
  *    512 <= K <= 16384. Group size g: g divides K and g is one of
  *    64, 128, 256, 512. Every pointer must be 16-byte aligned.
- *  - Preconditions not checked: inputs finite; `perm` a permutation of
- *    0..K-1; buffers large enough for the stated sizes; no overlap between
- *    inputs and outputs.
+ *  - Preconditions: inputs finite; `perm` a permutation of 0..K-1 (and
+ *    `block_order` of 0..K/32-1); buffers large enough for the stated sizes;
+ *    no overlap between inputs and outputs. Violations are undefined
+ *    behaviour (meaningless codes, never an out-of-bounds access). With the
+ *    environment variable RRS_DEBUG set to a non-zero value (read at every
+ *    call) the first two are checked after the checks above: the library
+ *    copies X or W, perm / block_order and the float32 scales a call reads
+ *    to host memory on `stream`, waits for them, and returns
+ *    RRS_ERR_PRECONDITION (nothing enqueued) on a non-finite value or a
+ *    non-permutation. Debug mode synchronises the stream, so it must not be
+ *    used while the stream is captured into a graph.
  *  - Device-side faults surface at the caller's next synchronisation, as with
  *    any HIP launch; launch failures are returned as RRS_ERR_HIP.
  *
@@ -83,7 +91,11 @@ enum {
   RRS_ERR_NO_DEVICE = -6,  /* no HIP device visible */
   RRS_ERR_ARCH = -7,       /* the current device is not gfx950 */
   RRS_ERR_HIP = -8,        /* a HIP runtime call or launch failed */
-  RRS_ERR_FLAGS = -9       /* unknown or unsupported flag bits (_ex functions) */
+  RRS_ERR_FLAGS = -9,      /* unknown or unsupported flag bits (_ex functions) */
+  RRS_ERR_PRECONDITION = -10, /* RRS_DEBUG only: an input is not finite, or perm /
+                                 block_order is not a permutation */
+  RRS_ERR_TIMEOUT = -11       /* RRS_DEBUG only: a bounded wait between workgroups ran
+                                 out (the affected outputs were written as NaN) */
 };
 
 /*
@@ -211,10 +223,38 @@ rrs_status rrs_linear_ex(const void* X, const void* Wq, const float* w_scale, in
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Test hook for the failure path of the few-token quantizer (not for
+ * computing: use rrs_rotate_smooth_quant). For 2 to 16 tokens without a
+ * static reorder, rrs_rotate_smooth_quant runs one workgroup per token row
+ * in a single launch; the rows exchange their group maxima through the
+ * workspace and each waits, with a bounded poll, until all M have arrived
+ * (Eq. 1 takes the maximum over every token). That needs the M workgroups to
+ * be resident at the same time, which holds on an otherwise idle device but
+ * not when other work fills every compute unit; a wait that runs out counts
+ * itself in the workspace, writes NaN into its row's a_scale (row 0 also
+ * into s_group) and ends, so the failure shows in the outputs.
+ * This hook runs that kernel with the arrival target raised by
+ * extra_arrivals (>= 1 makes it unreachable) and the wait cut to max_polls
+ * polls (>= 1), waits for `stream`, and stores the number of waits that ran
+ * out in *timeouts (host pointer). Arguments otherwise as
+ * rrs_rotate_smooth_quant with perm = NULL and 2 <= M <= 16; RRS_ERR_SHAPE
+ * for M outside 2..16, RRS_ERR_FLAGS for extra_arrivals < 0 or
+ * max_polls < 1. With RRS_DEBUG set, rrs_rotate_smooth_quant(_ex) and
+ * rrs_linear(_ex) read the same count after a call that used this kernel and
+ * return RRS_ERR_TIMEOUT when it is not zero.
+ */
+rrs_status rrs_test_quant_rows_wait(const void* X, int M, int K, int group_size,
+                                    int extra_arrivals, int max_polls, void* Xq,
+                                    float* a_scale, float* s_group, void* workspace,
+                                    size_t workspace_bytes, int32_t* timeouts, void* stream);
+
+/*
  * Test hook: the exact int32 group partials P[b][i][n] (b < K/g, i < M,
- * n < N; G x M x N int32, row-major) from the same GEMM main loop as
- * rrs_w4a4_gemm, before any scaling (Eq. 3's inner sums per block). Wq
- * row-major.
+ * n < N; G x M x N int32, row-major), before any scaling (Eq. 3's inner sums
+ * per block). Wq row-major. The call runs the same kernel that rrs_w4a4_gemm
+ * runs for this shape (the few-token kernels for M <= 64, the main kernel
+ * above), with the same accumulator seeding, and decodes each group's
+ * accumulators instead of rescaling them.
  */
 rrs_status rrs_w4a4_gemm_partials(const void* Xq, const void* Wq, int M, int N, int K,
                                   int group_size, int32_t* P, void* stream);

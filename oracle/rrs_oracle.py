@@ -56,8 +56,8 @@ Readings of the paper (it is silent or loose on these points):
   * Weights: u = H_K W (column FWHT), b_n = max_k |u_kn|, winv_n = fl(7/b_n),
     w_kn = clamp(rint(fl(u_kn winv_n)), -7, 7), beta_n = fl(b_n / 7).
   * Output: Y = fl32((alpha_i beta_n / K) * sum_b s_b P_b[i, n]), the sum and
-    the products taken in binary64 (the paper applies the smoothing scale to
-    the dequantized interim result of each block, Fig. 4 step (3)).
+    the products taken in binary64 (the group's smoothing scale multiplies
+    each block's dequantized partial product, Fig. 4 step (3)).
   * Packing: two's-complement nibbles, two per byte, low nibble = even index.
 """
 from __future__ import annotations

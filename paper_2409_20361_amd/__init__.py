@@ -29,6 +29,7 @@ from ._binding import (  # noqa: F401
     linear_workspace_bytes,
     prepare_weight,
     prepare_weight_sub_channel,
+    quant_rows_wait_hook,
     quantize_sub_channel,
     rotate_smooth_quant,
     rotate_smooth_quant_reorder,
@@ -47,7 +48,8 @@ __all__ = [
     "REORDER_BLOCK", "SCHEME_PER_CHANNEL", "SCHEME_RUNTIME_SMOOTH", "SCHEME_SUB_CHANNEL",
     "SKIP_ROTATION", "SKIP_SMOOTHING", "WEIGHT_TILED", "RRSError", "lib", "lib_path", "linear", "linear_reorder",
     "linear_reorder_workspace_bytes", "linear_workspace_bytes",
-    "prepare_weight", "prepare_weight_sub_channel", "quantize_sub_channel",
+    "prepare_weight", "prepare_weight_sub_channel", "quant_rows_wait_hook",
+    "quantize_sub_channel",
     "reorder_workspace_bytes", "rotate_smooth_quant", "rotate_smooth_quant_reorder",
     "status_string", "version", "w4a4_gemm", "w4a4_gemm_partials",
     "w4a4_gemm_per_channel", "w4a4_gemm_reorder", "w4a4_gemm_scheme", "workspace_bytes",

@@ -26,6 +26,8 @@ _SIGNATURES = {
     "rrs_w4a4_gemm": (ctypes.c_int32, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp]),
     "rrs_linear": (ctypes.c_int32, [_vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp, _sz, _vp]),
     "rrs_w4a4_gemm_partials": (ctypes.c_int32, [_vp, _vp, _i, _i, _i, _i, _vp, _vp]),
+    "rrs_test_quant_rows_wait": (ctypes.c_int32, [_vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _vp,
+                                                  _sz, _vp, _vp]),
     "rrs_prepare_weight_ex": (ctypes.c_int32, [_vp, _i, _i, _vp, _i, _vp, _vp, _vp]),
     "rrs_rotate_smooth_quant_ex": (ctypes.c_int32,
                                    [_vp, _i, _i, _i, _vp, _i, _vp, _vp, _vp, _vp, _sz, _vp]),
@@ -211,7 +213,8 @@ def linear(X: torch.Tensor, Wq: torch.Tensor, w_scale: torch.Tensor, g: int,
 
 
 def w4a4_gemm_partials(Xq: torch.Tensor, Wq: torch.Tensor, g: int) -> torch.Tensor:
-    """Exact int32 group partials P[b, i, n] from the GEMM main loop (test hook)."""
+    """Exact int32 group partials P[b, i, n] (test hook) from the kernel that
+    rrs_w4a4_gemm runs for this shape with row-major Wq."""
     M, Kh = Xq.shape
     K = 2 * Kh
     N = Wq.shape[0]
@@ -221,6 +224,27 @@ def w4a4_gemm_partials(Xq: torch.Tensor, Wq: torch.Tensor, g: int) -> torch.Tens
     _check(lib().rrs_w4a4_gemm_partials(xp, wp, M, N, K, g, P.data_ptr(), _stream(Xq.device)),
            "rrs_w4a4_gemm_partials")
     return P
+
+
+def quant_rows_wait_hook(X: torch.Tensor, g: int, extra_arrivals: int, max_polls: int,
+                         workspace: Optional[torch.Tensor] = None):
+    """Test hook of the few-token quantizer's bounded wait (2 <= M <= 16): runs it
+    with the arrival target raised by extra_arrivals and at most max_polls
+    polls; returns (Xq, a_scale, s_group, number of waits that ran out)."""
+    M, K = X.shape
+    xp = _dev(X, "X", torch.float16, (M, K))
+    Xq = torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
+    a = torch.empty((M,), dtype=torch.float32, device=X.device)
+    s = torch.empty((K // g,), dtype=torch.float32, device=X.device)
+    if workspace is None:
+        workspace = torch.empty((max(workspace_bytes(M, K, g), 1),), dtype=torch.uint8,
+                                device=X.device)
+    n = ctypes.c_int32(-1)
+    _check(lib().rrs_test_quant_rows_wait(
+        xp, M, K, g, extra_arrivals, max_polls, Xq.data_ptr(), a.data_ptr(), s.data_ptr(),
+        workspace.data_ptr(), workspace.numel() * workspace.element_size(), ctypes.byref(n),
+        _stream(X.device)), "rrs_test_quant_rows_wait")
+    return Xq, a, s, n.value
 
 
 def quantize_sub_channel(X: torch.Tensor, g: int, flags: int = 0

@@ -8,13 +8,14 @@
 #include <cstdlib>
 #include <cmath>
 #include <cstring>
+#include <vector>
 
 #include "rrs.h"
 #include "rrs_internal.h"
 
 namespace {
 
-constexpr int kVersion = 500;  // 0.5.0: row-major Wq by default, RRS_WEIGHT_TILED option
+constexpr int kVersion = 600;  // 0.6.0: RRS_DEBUG checks, weight-streaming few-token GEMM
 constexpr int kMaxDevices = 64;
 
 bool is_aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -43,12 +44,94 @@ float out_scale(int K, int flags) {
   return (flags & RRS_SKIP_ROTATION) ? s : s / (float)K;
 }
 
+// RRS_DEBUG is read at every call (a getenv, far below a launch's cost), so a
+// process can switch the checks on and off between calls.
 bool debug_enabled() {
-  static const bool on = [] {
-    const char* v = std::getenv("RRS_DEBUG");
-    return v != nullptr && v[0] != '\0' && v[0] != '0';
-  }();
-  return on;
+  const char* v = std::getenv("RRS_DEBUG");
+  return v != nullptr && v[0] != '\0' && v[0] != '0';
+}
+
+// ---------------------------------------------------------------------------
+// RRS_DEBUG precondition checks. They run after the regular validation (so
+// the pointers are non-null and aligned and the device is a gfx950), copy
+// the checked input to host memory on the caller's stream and wait for it,
+// so they must not be used while the stream is being captured into a graph.
+// ---------------------------------------------------------------------------
+
+// Copies `bytes` bytes of device memory to `host` on `st` and waits.
+rrs_status debug_fetch(void* host, const void* dev, size_t bytes, void* stream) {
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (bytes == 0) return RRS_OK;
+  if (hipMemcpyAsync(host, dev, bytes, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess) {
+    (void)hipGetLastError();
+    return RRS_ERR_HIP;
+  }
+  return RRS_OK;
+}
+
+// `perm` (n entries) holds every value of 0..n-1 exactly once.
+rrs_status debug_check_perm(const int32_t* perm, int n, const char* what, void* stream) {
+  if (!perm) return RRS_OK;
+  std::vector<int32_t> h((size_t)n);
+  if (rrs_status e = debug_fetch(h.data(), perm, (size_t)n * 4, stream)) return e;
+  std::vector<unsigned char> seen((size_t)n, 0);
+  for (int j = 0; j < n; ++j) {
+    const int32_t v = h[(size_t)j];
+    if (v < 0 || v >= n || seen[(size_t)v]) {
+      std::fprintf(stderr, "[rrs] RRS_DEBUG: %s is not a permutation of 0..%d (entry %d = %d)\n",
+                   what, n - 1, j, (int)v);
+      return RRS_ERR_PRECONDITION;
+    }
+    seen[(size_t)v] = 1;
+  }
+  return RRS_OK;
+}
+
+// Every float16 of the count at `p` is finite (exponent field not all ones).
+rrs_status debug_check_finite_f16(const void* p, size_t count, const char* what, void* stream) {
+  std::vector<uint16_t> h(count);
+  if (rrs_status e = debug_fetch(h.data(), p, count * 2, stream)) return e;
+  for (size_t i = 0; i < count; ++i) {
+    if ((h[i] & 0x7C00u) == 0x7C00u) {
+      std::fprintf(stderr, "[rrs] RRS_DEBUG: %s[%zu] is not finite (bits 0x%04x)\n", what, i,
+                   (unsigned)h[i]);
+      return RRS_ERR_PRECONDITION;
+    }
+  }
+  return RRS_OK;
+}
+
+// After a quantizer launch under RRS_DEBUG: waits for the stream and fails
+// when the per-row kernel (used for this shape) reported a wait that ran out.
+rrs_status debug_check_quant_wait(int M, int K, int g, const int32_t* perm, int flags,
+                                  const void* workspace, void* stream) {
+  if (!rrs::quant_rows_used(M, K, g, perm, flags & kQuantFlags) || M < 2) return RRS_OK;
+  uint32_t n = 0;
+  if (rrs::quant_rows_timeouts(workspace, static_cast<hipStream_t>(stream), &n) != hipSuccess) {
+    (void)hipGetLastError();
+    return RRS_ERR_HIP;
+  }
+  if (n) {
+    std::fprintf(stderr, "[rrs] RRS_DEBUG: %u workgroup waits ran out in the quantizer\n", n);
+    return RRS_ERR_TIMEOUT;
+  }
+  return RRS_OK;
+}
+
+// Every float32 of the count at `p` is finite.
+rrs_status debug_check_finite_f32(const float* p, size_t count, const char* what,
+                                  void* stream) {
+  std::vector<float> h(count);
+  if (rrs_status e = debug_fetch(h.data(), p, count * 4, stream)) return e;
+  for (size_t i = 0; i < count; ++i) {
+    if (!std::isfinite(h[i])) {
+      std::fprintf(stderr, "[rrs] RRS_DEBUG: %s[%zu] is not finite (%g)\n", what, i,
+                   (double)h[i]);
+      return RRS_ERR_PRECONDITION;
+    }
+  }
+  return RRS_OK;
 }
 
 // 0 = unknown, 1 = gfx950, 2 = other architecture.
@@ -111,6 +194,12 @@ const char* rrs_status_string(rrs_status s) {
     case RRS_ERR_ARCH: return "RRS_ERR_ARCH: current device is not gfx950";
     case RRS_ERR_HIP: return "RRS_ERR_HIP: a HIP call or kernel launch failed";
     case RRS_ERR_FLAGS: return "RRS_ERR_FLAGS: unknown or unsupported flag bits";
+    case RRS_ERR_TIMEOUT:
+      return "RRS_ERR_TIMEOUT: (RRS_DEBUG) a bounded wait between workgroups ran out; the "
+             "affected outputs are NaN";
+    case RRS_ERR_PRECONDITION:
+      return "RRS_ERR_PRECONDITION: (RRS_DEBUG) an input is not finite or a permutation is "
+             "not one";
     default: return "RRS_ERR_UNKNOWN";
   }
 }
@@ -139,6 +228,10 @@ rrs_status rrs_prepare_weight_ex(const void* W, int K, int N, const int32_t* per
   if (!is_aligned(W) || !is_aligned(Wq) || !is_aligned(w_scale) || (perm && !is_aligned(perm)))
     return RRS_ERR_ALIGN;
   if (rrs_status s = check_device()) return s;
+  if (debug_enabled()) {
+    if (rrs_status s = debug_check_finite_f16(W, (size_t)K * N, "W", stream)) return s;
+    if (rrs_status s = debug_check_perm(perm, K, "perm", stream)) return s;
+  }
   return from_hip(rrs::launch_prepare_weight(
       static_cast<const uint16_t*>(W), K, N, perm, !(flags & RRS_SKIP_ROTATION),
       static_cast<uint8_t*>(Wq), w_scale, static_cast<hipStream_t>(stream), layout(flags)));
@@ -168,9 +261,16 @@ rrs_status rrs_rotate_smooth_quant_ex(const void* X, int M, int K, int group_siz
     return RRS_ERR_ALIGN;
   if (workspace_bytes < rrs::quant_workspace_bytes(M, K)) return RRS_ERR_WORKSPACE;
   if (rrs_status s = check_device()) return s;
-  return from_hip(rrs::launch_rotate_smooth_quant(
+  if (debug_enabled()) {
+    if (rrs_status s = debug_check_finite_f16(X, (size_t)M * K, "X", stream)) return s;
+    if (rrs_status s = debug_check_perm(perm, K, "perm", stream)) return s;
+  }
+  const rrs_status st = from_hip(rrs::launch_rotate_smooth_quant(
       static_cast<const uint16_t*>(X), M, K, group_size, perm, flags & kQuantFlags,
       static_cast<uint8_t*>(Xq), a_scale, s_group, workspace, static_cast<hipStream_t>(stream)));
+  if (st == RRS_OK && debug_enabled())
+    return debug_check_quant_wait(M, K, group_size, perm, flags, workspace, stream);
+  return st;
 }
 
 rrs_status rrs_rotate_smooth_quant(const void* X, int M, int K, int group_size,
@@ -198,6 +298,12 @@ rrs_status rrs_w4a4_gemm_ex(const void* Xq, const float* a_scale, const float* s
       !is_aligned(w_scale) || !is_aligned(Y))
     return RRS_ERR_ALIGN;
   if (rrs_status s = check_device()) return s;
+  if (debug_enabled()) {
+    if (rrs_status s = debug_check_finite_f32(a_scale, (size_t)M, "a_scale", stream)) return s;
+    if (rrs_status s = debug_check_finite_f32(s_group, (size_t)(K / group_size), "s_group", stream))
+      return s;
+    if (rrs_status s = debug_check_finite_f32(w_scale, (size_t)N, "w_scale", stream)) return s;
+  }
   return from_hip(rrs::launch_w4a4_gemm(
       static_cast<const uint8_t*>(Xq), a_scale, s_group, static_cast<const uint8_t*>(Wq),
       w_scale, M, N, K, group_size, static_cast<uint16_t*>(Y), out_scale(K, flags),
@@ -228,6 +334,11 @@ rrs_status rrs_linear_ex(const void* X, const void* Wq, const float* w_scale, in
     return RRS_ERR_ALIGN;
   if (workspace_bytes < linear_ws_bytes(M, K, group_size)) return RRS_ERR_WORKSPACE;
   if (rrs_status s = check_device()) return s;
+  if (debug_enabled()) {
+    if (rrs_status s = debug_check_finite_f16(X, (size_t)M * K, "X", stream)) return s;
+    if (rrs_status s = debug_check_perm(perm, K, "perm", stream)) return s;
+    if (rrs_status s = debug_check_finite_f32(w_scale, (size_t)N, "w_scale", stream)) return s;
+  }
 
   char* ws = static_cast<char*>(workspace);
   void* qws = ws;
@@ -243,9 +354,12 @@ rrs_status rrs_linear_ex(const void* X, const void* Wq, const float* w_scale, in
                                                  group_size, perm, flags & kQuantFlags, xq, a,
                                                  s, qws, st);
   if (e != hipSuccess) return RRS_ERR_HIP;
-  return from_hip(rrs::launch_w4a4_gemm(xq, a, s, static_cast<const uint8_t*>(Wq), w_scale, M,
-                                        N, K, group_size, static_cast<uint16_t*>(Y),
-                                        out_scale(K, flags), st, layout(flags)));
+  const rrs_status r = from_hip(rrs::launch_w4a4_gemm(
+      xq, a, s, static_cast<const uint8_t*>(Wq), w_scale, M, N, K, group_size,
+      static_cast<uint16_t*>(Y), out_scale(K, flags), st, layout(flags)));
+  if (r == RRS_OK && debug_enabled())
+    return debug_check_quant_wait(M, K, group_size, perm, flags, qws, stream);
+  return r;
 }
 
 rrs_status rrs_linear(const void* X, const void* Wq, const float* w_scale, int M, int N,
@@ -266,6 +380,8 @@ rrs_status rrs_quantize_sub_channel(const void* X, int M, int K, int group_size,
   if (!valid_flags(flags, kRotationFlags)) return RRS_ERR_FLAGS;
   if (!is_aligned(X) || !is_aligned(Xq) || !is_aligned(a_sub)) return RRS_ERR_ALIGN;
   if (rrs_status s = check_device()) return s;
+  if (debug_enabled())
+    if (rrs_status s = debug_check_finite_f16(X, (size_t)M * K, "X", stream)) return s;
   return from_hip(rrs::launch_quantize_sub_channel(
       static_cast<const uint16_t*>(X), M, K, group_size, flags & RRS_SKIP_ROTATION,
       static_cast<uint8_t*>(Xq), a_sub,
@@ -283,6 +399,8 @@ rrs_status rrs_prepare_weight_sub_channel(const void* W, int K, int N, int group
   if (!valid_flags(flags, kRotationFlags)) return RRS_ERR_FLAGS;
   if (!is_aligned(W) || !is_aligned(Wq) || !is_aligned(w_sub)) return RRS_ERR_ALIGN;
   if (rrs_status s = check_device()) return s;
+  if (debug_enabled())
+    if (rrs_status s = debug_check_finite_f16(W, (size_t)K * N, "W", stream)) return s;
   return from_hip(rrs::launch_prepare_weight_sub_channel(
       static_cast<const uint16_t*>(W), K, N, group_size, !(flags & RRS_SKIP_ROTATION),
       static_cast<uint8_t*>(Wq), w_sub, static_cast<hipStream_t>(stream), layout(flags)));
@@ -364,6 +482,8 @@ rrs_status rrs_rotate_smooth_quant_reorder(const void* X, int M, int K, int grou
     return RRS_ERR_ALIGN;
   if (workspace_bytes < rrs::reorder_workspace_bytes(K)) return RRS_ERR_WORKSPACE;
   if (rrs_status s = check_device()) return s;
+  if (debug_enabled())
+    if (rrs_status s = debug_check_finite_f16(X, (size_t)M * K, "X", stream)) return s;
   return from_hip(rrs::launch_rotate_smooth_quant_reorder(
       static_cast<const uint16_t*>(X), M, K, group_size, flags & RRS_SKIP_ROTATION,
       static_cast<uint8_t*>(Xq), a_scale, s_group, block_order, workspace,
@@ -385,6 +505,14 @@ rrs_status rrs_w4a4_gemm_reorder(const void* Xq, const float* a_scale, const flo
       !is_aligned(w_scale) || !is_aligned(block_order) || !is_aligned(Y))
     return RRS_ERR_ALIGN;
   if (rrs_status s = check_device()) return s;
+  if (debug_enabled()) {
+    if (rrs_status s = debug_check_perm(block_order, K / RRS_REORDER_BLOCK, "block_order", stream))
+      return s;
+    if (rrs_status s = debug_check_finite_f32(a_scale, (size_t)M, "a_scale", stream)) return s;
+    if (rrs_status s = debug_check_finite_f32(s_group, (size_t)(K / group_size), "s_group", stream))
+      return s;
+    if (rrs_status s = debug_check_finite_f32(w_scale, (size_t)N, "w_scale", stream)) return s;
+  }
   return from_hip(rrs::launch_w4a4_gemm_reorder(
       static_cast<const uint8_t*>(Xq), a_scale, s_group, static_cast<const uint8_t*>(Wq),
       w_scale, block_order, M, N, K, group_size, static_cast<uint16_t*>(Y), out_scale(K, flags),
@@ -409,6 +537,10 @@ rrs_status rrs_linear_reorder(const void* X, const void* Wq, const float* w_scal
     return RRS_ERR_ALIGN;
   if (workspace_bytes < linear_reorder_ws_bytes(M, K, group_size)) return RRS_ERR_WORKSPACE;
   if (rrs_status s = check_device()) return s;
+  if (debug_enabled()) {
+    if (rrs_status s = debug_check_finite_f16(X, (size_t)M * K, "X", stream)) return s;
+    if (rrs_status s = debug_check_finite_f32(w_scale, (size_t)N, "w_scale", stream)) return s;
+  }
 
   char* ws = static_cast<char*>(workspace);
   void* qws = ws;
@@ -430,6 +562,35 @@ rrs_status rrs_linear_reorder(const void* X, const void* Wq, const float* w_scal
                                                 w_scale, order, M, N, K, group_size,
                                                 static_cast<uint16_t*>(Y), out_scale(K, flags),
                                                 st, layout(flags)));
+}
+
+rrs_status rrs_test_quant_rows_wait(const void* X, int M, int K, int group_size,
+                                    int extra_arrivals, int max_polls, void* Xq,
+                                    float* a_scale, float* s_group, void* workspace,
+                                    size_t workspace_bytes, int32_t* timeouts, void* stream) {
+  if (!X || !Xq || !a_scale || !s_group || !workspace || !timeouts) return RRS_ERR_NULL;
+  if (M < 2 || !rrs::quant_rows_fits(M) || !valid_k(K)) return RRS_ERR_SHAPE;
+  if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
+  if (extra_arrivals < 0 || max_polls < 1) return RRS_ERR_FLAGS;
+  if (!is_aligned(X) || !is_aligned(Xq) || !is_aligned(a_scale) || !is_aligned(s_group) ||
+      !is_aligned(workspace))
+    return RRS_ERR_ALIGN;
+  if (workspace_bytes < rrs::quant_workspace_bytes(M, K) ||
+      workspace_bytes < rrs::quant_rows_workspace_bytes(K, group_size))
+    return RRS_ERR_WORKSPACE;
+  if (rrs_status s = check_device()) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (rrs::launch_quant_rows(static_cast<const uint16_t*>(X), M, K, group_size, true,
+                             static_cast<uint8_t*>(Xq), a_scale, s_group, workspace, st,
+                             extra_arrivals, max_polls) != hipSuccess)
+    return RRS_ERR_HIP;
+  uint32_t n = 0;
+  if (rrs::quant_rows_timeouts(workspace, st, &n) != hipSuccess) {
+    (void)hipGetLastError();
+    return RRS_ERR_HIP;
+  }
+  *timeouts = (int32_t)n;
+  return RRS_OK;
 }
 
 rrs_status rrs_w4a4_gemm_partials(const void* Xq, const void* Wq, int M, int N, int K,

@@ -206,7 +206,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        acc[h][j][r] = (kPartials || kPerChannel || GS > 8) ? 0 : 0x4B400000;
+        acc[h][j][r] = (kPerChannel || GS > 8) ? 0 : 0x4B400000;
         f[h][j][r] = 0.0f;
       }
 
@@ -245,7 +245,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
         const int e = q0 + q;
         const int row = acc_row(m0, wm, h, e & 15, lane);
         const int col = acc_col(n0, wn, e >> 4, lane);
-        if (row < M && col < N) Pg[(size_t)row * N + col] = acc[h][e >> 4][e & 15] >> 8;
+        // The production seed: the accumulator holds 0x4B400000 + 256 P (g <= 256)
+        // or 256 P (g = 512); the hook undoes exactly that encoding.
+        const int32_t v = acc[h][e >> 4][e & 15];
+        if (row < M && col < N) Pg[(size_t)row * N + col] = (GS > 8 ? v : v - kMagic) >> 8;
       }
     }
   };
@@ -303,8 +306,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
 #pragma unroll
       for (int s = 0; s < PH; ++s) {
         const bool fresh = !kPerChannel && g_first && s == 0;
-        acc[0][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa0[s], fb[s][0], fresh ? ((kPartials || GS > 8) ? zero : magic) : acc[0][0], 0, 0, 0);
-        acc[0][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa0[s], fb[s][1], fresh ? ((kPartials || GS > 8) ? zero : magic) : acc[0][1], 0, 0, 0);
+        acc[0][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa0[s], fb[s][0], fresh ? (GS > 8 ? zero : magic) : acc[0][0], 0, 0, 0);
+        acc[0][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa0[s], fb[s][1], fresh ? (GS > 8 ? zero : magic) : acc[0][1], 0, 0, 0);
         fa1[s] = afrag(stage, 1, ks0 + s);
         if (g_first) {
           if (!kPartials || grp > 0) rescale(1, s * CONV, s_prev, grp - 1);
@@ -340,8 +343,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_main_kernel(
 #pragma unroll
       for (int s = 0; s < PH; ++s) {
         const bool fresh = !kPerChannel && g_first && s == 0;
-        acc[1][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa1[s], fb[s][0], fresh ? ((kPartials || GS > 8) ? zero : magic) : acc[1][0], 0, 0, 0);
-        acc[1][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa1[s], fb[s][1], fresh ? ((kPartials || GS > 8) ? zero : magic) : acc[1][1], 0, 0, 0);
+        acc[1][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa1[s], fb[s][0], fresh ? (GS > 8 ? zero : magic) : acc[1][0], 0, 0, 0);
+        acc[1][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa1[s], fb[s][1], fresh ? (GS > 8 ? zero : magic) : acc[1][1], 0, 0, 0);
         fb[s][0] = bfrag(nstage, 0, nks0 + s);
         fb[s][1] = bfrag(nstage, 1, nks0 + s);
         fa0[s] = afrag(nstage, 0, nks0 + s);
@@ -449,6 +452,9 @@ hipError_t launch_w4a4_gemm(const uint8_t* Xq, const float* a_scale, const float
                             const uint8_t* Wq, const float* w_scale, int M, int N, int K,
                             int g, uint16_t* Y, float out_scale, hipStream_t stream,
                             WqLayout lay) {
+  if (stream_kernel_fits(M, K, g))
+    return launch_w4a4_gemm_stream(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, out_scale,
+                                   stream, lay);
   if (decode_kernel_fits(M))
     return launch_w4a4_gemm_decode(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, out_scale,
                                    stream, nullptr, lay);
@@ -496,6 +502,11 @@ hipError_t launch_w4a4_gemm_reorder(const uint8_t* Xq, const float* a_scale,
 hipError_t launch_w4a4_gemm_partials(const uint8_t* Xq, const uint8_t* Wq, int M, int N,
                                      int K, int g, int32_t* P, hipStream_t stream,
                                      WqLayout lay) {
+  // The kernel rrs_w4a4_gemm would take for this shape (row-major Wq).
+  if (stream_kernel_fits(M, K, g))
+    return launch_w4a4_gemm_stream_partials(Xq, Wq, M, N, K, g, P, stream, lay);
+  if (decode_kernel_fits(M) && !lay.tiled)
+    return launch_w4a4_gemm_decode_partials(Xq, Wq, M, N, K, g, P, stream);
   if (!main_kernel_fits(K, g))
     return launch_w4a4_gemm_partials_small(Xq, Wq, M, N, K, g, P, stream, lay);
   return launch_main<true>(Xq, nullptr, nullptr, Wq, nullptr, M, N, K, g, nullptr, P, 0.0f,

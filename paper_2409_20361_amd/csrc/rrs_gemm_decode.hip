@@ -87,12 +87,14 @@ constexpr int kMaxTokenBlocks = 4;  // up to 64 tokens
 
 // GS = g / 64 MFMA k-steps per group; TB token blocks of 16 rows (tokens
 // 16 tb .. 16 tb + 15 in block tb), all multiplied with the same weight words.
-template <int GS, int TB, bool kTiled, int KB>
+// kPartials (test hook): instead of Y, write P[b][i][n] for every group b,
+// token i < M and column n, decoded from the same seeded accumulators.
+template <int GS, int TB, bool kTiled, int KB, bool kPartials = false>
 __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
     const float* __restrict__ w_scale, int M, int N, int K, uint16_t* __restrict__ Y,
-    float out_scale) {
+    float out_scale, int32_t* __restrict__ P = nullptr) {
   constexpr WqLayout lay{kTiled};
   constexpr int g = GS * 64;
   constexpr int NW = g / 32;                  // words per lane per group and block
@@ -162,7 +164,7 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
       for (int r = 0; r < 4; ++r) f[tb][j][r] = 0.0f;
 
   auto consume = [&](int d, int i) {
-    const float s = i < nb ? s_group[min(kq + 4 * i, G - 1)] : 0.0f;
+    const float s = (!kPartials && i < nb) ? s_group[min(kq + 4 * i, G - 1)] : 0.0f;
     v4i acc[TB][KB];
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb)
@@ -180,6 +182,23 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
         for (int j = 0; j < KB; ++j)
           acc[tb][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, bv[j], acc[tb][j], 0, 0, 0);
       }
+    }
+    if constexpr (kPartials) {
+      if (i < nb) {
+        int32_t* Pg = P + (size_t)(kq + 4 * i) * (size_t)M * (size_t)N;
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+          for (int j = 0; j < KB; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int row = 16 * tb + 4 * q + r;
+              const int col = n0 + j * kCols + c;
+              const int v = acc[tb][j][r];
+              if (row < M && col < N) Pg[(size_t)row * N + col] = (GS > 4 ? v : v - kMagic) >> 8;
+            }
+      }
+      return;
     }
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb)
@@ -209,6 +228,7 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_kernel(
 #pragma unroll
   for (int d = 0; d < D; ++d) consume(d, i + d);
 
+  if constexpr (kPartials) return;
   // Partial sums of the four K quarters, added in a fixed order.
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb)
@@ -438,6 +458,40 @@ __global__ __launch_bounds__(kThreads) void gemm_decode_gather_kernel(
 }  // namespace
 
 bool decode_kernel_fits(int M) { return M >= 1 && M <= kCols * kMaxTokenBlocks; }
+
+hipError_t launch_w4a4_gemm_decode_partials(const uint8_t* Xq, const uint8_t* Wq, int M, int N,
+                                            int K, int g, int32_t* P, hipStream_t stream) {
+  // The same block and token-block choice as the row-major Y launch below.
+  const int grid = (N / kCols + kBlocks - 1) / kBlocks;
+  const int grid4 = (N / kCols + 3) / 4;
+  const bool kb4 = M >= 8;
+  const int tbs = M <= kCols ? 1 : (M <= 2 * kCols ? 2 : 4);
+#define RRS_DECODE_P(GS_, TB_)                                                              \
+  if (kb4)                                                                                 \
+    gemm_decode_kernel<GS_, TB_, false, 4, true><<<grid4, kThreads, 0, stream>>>(            \
+        Xq, nullptr, nullptr, Wq, nullptr, M, N, K, nullptr, 0.0f, P);                      \
+  else                                                                                     \
+    gemm_decode_kernel<GS_, TB_, false, kBlocks, true><<<grid, kThreads, 0, stream>>>(      \
+        Xq, nullptr, nullptr, Wq, nullptr, M, N, K, nullptr, 0.0f, P)
+#define RRS_DECODE_P_TB(GS_) \
+  if (tbs == 1) {            \
+    RRS_DECODE_P(GS_, 1);    \
+  } else if (tbs == 2) {     \
+    RRS_DECODE_P(GS_, 2);    \
+  } else {                   \
+    RRS_DECODE_P(GS_, 4);    \
+  }
+  switch (g) {
+    case 64: RRS_DECODE_P_TB(1) break;
+    case 128: RRS_DECODE_P_TB(2) break;
+    case 256: RRS_DECODE_P_TB(4) break;
+    case 512: RRS_DECODE_P_TB(8) break;
+    default: return hipErrorInvalidValue;
+  }
+#undef RRS_DECODE_P_TB
+#undef RRS_DECODE_P
+  return hipGetLastError();
+}
 bool decode_gather_fits(int M) { return M >= 1 && M <= kCols; }
 
 hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,

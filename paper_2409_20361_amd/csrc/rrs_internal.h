@@ -92,6 +92,22 @@ hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
                                    uint16_t* Y, float out_scale, hipStream_t stream,
                                    const int32_t* border = nullptr, WqLayout lay = {false});
 
+hipError_t launch_w4a4_gemm_decode_partials(const uint8_t* Xq, const uint8_t* Wq, int M, int N,
+                                            int K, int g, int32_t* P, hipStream_t stream);
+
+// Weight-streaming kernel for up to 16 tokens (rrs_gemm_stream.hip): each
+// workgroup copies 16 whole rows of Wq into LDS with direct-to-LDS loads.
+// Needs K >= 4 g. Both layouts, bit-identical results.
+bool stream_kernel_fits(int M, int K, int g);
+hipError_t launch_w4a4_gemm_stream(const uint8_t* Xq, const float* a_scale,
+                                   const float* s_group, const uint8_t* Wq,
+                                   const float* w_scale, int M, int N, int K, int g,
+                                   uint16_t* Y, float out_scale, hipStream_t stream,
+                                   WqLayout lay);
+hipError_t launch_w4a4_gemm_stream_partials(const uint8_t* Xq, const uint8_t* Wq, int M, int N,
+                                            int K, int g, int32_t* P, hipStream_t stream,
+                                            WqLayout lay);
+
 // Baselines of the kernel comparison (per-channel / sub-channel A4W4).
 hipError_t launch_quantize_sub_channel(const uint16_t* X, int M, int K, int g, int flags,
                                        uint8_t* Xq, float* a_sub, hipStream_t stream);
@@ -144,10 +160,18 @@ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 // rotate + smooth + quant with one workgroup per row for M <= 16 tokens, no
 // static reorder, smoothing on (rrs_quant_rows.hip); the workspace holds
 // quant_rows_workspace_bytes(K, g) bytes of any content (set up by the call).
+// extra_arrivals > 0 and max_polls > 0 are for the test hook only: the
+// arrival target becomes M + extra_arrivals (unreachable, so every wait runs
+// out) and the wait gives up after max_polls polls (0 = the default bound).
 bool quant_rows_fits(int M);
 size_t quant_rows_workspace_bytes(int K, int g);
 hipError_t launch_quant_rows(const uint16_t* X, int M, int K, int g, bool rotate, uint8_t* Xq,
-                             float* a_scale, float* s_group, void* workspace,
-                             hipStream_t stream);
+                             float* a_scale, float* s_group, void* workspace, hipStream_t stream,
+                             int extra_arrivals = 0, int max_polls = 0);
+// Whether launch_rotate_smooth_quant takes the per-row kernel for this call.
+bool quant_rows_used(int M, int K, int g, const int32_t* perm, int flags);
+// Waits for `stream` and returns the per-row kernel's count of waits that ran
+// out, read from the workspace of its last call.
+hipError_t quant_rows_timeouts(const void* workspace, hipStream_t stream, uint32_t* count);
 
 }  // namespace rrs

@@ -647,8 +647,7 @@ hipError_t launch_rotate_smooth_quant(const uint16_t* X, int M, int K, int g,
                                       hipStream_t stream) {
   // Up to 16 tokens with smoothing and no static reorder: one workgroup per
   // row, the rows' group maxima exchanged in the workspace (rrs_quant_rows.hip).
-  if (quant_rows_fits(M) && !perm && !(flags & kSkipSmoothing) &&
-      quant_rows_workspace_bytes(K, g) <= quant_workspace_bytes(M, K))
+  if (quant_rows_used(M, K, g, perm, flags))
     return launch_quant_rows(X, M, K, g, !(flags & kSkipRotation), Xq, a_scale, s_group,
                              workspace, stream);
   // Few tokens with smoothing: one launch (each workgroup takes the channel

@@ -18,6 +18,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "rrs.h")
 
 OK, NULL, SHAPE, GROUP, ALIGN, WS, NODEV, ARCH, HIP, FLAGS = 0, -1, -2, -3, -4, -5, -6, -7, -8, -9
+PRECONDITION, TIMEOUT = -10, -11
 P = 0x10000     # 16-byte aligned fake pointer (never dereferenced)
 MIS = 0x10004   # misaligned fake pointer
 
@@ -41,9 +42,12 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings_and_version():
-    for code in (OK, NULL, SHAPE, GROUP, ALIGN, WS, NODEV, ARCH, HIP, FLAGS):
+    for code in (OK, NULL, SHAPE, GROUP, ALIGN, WS, NODEV, ARCH, HIP, FLAGS, PRECONDITION,
+                 TIMEOUT):
         s = rrs.status_string(code)
-        assert s.startswith("RRS_")
+        assert s.startswith("RRS_") and s != "RRS_ERR_UNKNOWN"
+    assert rrs.status_string(PRECONDITION).startswith("RRS_ERR_PRECONDITION")
+    assert rrs.status_string(TIMEOUT).startswith("RRS_ERR_TIMEOUT")
     assert rrs.status_string(-99) == "RRS_ERR_UNKNOWN"
     assert rrs.version() >= 200   # 0.2.0: the _ex entry points
 
@@ -442,3 +446,45 @@ def test_wq_tiling_helpers_follow_the_documented_layout(N, K):
     nb, c = (1, 1) if N >= 32 and K >= 256 else (0, 0)
     run = flat[nb * 8 * K + c * 1024: nb * 8 * K + c * 1024 + 1024]
     assert sorted(run.tolist()) == sorted(slot.reshape(-1).tolist())
+
+
+def _qwait(**kw):
+    a = dict(X=P, M=4, K=1024, g=128, extra=1, polls=8, Xq=P, a=P, s=P, ws=P, wsb=1 << 30,
+             n=P)
+    a.update(kw)
+    return rrs.lib().rrs_test_quant_rows_wait(a["X"], a["M"], a["K"], a["g"], a["extra"],
+                                              a["polls"], a["Xq"], a["a"], a["s"], a["ws"],
+                                              a["wsb"], a["n"], None)
+
+
+def test_quant_rows_wait_hook_checks():
+    # the failure-path test hook validates like the quantizer, in the same order
+    for key in ("X", "Xq", "a", "s", "ws", "n"):
+        assert _qwait(**{key: None}) == NULL, key
+    assert _qwait(M=1) == SHAPE       # the exchange needs 2..16 rows
+    assert _qwait(M=17) == SHAPE
+    assert _qwait(K=1000) == SHAPE
+    assert _qwait(g=96) == GROUP
+    assert _qwait(extra=-1) == FLAGS
+    assert _qwait(polls=0) == FLAGS
+    assert _qwait(X=MIS) == ALIGN
+    assert _qwait(wsb=16) == WS
+    assert _qwait(M=17, X=None) == NULL   # null pointers first
+
+
+def test_debug_checks_come_after_host_validation():
+    # RRS_DEBUG only adds checks after the regular ones: invalid arguments still
+    # get their usual codes, before any device access.
+    old = os.environ.get("RRS_DEBUG")
+    os.environ["RRS_DEBUG"] = "1"
+    try:
+        assert _rsq(X=None) == NULL
+        assert _rsq(K=1000) == SHAPE
+        assert _gemm(g=96) == GROUP
+        assert _lin(ws=MIS) == ALIGN
+        assert _prep(K=100) == SHAPE
+    finally:
+        if old is None:
+            del os.environ["RRS_DEBUG"]
+        else:
+            os.environ["RRS_DEBUG"] = old

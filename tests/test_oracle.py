@@ -704,3 +704,147 @@ def test_reorder_groups_outlier_channels_together():
     Y1, act1, *_ = O.linear_reorder(X, W, g, 1, rotate=False)
     assert act1.s[1] < act.s.min() / 10
     assert err(Y1) < 0.7 * err(Y0), (err(Y1), err(Y0))
+
+
+# ---------------------------------------------------------------- rounding-bound magnitudes
+#
+# output_abs_terms / output_sub_channel_abs_terms give T, the magnitude that the
+# elementwise output tolerance scales: the binary32 sum over the G group terms
+# of Eq. 3 (rescaled per block, Fig. 4 step (3)) rounds by at most about
+# G * 2^-24 * T in any order. The pins below fix T by hand-worked values, a
+# scalar brute force on mixed signs (so a dropped absolute value shows), the
+# 1 / norm factor (norm = K and norm = 1), the triangle inequality with equality
+# when every term has one sign, and the rounding bound itself over random
+# summation orders.
+
+def _dyadic(rng, shape, lo, hi, denom=8):
+    """Random multiples of 1/denom in [lo, hi], never 0: exact in binary32/64."""
+    v = rng.integers(int(lo * denom), int(hi * denom) + 1, size=shape).astype(np.float64)
+    v[v == 0] = 1.0
+    return v / denom
+
+
+def test_output_abs_terms_hand_worked():
+    # One output, two groups: P = (3, -5), s = (2, -0.5) (a negative s only
+    # tests the absolute value), alpha = -0.5, beta = 4, norm = 8:
+    # sum_b |s_b P_b| = 6 + 2.5 = 8.5 and T = 0.5 * 4 / 8 * 8.5 = 2.125.
+    P = np.array([3, -5]).reshape(2, 1, 1)
+    T = O.output_abs_terms(P, np.array([2.0, -0.5]), np.array([-0.5]), np.array([4.0]), 8)
+    assert T.shape == (1, 1) and T[0, 0] == 2.125
+    # norm = 1 gives 8 times that, and the signed output is 0.5 * 4 / 8 * (6 + 2.5).
+    T1 = O.output_abs_terms(P, np.array([2.0, -0.5]), np.array([-0.5]), np.array([4.0]), 1)
+    assert T1[0, 0] == 17.0
+    Y = O.output(P, np.array([2.0, 0.5]), np.array([0.5]), np.array([4.0]), 8)
+    assert Y[0, 0] == np.float32(0.25 * (6 - 2.5))
+
+
+@pytest.mark.parametrize("norm", [1, 512])
+def test_output_abs_terms_brute_force_mixed_signs(norm):
+    rng = np.random.default_rng(71 + norm)
+    G, M, N = 4, 3, 5
+    P = rng.integers(-6000, 6001, size=(G, M, N))
+    s = _dyadic(rng, G, -4, 4)
+    alpha = _dyadic(rng, M, -3, 3)
+    beta = _dyadic(rng, N, -3, 3)
+    T = O.output_abs_terms(P, s, alpha, beta, norm)
+    for i in range(M):
+        for n in range(N):
+            acc = 0.0
+            for b in range(G):
+                acc += abs(float(s[b]) * int(P[b, i, n]))
+            # every value is dyadic with few bits: all of this is exact in binary64
+            assert T[i, n] == abs(float(alpha[i])) * abs(float(beta[n])) * acc / norm
+
+
+def test_output_abs_terms_triangle_and_equality():
+    rng = np.random.default_rng(72)
+    G, M, N, K = 8, 4, 6, 4096
+    P = rng.integers(-6000, 6001, size=(G, M, N))
+    s = rng.uniform(0.01, 30, G).astype(np.float32)
+    alpha = rng.uniform(0.001, 2, M).astype(np.float32)
+    beta = rng.uniform(0.001, 0.1, N).astype(np.float32)
+    T = O.output_abs_terms(P, s, alpha, beta, K)
+    Y = O.output(P, s, alpha, beta, K).astype(np.float64)
+    # |Y| <= T up to the final binary32 rounding of Y
+    assert np.all(np.abs(Y) <= T * (1 + 2.0 ** -23))
+    # one sign in every term: T = |Y| (up to that rounding); a T that kept a
+    # factor K (a dropped 1 / norm) or summed before the absolute value fails
+    Pp = np.abs(P)
+    Tp = O.output_abs_terms(Pp, s, alpha, beta, K)
+    Yp = O.output(Pp, s, alpha, beta, K).astype(np.float64)
+    np.testing.assert_allclose(Tp, Yp, rtol=2.0 ** -23, atol=0)
+    Tn = O.output_abs_terms(-Pp, s, alpha, beta, K)
+    np.testing.assert_allclose(Tn, -O.output(-Pp, s, alpha, beta, K).astype(np.float64),
+                               rtol=2.0 ** -23, atol=0)
+    # one group: T = |Y| whatever the sign
+    T1 = O.output_abs_terms(P[:1], s[:1], alpha, beta, K)
+    Y1 = O.output(P[:1], s[:1], alpha, beta, K).astype(np.float64)
+    np.testing.assert_allclose(T1, np.abs(Y1), rtol=2.0 ** -23, atol=0)
+
+
+def test_output_abs_terms_bounds_binary32_sums_in_any_order():
+    # The use the tests make of T: a binary32 evaluation of sum_b s_b P_b in any
+    # order, scaled by fl(alpha beta / K), differs from the binary64 value by at
+    # most (G + 3) 2^-24 T. Outputs here cancel strongly (mixed-sign partials),
+    # which is where the bound, not the relative 1e-2, is what matters.
+    rng = np.random.default_rng(73)
+    G, M, N, K = 32, 6, 40, 4096
+    P = rng.integers(-3000, 3001, size=(G, M, N))
+    s = rng.uniform(0.5, 40, G).astype(np.float32)
+    alpha = rng.uniform(0.01, 3, M).astype(np.float32)
+    beta = rng.uniform(0.001, 0.05, N).astype(np.float32)
+    T = O.output_abs_terms(P, s, alpha, beta, K)
+    exact = (np.tensordot(s.astype(np.float64), P.astype(np.float64), axes=(0, 0))
+             * alpha.astype(np.float64)[:, None] * beta.astype(np.float64)[None, :] / K)
+    f = np.float32
+    worst = 0.0
+    for trial in range(12):
+        order = rng.permutation(G)
+        acc = np.zeros((M, N), np.float32)
+        for b in order:
+            acc = (acc + (f(s[b]) * P[b].astype(np.float32)).astype(np.float32)).astype(np.float32)
+        scale = ((alpha[:, None] * beta[None, :]).astype(np.float32) * f(1.0 / K)).astype(np.float32)
+        y = (acc * scale).astype(np.float32).astype(np.float64)
+        err = np.abs(y - exact)
+        assert np.all(err <= (G + 3) * 2.0 ** -24 * T)
+        worst = max(worst, float((err / T).max()))
+    # and the bound is not vacuous: the observed error reaches a visible part of it
+    assert worst > 2.0 ** -24
+
+
+def test_output_sub_channel_abs_terms_hand_worked_and_brute_force():
+    # Hand-worked: one output, two groups, P = (3, -5), token scales (0.5, -2),
+    # channel scales (-4, 0.25), norm = 8:
+    # |0.5 * -4 * 3| + |-2 * 0.25 * -5| = 6 + 2.5 = 8.5, T = 8.5 / 8.
+    P = np.array([3, -5]).reshape(2, 1, 1)
+    a = np.array([[0.5, -2.0]])
+    b = np.array([[-4.0, 0.25]])
+    assert O.output_sub_channel_abs_terms(P, a, b, 8)[0, 0] == 8.5 / 8
+    assert O.output_sub_channel_abs_terms(P, a, b, 1)[0, 0] == 8.5
+    # Brute force on mixed signs, dyadic values (exact), norm = K and 1.
+    rng = np.random.default_rng(74)
+    G, M, N = 3, 4, 5
+    P = rng.integers(-6000, 6001, size=(G, M, N))
+    a = _dyadic(rng, (M, G), -3, 3)
+    b = _dyadic(rng, (N, G), -3, 3)
+    for norm in (1, 256):
+        T = O.output_sub_channel_abs_terms(P, a, b, norm)
+        for i in range(M):
+            for n in range(N):
+                acc = 0.0
+                for k in range(G):
+                    acc += abs(float(a[i, k]) * float(b[n, k]) * int(P[k, i, n]))
+                assert T[i, n] == acc / norm
+    # one sign per term: T equals |Y|; equal scales across groups: the
+    # per-channel magnitude
+    Pp = np.abs(P)
+    ap, bp = np.abs(a), np.abs(b)
+    np.testing.assert_allclose(O.output_sub_channel_abs_terms(Pp, ap, bp, 8),
+                               O.output_sub_channel(Pp, ap, bp, 8).astype(np.float64),
+                               rtol=2.0 ** -23, atol=0)
+    alpha = _dyadic(rng, M, -2, 2)
+    beta = _dyadic(rng, N, -2, 2)
+    np.testing.assert_array_equal(
+        O.output_sub_channel_abs_terms(P, np.repeat(alpha[:, None], G, 1),
+                                       np.repeat(beta[:, None], G, 1), 8),
+        O.output_abs_terms(P, np.ones(G), alpha, beta, 8))

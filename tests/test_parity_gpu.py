@@ -186,7 +186,7 @@ def test_weight_prep(name):
     _weight_case(synth.WORKLOADS[name], label=name)
 
 
-@pytest.mark.parametrize("name", ["decode", "large"])
+@pytest.mark.parametrize("name", ["decode", "large", "gateup"])
 def test_weight_prep_sampled_columns(name):
     w = synth.WORKLOADS[name]
     cols = np.sort(np.random.default_rng(3).choice(w.N, 96, replace=False))
@@ -286,7 +286,7 @@ def test_linear_ragged(M, K, N, g):
     _linear_case(w, label=f"ragged {M}x{K}x{N}/g{g}")
 
 
-@pytest.mark.parametrize("name", ["qkv", "decode"])
+@pytest.mark.parametrize("name", ["qkv", "decode", "gateup"])
 def test_linear_full_size_sampled(name):
     # The benchmark's shapes and launch configuration; outputs checked on a
     # sample of rows x columns (plus the first/last row and column).
