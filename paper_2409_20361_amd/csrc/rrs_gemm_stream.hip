@@ -9,32 +9,43 @@
 // contiguous run of 8 K bytes in either layout; its four waves take a quarter
 // of K each (wave w: packed bytes [w R, w R + R) of every row, R = K / 8),
 // again one contiguous run of 16 R bytes in the tiled layout. A wave copies
-// its 16 x R bytes with direct-to-LDS loads (global_load_lds_dwordx4): every
-// instruction moves 1 KB of consecutive global bytes into the wave's LDS
-// region without passing through registers. The MFMA operand layout wants
-// lane (c, q) to hold row c, which a direct load of 1 KB cannot give; the LDS
-// region turns the contiguous stream into that layout, read back with one
-// ds_read_b128 per lane per 64-byte piece.
+// its 16 x R bytes through LDS with direct-to-LDS loads
+// (global_load_lds_dwordx4): every instruction moves 1 KB of global bytes into
+// LDS without passing through registers. The MFMA operand layout wants lane
+// (c, q) to hold row c, which a direct load of 1 KB cannot give; LDS turns the
+// stream into that layout, read back with one ds_read_b128 per lane per
+// 64-byte piece.
 //
-// LDS layout of a wave's region. Row-major Wq: a load instruction takes one
-// row piece of 1 KB, or several whole row pieces when R < 1 KB; row r sits
-// at r R with its 16-byte chunks permuted by chunk' = chunk ^ (r & 7), so
-// that the 16 lanes reading the same chunk of 16 rows hit different banks.
-// The permutation is applied on the global side (lane i of a direct load
-// lands at slot i and fetches the chunk that belongs there), so each load
-// instruction still covers a contiguous 1 KB range. Tiled Wq: a load
-// instruction takes one 1 KB tile (16 rows x 64 bytes, quarter by quarter)
-// unchanged, and the 16 lanes reading quarter q of the 16 rows read 256
-// consecutive bytes. Both layouts give the same operands in the same order,
-// so their results are bit-identical.
+// The kernel is persistent: two workgroups per compute unit, each taking the
+// column blocks blockIdx.x, blockIdx.x + gridDim.x, ... A wave streams its
+// quarters of those blocks as a sequence of sub-buffers of 16 rows x 512
+// bytes (8 KB; smaller when R is) through a ring of 16 KB of LDS: while it
+// multiplies one sub-buffer the next is in flight, and each one it has
+// multiplied is refilled at once (at smaller K the ring holds more, smaller
+// sub-buffers). Measured at the decode shape (M = 8, K = 8192, back-to-back
+// events): 16 rows x 512 bytes in a 16 KB ring with two workgroups per
+// compute unit 21.2 us; 16 x 256 bytes, four per ring, 28.3 us; 16 x 256
+// bytes, eight per ring, one workgroup per compute unit 29.4 us; 16 x 128
+// bytes 38.6 us: the fewer rows one load instruction touches, the faster.
+// Direct loads of a sub-buffer: row-major Wq, two rows x 512 contiguous
+// bytes per instruction, each row's 16-byte chunks permuted
+// by chunk' = chunk ^ (r & 7) in LDS so that the 16 lanes reading the same
+// chunk of 16 rows hit different banks (the permutation is applied on the
+// global side: lane i of a direct load lands at slot i and fetches the chunk
+// that belongs there); tiled Wq, one 1 KB tile per instruction, unchanged,
+// where the 16 lanes reading quarter q of the 16 rows read 256 consecutive
+// bytes. Both layouts give the same operands in the same order, so their
+// results are bit-identical. The direct loads are not tracked by the
+// compiler's wait insertion for the LDS reads that follow, so the kernel
+// waits for them explicitly: after issuing a refill it lets the loads of the
+// newer sub-buffers stay in flight (vmcnt((RS - 1) NL)) and retires the rest.
+// The weight loads are non-temporal (read once).
 //
-// The direct loads are not tracked by the compiler's wait insertion for the
-// LDS reads that follow, so the kernel waits for them explicitly (vmcnt(0))
-// before the first read. Each wave reads only its own region: no barrier.
-//
-// Token codes (M x K/2, a few KB, L2-resident) are loaded into registers:
-// lane (c, q) takes the same bytes of token row c (row M - 1 for c >= M, whose
-// outputs are never stored). Per group b of the wave, lane (c, q) holds
+// Token codes (M x K/2, a few KB, L2-resident) are loaded into registers once
+// per workgroup and reused for every column block: lane (c, q) takes the
+// same bytes of token row c (row M - 1 for c >= M, whose outputs are never
+// stored). (Loaded per block, as 16 rows x 64 bytes per instruction, they
+// cost up to 8 us at 8 to 16 tokens in a first, non-persistent version.) Per group b of the wave, lane (c, q) holds
 // bytes [64 h + 16 q, +16) of each 64-byte piece h of the group (g >= 128) or
 // bytes [8 q, +8) (g = 64); MFMA k-step s (v_mfma_i32_16x16x64_i8) takes the
 // lane's bytes [8 s, 8 s + 8) in that order for both operands, so every k-step
@@ -43,10 +54,12 @@
 // accumulators start from the bits of 1.5 * 2^23 (g <= 256), so that the
 // result read as a float is exactly 1.5 * 2^23 + 256 P_b and one subtraction
 // recovers 256 P_b before the FMA by s_b; for g = 512 they start from 0 and
-// are converted. The four waves' fp32 sums are added in a fixed order.
+// are converted. The four waves' fp32 sums of a block are added in a fixed
+// order, through LDS, after a workgroup barrier; each wave then stores a
+// quarter of the block's outputs.
 //
 // Needs K >= 4 g (every wave holds whole groups): K = 512 with g <= 128,
-// K = 1024 with g <= 256, any g from K = 2048.
+// K = 1024 with g <= 256, any g from K = 2048 (but g >= 256 at K = 16384).
 #include "rrs_internal.h"
 
 namespace rrs {
@@ -57,18 +70,27 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kRows = 16;  // weight rows (output columns) per workgroup
+constexpr int kRows = 16;  // weight rows (output columns) per column block
 constexpr int kMaxTokens = 16;
 
 template <int K>
 struct StreamShape {
   static constexpr int R = K / 2 / kWaves;            // packed bytes per row per wave
-  static constexpr int CPR = R / 16;                  // 16-byte chunks per row per wave
-  static constexpr int SW = CPR >= 8 ? 7 : CPR - 1;  // chunk permutation mask
-  static constexpr int REGION = kRows * R;            // LDS bytes per wave
-  static constexpr int NLD = REGION / 1024;           // direct loads of 1 KB per wave
-  static_assert(REGION % 1024 == 0, "a wave's region is a whole number of 1 KB loads");
+  static constexpr int SBW = R < 512 ? R : 512;        // bytes per row per sub-buffer
+  static constexpr int SPB = R / SBW;                  // sub-buffers per block
+  static constexpr int CPR = SBW / 16;                 // 16-byte chunks per row per sub-buffer
+  static constexpr int SW = CPR >= 8 ? 7 : CPR - 1;   // chunk permutation mask (row-major)
+  static constexpr int SB = kRows * SBW;               // LDS bytes per sub-buffer
+  static constexpr int NL = SB / 1024;                 // direct loads of 1 KB per sub-buffer
+  static constexpr int RS = 16384 / SB;                // sub-buffers in a wave's ring (16 KB)
+  static constexpr int RPI = 1024 / SBW;               // rows per direct load (row-major)
+  static_assert(SB % 1024 == 0, "a sub-buffer is a whole number of 1 KB loads");
+  static_assert(RS >= 2 && (RS - 1) * NL <= 63, "ring depth and vmcnt immediate");
 };
+
+// Cache policy of the weight loads: non-temporal (each weight byte is read
+// once; 5 % faster at the decode shape than the default policy).
+constexpr int kWeightPolicy = 2;
 
 __device__ __forceinline__ v4i unpack_pair(uint32_t w0, uint32_t w1) {
   v4i r;
@@ -81,6 +103,12 @@ __device__ __forceinline__ v4i unpack_pair(uint32_t w0, uint32_t w1) {
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
+// Waits until at most N vector-memory operations of this wave are in flight.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
 // kPartials (test hook): instead of Y, write P[b][i][n] for every group b,
 // token i < M and column n, decoded from the same seeded accumulators.
 template <int K, int GS, bool kTiled, bool kPartials>
@@ -91,53 +119,67 @@ __global__ __launch_bounds__(kThreads) void gemm_stream_kernel(
     int32_t* __restrict__ P, float out_scale) {
   using S = StreamShape<K>;
   constexpr int g = GS * 64;
-  constexpr int GB = g / 2;                 // packed bytes of a row per group
-  constexpr int NG = S::R / GB;             // groups per wave
+  constexpr int GB = g / 2;                   // packed bytes of a row per group
+  constexpr int NG = S::R / GB;               // groups per wave (its quarter of K)
+  constexpr int NGS = S::SBW / GB;            // groups per sub-buffer
   constexpr int NP = GB >= 64 ? GB / 64 : 1;  // 16-byte lane pieces per group
-  static_assert(NG >= 1 && S::R % GB == 0, "every wave holds whole groups");
-  __shared__ __attribute__((aligned(16))) uint8_t region[kWaves * S::REGION];
-  __shared__ __attribute__((aligned(16))) v4f part[kWaves][64];
+  static_assert(NGS >= 1 && S::SBW % GB == 0, "every sub-buffer holds whole groups");
+  __shared__ __attribute__((aligned(16))) uint8_t ring[kWaves * S::RS * S::SB];
+  __shared__ __attribute__((aligned(16))) v4f part[2][kWaves][64];
 
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int kq = __builtin_amdgcn_readfirstlane(t >> 6);  // K quarter of this wave
   const int c = lane & 15;
   const int q = lane >> 4;
-  const int n0 = blockIdx.x * kRows;
   constexpr size_t krow = (size_t)K / 2;
-  uint8_t* my = region + kq * S::REGION;
+  uint8_t* my = ring + kq * S::RS * S::SB;
+  const int nblk = N / kRows;
+  const int mine = (nblk - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x;
+  const int items = mine * S::SPB;  // sub-buffers this wave streams, in order
 
-  // 1. The wave's 16 rows x R bytes of Wq, straight into its LDS region
-  // (n0 is a multiple of 16: in the tiled layout the 16 rows are one block,
-  // and the wave's quarter of K is its tiles kq R / 64 .. (kq + 1) R / 64 - 1).
-  if constexpr (kTiled) {
-    const uint8_t* wbase = Wq + (size_t)n0 * krow + (size_t)kq * S::R * kRows;
+  // Direct loads of item i (sub-buffer i % SPB of column block i / SPB) into
+  // ring slot i % RS. Row-major: each instruction RPI rows x SBW bytes,
+  // chunks permuted; tiled: each instruction one tile (the block's 16 rows are
+  // one 16-row block, n0 a multiple of 16).
+  auto issue = [&](int i) {
+    const int blk = (int)blockIdx.x + (i / S::SPB) * (int)gridDim.x;
+    const int sp = i % S::SPB;
+    uint8_t* dst = my + (i % S::RS) * S::SB;
+    const uint8_t* base = Wq + (size_t)blk * kRows * krow;
+    if constexpr (kTiled) {
+      const uint8_t* src = base + (size_t)(kq * S::R + sp * S::SBW) * kRows;
 #pragma unroll
-    for (int ii = 0; ii < S::NLD; ++ii)
-      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(wbase + 1024 * ii + 16 * lane),
-                                       (lds_ptr_t)(my + 1024 * ii), 16, 0, 0);
-  } else {
-    const uint8_t* wbase = Wq + (size_t)n0 * krow + (size_t)kq * S::R;
+      for (int ii = 0; ii < S::NL; ++ii)
+        __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src + 1024 * ii + 16 * lane),
+                                         (lds_ptr_t)(dst + 1024 * ii), 16, 0, kWeightPolicy);
+    } else {
+      const uint8_t* src = base + kq * S::R + sp * S::SBW;
 #pragma unroll
-    for (int ii = 0; ii < S::NLD; ++ii) {
-      const int L = 64 * ii + lane;  // chunk slot in the region
-      const int r = L / S::CPR;
-      const int j = (L % S::CPR) ^ (r & S::SW);
-      __builtin_amdgcn_global_load_lds(
-          reinterpret_cast<const void*>(wbase + (size_t)r * krow + 16 * j),
-          (lds_ptr_t)(my + 1024 * ii), 16, 0, 0);
+      for (int ii = 0; ii < S::NL; ++ii) {
+        const int r = ii * S::RPI + lane / S::CPR;
+        const int j = (lane % S::CPR) ^ (r & S::SW);
+        __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src + (size_t)r * krow + 16 * j),
+                                         (lds_ptr_t)(dst + 1024 * ii), 16, 0, kWeightPolicy);
+      }
     }
-  }
-  // LDS offset of bytes [16 jc + 8 e, +8) of row c of the wave's quarter
-  // (jc: 16-byte chunk index within the quarter, e: 0 or 1).
+  };
+  // LDS offset, inside a sub-buffer, of bytes [16 jc + 8 e, +8) of row c
+  // (jc: 16-byte chunk index within the sub-buffer's SBW bytes of a row).
   auto woff = [&](int jc, int e) -> int {
     if constexpr (kTiled)
       return (jc >> 2) * 1024 + ((jc & 3) * 16 + c) * 16 + 8 * e;
     else
-      return c * S::R + 16 * (jc ^ (c & S::SW)) + 8 * e;
+      return c * S::SBW + 16 * (jc ^ (c & S::SW)) + 8 * e;
   };
 
-  // 2. Token codes of the same bytes, and the wave's group scales (one per lane).
+  // Fill the ring: the first RS - 1 sub-buffers.
+#pragma unroll
+  for (int i = 0; i < S::RS - 1; ++i)
+    if (i < items) issue(i);
+
+  // Token codes of the wave's quarter (once per workgroup) and its group
+  // scales (one per lane).
   const uint8_t* abase = Xq + (size_t)min(c, M - 1) * krow + (size_t)kq * S::R;
   uint32_t aw[NG][NP][4];
 #pragma unroll
@@ -162,120 +204,182 @@ __global__ __launch_bounds__(kThreads) void gemm_stream_kernel(
   float sv = 0.0f;
   if constexpr (!kPartials) sv = s_group[kq * NG + (lane < NG ? lane : 0)];
 
-  // Every direct load of this wave has landed in LDS.
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-
   constexpr int kMagic = 0x4B400000;  // bits of 1.5 * 2^23
   const v4i seed = GS > 4 ? v4i{0, 0, 0, 0} : v4i{kMagic, kMagic, kMagic, kMagic};
-  float f[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+
+  // Epilogue split: wave kq stores accumulator row kq of every lane, i.e.
+  // output row 4 q + kq, so the four waves share the stores.
+  const int orow = 4 * q + kq;
+  float oscale = 0.0f;  // alpha of that row times out_scale
+  if constexpr (!kPartials) oscale = a_scale[min(orow, M - 1)] * out_scale;
+
+  for (int tb = 0; tb < mine; ++tb) {
+    const int blk = (int)blockIdx.x + tb * (int)gridDim.x;
+    float bcol = 0.0f;  // beta of this lane's column, requested early
+    if constexpr (!kPartials) bcol = w_scale[blk * kRows + c];
+    float f[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-  for (int b = 0; b < NG; ++b) {
-    uint32_t ww[NP][4];
-#pragma unroll
-    for (int h = 0; h < NP; ++h) {
-      if constexpr (GB >= 64) {
-        const int jc = b * (GB / 16) + 4 * h + q;
-        const uint4 v = *reinterpret_cast<const uint4*>(my + woff(jc, 0));
-        ww[h][0] = v.x;
-        ww[h][1] = v.y;
-        ww[h][2] = v.z;
-        ww[h][3] = v.w;
+    for (int sp = 0; sp < S::SPB; ++sp) {
+      const int i = tb * S::SPB + sp;
+      // Refill the slot freed by the previous item, then retire item i: with
+      // RS - 1 items issued after it, at most (RS - 1) NL loads may remain.
+      if (i + S::RS - 1 < items) {
+        issue(i + S::RS - 1);
+        wait_vm<(S::RS - 1) * S::NL>();
       } else {
-        const int jc = 2 * b + (q >> 1);
-        const uint2 v = *reinterpret_cast<const uint2*>(my + woff(jc, q & 1));
-        ww[h][0] = v.x;
-        ww[h][1] = v.y;
-        ww[h][2] = 0u;
-        ww[h][3] = 0u;
+        wait_vm<0>();
       }
-    }
-    v4i acc = seed;
+      const uint8_t* buf = my + (i % S::RS) * S::SB;
 #pragma unroll
-    for (int st = 0; st < GS; ++st) {
-      const int h = st >> 1;
-      const int o = 2 * (st & 1);
-      acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(unpack_pair(aw[b][h][o], aw[b][h][o + 1]),
-                                                  unpack_pair(ww[h][o], ww[h][o + 1]), acc, 0,
-                                                  0, 0);
-    }
-    if constexpr (kPartials) {
-      int32_t* Pg = P + (size_t)(kq * NG + b) * (size_t)M * (size_t)N;
+      for (int bl = 0; bl < NGS; ++bl) {
+        const int b = sp * NGS + bl;  // group of the wave's quarter
+        uint32_t ww[NP][4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = 4 * q + r;
-        if (row < M) Pg[(size_t)row * N + n0 + c] = (GS > 4 ? acc[r] : acc[r] - kMagic) >> 8;
-      }
-    } else {
-      const float s = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
-                                                    __builtin_bit_cast(int, sv), b));
-      // Bit-cast the whole vector, then index: bit-casting a single element
-      // of an ext_vector is miscompiled (every element reads element 0).
-      const v4f accf = __builtin_bit_cast(v4f, acc);
+        for (int h = 0; h < NP; ++h) {
+          if constexpr (GB >= 64) {
+            const uint4 v = *reinterpret_cast<const uint4*>(buf + woff(bl * (GB / 16) + 4 * h + q, 0));
+            ww[h][0] = v.x;
+            ww[h][1] = v.y;
+            ww[h][2] = v.z;
+            ww[h][3] = v.w;
+          } else {
+            const uint2 v = *reinterpret_cast<const uint2*>(buf + woff(2 * bl + (q >> 1), q & 1));
+            ww[h][0] = v.x;
+            ww[h][1] = v.y;
+            ww[h][2] = 0u;
+            ww[h][3] = 0u;
+          }
+        }
+        v4i acc = seed;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float pv = GS > 4 ? (float)acc[r] : accf[r] - 12582912.0f;
-        f[r] = __builtin_fmaf(s, pv, f[r]);
-      }
-    }
-  }
-  if constexpr (!kPartials) {
-    // The four quarters' sums, added in the order kq = 0, 1, 2, 3.
-    part[kq][lane] = v4f{f[0], f[1], f[2], f[3]};
-    __syncthreads();
-    if (kq == 0) {
-      v4f sum = part[0][lane];
+        for (int st = 0; st < GS; ++st) {
+          const int h = st >> 1;
+          const int o = 2 * (st & 1);
+          acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(unpack_pair(aw[b][h][o], aw[b][h][o + 1]),
+                                                      unpack_pair(ww[h][o], ww[h][o + 1]), acc,
+                                                      0, 0, 0);
+        }
+        if constexpr (kPartials) {
+          int32_t* Pg = P + (size_t)(kq * NG + b) * (size_t)M * (size_t)N;
 #pragma unroll
-      for (int p = 1; p < kWaves; ++p) {
-        const v4f x = part[p][lane];
-        sum.x += x.x;
-        sum.y += x.y;
-        sum.z += x.z;
-        sum.w += x.w;
-      }
-      // out_scale = 2^-8 (undoes the 16 x 16 of the unpacked operands) / K (the
-      // unnormalized rotation; 1 without rotation), an exact power of two.
-      const int col = n0 + c;
-      const float bcol = w_scale[col];
-      const float sums[4] = {sum.x, sum.y, sum.z, sum.w};
+          for (int r = 0; r < 4; ++r) {
+            const int row = 4 * q + r;
+            if (row < M)
+              Pg[(size_t)row * N + blk * kRows + c] = (GS > 4 ? acc[r] : acc[r] - kMagic) >> 8;
+          }
+        } else {
+          const float s =
+              __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sv), b));
+          // Bit-cast the whole vector, then index: bit-casting a single element
+          // of an ext_vector is miscompiled (every element reads element 0).
+          const v4f accf = __builtin_bit_cast(v4f, acc);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = 4 * q + r;
-        if (row < M) {
-          const float sc = a_scale[row] * out_scale;
-          Y[(size_t)row * N + col] =
-              __builtin_bit_cast(uint16_t, (_Float16)((sums[r] * sc) * bcol));
+          for (int r = 0; r < 4; ++r) {
+            const float pv = GS > 4 ? (float)acc[r] : accf[r] - 12582912.0f;
+            f[r] = __builtin_fmaf(s, pv, f[r]);
+          }
         }
       }
     }
+    if constexpr (!kPartials) {
+      // The four quarters' sums of this block, added in the order kq = 0..3
+      // (part is double-buffered, so one barrier per block suffices).
+      part[tb & 1][kq][lane] = v4f{f[0], f[1], f[2], f[3]};
+      __syncthreads();
+      float sum = part[tb & 1][0][lane][kq];
+#pragma unroll
+      for (int p = 1; p < kWaves; ++p) sum += part[tb & 1][p][lane][kq];
+      // out_scale = 2^-8 (undoes the 16 x 16 of the unpacked operands) / K (the
+      // unnormalized rotation; 1 without rotation), an exact power of two.
+      if (orow < M)
+        Y[(size_t)orow * N + blk * kRows + c] =
+            __builtin_bit_cast(uint16_t, (_Float16)((sum * oscale) * bcol));
+    }
   }
+}
+
+int cu_count() {
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        n > 0)
+      cus = n;
+    else
+      cus = 256;
+  }
+  return cus;
+}
+
+// A persistent grid must not exceed the workgroups that can be resident at
+// once (the surplus would wait for a whole earlier workgroup to finish):
+// as many per compute unit as the runtime's occupancy query allows (two for
+// most shapes: 72 KB of LDS each; one where a wave needs more than 256
+// registers), times the compute units. Cached per kernel.
+template <typename Kern>
+int resident_grid(Kern kern, int nblk) {
+  static int per_cu = 0;
+  if (per_cu == 0) {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, kThreads, 0) != hipSuccess || n < 1)
+      n = 1;
+    per_cu = n;
+  }
+  const int cap = per_cu * cu_count();
+  return nblk < cap ? nblk : cap;
 }
 
 template <int K, bool kPartials>
 hipError_t launch_k(const uint8_t* Xq, const float* a_scale, const float* s_group,
                     const uint8_t* Wq, const float* w_scale, int M, int N, int g, uint16_t* Y,
                     int32_t* P, float out_scale, hipStream_t stream, bool tiled) {
-  const int grid = N / kRows;  // N % 16 == 0 (API precondition)
-#define RRS_STREAM(GS_)                                                                   \
-  if (tiled)                                                                              \
-    gemm_stream_kernel<K, GS_, true, kPartials><<<grid, kThreads, 0, stream>>>(          \
-        Xq, a_scale, s_group, Wq, w_scale, M, N, Y, P, out_scale);                        \
-  else                                                                                    \
-    gemm_stream_kernel<K, GS_, false, kPartials><<<grid, kThreads, 0, stream>>>(         \
-        Xq, a_scale, s_group, Wq, w_scale, M, N, Y, P, out_scale)
+  const int nblk = N / kRows;  // N % 16 == 0 (API precondition)
+#define RRS_STREAM_T(GS_, T_)                                                             \
+  {                                                                                       \
+    auto kern = gemm_stream_kernel<K, GS_, T_, kPartials>;                                \
+    kern<<<resident_grid(kern, nblk), kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq,    \
+                                                             w_scale, M, N, Y, P,         \
+                                                             out_scale);                  \
+  }
+#define RRS_STREAM(GS_)    \
+  if (tiled)               \
+    RRS_STREAM_T(GS_, true) \
+  else                     \
+    RRS_STREAM_T(GS_, false)
   switch (g) {
-    case 64: RRS_STREAM(1); break;
-    case 128: RRS_STREAM(2); break;
+    case 64:
+      if constexpr (K <= 8192) {
+        RRS_STREAM(1)
+      } else {
+        return hipErrorInvalidValue;
+      }
+      break;
+    case 128:
+      if constexpr (K <= 8192) {
+        RRS_STREAM(2)
+      } else {
+        return hipErrorInvalidValue;
+      }
+      break;
     case 256:
-      if constexpr (K >= 1024) RRS_STREAM(4);
-      else return hipErrorInvalidValue;
+      if constexpr (K >= 1024) {
+        RRS_STREAM(4)
+      } else {
+        return hipErrorInvalidValue;
+      }
       break;
     case 512:
-      if constexpr (K >= 2048) RRS_STREAM(8);
-      else return hipErrorInvalidValue;
+      if constexpr (K >= 2048) {
+        RRS_STREAM(8)
+      } else {
+        return hipErrorInvalidValue;
+      }
       break;
     default: return hipErrorInvalidValue;
   }
 #undef RRS_STREAM
+#undef RRS_STREAM_T
   return hipGetLastError();
 }
 
@@ -301,8 +405,11 @@ hipError_t launch_any(const uint8_t* Xq, const float* a_scale, const float* s_gr
 
 }  // namespace
 
+// K = 16384 with g <= 128 keeps 32 or 64 groups of token codes per wave,
+// which do not fit the registers next to the loop: the few-token kernel takes
+// those shapes.
 bool stream_kernel_fits(int M, int K, int g) {
-  return M >= 1 && M <= kMaxTokens && K >= 4 * g;
+  return M >= 1 && M <= kMaxTokens && K >= 4 * g && !(K == 16384 && g <= 128);
 }
 
 hipError_t launch_w4a4_gemm_stream(const uint8_t* Xq, const float* a_scale,
