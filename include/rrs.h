@@ -215,6 +215,29 @@ rrs_status rrs_linear(const void* X, const void* Wq, const float* w_scale, int M
                       int K, int group_size, const int32_t* perm, void* Y,
                       void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * rrs_linear without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). The call allocates nothing: the
+ * workspace of rrs_linear is taken from a scratch array that the library
+ * holds in device memory, RRS_NOALLOC_SCRATCH_BYTES (16 MiB) on each device
+ * the library runs on, kept until the process ends. Arguments, layouts and
+ * results as rrs_linear (bit-identical outputs).
+ *   Limit: rrs_linear_workspace_bytes(M, K, group_size) must not exceed
+ *   RRS_NOALLOC_SCRATCH_BYTES (about M K / 2 bytes: up to 8143 tokens at
+ *   K = 4096, 4059 at K = 8192, 2014 at K = 16384, with g = 128); larger
+ *   calls return RRS_ERR_WORKSPACE and enqueue nothing.
+ *   Every call on one device shares that device's scratch: calls that
+ *   overlap on one device (concurrent streams, or host threads using
+ *   different streams of the same device) race and give undefined results;
+ *   serialize them (one stream, or events). Calls on different devices are
+ *   independent.
+ */
+#define RRS_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+rrs_status rrs_linear_noalloc(const void* X, const void* Wq, const float* w_scale, int M, int N,
+                              int K, int group_size, const int32_t* perm, void* Y,
+                              void* stream);
+
 /* rrs_linear with ablation flags (quantization and GEMM as in their _ex
  * forms); Wq and w_scale must come from rrs_prepare_weight_ex with the same
  * RRS_SKIP_ROTATION and RRS_WEIGHT_TILED bits. */

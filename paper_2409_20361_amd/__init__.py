@@ -24,6 +24,7 @@ from ._binding import (  # noqa: F401
     lib,
     lib_path,
     linear,
+    linear_noalloc,
     linear_reorder,
     linear_reorder_workspace_bytes,
     linear_workspace_bytes,
@@ -46,7 +47,7 @@ from ._binding import (  # noqa: F401
 
 __all__ = [
     "REORDER_BLOCK", "SCHEME_PER_CHANNEL", "SCHEME_RUNTIME_SMOOTH", "SCHEME_SUB_CHANNEL",
-    "SKIP_ROTATION", "SKIP_SMOOTHING", "WEIGHT_TILED", "RRSError", "lib", "lib_path", "linear", "linear_reorder",
+    "SKIP_ROTATION", "SKIP_SMOOTHING", "WEIGHT_TILED", "RRSError", "lib", "lib_path", "linear", "linear_noalloc", "linear_reorder",
     "linear_reorder_workspace_bytes", "linear_workspace_bytes",
     "prepare_weight", "prepare_weight_sub_channel", "quant_rows_wait_hook",
     "quantize_sub_channel",

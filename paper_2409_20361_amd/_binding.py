@@ -26,6 +26,7 @@ _SIGNATURES = {
     "rrs_w4a4_gemm": (ctypes.c_int32, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp]),
     "rrs_linear": (ctypes.c_int32, [_vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp, _sz, _vp]),
     "rrs_w4a4_gemm_partials": (ctypes.c_int32, [_vp, _vp, _i, _i, _i, _i, _vp, _vp]),
+    "rrs_linear_noalloc": (ctypes.c_int32, [_vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp]),
     "rrs_test_quant_rows_wait": (ctypes.c_int32, [_vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _vp,
                                                   _sz, _vp, _vp]),
     "rrs_prepare_weight_ex": (ctypes.c_int32, [_vp, _i, _i, _vp, _i, _vp, _vp, _vp]),
@@ -209,6 +210,24 @@ def linear(X: torch.Tensor, Wq: torch.Tensor, w_scale: torch.Tensor, g: int,
     _check(lib().rrs_linear_ex(xp, wqp, wsp, M, N, K, g, _perm_ptr(perm, K), flags, yp,
                                workspace.data_ptr(), workspace.numel() * workspace.element_size(),
                                _stream(X.device)), "rrs_linear")
+    return Y
+
+
+def linear_noalloc(X: torch.Tensor, Wq: torch.Tensor, w_scale: torch.Tensor, g: int,
+                   perm: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None
+                   ) -> torch.Tensor:
+    """rrs_linear with the library-held scratch instead of a workspace: the C call
+    allocates nothing (for graph capture and serving loops). Only Y is
+    allocated here, and only when `out` is not given."""
+    M, K = X.shape
+    N = Wq.shape[0]
+    xp = _dev(X, "X", torch.float16, (M, K))
+    wqp = _dev(Wq, "Wq", torch.uint8, (N, K // 2))
+    wsp = _dev(w_scale, "w_scale", torch.float32, (N,))
+    Y = out if out is not None else torch.empty((M, N), dtype=torch.float16, device=X.device)
+    yp = _dev(Y, "Y", torch.float16, (M, N))
+    _check(lib().rrs_linear_noalloc(xp, wqp, wsp, M, N, K, g, _perm_ptr(perm, K), yp,
+                                    _stream(X.device)), "rrs_linear_noalloc")
     return Y
 
 

@@ -20,7 +20,7 @@ OBJDIR = os.path.join(PKG, "_build")
 
 SOURCES = ["rrs_api.cpp", "rrs_quant.hip", "rrs_weight.hip", "rrs_gemm.hip", "rrs_gemm_small.hip",
            "rrs_gemm_decode.hip", "rrs_quant_wave.hip", "rrs_reorder.hip", "rrs_quant_rows.hip",
-           "rrs_gemm_stream.hip"]
+           "rrs_gemm_stream.hip", "rrs_noalloc.hip"]
 
 # -packed-fp32-ops: no v_pk_{add,mul,fma}_f32 in any kernel.
 # -ffp-contract=off: every rounding in the rotation and scale chain is an

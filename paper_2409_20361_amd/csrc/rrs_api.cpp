@@ -176,6 +176,10 @@ size_t linear_reorder_ws_bytes(int M, int K, int g) {
          rrs::align256((size_t)(K / RRS_REORDER_BLOCK) * 4);
 }
 
+rrs_status linear_run(const void* X, const void* Wq, const float* w_scale, int M, int N, int K,
+                      int group_size, const int32_t* perm, int flags, void* Y, void* workspace,
+                      void* stream);
+
 }  // namespace
 
 extern "C" {
@@ -339,7 +343,18 @@ rrs_status rrs_linear_ex(const void* X, const void* Wq, const float* w_scale, in
     if (rrs_status s = debug_check_perm(perm, K, "perm", stream)) return s;
     if (rrs_status s = debug_check_finite_f32(w_scale, (size_t)N, "w_scale", stream)) return s;
   }
+  return linear_run(X, Wq, w_scale, M, N, K, group_size, perm, flags, Y, workspace, stream);
+}
 
+}  // extern "C"
+
+namespace {
+
+// The layer on a validated call: quantizer then GEMM, with Xq, alpha and s in
+// the workspace (rrs_linear_workspace_bytes bytes).
+rrs_status linear_run(const void* X, const void* Wq, const float* w_scale, int M, int N, int K,
+                      int group_size, const int32_t* perm, int flags, void* Y, void* workspace,
+                      void* stream) {
   char* ws = static_cast<char*>(workspace);
   void* qws = ws;
   ws += rrs::quant_workspace_bytes(M, K);
@@ -362,11 +377,44 @@ rrs_status rrs_linear_ex(const void* X, const void* Wq, const float* w_scale, in
   return r;
 }
 
+}  // namespace
+
+extern "C" {
+
 rrs_status rrs_linear(const void* X, const void* Wq, const float* w_scale, int M, int N,
                       int K, int group_size, const int32_t* perm, void* Y, void* workspace,
                       size_t workspace_bytes, void* stream) {
   return rrs_linear_ex(X, Wq, w_scale, M, N, K, group_size, perm, 0, Y, workspace,
                        workspace_bytes, stream);
+}
+
+rrs_status rrs_linear_noalloc(const void* X, const void* Wq, const float* w_scale, int M, int N,
+                              int K, int group_size, const int32_t* perm, void* Y,
+                              void* stream) {
+  if (debug_enabled())
+    std::fprintf(stderr,
+                 "[rrs] linear_noalloc X=%p Wq=%p w=%p M=%d N=%d K=%d g=%d perm=%p Y=%p\n", X,
+                 Wq, (const void*)w_scale, M, N, K, group_size, (const void*)perm, Y);
+  if (!X || !Wq || !w_scale || !Y) return RRS_ERR_NULL;
+  if (!valid_m(M) || !valid_n(N) || !valid_k(K)) return RRS_ERR_SHAPE;
+  if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
+  if (!is_aligned(X) || !is_aligned(Wq) || !is_aligned(w_scale) || !is_aligned(Y) ||
+      (perm && !is_aligned(perm)))
+    return RRS_ERR_ALIGN;
+  // The library-held scratch takes the place of the workspace.
+  if (linear_ws_bytes(M, K, group_size) > rrs::kNoAllocScratchBytes) return RRS_ERR_WORKSPACE;
+  if (rrs_status s = check_device()) return s;
+  if (debug_enabled()) {
+    if (rrs_status s = debug_check_finite_f16(X, (size_t)M * K, "X", stream)) return s;
+    if (rrs_status s = debug_check_perm(perm, K, "perm", stream)) return s;
+    if (rrs_status s = debug_check_finite_f32(w_scale, (size_t)N, "w_scale", stream)) return s;
+  }
+  void* ws = nullptr;
+  if (rrs::noalloc_scratch(&ws) != hipSuccess) {
+    (void)hipGetLastError();
+    return RRS_ERR_HIP;
+  }
+  return linear_run(X, Wq, w_scale, M, N, K, group_size, perm, 0, Y, ws, stream);
 }
 
 rrs_status rrs_quantize_sub_channel(const void* X, int M, int K, int group_size, int flags,

@@ -157,6 +157,12 @@ hipError_t launch_w4a4_gemm_reorder(const uint8_t* Xq, const float* a_scale,
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+// Library-held scratch of rrs_linear_noalloc (rrs_noalloc.hip): a device
+// array of kNoAllocScratchBytes per device; noalloc_scratch returns the
+// current device's copy (its address resolved once per device).
+constexpr size_t kNoAllocScratchBytes = (size_t)16 << 20;
+hipError_t noalloc_scratch(void** ptr);
+
 // rotate + smooth + quant with one workgroup per row for M <= 16 tokens, no
 // static reorder, smoothing on (rrs_quant_rows.hip); the workspace holds
 // quant_rows_workspace_bytes(K, g) bytes of any content (set up by the call).
