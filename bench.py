@@ -123,7 +123,7 @@ def qkv_step_bench(args, torch, rrs, synth):
     a = torch.empty((w.M,), dtype=torch.float32, device=dev)
     s = torch.empty((w.G,), dtype=torch.float32, device=dev)
     Y = torch.empty((w.M, w.N), dtype=torch.float16, device=dev)
-    ws = torch.empty((rrs.workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8, device=dev)
+    ws = torch.zeros((rrs.workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
 
     def step(evs=None):
@@ -167,7 +167,7 @@ def decode_bench(args, torch, rrs, synth):
     W = torch.from_numpy(synth.weights(w)).to(dev)
     Xq, a, s = rrs.rotate_smooth_quant(X, w.g)
     Y = torch.empty((w.M, w.N), dtype=torch.float16, device=dev)
-    lws = torch.empty((rrs.linear_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
+    lws = torch.zeros((rrs.linear_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
                       device=dev)
     alg = (w.M * w.K // 2 + 4 * w.M + 4 * w.G + w.N * w.K // 2 + 4 * w.N + 2 * w.M * w.N)
     n = args.decode_steps
@@ -248,7 +248,7 @@ def graph_bench(torch, rrs, synth, reps=50):
     a = torch.empty((w.M,), dtype=torch.float32, device=dev)
     s = torch.empty((w.G,), dtype=torch.float32, device=dev)
     Y = torch.empty((w.M, w.N), dtype=torch.float16, device=dev)
-    ws = torch.empty((rrs.workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8, device=dev)
+    ws = torch.zeros((rrs.workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8, device=dev)
 
     def step():
         rrs.rotate_smooth_quant(X, w.g, workspace=ws, out=(Xq, a, s))
@@ -265,7 +265,7 @@ def graph_bench(torch, rrs, synth, reps=50):
     copies = [Wq0] + [Wq0.clone() for _ in range(3)]
     Xq, a, s = rrs.rotate_smooth_quant(X, w.g)
     Y = torch.empty((w.M, w.N), dtype=torch.float16, device=dev)
-    lws = torch.empty((rrs.linear_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
+    lws = torch.zeros((rrs.linear_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
                       device=dev)
 
     def gemms():
@@ -308,8 +308,8 @@ def config_bench(torch, rrs, synth, names=("gateup", "large"), reps=10):
         a = torch.empty((w.M,), dtype=torch.float32, device=dev)
         s = torch.empty((w.G,), dtype=torch.float32, device=dev)
         Y = torch.empty((w.M, w.N), dtype=torch.float16, device=dev)
-        qws = torch.empty((rrs.workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8, device=dev)
-        lws = torch.empty((rrs.linear_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
+        qws = torch.zeros((rrs.workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8, device=dev)
+        lws = torch.zeros((rrs.linear_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
                           device=dev)
         rrs.rotate_smooth_quant(X, w.g, workspace=qws, out=(Xq, a, s))
         calls = {
@@ -367,8 +367,8 @@ def few_token_bench(torch, rrs, synth, reps=50):
         a = torch.empty((M,), dtype=torch.float32, device=dev)
         s = torch.empty((w.G,), dtype=torch.float32, device=dev)
         Y = torch.empty((M, w.N), dtype=torch.float16, device=dev)
-        qws = torch.empty((rrs.workspace_bytes(M, w.K, w.g),), dtype=torch.uint8, device=dev)
-        lws = torch.empty((rrs.linear_workspace_bytes(M, w.K, w.g),), dtype=torch.uint8,
+        qws = torch.zeros((rrs.workspace_bytes(M, w.K, w.g),), dtype=torch.uint8, device=dev)
+        lws = torch.zeros((rrs.linear_workspace_bytes(M, w.K, w.g),), dtype=torch.uint8,
                           device=dev)
         rrs.rotate_smooth_quant(X, w.g, workspace=qws, out=(Xq, a, s))
         calls = {
@@ -476,10 +476,10 @@ def reorder_bench(torch, rrs, synth, reps=50):
         Xq2, a2, s2 = torch.empty_like(Xq), torch.empty_like(a), torch.empty_like(s)
         bo = torch.empty((w.K // rrs.REORDER_BLOCK,), dtype=torch.int32, device=dev)
         Y = torch.empty((w.M, w.N), dtype=torch.float16, device=dev)
-        qws = torch.empty((rrs.workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8, device=dev)
+        qws = torch.zeros((rrs.workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8, device=dev)
         rws = torch.empty((rrs.reorder_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
                           device=dev)
-        lws = torch.empty((rrs.linear_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
+        lws = torch.zeros((rrs.linear_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
                           device=dev)
         lrws = torch.empty((rrs.linear_reorder_workspace_bytes(w.M, w.K, w.g),),
                            dtype=torch.uint8, device=dev)

@@ -126,7 +126,12 @@ int rrs_version(void);
 
 /*
  * Bytes of device workspace rrs_rotate_smooth_quant needs for this shape
- * (per-workgroup group-maximum partials: up to 256 rows of K/64 floats).
+ * (a 256-byte header and up to 256 rows of K/64 tagged 8-byte words for the
+ * one-launch kernels' exchange of group maxima, then up to 256 rows of K/64
+ * floats for the two-pass kernels). The workspace must hold zeros before its
+ * first use (e.g. allocated with hipMemsetAsync(ws, 0, bytes)); every call
+ * leaves it ready for the next call, with any shape, so one workspace can
+ * serve a whole model. Calls that share a workspace must not overlap.
  * Returns 0 when the shape or group size is invalid.
  */
 size_t rrs_workspace_bytes(int M, int K, int group_size);
@@ -202,6 +207,8 @@ rrs_status rrs_w4a4_gemm_ex(const void* Xq, const float* a_scale, const float* s
 /*
  * Bytes of workspace rrs_linear needs: rrs_workspace_bytes plus room for Xq,
  * a_scale and s_group, each sub-buffer aligned to 256 bytes. 0 when invalid.
+ * As for rrs_workspace_bytes, the workspace must hold zeros before its first
+ * use (the library-held scratch of rrs_linear_noalloc starts zeroed).
  */
 size_t rrs_linear_workspace_bytes(int M, int K, int group_size);
 
@@ -224,8 +231,8 @@ rrs_status rrs_linear(const void* X, const void* Wq, const float* w_scale, int M
  * the library runs on, kept until the process ends. Arguments, layouts and
  * results as rrs_linear (bit-identical outputs).
  *   Limit: rrs_linear_workspace_bytes(M, K, group_size) must not exceed
- *   RRS_NOALLOC_SCRATCH_BYTES (about M K / 2 bytes: up to 8143 tokens at
- *   K = 4096, 4059 at K = 8192, 2014 at K = 16384, with g = 128); larger
+ *   RRS_NOALLOC_SCRATCH_BYTES (about M K / 2 bytes: up to 8079 tokens at
+ *   K = 4096, 3995 at K = 8192, 1950 at K = 16384, with g = 128); larger
  *   calls return RRS_ERR_WORKSPACE and enqueue nothing.
  *   Every call on one device shares that device's scratch: calls that
  *   overlap on one device (concurrent streams, or host threads using
@@ -246,30 +253,34 @@ rrs_status rrs_linear_ex(const void* X, const void* Wq, const float* w_scale, in
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /*
- * Test hook for the failure path of the few-token quantizer (not for
- * computing: use rrs_rotate_smooth_quant). For 2 to 16 tokens without a
- * static reorder, rrs_rotate_smooth_quant runs one workgroup per token row
- * in a single launch; the rows exchange their group maxima through the
- * workspace and each waits, with a bounded poll, until all M have arrived
- * (Eq. 1 takes the maximum over every token). That needs the M workgroups to
- * be resident at the same time, which holds on an otherwise idle device but
- * not when other work fills every compute unit; a wait that runs out counts
- * itself in the workspace, writes NaN into its row's a_scale (row 0 also
- * into s_group) and ends, so the failure shows in the outputs.
- * This hook runs that kernel with the arrival target raised by
- * extra_arrivals (>= 1 makes it unreachable) and the wait cut to max_polls
- * polls (>= 1), waits for `stream`, and stores the number of waits that ran
- * out in *timeouts (host pointer). Arguments otherwise as
- * rrs_rotate_smooth_quant with perm = NULL and 2 <= M <= 16; RRS_ERR_SHAPE
- * for M outside 2..16, RRS_ERR_FLAGS for extra_arrivals < 0 or
- * max_polls < 1. With RRS_DEBUG set, rrs_rotate_smooth_quant(_ex) and
- * rrs_linear(_ex) read the same count after a call that used this kernel and
- * return RRS_ERR_TIMEOUT when it is not zero.
+ * Test hook for the failure path of the one-launch quantizers (not for
+ * computing: use rrs_rotate_smooth_quant). Without a static reorder,
+ * rrs_rotate_smooth_quant runs one launch for 2 to 16 tokens (one workgroup
+ * per token row) and, at K <= 4096, for more tokens too (one workgroup per
+ * compute unit, up to two rows per wave). The workgroups exchange their group
+ * maxima through the workspace (Eq. 1 takes the maximum over every token),
+ * each polling, with a bound, until the words it needs have arrived. That
+ * needs all workgroups of the launch to be resident at the same time, which
+ * holds on an otherwise idle device but not when other work fills every
+ * compute unit; a wait that runs out marks the call as failed in the
+ * workspace, writes NaN into its rows' a_scale (workgroup 0 also into
+ * s_group) and ends, so the failure shows in the outputs.
+ * This hook runs the kernel rrs_rotate_smooth_quant would choose for
+ * (M, K, group_size) with the readers also waiting for extra_rows rows of
+ * maxima that no workgroup writes (>= 1 makes every wait run out) and giving
+ * up after max_polls polling rounds (>= 1), waits for `stream`, and stores 1
+ * in *failed (host pointer) if the exchange failed, else 0. Arguments
+ * otherwise as rrs_rotate_smooth_quant with perm = NULL; RRS_ERR_SHAPE when
+ * no one-launch kernel serves the shape, RRS_ERR_FLAGS for extra_rows < 0,
+ * max_polls < 1 or more than 16 rows in all for the per-row kernel (256 for
+ * the fused one). With RRS_DEBUG set, rrs_rotate_smooth_quant(_ex) and
+ * rrs_linear(_ex) make the same check after a call that used a one-launch
+ * kernel and return RRS_ERR_TIMEOUT when it failed.
  */
 rrs_status rrs_test_quant_rows_wait(const void* X, int M, int K, int group_size,
-                                    int extra_arrivals, int max_polls, void* Xq,
-                                    float* a_scale, float* s_group, void* workspace,
-                                    size_t workspace_bytes, int32_t* timeouts, void* stream);
+                                    int extra_rows, int max_polls, void* Xq, float* a_scale,
+                                    float* s_group, void* workspace, size_t workspace_bytes,
+                                    int32_t* failed, void* stream);
 
 /*
  * Test hook: the exact int32 group partials P[b][i][n] (b < K/g, i < M,

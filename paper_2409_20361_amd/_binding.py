@@ -168,7 +168,7 @@ def rotate_smooth_quant(X: torch.Tensor, g: int, perm: Optional[torch.Tensor] = 
         Xq, a, s = out
     nbytes = workspace_bytes(M, K, g)
     if workspace is None:
-        workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=X.device)
+        workspace = torch.zeros((max(nbytes, 1),), dtype=torch.uint8, device=X.device)
     _check(lib().rrs_rotate_smooth_quant_ex(
         xp, M, K, g, _perm_ptr(perm, K), flags, Xq.data_ptr(), a.data_ptr(), s.data_ptr(),
         workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(X.device)),
@@ -204,7 +204,7 @@ def linear(X: torch.Tensor, Wq: torch.Tensor, w_scale: torch.Tensor, g: int,
     wsp = _dev(w_scale, "w_scale", torch.float32, (N,))
     nbytes = linear_workspace_bytes(M, K, g)
     if workspace is None:
-        workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=X.device)
+        workspace = torch.zeros((max(nbytes, 1),), dtype=torch.uint8, device=X.device)
     Y = out if out is not None else torch.empty((M, N), dtype=torch.float16, device=X.device)
     yp = _dev(Y, "Y", torch.float16, (M, N))
     _check(lib().rrs_linear_ex(xp, wqp, wsp, M, N, K, g, _perm_ptr(perm, K), flags, yp,
@@ -245,25 +245,26 @@ def w4a4_gemm_partials(Xq: torch.Tensor, Wq: torch.Tensor, g: int) -> torch.Tens
     return P
 
 
-def quant_rows_wait_hook(X: torch.Tensor, g: int, extra_arrivals: int, max_polls: int,
+def quant_rows_wait_hook(X: torch.Tensor, g: int, extra_rows: int, max_polls: int,
                          workspace: Optional[torch.Tensor] = None):
-    """Test hook of the few-token quantizer's bounded wait (2 <= M <= 16): runs it
-    with the arrival target raised by extra_arrivals and at most max_polls
-    polls; returns (Xq, a_scale, s_group, number of waits that ran out)."""
+    """Test hook of the one-launch quantizers' bounded wait: runs the kernel
+    rrs_rotate_smooth_quant would choose with the readers also waiting for
+    extra_rows rows that nobody writes and at most max_polls polling rounds;
+    returns (Xq, a_scale, s_group, failed)."""
     M, K = X.shape
     xp = _dev(X, "X", torch.float16, (M, K))
     Xq = torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
     a = torch.empty((M,), dtype=torch.float32, device=X.device)
     s = torch.empty((K // g,), dtype=torch.float32, device=X.device)
     if workspace is None:
-        workspace = torch.empty((max(workspace_bytes(M, K, g), 1),), dtype=torch.uint8,
+        workspace = torch.zeros((max(workspace_bytes(M, K, g), 1),), dtype=torch.uint8,
                                 device=X.device)
     n = ctypes.c_int32(-1)
     _check(lib().rrs_test_quant_rows_wait(
-        xp, M, K, g, extra_arrivals, max_polls, Xq.data_ptr(), a.data_ptr(), s.data_ptr(),
+        xp, M, K, g, extra_rows, max_polls, Xq.data_ptr(), a.data_ptr(), s.data_ptr(),
         workspace.data_ptr(), workspace.numel() * workspace.element_size(), ctypes.byref(n),
         _stream(X.device)), "rrs_test_quant_rows_wait")
-    return Xq, a, s, n.value
+    return Xq, a, s, bool(n.value)
 
 
 def quantize_sub_channel(X: torch.Tensor, g: int, flags: int = 0
@@ -363,7 +364,7 @@ def rotate_smooth_quant_reorder(X: torch.Tensor, g: int, workspace: Optional[tor
         Xq, a, s, order = out
     nbytes = reorder_workspace_bytes(M, K, g)
     if workspace is None:
-        workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=X.device)
+        workspace = torch.zeros((max(nbytes, 1),), dtype=torch.uint8, device=X.device)
     _check(lib().rrs_rotate_smooth_quant_reorder(
         xp, M, K, g, flags, Xq.data_ptr(), a.data_ptr(), s.data_ptr(), order.data_ptr(),
         workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(X.device)),
@@ -400,7 +401,7 @@ def linear_reorder(X: torch.Tensor, Wq: torch.Tensor, w_scale: torch.Tensor, g: 
     wsp = _dev(w_scale, "w_scale", torch.float32, (N,))
     nbytes = linear_reorder_workspace_bytes(M, K, g)
     if workspace is None:
-        workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=X.device)
+        workspace = torch.zeros((max(nbytes, 1),), dtype=torch.uint8, device=X.device)
     Y = out if out is not None else torch.empty((M, N), dtype=torch.float16, device=X.device)
     yp = _dev(Y, "Y", torch.float16, (M, N))
     _check(lib().rrs_linear_reorder(xp, wqp, wsp, M, N, K, g, flags, yp, workspace.data_ptr(),

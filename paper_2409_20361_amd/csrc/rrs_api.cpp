@@ -103,17 +103,20 @@ rrs_status debug_check_finite_f16(const void* p, size_t count, const char* what,
 }
 
 // After a quantizer launch under RRS_DEBUG: waits for the stream and fails
-// when the per-row kernel (used for this shape) reported a wait that ran out.
+// when a one-launch kernel (per-row or fused, used for this shape) reported a
+// wait that ran out in its exchange.
 rrs_status debug_check_quant_wait(int M, int K, int g, const int32_t* perm, int flags,
                                   const void* workspace, void* stream) {
-  if (!rrs::quant_rows_used(M, K, g, perm, flags & kQuantFlags) || M < 2) return RRS_OK;
-  uint32_t n = 0;
-  if (rrs::quant_rows_timeouts(workspace, static_cast<hipStream_t>(stream), &n) != hipSuccess) {
+  const bool rows = rrs::quant_rows_used(M, K, g, perm, flags & kQuantFlags) && M >= 2;
+  if (!rows && !rrs::fused_quant_used(M, K, g, perm, flags & kQuantFlags)) return RRS_OK;
+  bool failed = false;
+  if (rrs::quant_exchange_failed(workspace, static_cast<hipStream_t>(stream), &failed) !=
+      hipSuccess) {
     (void)hipGetLastError();
     return RRS_ERR_HIP;
   }
-  if (n) {
-    std::fprintf(stderr, "[rrs] RRS_DEBUG: %u workgroup waits ran out in the quantizer\n", n);
+  if (failed) {
+    std::fprintf(stderr, "[rrs] RRS_DEBUG: a wait between workgroups ran out in the quantizer\n");
     return RRS_ERR_TIMEOUT;
   }
   return RRS_OK;
@@ -613,31 +616,41 @@ rrs_status rrs_linear_reorder(const void* X, const void* Wq, const float* w_scal
 }
 
 rrs_status rrs_test_quant_rows_wait(const void* X, int M, int K, int group_size,
-                                    int extra_arrivals, int max_polls, void* Xq,
-                                    float* a_scale, float* s_group, void* workspace,
-                                    size_t workspace_bytes, int32_t* timeouts, void* stream) {
-  if (!X || !Xq || !a_scale || !s_group || !workspace || !timeouts) return RRS_ERR_NULL;
-  if (M < 2 || !rrs::quant_rows_fits(M) || !valid_k(K)) return RRS_ERR_SHAPE;
+                                    int extra_rows, int max_polls, void* Xq, float* a_scale,
+                                    float* s_group, void* workspace, size_t workspace_bytes,
+                                    int32_t* failed, void* stream) {
+  if (!X || !Xq || !a_scale || !s_group || !workspace || !failed) return RRS_ERR_NULL;
+  if (!valid_m(M) || !valid_k(K)) return RRS_ERR_SHAPE;
   if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
-  if (extra_arrivals < 0 || max_polls < 1) return RRS_ERR_FLAGS;
+  const bool rows = M >= 2 && rrs::quant_rows_used(M, K, group_size, nullptr, 0);
+  const bool fused = rrs::fused_quant_used(M, K, group_size, nullptr, 0);
+  if (!rows && !fused) return RRS_ERR_SHAPE;
+  if (extra_rows < 0 || max_polls < 1 || (rows && M + extra_rows > 16)) return RRS_ERR_FLAGS;
   if (!is_aligned(X) || !is_aligned(Xq) || !is_aligned(a_scale) || !is_aligned(s_group) ||
       !is_aligned(workspace))
     return RRS_ERR_ALIGN;
-  if (workspace_bytes < rrs::quant_workspace_bytes(M, K) ||
-      workspace_bytes < rrs::quant_rows_workspace_bytes(K, group_size))
-    return RRS_ERR_WORKSPACE;
+  if (workspace_bytes < rrs::quant_workspace_bytes(M, K)) return RRS_ERR_WORKSPACE;
   if (rrs_status s = check_device()) return s;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (rrs::launch_quant_rows(static_cast<const uint16_t*>(X), M, K, group_size, true,
-                             static_cast<uint8_t*>(Xq), a_scale, s_group, workspace, st,
-                             extra_arrivals, max_polls) != hipSuccess)
-    return RRS_ERR_HIP;
-  uint32_t n = 0;
-  if (rrs::quant_rows_timeouts(workspace, st, &n) != hipSuccess) {
+  const hipError_t e =
+      rows ? rrs::launch_quant_rows(static_cast<const uint16_t*>(X), M, K, group_size, true,
+                                    static_cast<uint8_t*>(Xq), a_scale, s_group, workspace, st,
+                                    extra_rows, max_polls)
+           : rrs::launch_rotate_smooth_quant_fused(static_cast<const uint16_t*>(X), M, K,
+                                                   group_size, true, static_cast<uint8_t*>(Xq),
+                                                   a_scale, s_group, workspace,
+                                                   rrs::fused_quant_wgs(), st, extra_rows,
+                                                   max_polls);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return e == hipErrorInvalidValue ? RRS_ERR_FLAGS : RRS_ERR_HIP;
+  }
+  bool f = false;
+  if (rrs::quant_exchange_failed(workspace, st, &f) != hipSuccess) {
     (void)hipGetLastError();
     return RRS_ERR_HIP;
   }
-  *timeouts = (int32_t)n;
+  *failed = f ? 1 : 0;
   return RRS_OK;
 }
 

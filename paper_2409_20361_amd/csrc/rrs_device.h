@@ -175,10 +175,76 @@ __device__ __forceinline__ float row_group_max(float lm, float* red, float* gm, 
   return r;
 }
 
+// ---------------------------------------------------------------------------
+// Exchange between the workgroups of one launch (the one-launch quantizers).
+//
+// Each exchanged float travels as one 64-bit word, a tag in the high half and
+// the float's bits in the low half, written with a single relaxed
+// agent-scope atomic store; a reader polls the words it needs with relaxed
+// agent-scope atomic loads until the tag is this call's. Each value carries
+// its own tag, so the exchange rests on per-location coherence alone: no
+// fence, no arrival count, no L2 write-back or invalidation (an agent-scope
+// release / acquire pair per workgroup cost about 40 us at 256 workgroups in
+// a probe; a count-based barrier with coherent data 6 us; tagged words 4 us).
+//
+// Tags come from an epoch word in the workspace header, zero before the
+// workspace's first use: every workgroup reads the epoch E at its start and
+// tags with T = next_epoch(E) (never 0, so zeroed words never match); once
+// workgroup 0 has read every word of the call it stores T as the new epoch
+// (all workgroups had read E before publishing, so none can see T too early).
+// Words of earlier calls carry older tags; the
+// tag repeats only after 2^32 - 1 calls. A wait that runs out stores T in
+// header word 1 instead, so that a host check can see that the latest call
+// failed (word 1 == word 0).
+// ---------------------------------------------------------------------------
+constexpr int kEpochWord = 0;
+constexpr int kFailWord = 1;
+
+__device__ __forceinline__ uint32_t next_epoch(uint32_t e) { return e + 1u == 0u ? 1u : e + 1u; }
+
+__device__ __forceinline__ void publish_tagged(unsigned long long* w, uint32_t tag, float v) {
+  __hip_atomic_store(w, ((unsigned long long)tag << 32) | __float_as_uint(v), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ unsigned long long load_tagged(const unsigned long long* w) {
+  return __hip_atomic_load(const_cast<unsigned long long*>(w), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ bool has_tag(unsigned long long x, uint32_t tag) {
+  return (uint32_t)(x >> 32) == tag;
+}
+
 // Symmetric INT4 code of v: clamp(rint(v), -7, 7) as a 4-bit two's complement nibble.
 __device__ __forceinline__ uint32_t int4_nibble(float v) {
   const float q = fminf(fmaxf(__builtin_rintf(v), -7.0f), 7.0f);
   return (uint32_t)((int)q) & 0xFu;
+}
+
+// Codes of v[0..7] * m packed into one word, low nibble = even index:
+// bit-identical to packing int4_nibble(v[e] * m) (same two roundings, same
+// clamp). fl(fl(v m) + 1.5 * 2^23) is fl(v m) rounded to an integer, half to
+// even (the binade of 1.5 * 2^23 has ulp 1), held in the low bits of the
+// float's bit pattern, 0x4B400000 + q; clamping those bits to
+// 0x4B400000 +- 7 (v_med3_i32) clamps q to [-7, 7], and the low nibble of
+// 0x4B400000 + q is q's two's-complement nibble. Values far outside the
+// binade clamp to +-7 as well; NaN (excluded by the preconditions) would
+// not. 3 VALU ops per code plus 11 per word, against about 8 per code for
+// rint / clamp / convert / pack.
+__device__ __forceinline__ uint32_t quant_pack8(const float* v, float m) {
+  int b[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int x = __builtin_bit_cast(int, __fadd_rn(__fmul_rn(v[e], m), 12582912.0f));
+    b[e] = min(max(x, 0x4B400000 - 7), 0x4B400000 + 7);
+  }
+  uint32_t p[4];  // byte k in the low 8 bits: codes 2k (low nibble) and 2k + 1
+#pragma unroll
+  for (int k = 0; k < 4; ++k) p[k] = ((uint32_t)b[2 * k + 1] << 4) | ((uint32_t)b[2 * k] & 0xFu);
+  const uint32_t lo = __builtin_amdgcn_perm(p[1], p[0], 0x0C0C0400u);  // bytes 0, 1
+  const uint32_t hi = __builtin_amdgcn_perm(p[3], p[2], 0x04000C0Cu);  // bytes 2, 3
+  return lo | hi;
 }
 
 // Store E/2 packed bytes (E nibbles, low nibble = even index) at dst.

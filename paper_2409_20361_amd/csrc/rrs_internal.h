@@ -13,6 +13,19 @@ namespace rrs {
 int quant_partial_rows(int M);
 size_t quant_workspace_bytes(int M, int K);
 
+// Workspace of rrs_rotate_smooth_quant, three disjoint regions:
+//   [0, 256)                      header of the one-launch kernels: word 0 the
+//                                 exchange epoch, word 1 the epoch of the last
+//                                 exchange whose wait ran out;
+//   [256, 256 + tagged_bytes(K))  tagged entries of the one-launch kernels
+//                                 (64 bits: epoch tag << 32 | float bits);
+//   then two_pass_bytes(K)        float partials of the two-pass kernels.
+// The one-launch kernels need the header and entries to hold zeros before the
+// workspace's first use (every call leaves them valid for the next).
+constexpr size_t kQuantHeaderBytes = 256;
+inline size_t quant_tagged_bytes(int K) { return ((size_t)256 * (K / 64) * 8 + 255) & ~size_t(255); }
+inline size_t quant_two_pass_offset(int K) { return kQuantHeaderBytes + quant_tagged_bytes(K); }
+
 // Ablation switches (the public RRS_SKIP_* flags).
 constexpr int kSkipRotation = 1;
 constexpr int kSkipSmoothing = 2;
@@ -52,6 +65,20 @@ hipError_t launch_rotate_smooth_quant_wave(const uint16_t* X, int M, int K, int 
                                            float* a_scale, float* s_group, void* workspace,
                                            int max_partials, int max_quant_wgs,
                                            hipStream_t stream);
+
+// One-launch rotate + smooth + quant for K <= 4096 (rrs_quant_wave.hip):
+// every row rotated once and kept in registers, the workgroups' group maxima
+// exchanged through the workspace (an error word at offset 0, 64-bit tagged
+// entries from byte 256), at most max_wgs workgroups (one per compute unit,
+// all resident), two rows per wave at most. extra_rows > 0 / max_polls > 0:
+// test hook only (the readers also wait for extra_rows rows that no
+// workgroup writes, so every wait runs out after max_polls polls).
+bool fused_quant_fits(int M, int K, int max_wgs);
+int fused_quant_wgs();  // workgroups of the fused kernel: one per compute unit, at most 256
+hipError_t launch_rotate_smooth_quant_fused(const uint16_t* X, int M, int K, int g, bool rotate,
+                                            uint8_t* Xq, float* a_scale, float* s_group,
+                                            void* workspace, int max_wgs, hipStream_t stream,
+                                            int extra_rows = 0, int max_polls = 0);
 
 // Every launcher that writes or reads Wq takes its layout (row-major unless
 // the caller asked for RRS_WEIGHT_TILED).
@@ -164,20 +191,22 @@ constexpr size_t kNoAllocScratchBytes = (size_t)16 << 20;
 hipError_t noalloc_scratch(void** ptr);
 
 // rotate + smooth + quant with one workgroup per row for M <= 16 tokens, no
-// static reorder, smoothing on (rrs_quant_rows.hip); the workspace holds
-// quant_rows_workspace_bytes(K, g) bytes of any content (set up by the call).
-// extra_arrivals > 0 and max_polls > 0 are for the test hook only: the
-// arrival target becomes M + extra_arrivals (unreachable, so every wait runs
-// out) and the wait gives up after max_polls polls (0 = the default bound).
+// static reorder, smoothing on (rrs_quant_rows.hip); uses the header and
+// tagged entries of the workspace (zero before its first use). extra_rows > 0
+// and max_polls > 0 are for the test hook only: the readers also wait for
+// extra_rows rows that no workgroup writes (so every wait runs out) and give
+// up after max_polls rounds (0 = the default bound).
 bool quant_rows_fits(int M);
 size_t quant_rows_workspace_bytes(int K, int g);
 hipError_t launch_quant_rows(const uint16_t* X, int M, int K, int g, bool rotate, uint8_t* Xq,
                              float* a_scale, float* s_group, void* workspace, hipStream_t stream,
-                             int extra_arrivals = 0, int max_polls = 0);
+                             int extra_rows = 0, int max_polls = 0);
 // Whether launch_rotate_smooth_quant takes the per-row kernel for this call.
 bool quant_rows_used(int M, int K, int g, const int32_t* perm, int flags);
-// Waits for `stream` and returns the per-row kernel's count of waits that ran
-// out, read from the workspace of its last call.
-hipError_t quant_rows_timeouts(const void* workspace, hipStream_t stream, uint32_t* count);
+// Waits for `stream` and reports whether the latest one-launch exchange in
+// this workspace (per-row or fused kernel) had a wait that ran out.
+hipError_t quant_exchange_failed(const void* workspace, hipStream_t stream, bool* failed);
+// Whether launch_rotate_smooth_quant takes the fused one-launch kernel.
+bool fused_quant_used(int M, int K, int g, const int32_t* perm, int flags);
 
 }  // namespace rrs

@@ -618,10 +618,19 @@ hipError_t launch_quantize_sub_channel(const uint16_t* X, int M, int K, int g, i
 
 int quant_partial_rows(int M) { return M < kMaxPartialRows ? M : kMaxPartialRows; }
 
+int fused_quant_wgs() { return num_cus() < kMaxPartialRows ? num_cus() : kMaxPartialRows; }
+
+bool fused_quant_used(int M, int K, int g, const int32_t* perm, int flags) {
+  (void)g;
+  return !quant_rows_used(M, K, g, perm, flags) && M > few_max_rows(K) && !perm &&
+         !(flags & kSkipSmoothing) && fused_quant_fits(M, K, fused_quant_wgs());
+}
+
 size_t quant_workspace_bytes(int M, int K) {
   (void)M;
-  // per-workgroup group maxima: at most 256 rows of K / 64 floats
-  return align256((size_t)kMaxPartialRows * (K / 64) * 4);
+  // header and tagged entries of the one-launch kernels, then the two-pass
+  // kernels' partial rows (at most 256 rows of K / 64 floats)
+  return quant_two_pass_offset(K) + align256((size_t)kMaxPartialRows * (K / 64) * 4);
 }
 
 namespace {
@@ -664,15 +673,24 @@ hipError_t launch_rotate_smooth_quant(const uint16_t* X, int M, int K, int g,
       default: return hipErrorInvalidValue;
     }
   }
+  // K <= 4096 without a static reorder: one launch, every row rotated once
+  // (rrs_quant_wave.hip), for up to two rows per wave on one workgroup per
+  // compute unit.
+  if (fused_quant_used(M, K, g, perm, flags))
+    return launch_rotate_smooth_quant_fused(X, M, K, g, !(flags & kSkipRotation), Xq, a_scale,
+                                            s_group, workspace, fused_quant_wgs(), stream);
+  // The two-pass kernels keep their partial rows clear of the one-launch
+  // kernels' header and tagged entries.
+  void* tp = static_cast<char*>(workspace) + quant_two_pass_offset(K);
   if (use_wave_kernels(M, K))
-    return launch_rotate_smooth_quant_wave(X, M, K, g, perm, flags, Xq, a_scale, s_group,
-                                           workspace, kMaxPartialRows, 2 * num_cus(), stream);
+    return launch_rotate_smooth_quant_wave(X, M, K, g, perm, flags, Xq, a_scale, s_group, tp,
+                                           kMaxPartialRows, 2 * num_cus(), stream);
   switch (K) {
-    case 512: return launch_k<512>(X, M, g, perm, flags, Xq, a_scale, s_group, workspace, stream);
-    case 1024: return launch_k<1024>(X, M, g, perm, flags, Xq, a_scale, s_group, workspace, stream);
-    case 2048: return launch_k<2048>(X, M, g, perm, flags, Xq, a_scale, s_group, workspace, stream);
-    case 8192: return launch_k<8192>(X, M, g, perm, flags, Xq, a_scale, s_group, workspace, stream);
-    case 16384: return launch_k<16384>(X, M, g, perm, flags, Xq, a_scale, s_group, workspace, stream);
+    case 512: return launch_k<512>(X, M, g, perm, flags, Xq, a_scale, s_group, tp, stream);
+    case 1024: return launch_k<1024>(X, M, g, perm, flags, Xq, a_scale, s_group, tp, stream);
+    case 2048: return launch_k<2048>(X, M, g, perm, flags, Xq, a_scale, s_group, tp, stream);
+    case 8192: return launch_k<8192>(X, M, g, perm, flags, Xq, a_scale, s_group, tp, stream);
+    case 16384: return launch_k<16384>(X, M, g, perm, flags, Xq, a_scale, s_group, tp, stream);
     default: return hipErrorInvalidValue;
   }
 }

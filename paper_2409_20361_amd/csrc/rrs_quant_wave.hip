@@ -310,6 +310,214 @@ __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// 3. One launch (K <= 4096, up to two rows per wave): rotate every row once,
+//    exchange the workgroups' group maxima, quantize the rows kept in
+//    registers.
+//
+// The two launches above rotate every row twice (the second pass cannot
+// keep the first pass's rows), and each pass is one row per wave of serial
+// latency: at 2048 x 4096 they took 9.9 + 14.9 us, with the FWHT's VALU work
+// twice over. Here each wave rotates its rows once, brings them back to
+// layout 1 (lane l holds positions 64 l .. 64 l + 63, one group) and keeps
+// them in registers (64 VGPRs per row). The workgroups (one per compute
+// unit, all resident) then exchange their rows of group maxima through the
+// workspace as tagged words, one per (workgroup, group), in the fence-free
+// protocol of rrs_device.h (epoch tags, per-location coherence). The polls
+// are bounded (max_polls rounds per thread): a wait that runs out marks the
+// call as failed in the header and the workgroup writes NaN into its rows'
+// alpha (workgroup 0 also into s_group), so a failed exchange shows in the
+// outputs. Same arithmetic in the same order as the two-pass kernels:
+// bit-identical codes and scales.
+// ---------------------------------------------------------------------------
+constexpr int kFusedWaves = 8;
+constexpr int kFusedMaxPolls = 1 << 20;
+
+template <int K, bool kRot, int SLOTS>
+__global__ __launch_bounds__(kFusedWaves * 64) void rot_quant_fused_kernel(
+    const uint16_t* __restrict__ X, int M, int g, int rows_per_wg, uint32_t* header,
+    unsigned long long* tagged, int nrows, int max_polls, uint8_t* __restrict__ Xq,
+    float* __restrict__ a_scale, float* __restrict__ s_group) {
+  using S = WaveRow<K>;
+  constexpr int NT = kFusedWaves * 64;
+  constexpr int GMAX = K / 64;  // groups at g = 64
+  __shared__ __attribute__((aligned(16))) float rows[kFusedWaves * S::RW * S::RF];
+  __shared__ float wmax[kFusedWaves][GMAX];
+  __shared__ float red[NT];
+  __shared__ float rg[GMAX];
+  __shared__ int missed;
+  __shared__ uint32_t tag_lds;
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  const int sub = lane >> S::LR;    // row of the wave
+  const int l = lane & (S::R - 1);  // lane within the row
+  float* row = rows + (wave * S::RW + sub) * S::RF;
+  const int G = K / g;
+  const int r0 = blockIdx.x * rows_per_wg;
+  const int r1 = min(M, r0 + rows_per_wg);
+  auto row_of = [&](int p) { return r0 + (p * kFusedWaves + wave) * S::RW + sub; };
+  // This call's tag (the header was written by earlier calls only): one
+  // thread requests it now and hands it over in LDS before the first barrier,
+  // so the load's latency hides behind the rotation.
+  uint32_t epoch = 0u;
+  if (tid == 0)
+    epoch = __hip_atomic_load(header + kEpochWord, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+  // Phase 1: rotate, back to layout 1, per-lane maxima.
+  float v[SLOTS][64];
+  float lm[SLOTS];
+  uint4 raw[8];
+  {
+    const int r = row_of(0);
+    load_raw64(X + (size_t)min(r, M - 1) * K + 64 * l, r < r1, raw);
+  }
+#pragma unroll
+  for (int p = 0; p < SLOTS; ++p) {
+    raw_to_float(raw, v[p]);
+    if (p + 1 < SLOTS) {
+      const int rn = row_of(p + 1);
+      load_raw64(X + (size_t)min(rn, M - 1) * K + 64 * l, rn < r1, raw);
+    }
+    fwht_wave_row<K, kRot>(v[p], row, l);  // v[e] = y[l + R e]
+#pragma unroll
+    for (int e = 0; e < 64; ++e) row[lds_a(l + S::R * e)] = v[p][e];
+#pragma unroll
+    for (int m = 0; m < 16; ++m) {
+      const float4 c = *reinterpret_cast<const float4*>(row + lds_a(64 * l + 4 * m));
+      v[p][4 * m] = c.x;
+      v[p][4 * m + 1] = c.y;
+      v[p][4 * m + 2] = c.z;
+      v[p][4 * m + 3] = c.w;
+    }
+    float x = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 64; ++e) x = fmaxf(x, fabsf(v[p][e]));
+    lm[p] = x;
+  }
+
+  // The workgroup's group maxima: over slots, over the wave's rows (lanes with
+  // the same l), over the g / 64 lanes of a group, then over the waves in LDS
+  // (a fixed tree, no atomics); published as tagged entries.
+  float pm = lm[0];
+#pragma unroll
+  for (int p = 1; p < SLOTS; ++p) pm = fmaxf(pm, lm[p]);
+#pragma unroll
+  for (int o = S::R; o < 64; o <<= 1) pm = fmaxf(pm, __shfl_xor(pm, o, 64));
+  for (int o = 1; o < g / 64; o <<= 1) pm = fmaxf(pm, __shfl_xor(pm, o, 64));
+  if (sub == 0 && (64 * l) % g == 0) wmax[wave][(64 * l) / g] = pm;
+  if (tid == 0) {
+    missed = 0;
+    tag_lds = next_epoch(epoch);
+  }
+  __syncthreads();
+  const uint32_t tag = tag_lds;
+  if (tid < G) {
+    float m = wmax[0][tid];
+#pragma unroll
+    for (int w = 1; w < kFusedWaves; ++w) m = fmaxf(m, wmax[w][tid]);
+    publish_tagged(tagged + (size_t)blockIdx.x * G + tid, tag, m);
+  }
+
+  // s_b = max over the nrows rows of maxima; r_b = fl(1 / s_b). Thread t takes
+  // group t % G of rows t / G, t / G + NT / G, ... (at most GMAX / 2 of them):
+  // all its entries are requested at once, and those whose tag is not set yet
+  // are requested again, within a budget of max_polls rounds.
+  {
+    constexpr int NE = GMAX / 2;  // entries per thread at most: 256 rows / (NT / G)
+    const int b = tid % G;
+    const int ns = NT / G;  // slices of rows
+    const unsigned long long none = (unsigned long long)tag << 32;  // an absent row: 0.0
+    unsigned long long x[NE];
+#pragma unroll
+    for (int k = 0; k < NE; ++k) {
+      const int i = tid / G + k * ns;
+      x[k] = i < nrows ? load_tagged(tagged + (size_t)i * G + b) : none;
+    }
+    bool ok = false;
+    for (int round = 0;; ++round) {
+      ok = true;
+#pragma unroll
+      for (int k = 0; k < NE; ++k) ok = ok && has_tag(x[k], tag);
+      if (ok || round >= max_polls) break;
+      __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+      for (int k = 0; k < NE; ++k) {
+        const int i = tid / G + k * ns;
+        if (!has_tag(x[k], tag)) x[k] = load_tagged(tagged + (size_t)i * G + b);
+      }
+    }
+    float m = 0.0f;
+#pragma unroll
+    for (int k = 0; k < NE; ++k) m = fmaxf(m, __uint_as_float((uint32_t)x[k]));
+    if (!ok) missed = 1;  // benign race: every writer writes 1
+    red[tid] = m;
+    __syncthreads();
+    // Every word of the call has been read (or given up on): advance the epoch
+    // (workgroup 0 only: one store instead of a contended one per workgroup).
+    if (tid == 0) {
+      if (missed)
+        __hip_atomic_store(header + kFailWord, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (blockIdx.x == 0)
+        __hip_atomic_store(header + kEpochWord, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (tid < G) {
+      float sv = red[tid];
+      for (int q = 1; q < ns; ++q) sv = fmaxf(sv, red[q * G + tid]);
+      rg[tid] = (sv == 0.0f) ? 0.0f : __fdiv_rn(1.0f, sv);
+      if (blockIdx.x == 0) s_group[tid] = missed ? __builtin_nanf("") : sv;
+    }
+    __syncthreads();
+  }
+  const bool failed = missed != 0;  // uniform over the workgroup
+
+  // Phase 2: token scale and codes of every kept row.
+  const float rb = rg[(64 * l) / g];
+#pragma unroll
+  for (int p = 0; p < SLOTS; ++p) {
+    const int r = row_of(p);
+    const float a = row_max<S::R>(lm[p] * rb);  // max over the row's groups of fl(M_ib r_b)
+    const float inv = (a == 0.0f) ? 0.0f : __fdiv_rn(7.0f, a);
+    const float m = rb * inv;                   // fl(r_b * inv_i)
+    if (r < r1) {
+      uint32_t wd[8];
+#pragma unroll
+      for (int w = 0; w < 8; ++w) wd[w] = quant_pack8(&v[p][8 * w], m);
+      uint4* dst = reinterpret_cast<uint4*>(Xq + (size_t)r * (K / 2) + 32 * l);
+      dst[0] = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+      dst[1] = make_uint4(wd[4], wd[5], wd[6], wd[7]);
+      if (l == 0) a_scale[r] = failed ? __builtin_nanf("") : __fdiv_rn(a, 7.0f);
+    }
+  }
+}
+
+template <int K>
+hipError_t launch_fused_k(const uint16_t* X, int M, int g, bool rot, uint8_t* Xq,
+                          float* a_scale, float* s_group, void* workspace, int max_wgs,
+                          int extra_rows, int max_polls, hipStream_t stream) {
+  constexpr int per_slot = kFusedWaves * WaveRow<K>::RW;  // rows per workgroup per slot
+  const int slots = M <= max_wgs * per_slot ? 1 : 2;
+  const int rpw = slots * per_slot;
+  const int wgs = (M + rpw - 1) / rpw;
+  const int nrows = wgs + extra_rows;  // rows of maxima the readers wait for
+  if (wgs > max_wgs || nrows > 256) return hipErrorInvalidValue;
+  uint32_t* header = static_cast<uint32_t*>(workspace);
+  unsigned long long* tagged =
+      reinterpret_cast<unsigned long long*>(static_cast<char*>(workspace) + kQuantHeaderBytes);
+  const int polls = max_polls > 0 ? max_polls : kFusedMaxPolls;
+#define RRS_FUSED(R_, S_)                                                                    \
+  rot_quant_fused_kernel<K, R_, S_><<<wgs, kFusedWaves * 64, 0, stream>>>(                   \
+      X, M, g, rpw, header, tagged, nrows, polls, Xq, a_scale, s_group)
+  if (rot) {
+    if (slots == 1) RRS_FUSED(true, 1); else RRS_FUSED(true, 2);
+  } else {
+    if (slots == 1) RRS_FUSED(false, 1); else RRS_FUSED(false, 2);
+  }
+#undef RRS_FUSED
+  return hipGetLastError();
+}
+
 // Rows of M per workgroup of `waves` waves, one row per wave where a grid of
 // at most `cap` workgroups allows it; returns the grid size.
 template <int K>
@@ -406,6 +614,29 @@ hipError_t launch_quantize_given_wave(const uint16_t* X, int M, int K, int g,
     case 1024: return launch_given_wave<1024>(X, M, g, perm, rotate, gmax, max_quant_wgs, Xq, a_scale, s_group, stream);
     case 2048: return launch_given_wave<2048>(X, M, g, perm, rotate, gmax, max_quant_wgs, Xq, a_scale, s_group, stream);
     case 4096: return launch_given_wave<4096>(X, M, g, perm, rotate, gmax, max_quant_wgs, Xq, a_scale, s_group, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+bool fused_quant_fits(int M, int K, int max_wgs) {
+  if (K < 512 || K > 4096) return false;
+  const int per_wg = 2 * kFusedWaves * (64 * 64 / K);  // two slots of rows per wave
+  return M >= 1 && M <= max_wgs * per_wg;
+}
+
+hipError_t launch_rotate_smooth_quant_fused(const uint16_t* X, int M, int K, int g, bool rotate,
+                                            uint8_t* Xq, float* a_scale, float* s_group,
+                                            void* workspace, int max_wgs, hipStream_t stream,
+                                            int extra_rows, int max_polls) {
+  switch (K) {
+#define RRS_FK(K_) \
+  case K_: return launch_fused_k<K_>(X, M, g, rotate, Xq, a_scale, s_group, workspace, max_wgs, \
+                                     extra_rows, max_polls, stream)
+    RRS_FK(512);
+    RRS_FK(1024);
+    RRS_FK(2048);
+    RRS_FK(4096);
+#undef RRS_FK
     default: return hipErrorInvalidValue;
   }
 }

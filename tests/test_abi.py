@@ -57,8 +57,11 @@ def test_workspace_queries():
     for M, K, g in ((16, 512, 128), (2048, 4096, 128), (8, 8192, 128), (8192, 8192, 64),
                     (3, 16384, 512)):
         q = lib.rrs_workspace_bytes(M, K, g)
-        # per-workgroup group maxima: 256 rows of K / 64 floats, 256-byte aligned
-        assert q == ((256 * (K // 64) * 4 + 255) // 256) * 256
+        # a 256-byte header and 256 rows of K / 64 tagged 8-byte words (the
+        # one-launch kernels), then 256 rows of K / 64 floats (the two-pass
+        # kernels), each region 256-byte aligned
+        a256 = lambda x: (x + 255) // 256 * 256  # noqa: E731
+        assert q == 256 + a256(256 * (K // 64) * 8) + a256(256 * (K // 64) * 4)
         lw = lib.rrs_linear_workspace_bytes(M, K, g)
         a256 = lambda x: (x + 255) // 256 * 256  # noqa: E731
         assert lw == q + a256(M * K // 2) + a256(4 * M) + a256(4 * (K // g))
@@ -461,15 +464,16 @@ def test_quant_rows_wait_hook_checks():
     # the failure-path test hook validates like the quantizer, in the same order
     for key in ("X", "Xq", "a", "s", "ws", "n"):
         assert _qwait(**{key: None}) == NULL, key
-    assert _qwait(M=1) == SHAPE       # the exchange needs 2..16 rows
-    assert _qwait(M=17) == SHAPE
+    assert _qwait(M=1) == SHAPE       # one row: no exchange
+    assert _qwait(M=17, K=8192) == SHAPE   # no one-launch kernel for this shape
     assert _qwait(K=1000) == SHAPE
     assert _qwait(g=96) == GROUP
     assert _qwait(extra=-1) == FLAGS
     assert _qwait(polls=0) == FLAGS
+    assert _qwait(M=4, extra=13) == FLAGS  # the per-row kernel waits for <= 16 rows
     assert _qwait(X=MIS) == ALIGN
     assert _qwait(wsb=16) == WS
-    assert _qwait(M=17, X=None) == NULL   # null pointers first
+    assert _qwait(M=17, K=8192, X=None) == NULL   # null pointers first
 
 
 def test_debug_checks_come_after_host_validation():

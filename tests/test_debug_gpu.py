@@ -4,12 +4,12 @@
     that is not a permutation returns RRS_ERR_PRECONDITION before anything is
     enqueued (outputs keep their sentinel bytes); valid inputs pass, and
     without RRS_DEBUG the same calls are not checked.
-  * The few-token quantizer's bounded wait (one workgroup per token row, the
-    rows' group maxima exchanged within the launch, Eq. 1 taking the maximum
-    over all tokens): the test hook raises the arrival target past M so that
-    every wait runs out after a few polls; the kernel must end, count every
-    workgroup in its error word and write NaN into alpha and s_group, and the
-    next ordinary call on the same workspace must be correct again.
+  * The one-launch quantizers' bounded wait (the workgroups' group maxima
+    exchanged within the launch, Eq. 1 taking the maximum over all tokens):
+    the test hook makes the readers also wait for a row of maxima that no
+    workgroup writes, so every wait runs out after a few polls; the kernel
+    must end, mark the call as failed and write NaN into alpha and s_group,
+    and the next ordinary call on the same workspace must be correct again.
 """
 import ctypes
 import os
@@ -152,7 +152,7 @@ def test_debug_rejects_bad_weight_and_scales(debug_env):
     assert lib.rrs_w4a4_gemm(Xq.data_ptr(), a.data_ptr(), s.data_ptr(), Wq.data_ptr(),
                              beta.data_ptr(), M, N, K, g, Y.data_ptr(), _stream()) == 0
     # the layer: a bad perm, then a valid call
-    ws = torch.empty((rrs.linear_workspace_bytes(M, K, g),), dtype=torch.uint8, device="cuda")
+    ws = torch.zeros((rrs.linear_workspace_bytes(M, K, g),), dtype=torch.uint8, device="cuda")
     assert lib.rrs_linear(X.data_ptr(), Wq.data_ptr(), beta.data_ptr(), M, N, K, g,
                           bad.data_ptr(), Y.data_ptr(), ws.data_ptr(), ws.numel(),
                           _stream()) == PRECONDITION
@@ -182,29 +182,30 @@ def test_debug_rejects_bad_block_order(debug_env):
 
 # ------------------------------------------------------------------ bounded wait
 
-@pytest.mark.parametrize("M", [2, 8, 16])
-@pytest.mark.parametrize("K,g", [(8192, 128), (1024, 64)])
-def test_quant_rows_wait_runs_out_loudly(M, K, g):
+@pytest.mark.parametrize("M,K,g", [(2, 8192, 128), (8, 8192, 128), (15, 1024, 64),
+                                   (300, 4096, 128), (2040, 4096, 128), (40, 1024, 64)])
+def test_one_launch_wait_runs_out_loudly(M, K, g):
+    # per-row kernel up to 16 tokens, fused kernel above (K <= 4096)
     rrs = _rrs()
     w = synth.custom("qw", M, K, 16, g, M + K, n_chan=max(1, K // 100), n_spike=2,
                      spike_mag=(100, 500))
     Xh = synth.activations(w)
     X = to_gpu(Xh)
-    ws = torch.full((rrs.workspace_bytes(M, K, g),), 0x5A, dtype=torch.uint8, device="cuda")
-    print(f"[case] quant rows wait runs out M={M} K={K} g={g}", flush=True)
-    Xq, a, s, n = rrs.quant_rows_wait_hook(X, g, extra_arrivals=1, max_polls=8, workspace=ws)
-    assert n == M, f"{n} waits ran out, expected {M}"
+    ws = torch.zeros((rrs.workspace_bytes(M, K, g),), dtype=torch.uint8, device="cuda")
+    print(f"[case] one-launch wait runs out M={M} K={K} g={g}", flush=True)
+    Xq, a, s, failed = rrs.quant_rows_wait_hook(X, g, extra_rows=1, max_polls=8, workspace=ws)
+    assert failed, "the exchange must report the waits that ran out"
     assert bool(torch.isnan(a).all()), "alpha must be NaN after a failed exchange"
     assert bool(torch.isnan(s).all()), "s_group must be NaN after a failed exchange"
-    # the same kernel with the real target passes, and so does the next
-    # ordinary call on the same workspace
-    Xq, a, s, n = rrs.quant_rows_wait_hook(X, g, extra_arrivals=0, max_polls=1 << 18,
-                                           workspace=ws)
-    assert n == 0
+    # the same kernel with nothing extra to wait for passes, and so does the
+    # next ordinary call on the same workspace
+    Xq, a, s, failed = rrs.quant_rows_wait_hook(X, g, extra_rows=0, max_polls=1 << 18,
+                                                workspace=ws)
+    assert not failed
     act = O.rotate_smooth_quant(Xh, g)
     np.testing.assert_array_equal(to_np(a), act.alpha)
     np.testing.assert_array_equal(to_np(s), act.s)
-    check_codes(to_np(Xq), act, "hook, real target")
+    check_codes(to_np(Xq), act, "hook, nothing extra")
     Xq, a, s = rrs.rotate_smooth_quant(X, g, workspace=ws)
     np.testing.assert_array_equal(to_np(a), act.alpha)
     np.testing.assert_array_equal(to_np(s), act.s)
@@ -229,8 +230,8 @@ def test_quant_rows_hook_argument_checks():
     call = lambda M, extra, polls: lib.rrs_test_quant_rows_wait(  # noqa: E731
         X.data_ptr(), M, 1024, 128, extra, polls, Xq.data_ptr(), a.data_ptr(), s.data_ptr(),
         ws.data_ptr(), ws.numel(), ctypes.byref(n), _stream())
-    assert call(1, 1, 8) == -2       # M outside 2..16
-    assert call(17, 1, 8) == -2
-    assert call(4, -1, 8) == -9      # flags-type argument error
+    assert call(1, 1, 8) == -2       # one row: no one-launch exchange
+    assert call(4, 13, 8) == -9      # more than 16 rows in all for the per-row kernel
+    assert call(4, -1, 8) == -9
     assert call(4, 1, 0) == -9
     assert _untouched(Xq, a, s)

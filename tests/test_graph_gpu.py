@@ -41,11 +41,11 @@ def test_graph_replay_matches_eager(M, K, N, g, reorder):
     X = to_gpu(synth.activations(w))
     Wq, beta = rrs.prepare_weight(to_gpu(synth.weights(w)))
     if reorder:
-        ws = torch.empty((rrs.linear_reorder_workspace_bytes(M, K, g),), dtype=torch.uint8,
+        ws = torch.zeros((rrs.linear_reorder_workspace_bytes(M, K, g),), dtype=torch.uint8,
                          device=X.device)
         call = lambda out: rrs.linear_reorder(X, Wq, beta, g, workspace=ws, out=out)  # noqa: E731
     else:
-        ws = torch.empty((rrs.linear_workspace_bytes(M, K, g),), dtype=torch.uint8,
+        ws = torch.zeros((rrs.linear_workspace_bytes(M, K, g),), dtype=torch.uint8,
                          device=X.device)
         call = lambda out: rrs.linear(X, Wq, beta, g, workspace=ws, out=out)  # noqa: E731
     Y_eager = torch.empty((M, N), dtype=torch.float16, device=X.device)

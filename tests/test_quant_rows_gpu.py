@@ -1,10 +1,11 @@
-"""rrs_rotate_smooth_quant for up to 16 tokens without a static reorder: one
-workgroup per token row, the rows' group maxima exchanged through the
-workspace within the launch. Codes must equal the oracle's (boundary flips
-aside), alpha and s bit for bit, whatever the workspace held before and when
-one workspace serves consecutive calls with different row counts. After a call
-with M > 1 the first two uint32 of the workspace read M rows arrived and no
-wait that ran out."""
+"""rrs_rotate_smooth_quant through its one-launch kernels: one workgroup per
+token row for up to 16 tokens, and the fused kernel (every row rotated once,
+kept in registers) for more tokens at K <= 4096. Both exchange the workgroups'
+group maxima within the launch as epoch-tagged words in the workspace. Codes
+must equal the oracle's (boundary flips aside), alpha and s bit for bit, on a
+zeroed workspace and when one workspace serves consecutive calls of any shape
+and kernel (per-row, fused, two-pass): every exchange advances the epoch in
+header word 0 by one and leaves word 1 (the last failed epoch) at 0."""
 import numpy as np
 import pytest
 
@@ -49,15 +50,18 @@ def _words(ws):
     return ws[:8].view(torch.int32).cpu().tolist()
 
 
+def _zeros(M, K, g):
+    return torch.zeros((_rrs().workspace_bytes(M, K, g),), dtype=torch.uint8, device="cuda")
+
+
 @pytest.mark.parametrize("M", [1, 2, 3, 7, 8, 9, 16])
 @pytest.mark.parametrize("K,g", [(8192, 128), (512, 64), (4096, 512), (16384, 256), (2048, 64)])
 def test_rows_match_oracle(M, K, g):
-    rrs = _rrs()
     print(f"[case] quant rows M={M} K={K} g={g}", flush=True)
-    ws = torch.empty((rrs.workspace_bytes(M, K, g),), dtype=torch.uint8, device="cuda")
+    ws = _zeros(M, K, g)
     _check(_x(M, K, g, 5 * M + K + g), g, ws, f"rows {M}x{K}/g{g}")
-    if M > 1:
-        assert _words(ws) == [M, 0]
+    # one exchange (none for a single row): epoch 0 -> 1, no failure
+    assert _words(ws)[:2] == ([1, 0] if M > 1 else [0, 0])
 
 
 @pytest.mark.parametrize("M", [4, 16])
@@ -65,22 +69,49 @@ def test_rows_without_rotation(M):
     rrs = _rrs()
     K, g = 4096, 128
     print(f"[case] quant rows without rotation M={M}", flush=True)
-    ws = torch.empty((rrs.workspace_bytes(M, K, g),), dtype=torch.uint8, device="cuda")
+    ws = _zeros(M, K, g)
     _check(_x(M, K, g, 31 + M), g, ws, f"rows no-rot M={M}", flags=rrs.SKIP_ROTATION)
-    assert _words(ws) == [M, 0]
+    assert _words(ws)[:2] == [1, 0]
 
 
-def test_rows_garbage_workspace_and_reuse():
-    # Workspace full of 0xFF (count included), then calls with 16, 5, 1 and 12
-    # rows on it: each is checked against the oracle on its own.
+@pytest.mark.parametrize("M,K,g", [(17, 4096, 128), (300, 4096, 64), (2048, 4096, 128),
+                                   (4096, 4096, 128), (3000, 2048, 512), (777, 512, 128),
+                                   (5000, 1024, 256)])
+def test_fused_match_oracle(M, K, g):
+    # more than 16 tokens at K <= 4096: the fused one-launch kernel (one or
+    # two rows per wave; 4096 rows at K = 4096 is its largest single-slot
+    # case, 5000 at K = 1024 takes two slots)
+    print(f"[case] quant fused M={M} K={K} g={g}", flush=True)
+    ws = _zeros(M, K, g)
+    _check(_x(M, K, g, 9 * M + K + g), g, ws, f"fused {M}x{K}/g{g}")
+    assert _words(ws)[:2] == [1, 0]
+
+
+def test_one_workspace_for_every_kernel():
+    # One zeroed workspace for consecutive calls with different shapes and
+    # kernels: per-row (16, 5, 1, 12 tokens), fused (1000 tokens), two-pass
+    # (static reorder: 300 tokens), per-row again. Each call is checked on its
+    # own against the oracle; the epoch counts the exchanges.
     rrs = _rrs()
-    K, g = 8192, 128
-    ws = torch.full((rrs.workspace_bytes(16, K, g),), 255, dtype=torch.uint8, device="cuda")
-    for i, M in enumerate([16, 5, 1, 12]):
-        print(f"[case] quant rows reuse call {i} M={M}", flush=True)
-        _check(_x(M, K, g, 700 + i), g, ws, f"reuse call {i} M={M}")
-        if M > 1:
-            assert _words(ws) == [M, 0]
+    K, g = 4096, 128
+    ws = _zeros(4096, K, g)
+    epoch = 0
+    for i, M in enumerate([16, 5, 1, 12, 1000, 300, 8]):
+        X = _x(M, K, g, 700 + i)
+        if M == 300:
+            perm = synth.permutation(K, 11)
+            print(f"[case] shared workspace call {i}: two-pass M={M}", flush=True)
+            Xq, a, s = rrs.rotate_smooth_quant(to_gpu(X), g, perm=to_gpu(perm), workspace=ws)
+            act = O.rotate_smooth_quant(X, g, perm=perm)
+            np.testing.assert_array_equal(to_np(a), act.alpha)
+            np.testing.assert_array_equal(to_np(s), act.s)
+            check_codes(to_np(Xq), act, f"shared call {i}")
+        else:
+            print(f"[case] shared workspace call {i}: M={M}", flush=True)
+            _check(X, g, ws, f"shared call {i} M={M}")
+            if M > 1:
+                epoch += 1
+        assert _words(ws)[:2] == [epoch, 0], f"call {i}"
 
 
 def test_static_reorder_keeps_the_team_path():
@@ -91,7 +122,7 @@ def test_static_reorder_keeps_the_team_path():
     print(f"[case] quant few tokens with perm M={M}", flush=True)
     X = _x(M, K, g, 77)
     perm = synth.permutation(K, 3)
-    ws = torch.empty((rrs.workspace_bytes(M, K, g),), dtype=torch.uint8, device="cuda")
+    ws = _zeros(M, K, g)
     Xq, a, s = rrs.rotate_smooth_quant(to_gpu(X), g, perm=to_gpu(perm), workspace=ws)
     act = O.rotate_smooth_quant(X, g, perm=perm)
     np.testing.assert_array_equal(to_np(a), act.alpha)
