@@ -477,11 +477,11 @@ def reorder_bench(torch, rrs, synth, reps=50):
         bo = torch.empty((w.K // rrs.REORDER_BLOCK,), dtype=torch.int32, device=dev)
         Y = torch.empty((w.M, w.N), dtype=torch.float16, device=dev)
         qws = torch.zeros((rrs.workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8, device=dev)
-        rws = torch.empty((rrs.reorder_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
+        rws = torch.zeros((rrs.reorder_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
                           device=dev)
         lws = torch.zeros((rrs.linear_workspace_bytes(w.M, w.K, w.g),), dtype=torch.uint8,
                           device=dev)
-        lrws = torch.empty((rrs.linear_reorder_workspace_bytes(w.M, w.K, w.g),),
+        lrws = torch.zeros((rrs.linear_reorder_workspace_bytes(w.M, w.K, w.g),),
                            dtype=torch.uint8, device=dev)
         rrs.rotate_smooth_quant(X, w.g, workspace=qws, out=(Xq, a, s))
         rrs.rotate_smooth_quant_reorder(X, w.g, workspace=rws, out=(Xq2, a2, s2, bo))

@@ -383,8 +383,11 @@ enum { RRS_REORDER_BLOCK = 32 };
 
 /*
  * Bytes of device workspace rrs_rotate_smooth_quant_reorder needs (0 for
- * invalid arguments). It holds up to 256 rows of K/32 block maxima, the
- * sorted group maxima and the channel permutation.
+ * invalid arguments). It holds the one-launch kernel's header and exchanged
+ * block maxima (16 rows of K/32 tagged words), then up to 256 rows of K/32
+ * block maxima for the two-launch path. As for
+ * rrs_workspace_bytes, the workspace must hold zeros before its first use and
+ * may then be reused by later calls (calls sharing one must not overlap).
  */
 size_t rrs_reorder_workspace_bytes(int M, int K, int group_size);
 
@@ -400,7 +403,12 @@ size_t rrs_reorder_workspace_bytes(int M, int K, int group_size);
  * flags: RRS_SKIP_ROTATION (reorder the unrotated channels: Runtime Smooth
  * with its reorder step); RRS_SKIP_SMOOTHING -> RRS_ERR_FLAGS (without
  * smoothing the order changes nothing); RRS_WEIGHT_TILED is accepted and
- * ignored. Three launches.
+ * ignored. Up to 16 tokens at K <= 8192 the call is one launch (one workgroup
+ * per token row; the rows exchange their K/32 block maxima in the workspace
+ * and every workgroup ranks the blocks itself, under the same residency
+ * condition and bounded waits as the one-launch rrs_rotate_smooth_quant,
+ * RRS_ERR_TIMEOUT under RRS_DEBUG); otherwise two launches (block maxima, then
+ * quantization, whose every workgroup ranks the blocks itself).
  */
 rrs_status rrs_rotate_smooth_quant_reorder(const void* X, int M, int K, int group_size,
                                            int flags, void* Xq, float* a_scale,
@@ -426,7 +434,8 @@ rrs_status rrs_w4a4_gemm_reorder(const void* Xq, const float* a_scale, const flo
                                  int group_size, int flags, void* Y, void* stream);
 
 /* Workspace of rrs_linear_reorder: the quantizer's workspace plus Xq,
- * a_scale, s_group and block_order (0 for invalid arguments). */
+ * a_scale, s_group and block_order (0 for invalid arguments). Zero before its
+ * first use, as the quantizer's. */
 size_t rrs_linear_reorder_workspace_bytes(int M, int K, int group_size);
 
 /*

@@ -15,7 +15,7 @@
 
 namespace {
 
-constexpr int kVersion = 600;  // 0.6.0: RRS_DEBUG checks, weight-streaming few-token GEMM
+constexpr int kVersion = 601;  // 0.6.1: one-launch runtime-reorder quantizer for up to 16 tokens
 constexpr int kMaxDevices = 64;
 
 bool is_aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -109,6 +109,23 @@ rrs_status debug_check_quant_wait(int M, int K, int g, const int32_t* perm, int 
                                   const void* workspace, void* stream) {
   const bool rows = rrs::quant_rows_used(M, K, g, perm, flags & kQuantFlags) && M >= 2;
   if (!rows && !rrs::fused_quant_used(M, K, g, perm, flags & kQuantFlags)) return RRS_OK;
+  bool failed = false;
+  if (rrs::quant_exchange_failed(workspace, static_cast<hipStream_t>(stream), &failed) !=
+      hipSuccess) {
+    (void)hipGetLastError();
+    return RRS_ERR_HIP;
+  }
+  if (failed) {
+    std::fprintf(stderr, "[rrs] RRS_DEBUG: a wait between workgroups ran out in the quantizer\n");
+    return RRS_ERR_TIMEOUT;
+  }
+  return RRS_OK;
+}
+
+// The same check for the runtime-reorder quantizer, which is one launch (an
+// exchange between the row workgroups) for up to 16 tokens at K <= 8192.
+rrs_status debug_check_reorder_wait(int M, int K, const void* workspace, void* stream) {
+  if (M < 2 || !rrs::reorder_one_launch(M, K)) return RRS_OK;
   bool failed = false;
   if (rrs::quant_exchange_failed(workspace, static_cast<hipStream_t>(stream), &failed) !=
       hipSuccess) {
@@ -535,10 +552,12 @@ rrs_status rrs_rotate_smooth_quant_reorder(const void* X, int M, int K, int grou
   if (rrs_status s = check_device()) return s;
   if (debug_enabled())
     if (rrs_status s = debug_check_finite_f16(X, (size_t)M * K, "X", stream)) return s;
-  return from_hip(rrs::launch_rotate_smooth_quant_reorder(
+  const rrs_status r = from_hip(rrs::launch_rotate_smooth_quant_reorder(
       static_cast<const uint16_t*>(X), M, K, group_size, flags & RRS_SKIP_ROTATION,
       static_cast<uint8_t*>(Xq), a_scale, s_group, block_order, workspace,
       static_cast<hipStream_t>(stream)));
+  if (r == RRS_OK && debug_enabled()) return debug_check_reorder_wait(M, K, workspace, stream);
+  return r;
 }
 
 rrs_status rrs_w4a4_gemm_reorder(const void* Xq, const float* a_scale, const float* s_group,
@@ -609,10 +628,11 @@ rrs_status rrs_linear_reorder(const void* X, const void* Wq, const float* w_scal
       static_cast<const uint16_t*>(X), M, K, group_size, flags & RRS_SKIP_ROTATION, xq, a, s,
       order, qws, st);
   if (e != hipSuccess) return RRS_ERR_HIP;
-  return from_hip(rrs::launch_w4a4_gemm_reorder(xq, a, s, static_cast<const uint8_t*>(Wq),
-                                                w_scale, order, M, N, K, group_size,
-                                                static_cast<uint16_t*>(Y), out_scale(K, flags),
-                                                st, layout(flags)));
+  const rrs_status r = from_hip(rrs::launch_w4a4_gemm_reorder(
+      xq, a, s, static_cast<const uint8_t*>(Wq), w_scale, order, M, N, K, group_size,
+      static_cast<uint16_t*>(Y), out_scale(K, flags), st, layout(flags)));
+  if (r == RRS_OK && debug_enabled()) return debug_check_reorder_wait(M, K, qws, stream);
+  return r;
 }
 
 rrs_status rrs_test_quant_rows_wait(const void* X, int M, int K, int group_size,

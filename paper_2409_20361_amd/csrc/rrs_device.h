@@ -248,6 +248,74 @@ __device__ __forceinline__ uint32_t quant_pack8(const float* v, float m) {
 }
 
 // Store E/2 packed bytes (E nibbles, low nibble = even index) at dst.
+// ---------------------------------------------------------------------------
+// Runtime reorder (Fig. 4 step (1) at run time), computed by every workgroup
+// of the quantizer's second pass: the key of block b (32 consecutive
+// channels) is the largest of the nrows partial rows part[r][b] (r < nrows,
+// NB = K / 32 entries per row); keys are ranked largest first, equal keys in
+// increasing block index. On return (after a barrier) sblk[p] is the block at
+// sorted position p and skey[p] its key. `red` holds at least 4 NT floats.
+// All NT threads of the workgroup must call it.
+// ---------------------------------------------------------------------------
+template <int NT, int NB>
+__device__ __forceinline__ void block_order_wg(const float* __restrict__ part, int nrows,
+                                               float* red, float* key, int* sblk, float* skey,
+                                               int tid) {
+  static_assert(NB % 4 == 0 && NB / 4 <= NT, "float4 columns, one per thread at least");
+  constexpr int NQ = NB / 4;   // float4 columns of a partial row
+  constexpr int NS = NT / NQ;  // row slices
+  const int qd = tid % NQ;
+  const int sl = tid / NQ;
+  float4 m = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  if (sl < NS) {
+    int i = sl;
+    // eight independent loads at a time so their latencies overlap
+    for (; i + 7 * NS < nrows; i += 8 * NS) {
+      float4 x[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) x[u] = reinterpret_cast<const float4*>(part + (size_t)(i + u * NS) * NB)[qd];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        m.x = fmaxf(m.x, x[u].x);
+        m.y = fmaxf(m.y, x[u].y);
+        m.z = fmaxf(m.z, x[u].z);
+        m.w = fmaxf(m.w, x[u].w);
+      }
+    }
+    for (; i < nrows; i += NS) {
+      const float4 x = reinterpret_cast<const float4*>(part + (size_t)i * NB)[qd];
+      m.x = fmaxf(m.x, x.x);
+      m.y = fmaxf(m.y, x.y);
+      m.z = fmaxf(m.z, x.z);
+      m.w = fmaxf(m.w, x.w);
+    }
+    reinterpret_cast<float4*>(red)[sl * NQ + qd] = m;
+  }
+  __syncthreads();
+  for (int b = tid; b < NB; b += NT) {
+    float k = red[b];
+    for (int q = 1; q < NS; ++q) k = fmaxf(k, red[q * NB + b]);
+    key[b] = k;
+  }
+  __syncthreads();
+  for (int b = tid; b < NB; b += NT) {
+    const float c = key[b];
+    int rank = 0;
+#pragma unroll 4
+    for (int q = 0; q < NB / 4; ++q) {
+      const float4 k4 = reinterpret_cast<const float4*>(key)[q];
+      const int j = 4 * q;
+      rank += (k4.x > c || (k4.x == c && j < b)) ? 1 : 0;
+      rank += (k4.y > c || (k4.y == c && j + 1 < b)) ? 1 : 0;
+      rank += (k4.z > c || (k4.z == c && j + 2 < b)) ? 1 : 0;
+      rank += (k4.w > c || (k4.w == c && j + 3 < b)) ? 1 : 0;
+    }
+    sblk[rank] = b;
+    skey[rank] = c;
+  }
+  __syncthreads();
+}
+
 template <int E>
 __device__ __forceinline__ void store_nibbles(uint8_t* __restrict__ dst, const uint32_t (&nib)[E]) {
   if constexpr (E >= 8) {

@@ -162,15 +162,19 @@ hipError_t launch_block_maxima(const uint16_t* X, int M, int K, bool rotate, flo
                                int* nrows, hipStream_t stream);
 hipError_t launch_block_maxima_wave(const uint16_t* X, int M, int K, bool rotate, float* part,
                                     int max_partials, int* nrows, hipStream_t stream);
-hipError_t launch_quantize_given_maxima(const uint16_t* X, int M, int K, int g,
-                                        const int32_t* perm, bool rotate, const float* gmax,
+// Runtime reorder, second pass: every workgroup ranks the K/32 blocks from the
+// nrows rows of block maxima in `part` itself, then quantizes its rows over
+// the sorted positions; workgroup 0 writes s_group and block_order.
+hipError_t launch_quantize_ordered(const uint16_t* X, int M, int K, int g, bool rotate,
+                                   const float* part, int nrows, uint8_t* Xq, float* a_scale,
+                                   float* s_group, int32_t* block_order, hipStream_t stream);
+hipError_t launch_quantize_ordered_wave(const uint16_t* X, int M, int K, int g, bool rotate,
+                                        const float* part, int nrows, int max_quant_wgs,
                                         uint8_t* Xq, float* a_scale, float* s_group,
-                                        hipStream_t stream);
-hipError_t launch_quantize_given_wave(const uint16_t* X, int M, int K, int g,
-                                      const int32_t* perm, bool rotate, const float* gmax,
-                                      int max_quant_wgs, uint8_t* Xq, float* a_scale,
-                                      float* s_group, hipStream_t stream);
+                                        int32_t* block_order, hipStream_t stream);
 size_t reorder_workspace_bytes(int K);
+// Whether the runtime-reorder quantizer is the one-launch per-row kernel.
+bool reorder_one_launch(int M, int K);
 hipError_t launch_rotate_smooth_quant_reorder(const uint16_t* X, int M, int K, int g, int flags,
                                               uint8_t* Xq, float* a_scale, float* s_group,
                                               int32_t* block_order, void* workspace,
@@ -203,6 +207,15 @@ hipError_t launch_quant_rows(const uint16_t* X, int M, int K, int g, bool rotate
                              int extra_rows = 0, int max_polls = 0);
 // Whether launch_rotate_smooth_quant takes the per-row kernel for this call.
 bool quant_rows_used(int M, int K, int g, const int32_t* perm, int flags);
+// The per-row kernel with the runtime reorder (up to 16 rows, K <= 8192): the
+// rows exchange their K/32 block maxima and every workgroup ranks the blocks
+// itself (one launch instead of block maxima, order and given-maxima passes).
+// Uses the header and quant_rows_reorder_workspace_bytes(K) bytes in all.
+bool quant_rows_reorder_fits(int M, int K);
+size_t quant_rows_reorder_workspace_bytes(int K);
+hipError_t launch_quant_rows_reorder(const uint16_t* X, int M, int K, int g, bool rotate,
+                                     uint8_t* Xq, float* a_scale, float* s_group,
+                                     int32_t* block_order, void* workspace, hipStream_t stream);
 // Waits for `stream` and reports whether the latest one-launch exchange in
 // this workspace (per-row or fused kernel) had a wait that ran out.
 hipError_t quant_exchange_failed(const void* workspace, hipStream_t stream, bool* failed);

@@ -169,19 +169,29 @@ __global__ __launch_bounds__(Teams<K>::threads) void rot_max_kernel(
 // ---------------------------------------------------------------------------
 // 2. group scales, per-token scale, codes
 // ---------------------------------------------------------------------------
-template <int K, bool kRot, bool kSmooth>
+// kOrder (runtime reorder): gpart holds nparts rows of K/32 block maxima; the
+// workgroup ranks the blocks itself (block_order_wg), takes s_b over the
+// sorted blocks of group b and reads position j from channel
+// 32 sblk[j / 32] + j % 32; workgroup 0 writes s_group and block_order.
+template <int K, bool kRot, bool kSmooth, bool kOrder = false>
 __global__ __launch_bounds__(Teams<K>::threads) void quant_kernel(
     const uint16_t* __restrict__ X, int M, int g, int rows_per_wg, int nparts,
     const int32_t* __restrict__ perm, const float* __restrict__ gpart,
-    uint8_t* __restrict__ Xq, float* __restrict__ a_scale, float* __restrict__ s_group) {
+    uint8_t* __restrict__ Xq, float* __restrict__ a_scale, float* __restrict__ s_group,
+    int32_t* __restrict__ block_order = nullptr) {
   using S = FwhtShape<K>;
   constexpr int E = S::E;
   constexpr int RF = lds_row_floats(K);
   constexpr int kTeams = Teams<K>::n;
   constexpr int kThreads = Teams<K>::threads;
-  __shared__ float slots[slot_floats<K>()];
+  constexpr int NB = K / kReorderBlock;
+  __shared__ __attribute__((aligned(16))) float slots[slot_floats<K>()];
   __shared__ float rg[256];
   __shared__ float red[16];
+  __shared__ __attribute__((aligned(16))) float key[kOrder ? NB : 4];
+  __shared__ float skey[kOrder ? NB : 1];
+  __shared__ int sblk[kOrder ? NB : 1];
+  __shared__ __attribute__((aligned(16))) float ored[kOrder ? 4 * kThreads : 4];
   float* cbuf = slots;  // reduction scratch before the rows start
   const int tid = threadIdx.x;
   const int team = tid >> 8;
@@ -203,6 +213,18 @@ __global__ __launch_bounds__(Teams<K>::threads) void quant_kernel(
       rg[tid] = 1.0f;
       if (blockIdx.x == 0) s_group[tid] = 1.0f;
     }
+    __syncthreads();
+  } else if constexpr (kOrder) {
+    block_order_wg<kThreads, NB>(gpart, nparts, ored, key, sblk, skey, tid);
+    if (tid < G) {
+      const int per = g / kReorderBlock;
+      float s = 0.0f;
+      for (int u = 0; u < per; ++u) s = fmaxf(s, skey[tid * per + u]);
+      rg[tid] = (s == 0.0f) ? 0.0f : __fdiv_rn(1.0f, s);
+      if (blockIdx.x == 0) s_group[tid] = s;
+    }
+    if (blockIdx.x == 0)
+      for (int b = tid; b < NB; b += kThreads) block_order[b] = sblk[b];
     __syncthreads();
   } else {
     // s_b = max over the partial rows; threads split (group, row slice) and
@@ -234,7 +256,13 @@ __global__ __launch_bounds__(Teams<K>::threads) void quant_kernel(
   }
   int src[E];  // position t*E + e of the reordered row reads channel src[e]
 #pragma unroll
-  for (int e = 0; e < E; ++e) src[e] = perm ? perm[t * E + e] : t * E + e;
+  for (int e = 0; e < E; ++e) {
+    const int j = t * E + e;
+    if constexpr (kOrder)  // masked into range, whatever the partial rows held
+      src[e] = (sblk[j / kReorderBlock] & (NB - 1)) * kReorderBlock + j % kReorderBlock;
+    else
+      src[e] = perm ? perm[j] : j;
+  }
   const float rb = rg[(t * E) / g];  // this thread's positions lie in one group
 
   for (int it = 0; it < iters; ++it) {
@@ -549,17 +577,17 @@ hipError_t launch_block_max_k(const uint16_t* X, int M, bool rot, float* part, i
 
 // Runtime reorder, pass 2: quant with one given row of group maxima.
 template <int K>
-hipError_t launch_given_k(const uint16_t* X, int M, int g, const int32_t* perm, bool rot,
-                          const float* gmax, uint8_t* Xq, float* a_scale, float* s_group,
-                          hipStream_t stream) {
+hipError_t launch_ordered_k(const uint16_t* X, int M, int g, bool rot, const float* part,
+                            int nrows, uint8_t* Xq, float* a_scale, float* s_group,
+                            int32_t* block_order, hipStream_t stream) {
   int rpw = 0;
   const int wgs = split_rows<K>(M, 4 * num_cus(), &rpw);
   if (rot)
-    quant_kernel<K, true, true><<<wgs, Teams<K>::threads, 0, stream>>>(
-        X, M, g, rpw, 1, perm, gmax, Xq, a_scale, s_group);
+    quant_kernel<K, true, true, true><<<wgs, Teams<K>::threads, 0, stream>>>(
+        X, M, g, rpw, nrows, nullptr, part, Xq, a_scale, s_group, block_order);
   else
-    quant_kernel<K, false, true><<<wgs, Teams<K>::threads, 0, stream>>>(
-        X, M, g, rpw, 1, perm, gmax, Xq, a_scale, s_group);
+    quant_kernel<K, false, true, true><<<wgs, Teams<K>::threads, 0, stream>>>(
+        X, M, g, rpw, nrows, nullptr, part, Xq, a_scale, s_group, block_order);
   return hipGetLastError();
 }
 
@@ -583,21 +611,23 @@ hipError_t launch_block_maxima(const uint16_t* X, int M, int K, bool rotate, flo
   }
 }
 
-hipError_t launch_quantize_given_maxima(const uint16_t* X, int M, int K, int g,
-                                        const int32_t* perm, bool rotate, const float* gmax,
-                                        uint8_t* Xq, float* a_scale, float* s_group,
-                                        hipStream_t stream) {
+hipError_t launch_quantize_ordered(const uint16_t* X, int M, int K, int g, bool rotate,
+                                   const float* part, int nrows, uint8_t* Xq, float* a_scale,
+                                   float* s_group, int32_t* block_order, hipStream_t stream) {
   if (use_wave_kernels(M, K))
-    return launch_quantize_given_wave(X, M, K, g, perm, rotate, gmax, 2 * num_cus(), Xq,
-                                      a_scale, s_group, stream);
+    return launch_quantize_ordered_wave(X, M, K, g, rotate, part, nrows, 2 * num_cus(), Xq,
+                                        a_scale, s_group, block_order, stream);
+#define RRS_ORD_K(K_) \
+  launch_ordered_k<K_>(X, M, g, rotate, part, nrows, Xq, a_scale, s_group, block_order, stream)
   switch (K) {
-    case 512: return launch_given_k<512>(X, M, g, perm, rotate, gmax, Xq, a_scale, s_group, stream);
-    case 1024: return launch_given_k<1024>(X, M, g, perm, rotate, gmax, Xq, a_scale, s_group, stream);
-    case 2048: return launch_given_k<2048>(X, M, g, perm, rotate, gmax, Xq, a_scale, s_group, stream);
-    case 8192: return launch_given_k<8192>(X, M, g, perm, rotate, gmax, Xq, a_scale, s_group, stream);
-    case 16384: return launch_given_k<16384>(X, M, g, perm, rotate, gmax, Xq, a_scale, s_group, stream);
+    case 512: return RRS_ORD_K(512);
+    case 1024: return RRS_ORD_K(1024);
+    case 2048: return RRS_ORD_K(2048);
+    case 8192: return RRS_ORD_K(8192);
+    case 16384: return RRS_ORD_K(16384);
     default: return hipErrorInvalidValue;
   }
+#undef RRS_ORD_K
 }
 
 int block_maxima_rows() { return kMaxPartialRows; }

@@ -30,21 +30,36 @@ namespace {
 constexpr int kMaxRows = 16;
 constexpr int kMaxPolls = 1 << 18;
 
-template <int K, bool kRot>
+// kReorder (runtime reorder, K <= 8192): the rows exchange their K/32 block
+// maxima instead of their group maxima; every workgroup then ranks the blocks
+// (keys largest first, equal keys in increasing block index), takes s_b over
+// the sorted blocks of group b, and quantizes its row with the blocks in that
+// order; workgroup 0 also writes block_order. The same order, scales and
+// codes as the three-launch path (block maxima, order, given-maxima pass).
+template <int K, bool kRot, bool kReorder>
 __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
     const uint16_t* __restrict__ X, int M, int g, uint8_t* __restrict__ Xq,
-    float* __restrict__ a_scale, float* __restrict__ s_group, uint32_t* header,
-    unsigned long long* tagged, int nrows, int max_polls) {
+    float* __restrict__ a_scale, float* __restrict__ s_group, int32_t* __restrict__ block_order,
+    uint32_t* header, unsigned long long* tagged, int nrows, int max_polls) {
   constexpr int E = FwhtShape<K>::E;  // this thread's channels: t + 256 e after the FWHT
+  constexpr int C = E < kReorderBlock ? E : kReorderBlock;  // positions per chunk maximum
+  constexpr int CH = E / C;                                 // chunks per thread (1 or 2)
+  constexpr int NB = K / kReorderBlock;
+  static_assert(!kReorder || NB <= kRowThreads, "one block key per thread");
   __shared__ float slot[lds_row_floats(K)];
-  __shared__ float red[kRowThreads];
+  __shared__ float red[kRowThreads * CH];
   __shared__ float rg[256];
   __shared__ float sg[256];
+  __shared__ __attribute__((aligned(16))) float key[kReorder ? NB : 4];
+  __shared__ float skey[kReorder ? NB : 1];
+  __shared__ int sblk[kReorder ? NB : 1];
   __shared__ int missed;
   __shared__ uint32_t tag_lds;
   const int t = threadIdx.x;
   const int p = blockIdx.x;
   const int G = K / g;
+  const int span = kReorder ? kReorderBlock : g;  // positions per exchanged word
+  const int W = K / span;                         // words per row
   // This call's tag (the header was written by earlier calls only): one
   // thread requests it now and hands it over in LDS after the rotation, so
   // the load's latency hides behind it.
@@ -61,34 +76,38 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
   }
   __syncthreads();                // slot is free again
 
-  // This row's group maxima: thread t takes positions t E .. t E + E - 1, all
-  // in one group (E <= 64 <= g).
+  // This row's maxima of the exchanged spans (groups of g channels, or blocks
+  // of 32 with the runtime reorder): thread t takes positions t E .. t E + E - 1
+  // as CH chunks of C, each inside one span (C <= 32 <= span).
 #pragma unroll
   for (int e = 0; e < E; ++e) slot[lds_pad(t + e * kRowThreads)] = fabsf(v[e]);
   __syncthreads();
-  float pm = 0.0f;
 #pragma unroll
-  for (int e = 0; e < E; ++e) pm = fmaxf(pm, slot[lds_pad(t * E + e)]);
-  red[t] = pm;
-  __syncthreads();
-  float gm = 0.0f;  // this row's maximum of group t (t < G)
-  if (t < G) {
-    const int per = g / E;  // threads per group
-    for (int u = 0; u < per; ++u) gm = fmaxf(gm, red[t * per + u]);
+  for (int k = 0; k < CH; ++k) {
+    float pm = 0.0f;
+#pragma unroll
+    for (int e = 0; e < C; ++e) pm = fmaxf(pm, slot[lds_pad(t * E + k * C + e)]);
+    red[t * CH + k] = pm;
   }
-  // s_b = max over the rows, r_b = fl(1 / s_b). With more than one row, every
-  // row's maxima are exchanged: thread t < G publishes group t of this row and
-  // reads group t of all nrows rows (all words requested at once, those not
-  // yet tagged requested again, within max_polls rounds).
+  __syncthreads();
+  float wm = 0.0f;  // this row's maximum of span t (t < W)
+  if (t < W) {
+    const int per = span / C;  // chunks per span
+    for (int u = 0; u < per; ++u) wm = fmaxf(wm, red[t * per + u]);
+  }
+  // Maxima over the rows. With more than one row, every row's maxima are
+  // exchanged: thread t < W publishes span t of this row and reads span t of
+  // all nrows rows (all words requested at once, those not yet tagged
+  // requested again, within max_polls rounds).
   const uint32_t tag = tag_lds;  // set before the barrier after the rotation
-  if (t < G) {
-    float s = gm;
+  if (t < W) {
+    float s = wm;
     if (M > 1) {
-      publish_tagged(tagged + (size_t)p * G + t, tag, gm);
+      publish_tagged(tagged + (size_t)p * W + t, tag, wm);
       unsigned long long x[kMaxRows];
 #pragma unroll
       for (int i = 0; i < kMaxRows; ++i)
-        x[i] = i < nrows ? load_tagged(tagged + (size_t)i * G + t) : ((unsigned long long)tag << 32);
+        x[i] = i < nrows ? load_tagged(tagged + (size_t)i * W + t) : ((unsigned long long)tag << 32);
       bool ok = false;
       for (int round = 0;; ++round) {
         ok = true;
@@ -98,17 +117,51 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
         __builtin_amdgcn_s_sleep(1);
 #pragma unroll
         for (int i = 0; i < kMaxRows; ++i)
-          if (i < nrows && !has_tag(x[i], tag)) x[i] = load_tagged(tagged + (size_t)i * G + t);
+          if (i < nrows && !has_tag(x[i], tag)) x[i] = load_tagged(tagged + (size_t)i * W + t);
       }
       if (!ok) missed = 1;  // benign race: every writer writes 1
       s = 0.0f;
 #pragma unroll
       for (int i = 0; i < kMaxRows; ++i) s = fmaxf(s, __uint_as_float((uint32_t)x[i]));
     }
-    rg[t] = (s == 0.0f) ? 0.0f : __fdiv_rn(1.0f, s);
-    sg[t] = s;
+    if constexpr (kReorder) {
+      key[t] = s;  // block t's key: its largest channel maximum
+    } else {
+      rg[t] = (s == 0.0f) ? 0.0f : __fdiv_rn(1.0f, s);  // s_b and r_b = fl(1 / s_b)
+      sg[t] = s;
+    }
   }
   __syncthreads();
+  if constexpr (kReorder) {
+    // Rank of block t: blocks with a larger key, or an equal key and a smaller
+    // index, come first (broadcast LDS reads).
+    if (t < NB) {
+      const float c = key[t];
+      int rank = 0;
+#pragma unroll 4
+      for (int q = 0; q < NB / 4; ++q) {
+        const float4 k4 = reinterpret_cast<const float4*>(key)[q];
+        const int b = 4 * q;
+        rank += (k4.x > c || (k4.x == c && b < t)) ? 1 : 0;
+        rank += (k4.y > c || (k4.y == c && b + 1 < t)) ? 1 : 0;
+        rank += (k4.z > c || (k4.z == c && b + 2 < t)) ? 1 : 0;
+        rank += (k4.w > c || (k4.w == c && b + 3 < t)) ? 1 : 0;
+      }
+      sblk[rank] = t;
+      skey[rank] = c;
+    }
+    __syncthreads();
+    // s_b over the sorted blocks of group b.
+    if (t < G) {
+      const int per = g / kReorderBlock;
+      float s = 0.0f;
+      for (int u = 0; u < per; ++u) s = fmaxf(s, skey[t * per + u]);
+      rg[t] = (s == 0.0f) ? 0.0f : __fdiv_rn(1.0f, s);
+      sg[t] = s;
+    }
+    if (p == 0 && t < NB) block_order[t] = sblk[t];
+    __syncthreads();
+  }
   const bool failed = missed != 0;  // uniform over the workgroup
   if (M > 1 && t == 0) {
     // Every word of the call has been read (or given up on): advance the epoch
@@ -126,8 +179,20 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
 #pragma unroll
   for (int e = 0; e < E; ++e) slot[lds_pad(t + e * kRowThreads)] = v[e];
   __syncthreads();
+  if constexpr (kReorder) {
+    // position j takes channel 32 sblk[j / 32] + j % 32 (masked into range:
+    // with keys read from a workspace that was not zeroed, ranks could collide
+    // and leave entries unset)
 #pragma unroll
-  for (int e = 0; e < E; ++e) v[e] = slot[lds_pad(t * E + e)];
+    for (int e = 0; e < E; ++e) {
+      const int j = t * E + e;
+      const int b = sblk[j / kReorderBlock] & (NB - 1);
+      v[e] = slot[lds_pad(b * kReorderBlock + j % kReorderBlock)];
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < E; ++e) v[e] = slot[lds_pad(t * E + e)];
+  }
   float lm = 0.0f;
 #pragma unroll
   for (int e = 0; e < E; ++e) lm = fmaxf(lm, fabsf(v[e]));
@@ -144,16 +209,16 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
   if (t == 0) a_scale[p] = failed ? __builtin_nanf("") : __fdiv_rn(a, 7.0f);
 }
 
-template <int K>
+template <int K, bool kReorder>
 hipError_t launch_k(const uint16_t* X, int M, int g, bool rotate, uint8_t* Xq, float* a_scale,
-                    float* s_group, uint32_t* header, unsigned long long* tagged, int nrows,
-                    int max_polls, hipStream_t stream) {
+                    float* s_group, int32_t* block_order, uint32_t* header,
+                    unsigned long long* tagged, int nrows, int max_polls, hipStream_t stream) {
   if (rotate)
-    quant_rows_kernel<K, true><<<M, kRowThreads, 0, stream>>>(X, M, g, Xq, a_scale, s_group,
-                                                              header, tagged, nrows, max_polls);
+    quant_rows_kernel<K, true, kReorder><<<M, kRowThreads, 0, stream>>>(
+        X, M, g, Xq, a_scale, s_group, block_order, header, tagged, nrows, max_polls);
   else
-    quant_rows_kernel<K, false><<<M, kRowThreads, 0, stream>>>(X, M, g, Xq, a_scale, s_group,
-                                                               header, tagged, nrows, max_polls);
+    quant_rows_kernel<K, false, kReorder><<<M, kRowThreads, 0, stream>>>(
+        X, M, g, Xq, a_scale, s_group, block_order, header, tagged, nrows, max_polls);
   return hipGetLastError();
 }
 
@@ -165,6 +230,33 @@ size_t quant_rows_workspace_bytes(int K, int g) {
   return kQuantHeaderBytes + align256((size_t)kMaxRows * (K / g) * 8);
 }
 
+bool quant_rows_reorder_fits(int M, int K) { return quant_rows_fits(M) && K <= 8192; }
+
+size_t quant_rows_reorder_workspace_bytes(int K) {
+  return kQuantHeaderBytes + align256((size_t)kMaxRows * (K / kReorderBlock) * 8);
+}
+
+hipError_t launch_quant_rows_reorder(const uint16_t* X, int M, int K, int g, bool rotate,
+                                     uint8_t* Xq, float* a_scale, float* s_group,
+                                     int32_t* block_order, void* workspace, hipStream_t stream) {
+  if (!quant_rows_reorder_fits(M, K)) return hipErrorInvalidValue;
+  uint32_t* header = static_cast<uint32_t*>(workspace);
+  unsigned long long* tagged =
+      reinterpret_cast<unsigned long long*>(static_cast<char*>(workspace) + kQuantHeaderBytes);
+#define RRS_ROWS_R(K_)                                                                      \
+  launch_k<K_, true>(X, M, g, rotate, Xq, a_scale, s_group, block_order, header, tagged, M, \
+                     kMaxPolls, stream)
+  switch (K) {
+    case 512: return RRS_ROWS_R(512);
+    case 1024: return RRS_ROWS_R(1024);
+    case 2048: return RRS_ROWS_R(2048);
+    case 4096: return RRS_ROWS_R(4096);
+    case 8192: return RRS_ROWS_R(8192);
+    default: return hipErrorInvalidValue;
+  }
+#undef RRS_ROWS_R
+}
+
 hipError_t launch_quant_rows(const uint16_t* X, int M, int K, int g, bool rotate, uint8_t* Xq,
                              float* a_scale, float* s_group, void* workspace, hipStream_t stream,
                              int extra_rows, int max_polls) {
@@ -174,8 +266,9 @@ hipError_t launch_quant_rows(const uint16_t* X, int M, int K, int g, bool rotate
   const int nrows = M + extra_rows;  // rows of maxima the readers wait for
   if (nrows > kMaxRows) return hipErrorInvalidValue;
   const int polls = max_polls > 0 ? max_polls : kMaxPolls;
-#define RRS_ROWS_K(K_) \
-  launch_k<K_>(X, M, g, rotate, Xq, a_scale, s_group, header, tagged, nrows, polls, stream)
+#define RRS_ROWS_K(K_)                                                                   \
+  launch_k<K_, false>(X, M, g, rotate, Xq, a_scale, s_group, nullptr, header, tagged, nrows, \
+                      polls, stream)
   switch (K) {
     case 512: return RRS_ROWS_K(512);
     case 1024: return RRS_ROWS_K(1024);

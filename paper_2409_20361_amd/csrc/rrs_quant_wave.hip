@@ -178,17 +178,26 @@ __global__ __launch_bounds__(kRotWaves * 64) void rot_max_wave_kernel(
 // ---------------------------------------------------------------------------
 constexpr int kQuantWaves = 4;
 
-template <int K, bool kRot, bool kSmooth>
+// kOrder (runtime reorder): gpart holds nparts rows of K/32 block maxima; the
+// workgroup ranks the blocks itself (block_order_wg), takes s_b over the
+// sorted blocks of group b, and reads position j of a row from channel
+// 32 sblk[j / 32] + j % 32; workgroup 0 writes s_group and block_order.
+template <int K, bool kRot, bool kSmooth, bool kOrder = false>
 __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
     const uint16_t* __restrict__ X, int M, int g, int rows_per_wg, int nparts,
     const int32_t* __restrict__ perm, const float* __restrict__ gpart,
-    uint8_t* __restrict__ Xq, float* __restrict__ a_scale, float* __restrict__ s_group) {
+    uint8_t* __restrict__ Xq, float* __restrict__ a_scale, float* __restrict__ s_group,
+    int32_t* __restrict__ block_order = nullptr) {
   using S = WaveRow<K>;
   constexpr int NT = kQuantWaves * 64;
   constexpr int GMAX = K / 64;  // groups at g = 64
+  constexpr int NB = K / kReorderBlock;
   __shared__ __attribute__((aligned(16))) float rows[kQuantWaves * S::RW * S::RF];
   __shared__ float rg[GMAX];
-  __shared__ float red[NT];
+  __shared__ __attribute__((aligned(16))) float red[kOrder ? 4 * NT : NT];
+  __shared__ __attribute__((aligned(16))) float key[kOrder ? NB : 4];
+  __shared__ float skey[kOrder ? NB : 1];
+  __shared__ int sblk[kOrder ? NB : 1];
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -220,8 +229,8 @@ __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
   // latency.
   constexpr int NS = NT / GMAX;
   constexpr int NL = (256 + NS - 1) / NS;  // loads per thread for up to 256 rows
-  float x[kSmooth ? NL : 1];
-  if constexpr (kSmooth) {
+  float x[kSmooth && !kOrder ? NL : 1];
+  if constexpr (kSmooth && !kOrder) {
     const int b = tid % GMAX;
     const int sl = tid / GMAX;
 #pragma unroll
@@ -250,6 +259,18 @@ __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
       if (blockIdx.x == 0) s_group[tid] = 1.0f;
     }
     __syncthreads();
+  } else if constexpr (kOrder) {
+    block_order_wg<NT, NB>(gpart, nparts, red, key, sblk, skey, tid);
+    if (tid < G) {
+      const int per = g / kReorderBlock;
+      float sv = 0.0f;
+      for (int u = 0; u < per; ++u) sv = fmaxf(sv, skey[tid * per + u]);
+      rg[tid] = (sv == 0.0f) ? 0.0f : __fdiv_rn(1.0f, sv);
+      if (blockIdx.x == 0) s_group[tid] = sv;
+    }
+    if (blockIdx.x == 0)
+      for (int b = tid; b < NB; b += NT) block_order[b] = sblk[b];
+    __syncthreads();
   } else {
     float m = 0.0f;
 #pragma unroll
@@ -274,7 +295,17 @@ __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
     // back to layout 1 through LDS, with the static reorder applied
 #pragma unroll
     for (int e = 0; e < 64; ++e) row[lds_a(l + S::R * e)] = v[e];
-    if (perm) {
+    if constexpr (kOrder) {
+      // positions 64 l .. 64 l + 63 are blocks 2 l and 2 l + 1 (masked into
+      // range, as the team kernels do)
+      const int c0 = (sblk[2 * l] & (NB - 1)) * kReorderBlock;
+      const int c1 = (sblk[2 * l + 1] & (NB - 1)) * kReorderBlock;
+#pragma unroll
+      for (int e = 0; e < 32; ++e) {
+        v[e] = row[lds_a(c0 + e)];
+        v[32 + e] = row[lds_a(c1 + e)];
+      }
+    } else if (perm) {
       const int4* pp = reinterpret_cast<const int4*>(perm + 64 * l);
 #pragma unroll
       for (int m = 0; m < 16; ++m) {
@@ -575,20 +606,20 @@ hipError_t launch_block_max_wave(const uint16_t* X, int M, bool rot, float* part
   return hipGetLastError();
 }
 
-// Runtime reorder, pass 2: quant with one given row of group maxima. The
-// kernel reads K / 64 entries of that row (those past K / g are ignored).
+// Runtime reorder, pass 2: every workgroup orders the blocks from the nrows
+// rows of block maxima itself, then quantizes its rows.
 template <int K>
-hipError_t launch_given_wave(const uint16_t* X, int M, int g, const int32_t* perm, bool rot,
-                             const float* gmax, int max_quant_wgs, uint8_t* Xq, float* a_scale,
-                             float* s_group, hipStream_t stream) {
+hipError_t launch_ordered_wave(const uint16_t* X, int M, int g, bool rot, const float* part,
+                               int nrows, int max_quant_wgs, uint8_t* Xq, float* a_scale,
+                               float* s_group, int32_t* block_order, hipStream_t stream) {
   int rpw = 0;
   const int wgs = wave_split<K>(M, kQuantWaves, max_quant_wgs, &rpw);
   if (rot)
-    quant_wave_kernel<K, true, true><<<wgs, kQuantWaves * 64, 0, stream>>>(
-        X, M, g, rpw, 1, perm, gmax, Xq, a_scale, s_group);
+    quant_wave_kernel<K, true, true, true><<<wgs, kQuantWaves * 64, 0, stream>>>(
+        X, M, g, rpw, nrows, nullptr, part, Xq, a_scale, s_group, block_order);
   else
-    quant_wave_kernel<K, false, true><<<wgs, kQuantWaves * 64, 0, stream>>>(
-        X, M, g, rpw, 1, perm, gmax, Xq, a_scale, s_group);
+    quant_wave_kernel<K, false, true, true><<<wgs, kQuantWaves * 64, 0, stream>>>(
+        X, M, g, rpw, nrows, nullptr, part, Xq, a_scale, s_group, block_order);
   return hipGetLastError();
 }
 
@@ -605,17 +636,21 @@ hipError_t launch_block_maxima_wave(const uint16_t* X, int M, int K, bool rotate
   }
 }
 
-hipError_t launch_quantize_given_wave(const uint16_t* X, int M, int K, int g,
-                                      const int32_t* perm, bool rotate, const float* gmax,
-                                      int max_quant_wgs, uint8_t* Xq, float* a_scale,
-                                      float* s_group, hipStream_t stream) {
+hipError_t launch_quantize_ordered_wave(const uint16_t* X, int M, int K, int g, bool rotate,
+                                        const float* part, int nrows, int max_quant_wgs,
+                                        uint8_t* Xq, float* a_scale, float* s_group,
+                                        int32_t* block_order, hipStream_t stream) {
+#define RRS_ORD_W(K_)                                                                     \
+  launch_ordered_wave<K_>(X, M, g, rotate, part, nrows, max_quant_wgs, Xq, a_scale, s_group, \
+                          block_order, stream)
   switch (K) {
-    case 512: return launch_given_wave<512>(X, M, g, perm, rotate, gmax, max_quant_wgs, Xq, a_scale, s_group, stream);
-    case 1024: return launch_given_wave<1024>(X, M, g, perm, rotate, gmax, max_quant_wgs, Xq, a_scale, s_group, stream);
-    case 2048: return launch_given_wave<2048>(X, M, g, perm, rotate, gmax, max_quant_wgs, Xq, a_scale, s_group, stream);
-    case 4096: return launch_given_wave<4096>(X, M, g, perm, rotate, gmax, max_quant_wgs, Xq, a_scale, s_group, stream);
+    case 512: return RRS_ORD_W(512);
+    case 1024: return RRS_ORD_W(1024);
+    case 2048: return RRS_ORD_W(2048);
+    case 4096: return RRS_ORD_W(4096);
     default: return hipErrorInvalidValue;
   }
+#undef RRS_ORD_W
 }
 
 bool fused_quant_fits(int M, int K, int max_wgs) {

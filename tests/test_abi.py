@@ -377,8 +377,9 @@ def test_reorder_workspace_queries():
     a256 = lambda x: (x + 255) // 256 * 256  # noqa: E731
     for M, K, g in ((16, 512, 128), (2048, 4096, 128), (8, 8192, 64), (3, 16384, 512)):
         q = lib.rrs_reorder_workspace_bytes(M, K, g)
-        # 256 rows of K/32 block maxima, max(K/64, 64) group maxima, K permutation entries
-        assert q == a256(256 * (K // 32) * 4) + a256(4 * max(K // 64, 64)) + a256(4 * K)
+        # the one-launch kernel's header and 16 rows of K/32 tagged words, then
+        # 256 rows of K/32 block maxima (the two-launch path)
+        assert q == 256 + a256(16 * (K // 32) * 8) + a256(256 * (K // 32) * 4)
         lw = lib.rrs_linear_reorder_workspace_bytes(M, K, g)
         assert lw == q + a256(M * K // 2) + a256(4 * M) + a256(4 * (K // g)) + a256(4 * (K // 32))
     for bad in ((0, 512, 128), (16, 500, 128), (16, 512, 32), (16, 512, 1024)):
