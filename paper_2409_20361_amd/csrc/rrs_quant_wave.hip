@@ -99,7 +99,6 @@ __global__ __launch_bounds__(kRotWaves * 64) void rot_max_wave_kernel(
     const int32_t* __restrict__ perm, float* __restrict__ gpart) {
   using S = WaveRow<K>;
   __shared__ __attribute__((aligned(16))) float rows[kRotWaves * S::RW * S::RF];
-  __shared__ uint32_t cbuf[K];     // channel maxima (bits of non-negative floats)
   __shared__ float red[kRotWaves * 64];
 
   const int tid = threadIdx.x;
@@ -108,7 +107,6 @@ __global__ __launch_bounds__(kRotWaves * 64) void rot_max_wave_kernel(
   const int sub = lane >> S::LR;   // row of the wave
   const int l = lane & (S::R - 1);  // lane within the row
   float* row = rows + (wave * S::RW + sub) * S::RF;
-  for (int i = tid; i < K; i += kRotWaves * 64) cbuf[i] = 0u;
 
   const int r0 = blockIdx.x * rows_per_wg;
   const int r1 = min(M, r0 + rows_per_wg);
@@ -140,12 +138,21 @@ __global__ __launch_bounds__(kRotWaves * 64) void rot_max_wave_kernel(
   for (int e = 0; e < 64; ++e)
 #pragma unroll
     for (int o = S::R; o < 64; o <<= 1) cm[e] = fmaxf(cm[e], __shfl_xor(cm[e], o, 64));
-  __syncthreads();  // cbuf zeroed
+  // Each wave's channel maxima go into its own first row region (its rows
+  // are done with it); the workgroup's maximum of channel c is then taken
+  // over the waves in a fixed order (no atomics).
   if (sub == 0) {
+    float* cw = rows + wave * S::RW * S::RF;
 #pragma unroll
-    for (int e = 0; e < 64; ++e) atomicMax(&cbuf[l + S::R * e], __float_as_uint(cm[e]));
+    for (int e = 0; e < 64; ++e) cw[lds_a(l + S::R * e)] = cm[e];
   }
   __syncthreads();
+  auto chan_max = [&](int c) {
+    float m = rows[lds_a(c)];
+#pragma unroll
+    for (int w = 1; w < kRotWaves; ++w) m = fmaxf(m, rows[w * S::RW * S::RF + lds_a(c)]);
+    return m;
+  };
   // Group maxima over the (reordered) positions: thread t covers P = K / 512
   // (at least 1) consecutive positions, all in one group (P <= 8 < g).
   constexpr int NT = kRotWaves * 64;
@@ -157,10 +164,10 @@ __global__ __launch_bounds__(kRotWaves * 64) void rot_max_wave_kernel(
 #pragma unroll
     for (int q = 0; q < P; ++q) idx[q] = perm[tid * P + q];
 #pragma unroll
-    for (int q = 0; q < P; ++q) pm = fmaxf(pm, __uint_as_float(cbuf[idx[q]]));
+    for (int q = 0; q < P; ++q) pm = fmaxf(pm, chan_max(idx[q]));
   } else {
 #pragma unroll
-    for (int q = 0; q < P; ++q) pm = fmaxf(pm, __uint_as_float(cbuf[tid * P + q]));
+    for (int q = 0; q < P; ++q) pm = fmaxf(pm, chan_max(tid * P + q));
   }
   red[tid] = pm;
   __syncthreads();
