@@ -283,6 +283,26 @@ rrs_status rrs_test_quant_rows_wait(const void* X, int M, int K, int group_size,
                                     int32_t* failed, void* stream);
 
 /*
+ * Test hook for the failure path of the one-launch runtime-reorder quantizer
+ * (not for computing: use rrs_rotate_smooth_quant_reorder). For 2 to 16 tokens
+ * at K <= 8192, rrs_rotate_smooth_quant_reorder is one launch of one
+ * workgroup per token row whose rows exchange their K/32 block maxima through
+ * the workspace, under the same residency condition and bounded waits as the
+ * one-launch rrs_rotate_smooth_quant (see rrs_test_quant_rows_wait). This
+ * hook runs that kernel with the readers also waiting for extra_rows rows of
+ * block maxima that no workgroup writes and giving up after max_polls rounds,
+ * waits for `stream`, and stores 1 in *failed (host pointer) if the exchange
+ * failed, else 0; a failed call leaves NaN in a_scale and s_group. Arguments
+ * otherwise as rrs_rotate_smooth_quant_reorder (flags = 0); RRS_ERR_SHAPE
+ * when the shape has no one-launch reorder (M < 2, M > 16 or K > 8192),
+ * RRS_ERR_FLAGS for extra_rows < 0, max_polls < 1 or more than 16 rows in all.
+ */
+rrs_status rrs_test_quant_reorder_wait(const void* X, int M, int K, int group_size,
+                                      int extra_rows, int max_polls, void* Xq, float* a_scale,
+                                      float* s_group, int32_t* block_order, void* workspace,
+                                      size_t workspace_bytes, int32_t* failed, void* stream);
+
+/*
  * Test hook: the exact int32 group partials P[b][i][n] (b < K/g, i < M,
  * n < N; G x M x N int32, row-major), before any scaling (Eq. 3's inner sums
  * per block). Wq row-major. The call runs the same kernel that rrs_w4a4_gemm

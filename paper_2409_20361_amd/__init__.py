@@ -31,6 +31,7 @@ from ._binding import (  # noqa: F401
     prepare_weight,
     prepare_weight_sub_channel,
     quant_rows_wait_hook,
+    quant_reorder_wait_hook,
     quantize_sub_channel,
     rotate_smooth_quant,
     rotate_smooth_quant_reorder,
@@ -50,6 +51,7 @@ __all__ = [
     "SKIP_ROTATION", "SKIP_SMOOTHING", "WEIGHT_TILED", "RRSError", "lib", "lib_path", "linear", "linear_noalloc", "linear_reorder",
     "linear_reorder_workspace_bytes", "linear_workspace_bytes",
     "prepare_weight", "prepare_weight_sub_channel", "quant_rows_wait_hook",
+    "quant_reorder_wait_hook",
     "quantize_sub_channel",
     "reorder_workspace_bytes", "rotate_smooth_quant", "rotate_smooth_quant_reorder",
     "status_string", "version", "w4a4_gemm", "w4a4_gemm_partials",

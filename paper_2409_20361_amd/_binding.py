@@ -29,6 +29,8 @@ _SIGNATURES = {
     "rrs_linear_noalloc": (ctypes.c_int32, [_vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp]),
     "rrs_test_quant_rows_wait": (ctypes.c_int32, [_vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _vp,
                                                   _sz, _vp, _vp]),
+    "rrs_test_quant_reorder_wait": (ctypes.c_int32, [_vp, _i, _i, _i, _i, _i, _vp, _vp, _vp,
+                                                     _vp, _vp, _sz, _vp, _vp]),
     "rrs_prepare_weight_ex": (ctypes.c_int32, [_vp, _i, _i, _vp, _i, _vp, _vp, _vp]),
     "rrs_rotate_smooth_quant_ex": (ctypes.c_int32,
                                    [_vp, _i, _i, _i, _vp, _i, _vp, _vp, _vp, _vp, _sz, _vp]),
@@ -265,6 +267,27 @@ def quant_rows_wait_hook(X: torch.Tensor, g: int, extra_rows: int, max_polls: in
         workspace.data_ptr(), workspace.numel() * workspace.element_size(), ctypes.byref(n),
         _stream(X.device)), "rrs_test_quant_rows_wait")
     return Xq, a, s, bool(n.value)
+
+
+def quant_reorder_wait_hook(X: torch.Tensor, g: int, extra_rows: int, max_polls: int,
+                            workspace: Optional[torch.Tensor] = None):
+    """Test hook of the one-launch runtime-reorder quantizer's bounded wait (as
+    quant_rows_wait_hook); returns (Xq, a_scale, s_group, block_order, failed)."""
+    M, K = X.shape
+    xp = _dev(X, "X", torch.float16, (M, K))
+    Xq = torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
+    a = torch.empty((M,), dtype=torch.float32, device=X.device)
+    s = torch.empty((K // g,), dtype=torch.float32, device=X.device)
+    order = torch.empty((K // REORDER_BLOCK,), dtype=torch.int32, device=X.device)
+    if workspace is None:
+        workspace = torch.zeros((max(reorder_workspace_bytes(M, K, g), 1),), dtype=torch.uint8,
+                                device=X.device)
+    n = ctypes.c_int32(-1)
+    _check(lib().rrs_test_quant_reorder_wait(
+        xp, M, K, g, extra_rows, max_polls, Xq.data_ptr(), a.data_ptr(), s.data_ptr(),
+        order.data_ptr(), workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+        ctypes.byref(n), _stream(X.device)), "rrs_test_quant_reorder_wait")
+    return Xq, a, s, order, bool(n.value)
 
 
 def quantize_sub_channel(X: torch.Tensor, g: int, flags: int = 0

@@ -674,6 +674,38 @@ rrs_status rrs_test_quant_rows_wait(const void* X, int M, int K, int group_size,
   return RRS_OK;
 }
 
+rrs_status rrs_test_quant_reorder_wait(const void* X, int M, int K, int group_size,
+                                      int extra_rows, int max_polls, void* Xq, float* a_scale,
+                                      float* s_group, int32_t* block_order, void* workspace,
+                                      size_t workspace_bytes, int32_t* failed, void* stream) {
+  if (!X || !Xq || !a_scale || !s_group || !block_order || !workspace || !failed)
+    return RRS_ERR_NULL;
+  if (!valid_m(M) || !valid_k(K)) return RRS_ERR_SHAPE;
+  if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
+  if (M < 2 || !rrs::reorder_one_launch(M, K)) return RRS_ERR_SHAPE;
+  if (extra_rows < 0 || max_polls < 1 || M + extra_rows > 16) return RRS_ERR_FLAGS;
+  if (!is_aligned(X) || !is_aligned(Xq) || !is_aligned(a_scale) || !is_aligned(s_group) ||
+      !is_aligned(block_order) || !is_aligned(workspace))
+    return RRS_ERR_ALIGN;
+  if (workspace_bytes < rrs::reorder_workspace_bytes(K)) return RRS_ERR_WORKSPACE;
+  if (rrs_status s = check_device()) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const hipError_t e = rrs::launch_quant_rows_reorder(
+      static_cast<const uint16_t*>(X), M, K, group_size, true, static_cast<uint8_t*>(Xq),
+      a_scale, s_group, block_order, workspace, st, extra_rows, max_polls);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return e == hipErrorInvalidValue ? RRS_ERR_FLAGS : RRS_ERR_HIP;
+  }
+  bool f = false;
+  if (rrs::quant_exchange_failed(workspace, st, &f) != hipSuccess) {
+    (void)hipGetLastError();
+    return RRS_ERR_HIP;
+  }
+  *failed = f ? 1 : 0;
+  return RRS_OK;
+}
+
 rrs_status rrs_w4a4_gemm_partials(const void* Xq, const void* Wq, int M, int N, int K,
                                   int group_size, int32_t* P, void* stream) {
   if (!Xq || !Wq || !P) return RRS_ERR_NULL;

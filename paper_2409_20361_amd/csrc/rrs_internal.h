@@ -213,9 +213,11 @@ bool quant_rows_used(int M, int K, int g, const int32_t* perm, int flags);
 // Uses the header and quant_rows_reorder_workspace_bytes(K) bytes in all.
 bool quant_rows_reorder_fits(int M, int K);
 size_t quant_rows_reorder_workspace_bytes(int K);
+// extra_rows, max_polls: as launch_quant_rows (test hook only).
 hipError_t launch_quant_rows_reorder(const uint16_t* X, int M, int K, int g, bool rotate,
                                      uint8_t* Xq, float* a_scale, float* s_group,
-                                     int32_t* block_order, void* workspace, hipStream_t stream);
+                                     int32_t* block_order, void* workspace, hipStream_t stream,
+                                     int extra_rows = 0, int max_polls = 0);
 // Waits for `stream` and reports whether the latest one-launch exchange in
 // this workspace (per-row or fused kernel) had a wait that ran out.
 hipError_t quant_exchange_failed(const void* workspace, hipStream_t stream, bool* failed);

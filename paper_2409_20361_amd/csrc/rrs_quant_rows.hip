@@ -238,14 +238,17 @@ size_t quant_rows_reorder_workspace_bytes(int K) {
 
 hipError_t launch_quant_rows_reorder(const uint16_t* X, int M, int K, int g, bool rotate,
                                      uint8_t* Xq, float* a_scale, float* s_group,
-                                     int32_t* block_order, void* workspace, hipStream_t stream) {
-  if (!quant_rows_reorder_fits(M, K)) return hipErrorInvalidValue;
+                                     int32_t* block_order, void* workspace, hipStream_t stream,
+                                     int extra_rows, int max_polls) {
+  const int nrows = M + extra_rows;  // rows of block maxima the readers wait for
+  if (!quant_rows_reorder_fits(M, K) || nrows > kMaxRows) return hipErrorInvalidValue;
+  const int polls = max_polls > 0 ? max_polls : kMaxPolls;
   uint32_t* header = static_cast<uint32_t*>(workspace);
   unsigned long long* tagged =
       reinterpret_cast<unsigned long long*>(static_cast<char*>(workspace) + kQuantHeaderBytes);
-#define RRS_ROWS_R(K_)                                                                      \
-  launch_k<K_, true>(X, M, g, rotate, Xq, a_scale, s_group, block_order, header, tagged, M, \
-                     kMaxPolls, stream)
+#define RRS_ROWS_R(K_)                                                                          \
+  launch_k<K_, true>(X, M, g, rotate, Xq, a_scale, s_group, block_order, header, tagged, nrows, \
+                     polls, stream)
   switch (K) {
     case 512: return RRS_ROWS_R(512);
     case 1024: return RRS_ROWS_R(1024);

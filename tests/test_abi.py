@@ -477,6 +477,31 @@ def test_quant_rows_wait_hook_checks():
     assert _qwait(M=17, K=8192, X=None) == NULL   # null pointers first
 
 
+def _rwait(**kw):
+    a = dict(X=P, M=4, K=1024, g=128, extra=1, polls=8, Xq=P, a=P, s=P, o=P, ws=P,
+             wsb=1 << 30, n=P)
+    a.update(kw)
+    return rrs.lib().rrs_test_quant_reorder_wait(a["X"], a["M"], a["K"], a["g"], a["extra"],
+                                                 a["polls"], a["Xq"], a["a"], a["s"], a["o"],
+                                                 a["ws"], a["wsb"], a["n"], None)
+
+
+def test_quant_reorder_wait_hook_checks():
+    for key in ("X", "Xq", "a", "s", "o", "ws", "n"):
+        assert _rwait(**{key: None}) == NULL, key
+    assert _rwait(M=1) == SHAPE            # one row: no exchange
+    assert _rwait(M=17) == SHAPE           # more than 16 rows: two launches
+    assert _rwait(K=16384) == SHAPE        # K > 8192: two launches
+    assert _rwait(K=1000) == SHAPE
+    assert _rwait(g=96) == GROUP
+    assert _rwait(extra=-1) == FLAGS
+    assert _rwait(polls=0) == FLAGS
+    assert _rwait(M=4, extra=13) == FLAGS  # at most 16 rows in all
+    assert _rwait(o=MIS) == ALIGN
+    assert _rwait(wsb=16) == WS
+    assert _rwait(M=17, X=None) == NULL    # null pointers first
+
+
 def test_debug_checks_come_after_host_validation():
     # RRS_DEBUG only adds checks after the regular ones: invalid arguments still
     # get their usual codes, before any device access.

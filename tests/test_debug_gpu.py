@@ -211,6 +211,36 @@ def test_one_launch_wait_runs_out_loudly(M, K, g):
     np.testing.assert_array_equal(to_np(s), act.s)
 
 
+@pytest.mark.parametrize("M,K,g", [(2, 8192, 128), (8, 8192, 64), (15, 1024, 256)])
+def test_reorder_one_launch_wait_runs_out_loudly(M, K, g):
+    # the runtime-reorder quantizer's one-launch form (rows exchange block maxima)
+    rrs = _rrs()
+    w = synth.custom("rw", M, K, 16, g, M + K + 1, n_chan=max(1, K // 100), n_spike=2,
+                     spike_mag=(100, 500))
+    Xh = synth.activations(w)
+    X = to_gpu(Xh)
+    ws = torch.zeros((rrs.reorder_workspace_bytes(M, K, g),), dtype=torch.uint8, device="cuda")
+    print(f"[case] reorder one-launch wait runs out M={M} K={K} g={g}", flush=True)
+    Xq, a, s, order, failed = rrs.quant_reorder_wait_hook(X, g, extra_rows=1, max_polls=8,
+                                                          workspace=ws)
+    assert failed, "the exchange must report the waits that ran out"
+    assert bool(torch.isnan(a).all()), "alpha must be NaN after a failed exchange"
+    assert bool(torch.isnan(s).all()), "s_group must be NaN after a failed exchange"
+    # nothing extra to wait for: the hook and the ordinary call on the same
+    # workspace both match the oracle
+    act, border, _ = O.rotate_smooth_quant_reorder(Xh, g, 32)
+    Xq, a, s, order, failed = rrs.quant_reorder_wait_hook(X, g, extra_rows=0,
+                                                          max_polls=1 << 18, workspace=ws)
+    assert not failed
+    np.testing.assert_array_equal(to_np(order), border)
+    np.testing.assert_array_equal(to_np(a), act.alpha)
+    np.testing.assert_array_equal(to_np(s), act.s)
+    check_codes(to_np(Xq), act, "reorder hook, nothing extra")
+    Xq, a, s, order = rrs.rotate_smooth_quant_reorder(X, g, workspace=ws)
+    np.testing.assert_array_equal(to_np(order), border)
+    np.testing.assert_array_equal(to_np(a), act.alpha)
+
+
 def test_quant_rows_debug_reports_no_false_timeout(debug_env):
     rrs = _rrs()
     M, K, g = 8, 8192, 128
