@@ -20,7 +20,12 @@ OBJDIR = os.path.join(PKG, "_build")
 
 SOURCES = ["rrs_api.cpp", "rrs_quant.hip", "rrs_weight.hip", "rrs_gemm.hip", "rrs_gemm_small.hip",
            "rrs_gemm_decode.hip", "rrs_quant_wave.hip", "rrs_reorder.hip", "rrs_quant_rows.hip",
-           "rrs_gemm_stream.hip", "rrs_noalloc.hip"]
+           "rrs_gemm_stream.hip", "rrs_gemm_stream_gather.hip", "rrs_noalloc.hip"]
+
+# Per-source code-generation options on top of COMMON.
+# rrs_gemm_stream_gather.hip: keep MFMA results in VGPRs (the per-block
+#   rescale reads every accumulator; in AGPRs each read is an extra copy).
+EXTRA = {"rrs_gemm_stream_gather.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 # -packed-fp32-ops: no v_pk_{add,mul,fma}_f32 in any kernel.
 # -ffp-contract=off: every rounding in the rotation and scale chain is an
@@ -44,7 +49,7 @@ def hipcc() -> str:
 def _compile(src: str) -> str:
     obj = os.path.join(OBJDIR, os.path.splitext(src)[0] + ".o")
     lang = ["-x", "hip"] if src.endswith(".hip") else []
-    cmd = [hipcc()] + COMMON + ["-c"] + lang + [os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc()] + COMMON + EXTRA.get(src, []) + ["-c"] + lang + [os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

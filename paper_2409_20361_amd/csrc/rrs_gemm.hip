@@ -489,6 +489,9 @@ hipError_t launch_w4a4_gemm_reorder(const uint8_t* Xq, const float* a_scale,
                                     const float* w_scale, const int32_t* border, int M, int N,
                                     int K, int g, uint16_t* Y, float out_scale,
                                     hipStream_t stream, WqLayout lay) {
+  if (stream_gather_fits(M, K))
+    return launch_w4a4_gemm_stream_gather(Xq, a_scale, s_group, Wq, w_scale, border, M, N, K, g,
+                                          Y, out_scale, stream, lay);
   if (decode_gather_fits(M))
     return launch_w4a4_gemm_decode(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, out_scale,
                                    stream, border, lay);

@@ -60,54 +60,12 @@
 //
 // Needs K >= 4 g (every wave holds whole groups): K = 512 with g <= 128,
 // K = 1024 with g <= 256, any g from K = 2048 (but g >= 256 at K = 16384).
-#include "rrs_internal.h"
+#include "rrs_stream.h"
 
 namespace rrs {
 namespace {
 
-typedef int v4i __attribute__((ext_vector_type(4)));
-typedef float v4f __attribute__((ext_vector_type(4)));
-
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
-constexpr int kRows = 16;  // weight rows (output columns) per column block
-constexpr int kMaxTokens = 16;
-
-template <int K>
-struct StreamShape {
-  static constexpr int R = K / 2 / kWaves;            // packed bytes per row per wave
-  static constexpr int SBW = R < 512 ? R : 512;        // bytes per row per sub-buffer
-  static constexpr int SPB = R / SBW;                  // sub-buffers per block
-  static constexpr int CPR = SBW / 16;                 // 16-byte chunks per row per sub-buffer
-  static constexpr int SW = CPR >= 8 ? 7 : CPR - 1;   // chunk permutation mask (row-major)
-  static constexpr int SB = kRows * SBW;               // LDS bytes per sub-buffer
-  static constexpr int NL = SB / 1024;                 // direct loads of 1 KB per sub-buffer
-  static constexpr int RS = 16384 / SB;                // sub-buffers in a wave's ring (16 KB)
-  static constexpr int RPI = 1024 / SBW;               // rows per direct load (row-major)
-  static_assert(SB % 1024 == 0, "a sub-buffer is a whole number of 1 KB loads");
-  static_assert(RS >= 2 && (RS - 1) * NL <= 63, "ring depth and vmcnt immediate");
-};
-
-// Cache policy of the weight loads: non-temporal (each weight byte is read
-// once; 5 % faster at the decode shape than the default policy).
-constexpr int kWeightPolicy = 2;
-
-__device__ __forceinline__ v4i unpack_pair(uint32_t w0, uint32_t w1) {
-  v4i r;
-  r.x = (int)((w0 << 4) & 0xF0F0F0F0u);
-  r.y = (int)(w0 & 0xF0F0F0F0u);
-  r.z = (int)((w1 << 4) & 0xF0F0F0F0u);
-  r.w = (int)(w1 & 0xF0F0F0F0u);
-  return r;
-}
-
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
-
-// Waits until at most N vector-memory operations of this wave are in flight.
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
+using namespace stream;
 
 // kPartials (test hook): instead of Y, write P[b][i][n] for every group b,
 // token i < M and column n, decoded from the same seeded accumulators.
@@ -296,38 +254,6 @@ __global__ __launch_bounds__(kThreads) void gemm_stream_kernel(
             __builtin_bit_cast(uint16_t, (_Float16)((sum * oscale) * bcol));
     }
   }
-}
-
-int cu_count() {
-  static int cus = 0;
-  if (cus == 0) {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-        n > 0)
-      cus = n;
-    else
-      cus = 256;
-  }
-  return cus;
-}
-
-// A persistent grid must not exceed the workgroups that can be resident at
-// once (the surplus would wait for a whole earlier workgroup to finish):
-// as many per compute unit as the runtime's occupancy query allows (two for
-// most shapes: 72 KB of LDS each; one where a wave needs more than 256
-// registers), times the compute units. Cached per kernel.
-template <typename Kern>
-int resident_grid(Kern kern, int nblk) {
-  static int per_cu = 0;
-  if (per_cu == 0) {
-    int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, kThreads, 0) != hipSuccess || n < 1)
-      n = 1;
-    per_cu = n;
-  }
-  const int cap = per_cu * cu_count();
-  return nblk < cap ? nblk : cap;
 }
 
 template <int K, bool kPartials>

@@ -113,6 +113,14 @@ hipError_t launch_w4a4_gemm_partials_small(const uint8_t* Xq, const uint8_t* Wq,
 // of 16 tokens); its runtime-reorder variant takes M <= 16.
 bool decode_kernel_fits(int M);
 bool decode_gather_fits(int M);
+// Runtime-reorder GEMM on the weight stream (rrs_gemm_stream.hip): up to 16
+// tokens, K <= 8192, any g, either layout.
+bool stream_gather_fits(int M, int K);
+hipError_t launch_w4a4_gemm_stream_gather(const uint8_t* Xq, const float* a_scale,
+                                          const float* s_group, const uint8_t* Wq,
+                                          const float* w_scale, const int32_t* border, int M,
+                                          int N, int K, int g, uint16_t* Y, float out_scale,
+                                          hipStream_t stream, WqLayout lay);
 hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
                                    const float* s_group, const uint8_t* Wq,
                                    const float* w_scale, int M, int N, int K, int g,
