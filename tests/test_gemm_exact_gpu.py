@@ -58,6 +58,9 @@ CASES = [
     # main kernel, partial row and column tiles
     (65, 2048, 144, 128, False), (300, 4096, 272, 64, False), (257, 2048, 400, 512, True),
     (130, 1024, 128, 256, True),
+    # main kernel, more tiles than one pass of workgroups (776 tiles: up to four
+    # per workgroup, ragged last row and column tiles among them)
+    (2000, 512, 12400, 128, False), (1800, 512, 12400, 64, True),
 ]
 
 
