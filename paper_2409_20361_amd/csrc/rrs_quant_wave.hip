@@ -368,19 +368,21 @@ __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
 // outputs. Same arithmetic in the same order as the two-pass kernels:
 // bit-identical codes and scales.
 // ---------------------------------------------------------------------------
-constexpr int kFusedWaves = 8;
+constexpr int kFusedWaves = 8;  // waves per workgroup (4 when that fills every compute unit)
 constexpr int kFusedMaxPolls = 1 << 20;
 
-template <int K, bool kRot, int SLOTS>
-__global__ __launch_bounds__(kFusedWaves * 64) void rot_quant_fused_kernel(
+// kWideG: g = 64 (K / 64 groups); otherwise g >= 128, and the exchange holds
+// half as many entries per thread.
+template <int K, bool kRot, int SLOTS, int WAVES, bool kWideG>
+__global__ __launch_bounds__(WAVES * 64) void rot_quant_fused_kernel(
     const uint16_t* __restrict__ X, int M, int g, int rows_per_wg, uint32_t* header,
     unsigned long long* tagged, int nrows, int max_polls, uint8_t* __restrict__ Xq,
     float* __restrict__ a_scale, float* __restrict__ s_group) {
   using S = WaveRow<K>;
-  constexpr int NT = kFusedWaves * 64;
+  constexpr int NT = WAVES * 64;
   constexpr int GMAX = K / 64;  // groups at g = 64
-  __shared__ __attribute__((aligned(16))) float rows[kFusedWaves * S::RW * S::RF];
-  __shared__ float wmax[kFusedWaves][GMAX];
+  __shared__ __attribute__((aligned(16))) float rows[WAVES * S::RW * S::RF];
+  __shared__ float wmax[WAVES][GMAX];
   __shared__ float red[NT];
   __shared__ float rg[GMAX];
   __shared__ int missed;
@@ -395,7 +397,7 @@ __global__ __launch_bounds__(kFusedWaves * 64) void rot_quant_fused_kernel(
   const int G = K / g;
   const int r0 = blockIdx.x * rows_per_wg;
   const int r1 = min(M, r0 + rows_per_wg);
-  auto row_of = [&](int p) { return r0 + (p * kFusedWaves + wave) * S::RW + sub; };
+  auto row_of = [&](int p) { return r0 + (p * WAVES + wave) * S::RW + sub; };
   // This call's tag (the header was written by earlier calls only): one
   // thread requests it now and hands it over in LDS before the first barrier,
   // so the load's latency hides behind the rotation.
@@ -454,7 +456,7 @@ __global__ __launch_bounds__(kFusedWaves * 64) void rot_quant_fused_kernel(
   if (tid < G) {
     float m = wmax[0][tid];
 #pragma unroll
-    for (int w = 1; w < kFusedWaves; ++w) m = fmaxf(m, wmax[w][tid]);
+    for (int w = 1; w < WAVES; ++w) m = fmaxf(m, wmax[w][tid]);
     publish_tagged(tagged + (size_t)blockIdx.x * G + tid, tag, m);
   }
 
@@ -463,7 +465,8 @@ __global__ __launch_bounds__(kFusedWaves * 64) void rot_quant_fused_kernel(
   // all its entries are requested at once, and those whose tag is not set yet
   // are requested again, within a budget of max_polls rounds.
   {
-    constexpr int NE = GMAX / 2;  // entries per thread at most: 256 rows / (NT / G)
+    // Entries per thread at most: 256 rows / (NT / G).
+    constexpr int NE = 256 * (kWideG ? GMAX : GMAX / 2) / NT;
     const int b = tid % G;
     const int ns = NT / G;  // slices of rows
     const unsigned long long none = (unsigned long long)tag << 32;  // an absent row: 0.0
@@ -534,7 +537,16 @@ template <int K>
 hipError_t launch_fused_k(const uint16_t* X, int M, int g, bool rot, uint8_t* Xq,
                           float* a_scale, float* s_group, void* workspace, int max_wgs,
                           int extra_rows, int max_polls, hipStream_t stream) {
-  constexpr int per_slot = kFusedWaves * WaveRow<K>::RW;  // rows per workgroup per slot
+  // Four waves per workgroup when one row per wave then still needs every
+  // compute unit's workgroup (at 1024 x 4096 about 20 % faster than eight
+  // waves on half of them) and g >= 128 (the four-wave form reads at most
+  // K / 128 group maxima per row); otherwise eight waves, with two rows per
+  // wave when one is not enough. One row per wave on two waves per SIMD
+  // beats two rows per wave on one (at 2048 x 4096: 13.8 against 14.8 us).
+  constexpr int RW = WaveRow<K>::RW;
+  const bool wide = g < 128;
+  const int waves = (M <= max_wgs * 4 * RW && !wide) ? 4 : kFusedWaves;
+  const int per_slot = waves * RW;  // rows per workgroup per slot
   const int slots = M <= max_wgs * per_slot ? 1 : 2;
   const int rpw = slots * per_slot;
   const int wgs = (M + rpw - 1) / rpw;
@@ -544,14 +556,22 @@ hipError_t launch_fused_k(const uint16_t* X, int M, int g, bool rot, uint8_t* Xq
   unsigned long long* tagged =
       reinterpret_cast<unsigned long long*>(static_cast<char*>(workspace) + kQuantHeaderBytes);
   const int polls = max_polls > 0 ? max_polls : kFusedMaxPolls;
-#define RRS_FUSED(R_, S_)                                                                    \
-  rot_quant_fused_kernel<K, R_, S_><<<wgs, kFusedWaves * 64, 0, stream>>>(                   \
+#define RRS_FUSED(R_, S_, W_, WG_)                                                 \
+  rot_quant_fused_kernel<K, R_, S_, W_, WG_><<<wgs, W_ * 64, 0, stream>>>(         \
       X, M, g, rpw, header, tagged, nrows, polls, Xq, a_scale, s_group)
-  if (rot) {
-    if (slots == 1) RRS_FUSED(true, 1); else RRS_FUSED(true, 2);
+#define RRS_FUSED8(R_, WG_)                         \
+  if (slots == 1)                                   \
+    RRS_FUSED(R_, 1, kFusedWaves, WG_);             \
+  else                                              \
+    RRS_FUSED(R_, 2, kFusedWaves, WG_);
+  if (waves == 4) {
+    if (rot) RRS_FUSED(true, 1, 4, false); else RRS_FUSED(false, 1, 4, false);
+  } else if (rot) {
+    if (wide) { RRS_FUSED8(true, true) } else { RRS_FUSED8(true, false) }
   } else {
-    if (slots == 1) RRS_FUSED(false, 1); else RRS_FUSED(false, 2);
+    if (wide) { RRS_FUSED8(false, true) } else { RRS_FUSED8(false, false) }
   }
+#undef RRS_FUSED8
 #undef RRS_FUSED
   return hipGetLastError();
 }
