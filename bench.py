@@ -40,7 +40,7 @@ METRIC = "effective W4A4 TOPS at M=2048,K=4096,N=12288; HBM GB/s at M=8 decode"
 # --pmc runs (FETCH_SIZE, WRITE_SIZE) scaled by a 256 MiB copy-kernel
 # calibration (profiles/gemm_main_kernel_qkv.md), keyed by the sha1 prefix of
 # the kernel source they were measured on. Any other source reports null.
-GEMM_TRAFFIC_BYTES = {"d79338a8add9": 159.90e6}
+GEMM_TRAFFIC_BYTES = {"a55e13cd5d24": 159.81e6}
 INT8_MFMA_PEAK_TOPS = 5000.0   # MI355X dense int8 MFMA, 5.0 POP/s
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 
