@@ -30,24 +30,48 @@ namespace {
 constexpr int kMaxRows = 16;
 constexpr int kMaxPolls = 1 << 18;
 
+// LDS address of position q of the rotated row in position-major order: row
+// a = q / E (E floats) holds positions [a E, a E + E), thread a's share; its
+// 4-float chunks are permuted by h(a) so that both the strided writes of the
+// rotation's output (position t + 256 e from thread t) and the 128-bit chunk
+// reads of the owner are free of bank conflicts.
+template <int E>
+__device__ __forceinline__ int pos_addr(int q) {
+  constexpr int CH = E < 4 ? E : 4;  // floats per chunk
+  constexpr int NCH = E / CH;        // chunks per row
+  constexpr int S = ilog2(64 / E);   // rows per 64 banks = 2^S
+  const int a = q / E;
+  const int b = q % E;
+  const int h = NCH > 1 ? (a >> S) & (NCH - 1) : 0;
+  return a * E + ((b / CH) ^ h) * CH + b % CH;
+}
+
 // kReorder (runtime reorder, K <= 8192): the rows exchange their K/32 block
 // maxima instead of their group maxima; every workgroup then ranks the blocks
 // (keys largest first, equal keys in increasing block index), takes s_b over
 // the sorted blocks of group b, and quantizes its row with the blocks in that
 // order; workgroup 0 also writes block_order. The same order, scales and
 // codes as the three-launch path (block maxima, order, given-maxima pass).
+//
+// After the rotation the row goes once through LDS into position-major order,
+// so each thread holds E consecutive positions, all in one span (a group, or
+// a block of 32 with the runtime reorder; E <= span): the span maxima come
+// from registers and shuffles, and the codes are packed from the same
+// registers (with the runtime reorder the sorted positions are gathered from
+// the position-major copy).
 template <int K, bool kRot, bool kReorder>
 __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
     const uint16_t* __restrict__ X, int M, int g, uint8_t* __restrict__ Xq,
     float* __restrict__ a_scale, float* __restrict__ s_group, int32_t* __restrict__ block_order,
     uint32_t* header, unsigned long long* tagged, int nrows, int max_polls) {
   constexpr int E = FwhtShape<K>::E;  // this thread's channels: t + 256 e after the FWHT
-  constexpr int C = E < kReorderBlock ? E : kReorderBlock;  // positions per chunk maximum
-  constexpr int CH = E / C;                                 // chunks per thread (1 or 2)
+  constexpr int CH = E < 4 ? E : 4;
   constexpr int NB = K / kReorderBlock;
   static_assert(!kReorder || NB <= kRowThreads, "one block key per thread");
-  __shared__ float slot[lds_row_floats(K)];
-  __shared__ float red[kRowThreads * CH];
+  static_assert(E <= 64 && (!kReorder || E <= kReorderBlock), "a thread's positions in one span");
+  __shared__ float slot[lds_row_floats(K)];                   // the rotation's scratch
+  __shared__ __attribute__((aligned(16))) float row[K];      // position-major (pos_addr)
+  __shared__ float red[4];
   __shared__ float rg[256];
   __shared__ float sg[256];
   __shared__ __attribute__((aligned(16))) float key[kReorder ? NB : 4];
@@ -70,44 +94,70 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
   float v[E];
   load_halves<E>(X + (size_t)p * K + (size_t)t * E, v);
   fwht_row<K, kRot>(v, slot, t);  // v[e] = y[t + 256 e]
+#pragma unroll
+  for (int e = 0; e < E; ++e) row[pos_addr<E>(t + e * kRowThreads)] = v[e];
   if (t == 0) {
     missed = 0;
     tag_lds = next_epoch(epoch);
   }
-  __syncthreads();                // slot is free again
+  __syncthreads();
+  {
+    constexpr int NCH = E / CH;
+    const int h = NCH > 1 ? (t >> ilog2(64 / E)) & (NCH - 1) : 0;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const float* src = row + t * E + (c ^ h) * CH;
+      if constexpr (CH == 4) {
+        const float4 x = *reinterpret_cast<const float4*>(src);
+        v[4 * c] = x.x;
+        v[4 * c + 1] = x.y;
+        v[4 * c + 2] = x.z;
+        v[4 * c + 3] = x.w;
+      } else {
+#pragma unroll
+        for (int i = 0; i < CH; ++i) v[CH * c + i] = src[i];
+      }
+    }
+  }  // v[e] = y[t E + e]
 
-  // This row's maxima of the exchanged spans (groups of g channels, or blocks
-  // of 32 with the runtime reorder): thread t takes positions t E .. t E + E - 1
-  // as CH chunks of C, each inside one span (C <= 32 <= span).
+  // This row's maximum of each exchanged span: over the thread's E positions,
+  // then over the tps threads of the span (shuffles within a wave, LDS across
+  // waves when a span is wider than a wave).
+  float pm = 0.0f;
 #pragma unroll
-  for (int e = 0; e < E; ++e) slot[lds_pad(t + e * kRowThreads)] = fabsf(v[e]);
-  __syncthreads();
-#pragma unroll
-  for (int k = 0; k < CH; ++k) {
-    float pm = 0.0f;
-#pragma unroll
-    for (int e = 0; e < C; ++e) pm = fmaxf(pm, slot[lds_pad(t * E + k * C + e)]);
-    red[t * CH + k] = pm;
+  for (int e = 0; e < E; ++e) pm = fmaxf(pm, fabsf(v[e]));
+  const int tps = span / E;
+  for (int o = 1; o < tps && o < 64; o <<= 1) pm = fmaxf(pm, __shfl_xor(pm, o, 64));
+  bool owner;  // this thread publishes / reduces span b
+  int b;
+  if (tps <= 64) {
+    owner = (t & (tps - 1)) == 0;
+    b = t / tps;
+  } else {
+    if ((t & 63) == 0) red[t >> 6] = pm;
+    __syncthreads();
+    owner = t < W;
+    b = t;
+    if (owner) {
+      const int per = tps / 64;  // waves per span
+      pm = red[t * per];
+      for (int u = 1; u < per; ++u) pm = fmaxf(pm, red[t * per + u]);
+    }
   }
-  __syncthreads();
-  float wm = 0.0f;  // this row's maximum of span t (t < W)
-  if (t < W) {
-    const int per = span / C;  // chunks per span
-    for (int u = 0; u < per; ++u) wm = fmaxf(wm, red[t * per + u]);
-  }
+
   // Maxima over the rows. With more than one row, every row's maxima are
-  // exchanged: thread t < W publishes span t of this row and reads span t of
-  // all nrows rows (all words requested at once, those not yet tagged
-  // requested again, within max_polls rounds).
-  const uint32_t tag = tag_lds;  // set before the barrier after the rotation
-  if (t < W) {
-    float s = wm;
+  // exchanged: the owner of span b publishes this row's maximum and reads
+  // span b of all nrows rows (all words requested at once, those not yet
+  // tagged requested again, within max_polls rounds).
+  const uint32_t tag = tag_lds;  // set before the barrier above
+  if (owner) {
+    float s = pm;
     if (M > 1) {
-      publish_tagged(tagged + (size_t)p * W + t, tag, wm);
+      publish_tagged(tagged + (size_t)p * W + b, tag, pm);
       unsigned long long x[kMaxRows];
 #pragma unroll
       for (int i = 0; i < kMaxRows; ++i)
-        x[i] = i < nrows ? load_tagged(tagged + (size_t)i * W + t) : ((unsigned long long)tag << 32);
+        x[i] = i < nrows ? load_tagged(tagged + (size_t)i * W + b) : ((unsigned long long)tag << 32);
       bool ok = false;
       for (int round = 0;; ++round) {
         ok = true;
@@ -117,7 +167,7 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
         __builtin_amdgcn_s_sleep(1);
 #pragma unroll
         for (int i = 0; i < kMaxRows; ++i)
-          if (i < nrows && !has_tag(x[i], tag)) x[i] = load_tagged(tagged + (size_t)i * W + t);
+          if (i < nrows && !has_tag(x[i], tag)) x[i] = load_tagged(tagged + (size_t)i * W + b);
       }
       if (!ok) missed = 1;  // benign race: every writer writes 1
       s = 0.0f;
@@ -125,10 +175,10 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
       for (int i = 0; i < kMaxRows; ++i) s = fmaxf(s, __uint_as_float((uint32_t)x[i]));
     }
     if constexpr (kReorder) {
-      key[t] = s;  // block t's key: its largest channel maximum
+      key[b] = s;  // block b's key: its largest channel maximum
     } else {
-      rg[t] = (s == 0.0f) ? 0.0f : __fdiv_rn(1.0f, s);  // s_b and r_b = fl(1 / s_b)
-      sg[t] = s;
+      rg[b] = (s == 0.0f) ? 0.0f : __fdiv_rn(1.0f, s);  // s_b and r_b = fl(1 / s_b)
+      sg[b] = s;
     }
   }
   __syncthreads();
@@ -141,11 +191,11 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
 #pragma unroll 4
       for (int q = 0; q < NB / 4; ++q) {
         const float4 k4 = reinterpret_cast<const float4*>(key)[q];
-        const int b = 4 * q;
-        rank += (k4.x > c || (k4.x == c && b < t)) ? 1 : 0;
-        rank += (k4.y > c || (k4.y == c && b + 1 < t)) ? 1 : 0;
-        rank += (k4.z > c || (k4.z == c && b + 2 < t)) ? 1 : 0;
-        rank += (k4.w > c || (k4.w == c && b + 3 < t)) ? 1 : 0;
+        const int bb = 4 * q;
+        rank += (k4.x > c || (k4.x == c && bb < t)) ? 1 : 0;
+        rank += (k4.y > c || (k4.y == c && bb + 1 < t)) ? 1 : 0;
+        rank += (k4.z > c || (k4.z == c && bb + 2 < t)) ? 1 : 0;
+        rank += (k4.w > c || (k4.w == c && bb + 3 < t)) ? 1 : 0;
       }
       sblk[rank] = t;
       skey[rank] = c;
@@ -161,6 +211,15 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
     }
     if (p == 0 && t < NB) block_order[t] = sblk[t];
     __syncthreads();
+    // position j takes channel 32 sblk[j / 32] + j % 32 (masked into range:
+    // with keys read from a workspace that was not zeroed, ranks could collide
+    // and leave entries unset)
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int j = t * E + e;
+      const int bl = sblk[j / kReorderBlock] & (NB - 1);
+      v[e] = row[pos_addr<E>(bl * kReorderBlock + j % kReorderBlock)];
+    }
   }
   const bool failed = missed != 0;  // uniform over the workgroup
   if (M > 1 && t == 0) {
@@ -172,27 +231,9 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
       __hip_atomic_store(header + kEpochWord, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   if (t < G && p == 0) s_group[t] = failed ? __builtin_nanf("") : sg[t];
-  __syncthreads();
 
   // The row's codes, as the second pass: positions t E .. t E + E - 1.
   const float rb = rg[(t * E) / g];
-#pragma unroll
-  for (int e = 0; e < E; ++e) slot[lds_pad(t + e * kRowThreads)] = v[e];
-  __syncthreads();
-  if constexpr (kReorder) {
-    // position j takes channel 32 sblk[j / 32] + j % 32 (masked into range:
-    // with keys read from a workspace that was not zeroed, ranks could collide
-    // and leave entries unset)
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const int j = t * E + e;
-      const int b = sblk[j / kReorderBlock] & (NB - 1);
-      v[e] = slot[lds_pad(b * kReorderBlock + j % kReorderBlock)];
-    }
-  } else {
-#pragma unroll
-    for (int e = 0; e < E; ++e) v[e] = slot[lds_pad(t * E + e)];
-  }
   float lm = 0.0f;
 #pragma unroll
   for (int e = 0; e < E; ++e) lm = fmaxf(lm, fabsf(v[e]));
@@ -202,10 +243,26 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
   const float a = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   const float inv = (a == 0.0f) ? 0.0f : __fdiv_rn(7.0f, a);
   const float m = rb * inv;  // fl(r_b * inv_i)
-  uint32_t nib[E];
+  uint8_t* dst = Xq + (size_t)p * (K / 2) + (size_t)t * (E / 2);
+  if constexpr (E >= 8) {
+    uint32_t wd[E / 8];
 #pragma unroll
-  for (int e = 0; e < E; ++e) nib[e] = int4_nibble(v[e] * m);
-  store_nibbles<E>(Xq + (size_t)p * (K / 2) + (size_t)t * (E / 2), nib);
+    for (int w = 0; w < E / 8; ++w) wd[w] = quant_pack8(&v[8 * w], m);
+    if constexpr (E == 8) {
+      *reinterpret_cast<uint32_t*>(dst) = wd[0];
+    } else if constexpr (E == 16) {
+      *reinterpret_cast<uint2*>(dst) = make_uint2(wd[0], wd[1]);
+    } else {
+#pragma unroll
+      for (int w = 0; w < E / 8; w += 4)
+        *reinterpret_cast<uint4*>(dst + 4 * w) = make_uint4(wd[w], wd[w + 1], wd[w + 2], wd[w + 3]);
+    }
+  } else {
+    uint32_t nib[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) nib[e] = int4_nibble(v[e] * m);
+    store_nibbles<E>(dst, nib);
+  }
   if (t == 0) a_scale[p] = failed ? __builtin_nanf("") : __fdiv_rn(a, 7.0f);
 }
 

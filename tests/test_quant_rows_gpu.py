@@ -55,7 +55,8 @@ def _zeros(M, K, g):
 
 
 @pytest.mark.parametrize("M", [1, 2, 3, 7, 8, 9, 16])
-@pytest.mark.parametrize("K,g", [(8192, 128), (512, 64), (4096, 512), (16384, 256), (2048, 64)])
+@pytest.mark.parametrize("K,g", [(8192, 128), (512, 64), (4096, 512), (16384, 256), (2048, 64),
+                                 (512, 256), (1024, 512)])
 def test_rows_match_oracle(M, K, g):
     print(f"[case] quant rows M={M} K={K} g={g}", flush=True)
     ws = _zeros(M, K, g)
@@ -76,7 +77,7 @@ def test_rows_without_rotation(M):
 
 @pytest.mark.parametrize("M,K,g", [(17, 4096, 128), (300, 4096, 64), (2048, 4096, 128),
                                    (4096, 4096, 128), (3000, 2048, 512), (777, 512, 128),
-                                   (5000, 1024, 256)])
+                                   (5000, 1024, 256), (1000, 2048, 256), (1024, 4096, 128)])
 def test_fused_match_oracle(M, K, g):
     # more than 16 tokens at K <= 4096: the fused one-launch kernel (one or
     # two rows per wave; 4096 rows at K = 4096 is its largest single-slot
