@@ -461,37 +461,45 @@ __global__ __launch_bounds__(WAVES * 64) void rot_quant_fused_kernel(
   }
 
   // s_b = max over the nrows rows of maxima; r_b = fl(1 / s_b). Thread t takes
-  // group t % G of rows t / G, t / G + NT / G, ... (at most GMAX / 2 of them):
-  // all its entries are requested at once, and those whose tag is not set yet
-  // are requested again, within a budget of max_polls rounds.
+  // group t % G of rows t / G, t / G + NT / G, ...: the entries of a batch are
+  // requested at once, and those whose tag is not set yet are requested again,
+  // within a budget of max_polls rounds per batch.
   {
-    // Entries per thread at most: 256 rows / (NT / G).
+    // Entries per thread at most: 256 rows / (NT / G). One batch, except at
+    // eight waves for g = 64 (two batches of 16: one more round trip, and the
+    // words stay in registers next to the kept rows).
     constexpr int NE = 256 * (kWideG ? GMAX : GMAX / 2) / NT;
+    constexpr int NEB = (WAVES == 8 && NE > 16) ? 16 : NE;
     const int b = tid % G;
     const int ns = NT / G;  // slices of rows
     const unsigned long long none = (unsigned long long)tag << 32;  // an absent row: 0.0
-    unsigned long long x[NE];
-#pragma unroll
-    for (int k = 0; k < NE; ++k) {
-      const int i = tid / G + k * ns;
-      x[k] = i < nrows ? load_tagged(tagged + (size_t)i * G + b) : none;
-    }
-    bool ok = false;
-    for (int round = 0;; ++round) {
-      ok = true;
-#pragma unroll
-      for (int k = 0; k < NE; ++k) ok = ok && has_tag(x[k], tag);
-      if (ok || round >= max_polls) break;
-      __builtin_amdgcn_s_sleep(1);
-#pragma unroll
-      for (int k = 0; k < NE; ++k) {
-        const int i = tid / G + k * ns;
-        if (!has_tag(x[k], tag)) x[k] = load_tagged(tagged + (size_t)i * G + b);
-      }
-    }
     float m = 0.0f;
+    bool ok = true;
 #pragma unroll
-    for (int k = 0; k < NE; ++k) m = fmaxf(m, __uint_as_float((uint32_t)x[k]));
+    for (int k0 = 0; k0 < NE; k0 += NEB) {
+      unsigned long long x[NEB];
+#pragma unroll
+      for (int k = 0; k < NEB; ++k) {
+        const int i = tid / G + (k0 + k) * ns;
+        x[k] = i < nrows ? load_tagged(tagged + (size_t)i * G + b) : none;
+      }
+      bool bok = false;
+      for (int round = 0;; ++round) {
+        bok = true;
+#pragma unroll
+        for (int k = 0; k < NEB; ++k) bok = bok && has_tag(x[k], tag);
+        if (bok || round >= max_polls) break;
+        __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+        for (int k = 0; k < NEB; ++k) {
+          const int i = tid / G + (k0 + k) * ns;
+          if (!has_tag(x[k], tag)) x[k] = load_tagged(tagged + (size_t)i * G + b);
+        }
+      }
+      ok = ok && bok;
+#pragma unroll
+      for (int k = 0; k < NEB; ++k) m = fmaxf(m, __uint_as_float((uint32_t)x[k]));
+    }
     if (!ok) missed = 1;  // benign race: every writer writes 1
     red[tid] = m;
     __syncthreads();
