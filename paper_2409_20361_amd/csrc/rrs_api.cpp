@@ -683,14 +683,15 @@ rrs_status rrs_test_quant_reorder_wait(const void* X, int M, int K, int group_si
   if (!valid_m(M) || !valid_k(K)) return RRS_ERR_SHAPE;
   if (!valid_group(K, group_size)) return RRS_ERR_GROUP;
   if (M < 2 || !rrs::reorder_one_launch(M, K)) return RRS_ERR_SHAPE;
-  if (extra_rows < 0 || max_polls < 1 || M + extra_rows > 16) return RRS_ERR_FLAGS;
+  if (extra_rows < 0 || max_polls < 1) return RRS_ERR_FLAGS;
+  if (rrs::quant_rows_reorder_fits(M, K) && M + extra_rows > 16) return RRS_ERR_FLAGS;
   if (!is_aligned(X) || !is_aligned(Xq) || !is_aligned(a_scale) || !is_aligned(s_group) ||
       !is_aligned(block_order) || !is_aligned(workspace))
     return RRS_ERR_ALIGN;
   if (workspace_bytes < rrs::reorder_workspace_bytes(K)) return RRS_ERR_WORKSPACE;
   if (rrs_status s = check_device()) return s;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const hipError_t e = rrs::launch_quant_rows_reorder(
+  const hipError_t e = rrs::launch_reorder_one_launch(
       static_cast<const uint16_t*>(X), M, K, group_size, true, static_cast<uint8_t*>(Xq),
       a_scale, s_group, block_order, workspace, st, extra_rows, max_polls);
   if (e != hipSuccess) {

@@ -80,6 +80,17 @@ hipError_t launch_rotate_smooth_quant_fused(const uint16_t* X, int M, int K, int
                                             void* workspace, int max_wgs, hipStream_t stream,
                                             int extra_rows = 0, int max_polls = 0);
 
+// The same one-launch kernel with the runtime reorder (K <= 4096, the shapes
+// fused_quant_fits accepts): block words of each workgroup in `tagged` (256 x
+// K/32), of each run of 16 workgroups in `tagged2` (16 x K/32), under `header`.
+hipError_t launch_rotate_smooth_quant_fused_order(const uint16_t* X, int M, int K, int g,
+                                                  bool rotate, uint8_t* Xq, float* a_scale,
+                                                  float* s_group, int32_t* block_order,
+                                                  uint32_t* header, unsigned long long* tagged,
+                                                  unsigned long long* tagged2, int max_wgs,
+                                                  hipStream_t stream, int extra_rows = 0,
+                                                  int max_polls = 0);
+
 // Every launcher that writes or reads Wq takes its layout (row-major unless
 // the caller asked for RRS_WEIGHT_TILED).
 hipError_t launch_prepare_weight(const uint16_t* W, int K, int N, const int32_t* perm,
@@ -181,8 +192,15 @@ hipError_t launch_quantize_ordered_wave(const uint16_t* X, int M, int K, int g, 
                                         uint8_t* Xq, float* a_scale, float* s_group,
                                         int32_t* block_order, hipStream_t stream);
 size_t reorder_workspace_bytes(int K);
-// Whether the runtime-reorder quantizer is the one-launch per-row kernel.
+// Whether the runtime-reorder quantizer is one launch (the per-row kernel up
+// to 16 tokens, the one-row-per-wave kernel for more at K <= 4096), and that
+// launch with readers that also wait for extra_rows rows of words no
+// workgroup writes, polling at most max_polls rounds (0: the default).
 bool reorder_one_launch(int M, int K);
+hipError_t launch_reorder_one_launch(const uint16_t* X, int M, int K, int g, bool rot,
+                                     uint8_t* Xq, float* a_scale, float* s_group,
+                                     int32_t* block_order, void* workspace, hipStream_t stream,
+                                     int extra_rows, int max_polls);
 hipError_t launch_rotate_smooth_quant_reorder(const uint16_t* X, int M, int K, int g, int flags,
                                               uint8_t* Xq, float* a_scale, float* s_group,
                                               int32_t* block_order, void* workspace,

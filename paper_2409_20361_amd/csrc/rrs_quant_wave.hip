@@ -370,21 +370,33 @@ __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
 // ---------------------------------------------------------------------------
 constexpr int kFusedWaves = 8;  // waves per workgroup (4 when that fills every compute unit)
 constexpr int kFusedMaxPolls = 1 << 20;
+constexpr int kOrderRun = 16;   // workgroups per level-1 run of the reorder exchange
 
 // kWideG: g = 64 (K / 64 groups); otherwise g >= 128, and the exchange holds
 // half as many entries per thread.
-template <int K, bool kRot, int SLOTS, int WAVES, bool kWideG>
+// kOrder (runtime reorder): the workgroups exchange K/32 block maxima instead
+// of group maxima, in two levels (below); every workgroup ranks the blocks,
+// takes s_b over the sorted blocks of group b and quantizes its kept rows over
+// the sorted positions; workgroup 0 writes s_group and block_order. `tagged`
+// then holds one row of block words per workgroup and `tagged2` one per level-1
+// group.
+template <int K, bool kRot, int SLOTS, int WAVES, bool kWideG, bool kOrder = false>
 __global__ __launch_bounds__(WAVES * 64) void rot_quant_fused_kernel(
     const uint16_t* __restrict__ X, int M, int g, int rows_per_wg, uint32_t* header,
     unsigned long long* tagged, int nrows, int max_polls, uint8_t* __restrict__ Xq,
-    float* __restrict__ a_scale, float* __restrict__ s_group) {
+    float* __restrict__ a_scale, float* __restrict__ s_group,
+    unsigned long long* tagged2 = nullptr, int32_t* __restrict__ block_order = nullptr) {
   using S = WaveRow<K>;
   constexpr int NT = WAVES * 64;
   constexpr int GMAX = K / 64;  // groups at g = 64
+  constexpr int NB = K / kReorderBlock;
   __shared__ __attribute__((aligned(16))) float rows[WAVES * S::RW * S::RF];
-  __shared__ float wmax[WAVES][GMAX];
+  __shared__ float wmax[WAVES][kOrder ? NB : GMAX];
   __shared__ float red[NT];
   __shared__ float rg[GMAX];
+  __shared__ __attribute__((aligned(16))) float key[kOrder ? NB : 4];
+  __shared__ float skey[kOrder ? NB : 1];
+  __shared__ int sblk[kOrder ? NB : 1];
   __shared__ int missed;
   __shared__ uint32_t tag_lds;
 
@@ -437,106 +449,298 @@ __global__ __launch_bounds__(WAVES * 64) void rot_quant_fused_kernel(
     lm[p] = x;
   }
 
-  // The workgroup's group maxima: over slots, over the wave's rows (lanes with
-  // the same l), over the g / 64 lanes of a group, then over the waves in LDS
-  // (a fixed tree, no atomics); published as tagged entries.
-  float pm = lm[0];
+  if constexpr (kOrder) {
+    // The workgroup's block maxima: lane l's positions 64 l .. 64 l + 63 are
+    // blocks 2 l and 2 l + 1; over slots, over the wave's rows, then over the
+    // waves in LDS (a fixed order, no atomics).
+    float b0 = 0.0f, b1 = 0.0f;
 #pragma unroll
-  for (int p = 1; p < SLOTS; ++p) pm = fmaxf(pm, lm[p]);
+    for (int p = 0; p < SLOTS; ++p)
 #pragma unroll
-  for (int o = S::R; o < 64; o <<= 1) pm = fmaxf(pm, __shfl_xor(pm, o, 64));
-  for (int o = 1; o < g / 64; o <<= 1) pm = fmaxf(pm, __shfl_xor(pm, o, 64));
-  if (sub == 0 && (64 * l) % g == 0) wmax[wave][(64 * l) / g] = pm;
-  if (tid == 0) {
-    missed = 0;
-    tag_lds = next_epoch(epoch);
-  }
-  __syncthreads();
-  const uint32_t tag = tag_lds;
-  if (tid < G) {
-    float m = wmax[0][tid];
-#pragma unroll
-    for (int w = 1; w < WAVES; ++w) m = fmaxf(m, wmax[w][tid]);
-    publish_tagged(tagged + (size_t)blockIdx.x * G + tid, tag, m);
-  }
-
-  // s_b = max over the nrows rows of maxima; r_b = fl(1 / s_b). Thread t takes
-  // group t % G of rows t / G, t / G + NT / G, ...: the entries of a batch are
-  // requested at once, and those whose tag is not set yet are requested again,
-  // within a budget of max_polls rounds per batch.
-  {
-    // Entries per thread at most: 256 rows / (NT / G). One batch, except at
-    // eight waves for g = 64 (two batches of 16: one more round trip, and the
-    // words stay in registers next to the kept rows).
-    constexpr int NE = 256 * (kWideG ? GMAX : GMAX / 2) / NT;
-    constexpr int NEB = (WAVES == 8 && NE > 16) ? 16 : NE;
-    const int b = tid % G;
-    const int ns = NT / G;  // slices of rows
-    const unsigned long long none = (unsigned long long)tag << 32;  // an absent row: 0.0
-    float m = 0.0f;
-    bool ok = true;
-#pragma unroll
-    for (int k0 = 0; k0 < NE; k0 += NEB) {
-      unsigned long long x[NEB];
-#pragma unroll
-      for (int k = 0; k < NEB; ++k) {
-        const int i = tid / G + (k0 + k) * ns;
-        x[k] = i < nrows ? load_tagged(tagged + (size_t)i * G + b) : none;
+      for (int e = 0; e < 32; ++e) {
+        b0 = fmaxf(b0, fabsf(v[p][e]));
+        b1 = fmaxf(b1, fabsf(v[p][32 + e]));
       }
-      bool bok = false;
-      for (int round = 0;; ++round) {
-        bok = true;
 #pragma unroll
-        for (int k = 0; k < NEB; ++k) bok = bok && has_tag(x[k], tag);
-        if (bok || round >= max_polls) break;
+    for (int o = S::R; o < 64; o <<= 1) {
+      b0 = fmaxf(b0, __shfl_xor(b0, o, 64));
+      b1 = fmaxf(b1, __shfl_xor(b1, o, 64));
+    }
+    if (sub == 0) {
+      wmax[wave][2 * l] = b0;
+      wmax[wave][2 * l + 1] = b1;
+    }
+    if (tid == 0) {
+      missed = 0;
+      tag_lds = next_epoch(epoch);
+    }
+    __syncthreads();
+    const uint32_t tag = tag_lds;
+    if (tid < NB) {
+      float m = wmax[0][tid];
+#pragma unroll
+      for (int w = 1; w < WAVES; ++w) m = fmaxf(m, wmax[w][tid]);
+      publish_tagged(tagged + (size_t)blockIdx.x * NB + tid, tag, m);
+    }
+
+    // Keys over all rows, in two levels so that no workgroup reads every
+    // workgroup's row of words: the first workgroup of each run of kOrderRun
+    // (the run's leader) reads the run's rows and publishes their maximum as
+    // the run's row in tagged2; every workgroup then reads the runs' rows. A
+    // leader whose wait ran out publishes its row as failed (sign bit set:
+    // keys are never negative), so the failure reaches every reader. Thread
+    // t serves block t / TPB, and reads every TPB-th word of a run.
+    constexpr int TPB = NT / NB < kOrderRun ? NT / NB : kOrderRun;  // threads per block
+    constexpr int NW = kOrderRun / TPB;                            // words per thread
+    const int bb = tid / TPB;
+    const int tp = tid % TPB;
+    const bool serve = bb < NB;
+    const unsigned long long none = (unsigned long long)tag << 32;  // absent: 0.0
+    // Maximum of the NW words this thread reads from rows[first + tp + k TPB]
+    // (k < NW, row index < count) of `words`; false if a wait ran out or a
+    // word was marked failed.
+    auto gather = [&](const unsigned long long* words, int first, int count, float* out) {
+      unsigned long long x[NW];
+#pragma unroll
+      for (int k = 0; k < NW; ++k) {
+        const int i = tp + k * TPB;
+        x[k] = (serve && i < count) ? load_tagged(words + (size_t)(first + i) * NB + bb) : none;
+      }
+      bool ok = false;
+      for (int round = 0;; ++round) {
+        ok = true;
+#pragma unroll
+        for (int k = 0; k < NW; ++k) ok = ok && has_tag(x[k], tag);
+        if (ok || round >= max_polls) break;
         __builtin_amdgcn_s_sleep(1);
 #pragma unroll
-        for (int k = 0; k < NEB; ++k) {
-          const int i = tid / G + (k0 + k) * ns;
-          if (!has_tag(x[k], tag)) x[k] = load_tagged(tagged + (size_t)i * G + b);
+        for (int k = 0; k < NW; ++k) {
+          const int i = tp + k * TPB;
+          if (!has_tag(x[k], tag)) x[k] = load_tagged(words + (size_t)(first + i) * NB + bb);
         }
       }
-      ok = ok && bok;
+      float m = 0.0f;
 #pragma unroll
-      for (int k = 0; k < NEB; ++k) m = fmaxf(m, __uint_as_float((uint32_t)x[k]));
+      for (int k = 0; k < NW; ++k) {
+        const uint32_t fb = (uint32_t)x[k];
+        ok = ok && !(fb >> 31);
+        m = fmaxf(m, __uint_as_float(fb & 0x7FFFFFFFu));
+      }
+      // over the TPB threads of the block (consecutive lanes)
+      int okv = ok ? 1 : 0;
+#pragma unroll
+      for (int o = 1; o < TPB; o <<= 1) {
+        m = fmaxf(m, __shfl_xor(m, o, 64));
+        okv &= __shfl_xor(okv, o, 64);
+      }
+      *out = m;
+      return okv != 0;
+    };
+    const int run = blockIdx.x / kOrderRun;
+    const int nruns = (nrows + kOrderRun - 1) / kOrderRun;
+    if (blockIdx.x % kOrderRun == 0) {
+      float m1 = 0.0f;
+      const int first = run * kOrderRun;
+      const bool ok1 = gather(tagged, first, min(kOrderRun, nrows - first), &m1);
+      if (serve && tp == 0)
+        publish_tagged(tagged2 + (size_t)run * NB + bb, tag,
+                       ok1 ? m1 : __uint_as_float(0x80000000u));
     }
-    if (!ok) missed = 1;  // benign race: every writer writes 1
-    red[tid] = m;
+    {
+      float m2 = 0.0f;
+      bool ok2 = true;
+      for (int r0 = 0; r0 < nruns; r0 += kOrderRun) {
+        float mm = 0.0f;
+        ok2 = gather(tagged2, r0, min(kOrderRun, nruns - r0), &mm) && ok2;
+        m2 = fmaxf(m2, mm);
+      }
+      if (!ok2) missed = 1;  // benign race: every writer writes 1
+      if (serve && tp == 0) key[bb] = m2;
+    }
     __syncthreads();
-    // Every word of the call has been read (or given up on): advance the epoch
-    // (workgroup 0 only: one store instead of a contended one per workgroup).
     if (tid == 0) {
+      // Every word of the call has been read (or given up on): advance the
+      // epoch (workgroup 0 only).
       if (missed)
         __hip_atomic_store(header + kFailWord, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (blockIdx.x == 0)
         __hip_atomic_store(header + kEpochWord, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    if (tid < G) {
-      float sv = red[tid];
-      for (int q = 1; q < ns; ++q) sv = fmaxf(sv, red[q * G + tid]);
-      rg[tid] = (sv == 0.0f) ? 0.0f : __fdiv_rn(1.0f, sv);
-      if (blockIdx.x == 0) s_group[tid] = missed ? __builtin_nanf("") : sv;
+    // Rank of block t: blocks with a larger key, or an equal key and a smaller
+    // index, come first (broadcast LDS reads).
+    if (tid < NB) {
+      const float c = key[tid];
+      int rank = 0;
+#pragma unroll 4
+      for (int q = 0; q < NB / 4; ++q) {
+        const float4 k4 = reinterpret_cast<const float4*>(key)[q];
+        const int b4 = 4 * q;
+        rank += (k4.x > c || (k4.x == c && b4 < tid)) ? 1 : 0;
+        rank += (k4.y > c || (k4.y == c && b4 + 1 < tid)) ? 1 : 0;
+        rank += (k4.z > c || (k4.z == c && b4 + 2 < tid)) ? 1 : 0;
+        rank += (k4.w > c || (k4.w == c && b4 + 3 < tid)) ? 1 : 0;
+      }
+      sblk[rank] = tid;
+      skey[rank] = c;
     }
     __syncthreads();
-  }
-  const bool failed = missed != 0;  // uniform over the workgroup
+    const bool failed = missed != 0;  // uniform over the workgroup
+    // s_b over the sorted blocks of group b.
+    if (tid < G) {
+      const int per = g / kReorderBlock;
+      float sv = 0.0f;
+      for (int u = 0; u < per; ++u) sv = fmaxf(sv, skey[tid * per + u]);
+      rg[tid] = (sv == 0.0f) ? 0.0f : __fdiv_rn(1.0f, sv);
+      if (blockIdx.x == 0) s_group[tid] = failed ? __builtin_nanf("") : sv;
+    }
+    if (blockIdx.x == 0 && tid < NB) block_order[tid] = sblk[tid];
+    __syncthreads();
 
-  // Phase 2: token scale and codes of every kept row.
-  const float rb = rg[(64 * l) / g];
+    // Phase 2 over the sorted positions: 64 l .. 64 l + 63 are sorted blocks
+    // 2 l and 2 l + 1 (masked into range, as the other reorder kernels do),
+    // gathered from the kept row through this row's LDS region.
+    const float rb = rg[(64 * l) / g];
+    const int c0 = (sblk[2 * l] & (NB - 1)) * kReorderBlock;
+    const int c1 = (sblk[2 * l + 1] & (NB - 1)) * kReorderBlock;
 #pragma unroll
-  for (int p = 0; p < SLOTS; ++p) {
-    const int r = row_of(p);
-    const float a = row_max<S::R>(lm[p] * rb);  // max over the row's groups of fl(M_ib r_b)
-    const float inv = (a == 0.0f) ? 0.0f : __fdiv_rn(7.0f, a);
-    const float m = rb * inv;                   // fl(r_b * inv_i)
-    if (r < r1) {
-      uint32_t wd[8];
+    for (int p = 0; p < SLOTS; ++p) {
+      const int r = row_of(p);
 #pragma unroll
-      for (int w = 0; w < 8; ++w) wd[w] = quant_pack8(&v[p][8 * w], m);
-      uint4* dst = reinterpret_cast<uint4*>(Xq + (size_t)r * (K / 2) + 32 * l);
-      dst[0] = make_uint4(wd[0], wd[1], wd[2], wd[3]);
-      dst[1] = make_uint4(wd[4], wd[5], wd[6], wd[7]);
-      if (l == 0) a_scale[r] = failed ? __builtin_nanf("") : __fdiv_rn(a, 7.0f);
+      for (int m = 0; m < 16; ++m)
+        *reinterpret_cast<float4*>(row + lds_a(64 * l + 4 * m)) =
+            make_float4(v[p][4 * m], v[p][4 * m + 1], v[p][4 * m + 2], v[p][4 * m + 3]);
+      float* u = v[p];  // the natural order is in LDS now
+#pragma unroll
+      for (int m = 0; m < 8; ++m) {
+        const float4 x0 = *reinterpret_cast<const float4*>(row + lds_a(c0 + 4 * m));
+        const float4 x1 = *reinterpret_cast<const float4*>(row + lds_a(c1 + 4 * m));
+        u[4 * m] = x0.x;
+        u[4 * m + 1] = x0.y;
+        u[4 * m + 2] = x0.z;
+        u[4 * m + 3] = x0.w;
+        u[32 + 4 * m] = x1.x;
+        u[32 + 4 * m + 1] = x1.y;
+        u[32 + 4 * m + 2] = x1.z;
+        u[32 + 4 * m + 3] = x1.w;
+      }
+      float x = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 64; ++e) x = fmaxf(x, fabsf(u[e]));
+      const float a = row_max<S::R>(x * rb);  // max over the row's groups of fl(M_ib r_b)
+      const float inv = (a == 0.0f) ? 0.0f : __fdiv_rn(7.0f, a);
+      const float mm = rb * inv;             // fl(r_b * inv_i)
+      if (r < r1) {
+        uint32_t wd[8];
+#pragma unroll
+        for (int w = 0; w < 8; ++w) wd[w] = quant_pack8(&u[8 * w], mm);
+        uint4* dst = reinterpret_cast<uint4*>(Xq + (size_t)r * (K / 2) + 32 * l);
+        dst[0] = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+        dst[1] = make_uint4(wd[4], wd[5], wd[6], wd[7]);
+        if (l == 0) a_scale[r] = failed ? __builtin_nanf("") : __fdiv_rn(a, 7.0f);
+      }
+    }
+  } else {
+    // The workgroup's group maxima: over slots, over the wave's rows (lanes with
+    // the same l), over the g / 64 lanes of a group, then over the waves in LDS
+    // (a fixed tree, no atomics); published as tagged entries.
+    float pm = lm[0];
+#pragma unroll
+    for (int p = 1; p < SLOTS; ++p) pm = fmaxf(pm, lm[p]);
+#pragma unroll
+    for (int o = S::R; o < 64; o <<= 1) pm = fmaxf(pm, __shfl_xor(pm, o, 64));
+    for (int o = 1; o < g / 64; o <<= 1) pm = fmaxf(pm, __shfl_xor(pm, o, 64));
+    if (sub == 0 && (64 * l) % g == 0) wmax[wave][(64 * l) / g] = pm;
+    if (tid == 0) {
+      missed = 0;
+      tag_lds = next_epoch(epoch);
+    }
+    __syncthreads();
+    const uint32_t tag = tag_lds;
+    if (tid < G) {
+      float m = wmax[0][tid];
+#pragma unroll
+      for (int w = 1; w < WAVES; ++w) m = fmaxf(m, wmax[w][tid]);
+      publish_tagged(tagged + (size_t)blockIdx.x * G + tid, tag, m);
+    }
+
+    // s_b = max over the nrows rows of maxima; r_b = fl(1 / s_b). Thread t takes
+    // group t % G of rows t / G, t / G + NT / G, ...: the entries of a batch are
+    // requested at once, and those whose tag is not set yet are requested again,
+    // within a budget of max_polls rounds per batch.
+    {
+      // Entries per thread at most: 256 rows / (NT / G). One batch, except at
+      // eight waves for g = 64 (two batches of 16: one more round trip, and the
+      // words stay in registers next to the kept rows).
+      constexpr int NE = 256 * (kWideG ? GMAX : GMAX / 2) / NT;
+      constexpr int NEB = (WAVES == 8 && NE > 16) ? 16 : NE;
+      const int b = tid % G;
+      const int ns = NT / G;  // slices of rows
+      const unsigned long long none = (unsigned long long)tag << 32;  // an absent row: 0.0
+      float m = 0.0f;
+      bool ok = true;
+#pragma unroll
+      for (int k0 = 0; k0 < NE; k0 += NEB) {
+        unsigned long long x[NEB];
+#pragma unroll
+        for (int k = 0; k < NEB; ++k) {
+          const int i = tid / G + (k0 + k) * ns;
+          x[k] = i < nrows ? load_tagged(tagged + (size_t)i * G + b) : none;
+        }
+        bool bok = false;
+        for (int round = 0;; ++round) {
+          bok = true;
+#pragma unroll
+          for (int k = 0; k < NEB; ++k) bok = bok && has_tag(x[k], tag);
+          if (bok || round >= max_polls) break;
+          __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+          for (int k = 0; k < NEB; ++k) {
+            const int i = tid / G + (k0 + k) * ns;
+            if (!has_tag(x[k], tag)) x[k] = load_tagged(tagged + (size_t)i * G + b);
+          }
+        }
+        ok = ok && bok;
+#pragma unroll
+        for (int k = 0; k < NEB; ++k) m = fmaxf(m, __uint_as_float((uint32_t)x[k]));
+      }
+      if (!ok) missed = 1;  // benign race: every writer writes 1
+      red[tid] = m;
+      __syncthreads();
+      // Every word of the call has been read (or given up on): advance the epoch
+      // (workgroup 0 only: one store instead of a contended one per workgroup).
+      if (tid == 0) {
+        if (missed)
+          __hip_atomic_store(header + kFailWord, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (blockIdx.x == 0)
+          __hip_atomic_store(header + kEpochWord, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      if (tid < G) {
+        float sv = red[tid];
+        for (int q = 1; q < ns; ++q) sv = fmaxf(sv, red[q * G + tid]);
+        rg[tid] = (sv == 0.0f) ? 0.0f : __fdiv_rn(1.0f, sv);
+        if (blockIdx.x == 0) s_group[tid] = missed ? __builtin_nanf("") : sv;
+      }
+      __syncthreads();
+    }
+    const bool failed = missed != 0;  // uniform over the workgroup
+
+    // Phase 2: token scale and codes of every kept row.
+    const float rb = rg[(64 * l) / g];
+#pragma unroll
+    for (int p = 0; p < SLOTS; ++p) {
+      const int r = row_of(p);
+      const float a = row_max<S::R>(lm[p] * rb);  // max over the row's groups of fl(M_ib r_b)
+      const float inv = (a == 0.0f) ? 0.0f : __fdiv_rn(7.0f, a);
+      const float m = rb * inv;                   // fl(r_b * inv_i)
+      if (r < r1) {
+        uint32_t wd[8];
+#pragma unroll
+        for (int w = 0; w < 8; ++w) wd[w] = quant_pack8(&v[p][8 * w], m);
+        uint4* dst = reinterpret_cast<uint4*>(Xq + (size_t)r * (K / 2) + 32 * l);
+        dst[0] = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+        dst[1] = make_uint4(wd[4], wd[5], wd[6], wd[7]);
+        if (l == 0) a_scale[r] = failed ? __builtin_nanf("") : __fdiv_rn(a, 7.0f);
+      }
     }
   }
 }
@@ -688,6 +892,37 @@ hipError_t launch_quantize_ordered_wave(const uint16_t* X, int M, int K, int g, 
 #undef RRS_ORD_W
 }
 
+template <int K>
+hipError_t launch_fused_order_k(const uint16_t* X, int M, int g, bool rot, uint8_t* Xq,
+                                float* a_scale, float* s_group, int32_t* block_order,
+                                uint32_t* header, unsigned long long* tagged,
+                                unsigned long long* tagged2, int max_wgs, int extra_rows,
+                                int max_polls, hipStream_t stream) {
+  // Same shapes as the plain form (the block words need no more registers at
+  // four waves than at eight).
+  constexpr int RW = WaveRow<K>::RW;
+  const int waves = M <= max_wgs * 4 * RW ? 4 : kFusedWaves;
+  const int per_slot = waves * RW;
+  const int slots = M <= max_wgs * per_slot ? 1 : 2;
+  const int rpw = slots * per_slot;
+  const int wgs = (M + rpw - 1) / rpw;
+  const int nrows = wgs + extra_rows;  // rows of block words the readers wait for
+  if (wgs > max_wgs || nrows > 256) return hipErrorInvalidValue;
+  const int polls = max_polls > 0 ? max_polls : kFusedMaxPolls;
+#define RRS_FUSED_O(R_, S_, W_)                                                                 \
+  rot_quant_fused_kernel<K, R_, S_, W_, false, true><<<wgs, W_ * 64, 0, stream>>>(              \
+      X, M, g, rpw, header, tagged, nrows, polls, Xq, a_scale, s_group, tagged2, block_order)
+  if (waves == 4) {
+    if (rot) RRS_FUSED_O(true, 1, 4); else RRS_FUSED_O(false, 1, 4);
+  } else if (rot) {
+    if (slots == 1) RRS_FUSED_O(true, 1, kFusedWaves); else RRS_FUSED_O(true, 2, kFusedWaves);
+  } else {
+    if (slots == 1) RRS_FUSED_O(false, 1, kFusedWaves); else RRS_FUSED_O(false, 2, kFusedWaves);
+  }
+#undef RRS_FUSED_O
+  return hipGetLastError();
+}
+
 bool fused_quant_fits(int M, int K, int max_wgs) {
   if (K < 512 || K > 4096) return false;
   const int per_wg = 2 * kFusedWaves * (64 * 64 / K);  // two slots of rows per wave
@@ -707,6 +942,27 @@ hipError_t launch_rotate_smooth_quant_fused(const uint16_t* X, int M, int K, int
     RRS_FK(2048);
     RRS_FK(4096);
 #undef RRS_FK
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_rotate_smooth_quant_fused_order(const uint16_t* X, int M, int K, int g,
+                                                  bool rotate, uint8_t* Xq, float* a_scale,
+                                                  float* s_group, int32_t* block_order,
+                                                  uint32_t* header, unsigned long long* tagged,
+                                                  unsigned long long* tagged2, int max_wgs,
+                                                  hipStream_t stream, int extra_rows,
+                                                  int max_polls) {
+  switch (K) {
+#define RRS_FO(K_)                                                                            \
+  case K_: return launch_fused_order_k<K_>(X, M, g, rotate, Xq, a_scale, s_group, block_order, \
+                                           header, tagged, tagged2, max_wgs, extra_rows,       \
+                                           max_polls, stream)
+    RRS_FO(512);
+    RRS_FO(1024);
+    RRS_FO(2048);
+    RRS_FO(4096);
+#undef RRS_FO
     default: return hipErrorInvalidValue;
   }
 }

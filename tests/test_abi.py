@@ -377,9 +377,11 @@ def test_reorder_workspace_queries():
     a256 = lambda x: (x + 255) // 256 * 256  # noqa: E731
     for M, K, g in ((16, 512, 128), (2048, 4096, 128), (8, 8192, 64), (3, 16384, 512)):
         q = lib.rrs_reorder_workspace_bytes(M, K, g)
-        # the one-launch kernel's header and 16 rows of K/32 tagged words, then
-        # 256 rows of K/32 block maxima (the two-launch path)
-        assert q == 256 + a256(16 * (K // 32) * 8) + a256(256 * (K // 32) * 4)
+        # the one-launch kernels' header and 16 rows of K/32 tagged words, then
+        # 256 rows of K/32 block maxima (the two-launch path), then, at K <= 4096,
+        # 256 rows of K/32 tagged words (the many-token one-launch kernel)
+        words = a256(256 * (K // 32) * 8) if K <= 4096 else 0
+        assert q == 256 + a256(16 * (K // 32) * 8) + a256(256 * (K // 32) * 4) + words
         lw = lib.rrs_linear_reorder_workspace_bytes(M, K, g)
         assert lw == q + a256(M * K // 2) + a256(4 * M) + a256(4 * (K // g)) + a256(4 * (K // 32))
     for bad in ((0, 512, 128), (16, 500, 128), (16, 512, 32), (16, 512, 1024)):
@@ -490,7 +492,8 @@ def test_quant_reorder_wait_hook_checks():
     for key in ("X", "Xq", "a", "s", "o", "ws", "n"):
         assert _rwait(**{key: None}) == NULL, key
     assert _rwait(M=1) == SHAPE            # one row: no exchange
-    assert _rwait(M=17) == SHAPE           # more than 16 rows: two launches
+    assert _rwait(M=17, K=8192) == SHAPE   # more than 16 rows above K = 4096: two launches
+    assert _rwait(M=5000, K=4096) == SHAPE  # more rows than one launch holds at K = 4096
     assert _rwait(K=16384) == SHAPE        # K > 8192: two launches
     assert _rwait(K=1000) == SHAPE
     assert _rwait(g=96) == GROUP

@@ -211,9 +211,13 @@ def test_one_launch_wait_runs_out_loudly(M, K, g):
     np.testing.assert_array_equal(to_np(s), act.s)
 
 
-@pytest.mark.parametrize("M,K,g", [(2, 8192, 128), (8, 8192, 64), (15, 1024, 256)])
+@pytest.mark.parametrize("M,K,g", [(2, 8192, 128), (8, 8192, 64), (15, 1024, 256),
+                                   (64, 4096, 128), (100, 4096, 128), (600, 1024, 256)])
 def test_reorder_one_launch_wait_runs_out_loudly(M, K, g):
-    # the runtime-reorder quantizer's one-launch form (rows exchange block maxima)
+    # the runtime-reorder quantizer's one-launch forms: up to 16 rows, one
+    # workgroup per row; more rows at K <= 4096, runs of 16 workgroups (at
+    # 64 x 4096 the extra row opens a run with no workgroup to lead it, at
+    # 100 x 4096 and 600 x 1024 the last run's leader waits for it)
     rrs = _rrs()
     w = synth.custom("rw", M, K, 16, g, M + K + 1, n_chan=max(1, K // 100), n_spike=2,
                      spike_mag=(100, 500))

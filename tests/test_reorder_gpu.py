@@ -52,16 +52,18 @@ def _quant_case(X, g, flags, label):
     return act, order, (Xq, a, s, bo)
 
 
-# Three launches: team kernels (K in 512..2048 with more than 16 rows, 8192,
-# 16384) and one-wave-per-row kernels (K = 4096; K = 2048 from 512 rows). One
-# launch (the per-row kernel exchanging block maxima): up to 16 rows at
-# K <= 8192, including the decode shape.
+# One launch: the per-row kernel exchanging block maxima, up to 16 rows at
+# K <= 8192 (including the decode shape); the one-row-per-wave kernel with its
+# two-level exchange, more rows at K <= 4096 (four or eight waves, one or two
+# rows per wave). Two launches: K = 8192 / 16384 with more than 16 rows, and
+# more rows than the one-launch kernel holds.
 @pytest.mark.parametrize("M,K,g,flags", [
     (16, 512, 128, 0), (1, 512, 64, 0), (100, 1024, 256, 0), (37, 2048, 64, 0),
     (700, 2048, 128, 0), (5, 4096, 512, 0), (300, 8192, 64, 0), (9, 16384, 128, 0),
     (64, 4096, 128, 1), (20, 8192, 256, 1), (513, 1024, 512, 1),
     (2, 1024, 64, 0), (8, 8192, 128, 0), (16, 8192, 64, 0), (3, 2048, 256, 1),
     (12, 4096, 128, 1), (2, 8192, 512, 0), (1, 8192, 128, 0), (17, 8192, 128, 0),
+    (3000, 4096, 128, 0), (5000, 512, 64, 0), (9000, 1024, 128, 0), (4500, 4096, 256, 0),
 ])
 def test_quant_reorder(M, K, g, flags):
     _, X, _ = _case(M, K, 16, g, 7 + M + K + g)
@@ -79,6 +81,25 @@ def test_quant_reorder_one_launch_reuses_workspace():
         _, X, _ = _case(M, K, 16, g, 101 + i)
         act, order, _ = O.rotate_smooth_quant_reorder(X, g, BLOCK)
         print(f"[case] reorder one-launch reuse call {i} M={M}", flush=True)
+        Xq, a, s, bo = rrs.rotate_smooth_quant_reorder(to_gpu(X), g, workspace=ws)
+        np.testing.assert_array_equal(to_np(bo), order, err_msg=f"call {i}: block order")
+        np.testing.assert_array_equal(to_np(s), act.s, err_msg=f"call {i}: s_group")
+        np.testing.assert_array_equal(to_np(a), act.alpha, err_msg=f"call {i}: alpha")
+        flips = check_codes(to_np(Xq), act, f"call {i}")
+        assert flips == 0 or flips < 1e-6 * X.size
+
+
+def test_quant_reorder_many_rows_reuses_workspace():
+    # The many-token one-launch form: runs of workgroups and their leaders
+    # change with the row count; consecutive calls on one workspace must each
+    # match the oracle.
+    rrs = _rrs()
+    K, g = 4096, 128
+    ws = torch.zeros(rrs.reorder_workspace_bytes(2048, K, g), dtype=torch.uint8, device="cuda")
+    for i, M in enumerate((300, 2048, 17, 1000, 300)):
+        _, X, _ = _case(M, K, 16, g, 211 + i)
+        act, order, _ = O.rotate_smooth_quant_reorder(X, g, BLOCK)
+        print(f"[case] reorder many-row reuse call {i} M={M}", flush=True)
         Xq, a, s, bo = rrs.rotate_smooth_quant_reorder(to_gpu(X), g, workspace=ws)
         np.testing.assert_array_equal(to_np(bo), order, err_msg=f"call {i}: block order")
         np.testing.assert_array_equal(to_np(s), act.s, err_msg=f"call {i}: s_group")
