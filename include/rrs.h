@@ -287,15 +287,22 @@ rrs_status rrs_test_quant_rows_wait(const void* X, int M, int K, int group_size,
  * (not for computing: use rrs_rotate_smooth_quant_reorder). For 2 to 16 tokens
  * at K <= 8192, rrs_rotate_smooth_quant_reorder is one launch of one
  * workgroup per token row whose rows exchange their K/32 block maxima through
- * the workspace, under the same residency condition and bounded waits as the
- * one-launch rrs_rotate_smooth_quant (see rrs_test_quant_rows_wait). This
- * hook runs that kernel with the readers also waiting for extra_rows rows of
- * block maxima that no workgroup writes and giving up after max_polls rounds,
- * waits for `stream`, and stores 1 in *failed (host pointer) if the exchange
- * failed, else 0; a failed call leaves NaN in a_scale and s_group. Arguments
- * otherwise as rrs_rotate_smooth_quant_reorder (flags = 0); RRS_ERR_SHAPE
- * when the shape has no one-launch reorder (M < 2, M > 16 or K > 8192),
- * RRS_ERR_FLAGS for extra_rows < 0, max_polls < 1 or more than 16 rows in all.
+ * the workspace; for more tokens at K <= 4096 (as many as the one-launch
+ * rrs_rotate_smooth_quant takes) one launch of at most one workgroup per
+ * compute unit, whose workgroups exchange their block maxima in two levels
+ * (runs of 16 workgroups, then the runs). Both run under the same residency
+ * condition and bounded waits as the one-launch rrs_rotate_smooth_quant (see
+ * rrs_test_quant_rows_wait). This hook runs that kernel with the readers also
+ * waiting for extra_rows rows of block maxima (token rows, or workgroups in
+ * the many-token form) that no workgroup writes and giving up after
+ * max_polls rounds, waits for `stream`, and stores 1 in *failed (host
+ * pointer) if the exchange failed, else 0; a failed call leaves NaN in
+ * a_scale and s_group. Arguments otherwise as rrs_rotate_smooth_quant_reorder
+ * (flags = 0); RRS_ERR_SHAPE when the shape has no one-launch reorder (M < 2,
+ * K > 8192, or more than 16 tokens at K > 4096 or beyond the one-launch
+ * limit), RRS_ERR_FLAGS for extra_rows < 0, max_polls < 1, more than 16 rows
+ * in all (per-row form) or more than 256 workgroups' rows in all
+ * (many-token form).
  */
 rrs_status rrs_test_quant_reorder_wait(const void* X, int M, int K, int group_size,
                                       int extra_rows, int max_polls, void* Xq, float* a_scale,
@@ -403,9 +410,10 @@ enum { RRS_REORDER_BLOCK = 32 };
 
 /*
  * Bytes of device workspace rrs_rotate_smooth_quant_reorder needs (0 for
- * invalid arguments). It holds the one-launch kernel's header and exchanged
+ * invalid arguments). It holds the one-launch kernels' header and exchanged
  * block maxima (16 rows of K/32 tagged words), then up to 256 rows of K/32
- * block maxima for the two-launch path. As for
+ * block maxima for the two-launch path, then, at K <= 4096, 256 rows of K/32
+ * tagged words for the many-token one-launch kernel. As for
  * rrs_workspace_bytes, the workspace must hold zeros before its first use and
  * may then be reused by later calls (calls sharing one must not overlap).
  */
@@ -425,10 +433,13 @@ size_t rrs_reorder_workspace_bytes(int M, int K, int group_size);
  * smoothing the order changes nothing); RRS_WEIGHT_TILED is accepted and
  * ignored. Up to 16 tokens at K <= 8192 the call is one launch (one workgroup
  * per token row; the rows exchange their K/32 block maxima in the workspace
- * and every workgroup ranks the blocks itself, under the same residency
- * condition and bounded waits as the one-launch rrs_rotate_smooth_quant,
- * RRS_ERR_TIMEOUT under RRS_DEBUG); otherwise two launches (block maxima, then
- * quantization, whose every workgroup ranks the blocks itself).
+ * and every workgroup ranks the blocks itself); for more tokens at K <= 4096,
+ * as many as the one-launch rrs_rotate_smooth_quant takes, also one launch
+ * (workgroups exchange block maxima in two levels, rank the blocks and
+ * quantize the rows they kept). Both under the same residency condition and
+ * bounded waits as the one-launch rrs_rotate_smooth_quant (RRS_ERR_TIMEOUT
+ * under RRS_DEBUG). Otherwise two launches (block maxima, then quantization,
+ * whose every workgroup ranks the blocks itself).
  */
 rrs_status rrs_rotate_smooth_quant_reorder(const void* X, int M, int K, int group_size,
                                            int flags, void* Xq, float* a_scale,
