@@ -663,6 +663,7 @@ __global__ __launch_bounds__(WAVES * 64) void rot_quant_fused_kernel(
       publish_tagged(tagged + (size_t)blockIdx.x * G + tid, tag, m);
     }
 
+    float rb;  // r_b = fl(1 / s_b) of this lane's group
     // s_b = max over the nrows rows of maxima; r_b = fl(1 / s_b). Thread t takes
     // group t % G of rows t / G, t / G + NT / G, ...: the entries of a batch are
     // requested at once, and those whose tag is not set yet are requested again,
@@ -714,18 +715,21 @@ __global__ __launch_bounds__(WAVES * 64) void rot_quant_fused_kernel(
         if (blockIdx.x == 0)
           __hip_atomic_store(header + kEpochWord, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
-      if (tid < G) {
-        float sv = red[tid];
-        for (int q = 1; q < ns; ++q) sv = fmaxf(sv, red[q * G + tid]);
-        rg[tid] = (sv == 0.0f) ? 0.0f : __fdiv_rn(1.0f, sv);
-        if (blockIdx.x == 0) s_group[tid] = missed ? __builtin_nanf("") : sv;
+      // Every lane reduces the slices of its own group (positions 64 l ..
+      // 64 l + 63 lie in one group), so no barrier is needed before phase 2.
+      const int gb = (64 * l) / g;
+      float sv = red[gb];
+      for (int q = 1; q < ns; ++q) sv = fmaxf(sv, red[q * G + gb]);
+      rb = (sv == 0.0f) ? 0.0f : __fdiv_rn(1.0f, sv);
+      if (blockIdx.x == 0 && tid < G) {
+        float sg = red[tid];
+        for (int q = 1; q < ns; ++q) sg = fmaxf(sg, red[q * G + tid]);
+        s_group[tid] = missed ? __builtin_nanf("") : sg;
       }
-      __syncthreads();
     }
     const bool failed = missed != 0;  // uniform over the workgroup
 
     // Phase 2: token scale and codes of every kept row.
-    const float rb = rg[(64 * l) / g];
 #pragma unroll
     for (int p = 0; p < SLOTS; ++p) {
       const int r = row_of(p);
