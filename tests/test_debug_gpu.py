@@ -255,6 +255,20 @@ def test_quant_rows_debug_reports_no_false_timeout(debug_env):
     np.testing.assert_array_equal(to_np(a), act.alpha)
 
 
+@pytest.mark.parametrize("M,K", [(8, 8192), (300, 4096)])
+def test_reorder_debug_reports_no_false_timeout(debug_env, M, K):
+    # RRS_DEBUG checks the fail word after both one-launch reorder forms (per
+    # row, and runs of workgroups); a completed exchange must not report one.
+    rrs = _rrs()
+    g = 128
+    w = synth.custom("rd", M, K, 16, g, 78 + M, n_chan=80, n_spike=2)
+    Xh = synth.activations(w)
+    Xq, a, s, order = rrs.rotate_smooth_quant_reorder(to_gpu(Xh), g)  # raises on failure
+    act, border, _ = O.rotate_smooth_quant_reorder(Xh, g, 32)
+    np.testing.assert_array_equal(to_np(order), border)
+    np.testing.assert_array_equal(to_np(a), act.alpha)
+
+
 def test_quant_rows_hook_argument_checks():
     rrs = _rrs()
     lib = rrs.lib()
