@@ -365,7 +365,8 @@ def few_token_bench(torch, rrs, synth, reps=50):
     M = 1, 2, 4, 8, 16, 32, 64: quantizer, GEMM and the whole layer, each timed
     with HIP events around 50 back-to-back calls, weights cycling through 4
     copies. Up to M = 16 the quantizer is one launch with one workgroup per
-    row; up to M = 64 the GEMM is the few-token kernel. The *_tiled entries
+    row; the GEMM is the weight-streaming kernel up to M = 32 (eight waves
+    from 17 tokens) and the few-token kernel at M = 64. The *_tiled entries
     run the same calls on the tiled weight layout."""
     dev = torch.device("cuda:0")
     base = synth.WORKLOADS["decode"]

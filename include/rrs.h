@@ -56,7 +56,7 @@
  *      (n / 16) * 8K + (j / 64) * 1024 + ((j % 64) / 16) * 256
  *        + (n % 16) * 16 + j % 16.
  *    There a wave's load of one K tile of 16 channels is one contiguous 1 KB
- *    run: for 17 to 64 tokens the few-token GEMM streams it about 20 % faster
+ *    run: for 17 to 64 tokens the GEMM streams it about 15 to 20 % faster
  *    than the row-major rows (up to 16 tokens both layouts stream at about
  *    the same rate). Results are bit-identical in both layouts; a weight
  *    prepared with the flag must be multiplied with it, and one prepared

@@ -60,6 +60,15 @@
 //
 // Needs K >= 4 g (every wave holds whole groups): K = 512 with g <= 128,
 // K = 1024 with g <= 256, any g from K = 2048 (but g >= 256 at K = 16384).
+//
+// 17 to 32 tokens at K = 8192: the same loop with eight waves, each streaming
+// an eighth of K (16 rows x 512 bytes per block, the same 16 KB ring per wave)
+// and holding the codes of two blocks of 16 tokens (64 registers per block,
+// half of what a quarter of K would take), one workgroup of 512 threads per
+// compute unit (128 KB of ring and 32 KB of partial sums). Every weight
+// fragment is unpacked once for both token blocks; the 2 x 4 (token block,
+// accumulator row) pairs of each lane are dealt to the eight waves for the
+// fixed-order sum and the stores.
 #include "rrs_stream.h"
 
 namespace rrs {
@@ -67,27 +76,38 @@ namespace {
 
 using namespace stream;
 
-// kPartials (test hook): instead of Y, write P[b][i][n] for every group b,
-// token i < M and column n, decoded from the same seeded accumulators.
-template <int K, int GS, bool kTiled, bool kPartials>
-__global__ __launch_bounds__(kThreads) void gemm_stream_kernel(
+// W waves per workgroup, each streaming a 1/W slice of K; TB blocks of 16
+// tokens (tokens 16 u .. 16 u + 15 in block u), all multiplied with the same
+// weight operands. kPartials (test hook): instead of Y, write P[b][i][n] for
+// every group b, token i < M and column n, decoded from the same seeded
+// accumulators.
+template <int K, int GS, int W, int TB, bool kTiled, bool kPartials>
+__global__ __launch_bounds__(64 * W) void gemm_stream_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
     const float* __restrict__ w_scale, int M, int N, uint16_t* __restrict__ Y,
     int32_t* __restrict__ P, float out_scale) {
-  using S = StreamShape<K>;
+  using S = StreamShape<K, W>;
   constexpr int g = GS * 64;
   constexpr int GB = g / 2;                   // packed bytes of a row per group
-  constexpr int NG = S::R / GB;               // groups per wave (its quarter of K)
+  constexpr int NG = S::R / GB;               // groups per wave (its slice of K)
   constexpr int NGS = S::SBW / GB;            // groups per sub-buffer
   constexpr int NP = GB >= 64 ? GB / 64 : 1;  // 16-byte lane pieces per group
   static_assert(NGS >= 1 && S::SBW % GB == 0, "every sub-buffer holds whole groups");
-  __shared__ __attribute__((aligned(16))) uint8_t ring[kWaves * S::RS * S::SB];
-  __shared__ __attribute__((aligned(16))) v4f part[2][kWaves][64];
+  static_assert(NG <= 64, "one group scale per lane");
+  // The waves' fp32 sums of a block meet in `part`: double-buffered (one
+  // barrier per block) when both copies fit beside the ring, else one copy
+  // and a second barrier.
+  constexpr int kRingBytes = W * S::RS * S::SB;
+  constexpr int kPartBytes = W * TB * 64 * 16;
+  constexpr int PB = kRingBytes + 2 * kPartBytes <= 163840 ? 2 : 1;
+  static_assert(kRingBytes + PB * kPartBytes <= 163840, "LDS of one workgroup");
+  __shared__ __attribute__((aligned(16))) uint8_t ring[kRingBytes];
+  __shared__ __attribute__((aligned(16))) v4f part[PB][W][TB][64];
 
   const int t = threadIdx.x;
   const int lane = t & 63;
-  const int kq = __builtin_amdgcn_readfirstlane(t >> 6);  // K quarter of this wave
+  const int kq = __builtin_amdgcn_readfirstlane(t >> 6);  // K slice of this wave
   const int c = lane & 15;
   const int q = lane >> 4;
   constexpr size_t krow = (size_t)K / 2;
@@ -136,27 +156,30 @@ __global__ __launch_bounds__(kThreads) void gemm_stream_kernel(
   for (int i = 0; i < S::RS - 1; ++i)
     if (i < items) issue(i);
 
-  // Token codes of the wave's quarter (once per workgroup) and its group
+  // Token codes of the wave's slice (once per workgroup) and its group
   // scales (one per lane).
-  const uint8_t* abase = Xq + (size_t)min(c, M - 1) * krow + (size_t)kq * S::R;
-  uint32_t aw[NG][NP][4];
+  uint32_t aw[TB][NG][NP][4];
 #pragma unroll
-  for (int b = 0; b < NG; ++b) {
-    if constexpr (GB >= 64) {
+  for (int u = 0; u < TB; ++u) {
+    const uint8_t* abase = Xq + (size_t)min(16 * u + c, M - 1) * krow + (size_t)kq * S::R;
 #pragma unroll
-      for (int h = 0; h < NP; ++h) {
-        const uint4 v = *reinterpret_cast<const uint4*>(abase + b * GB + 64 * h + 16 * q);
-        aw[b][h][0] = v.x;
-        aw[b][h][1] = v.y;
-        aw[b][h][2] = v.z;
-        aw[b][h][3] = v.w;
+    for (int b = 0; b < NG; ++b) {
+      if constexpr (GB >= 64) {
+#pragma unroll
+        for (int h = 0; h < NP; ++h) {
+          const uint4 v = *reinterpret_cast<const uint4*>(abase + b * GB + 64 * h + 16 * q);
+          aw[u][b][h][0] = v.x;
+          aw[u][b][h][1] = v.y;
+          aw[u][b][h][2] = v.z;
+          aw[u][b][h][3] = v.w;
+        }
+      } else {
+        const uint2 v = *reinterpret_cast<const uint2*>(abase + b * GB + 8 * q);
+        aw[u][b][0][0] = v.x;
+        aw[u][b][0][1] = v.y;
+        aw[u][b][0][2] = 0u;
+        aw[u][b][0][3] = 0u;
       }
-    } else {
-      const uint2 v = *reinterpret_cast<const uint2*>(abase + b * GB + 8 * q);
-      aw[b][0][0] = v.x;
-      aw[b][0][1] = v.y;
-      aw[b][0][2] = 0u;
-      aw[b][0][3] = 0u;
     }
   }
   float sv = 0.0f;
@@ -165,17 +188,29 @@ __global__ __launch_bounds__(kThreads) void gemm_stream_kernel(
   constexpr int kMagic = 0x4B400000;  // bits of 1.5 * 2^23
   const v4i seed = GS > 4 ? v4i{0, 0, 0, 0} : v4i{kMagic, kMagic, kMagic, kMagic};
 
-  // Epilogue split: wave kq stores accumulator row kq of every lane, i.e.
-  // output row 4 q + kq, so the four waves share the stores.
-  const int orow = 4 * q + kq;
-  float oscale = 0.0f;  // alpha of that row times out_scale
-  if constexpr (!kPartials) oscale = a_scale[min(orow, M - 1)] * out_scale;
+  // Epilogue split: the TB x 4 pairs (token block u, accumulator row r) of
+  // every lane are dealt to the waves, pair x to wave x % W; pair (u, r) of
+  // lane (c, q) is output row 16 u + 4 q + r. With W = 4 and one token block,
+  // wave kq stores row 4 q + kq.
+  constexpr int NX = (4 * TB + W - 1) / W;  // pairs per wave
+  float oscale[NX];                         // alpha of the pair's row times out_scale
+#pragma unroll
+  for (int x = 0; x < NX; ++x) {
+    const int pi = kq + x * W;
+    const int row = 16 * (pi >> 2) + 4 * q + (pi & 3);
+    oscale[x] = 0.0f;
+    if constexpr (!kPartials) oscale[x] = a_scale[min(row, M - 1)] * out_scale;
+  }
 
   for (int tb = 0; tb < mine; ++tb) {
     const int blk = (int)blockIdx.x + tb * (int)gridDim.x;
     float bcol = 0.0f;  // beta of this lane's column, requested early
     if constexpr (!kPartials) bcol = w_scale[blk * kRows + c];
-    float f[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    float f[TB][4];
+#pragma unroll
+    for (int u = 0; u < TB; ++u)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) f[u][r] = 0.0f;
 #pragma unroll
     for (int sp = 0; sp < S::SPB; ++sp) {
       const int i = tb * S::SPB + sp;
@@ -190,7 +225,7 @@ __global__ __launch_bounds__(kThreads) void gemm_stream_kernel(
       const uint8_t* buf = my + (i % S::RS) * S::SB;
 #pragma unroll
       for (int bl = 0; bl < NGS; ++bl) {
-        const int b = sp * NGS + bl;  // group of the wave's quarter
+        const int b = sp * NGS + bl;  // group of the wave's slice
         uint32_t ww[NP][4];
 #pragma unroll
         for (int h = 0; h < NP; ++h) {
@@ -208,100 +243,118 @@ __global__ __launch_bounds__(kThreads) void gemm_stream_kernel(
             ww[h][3] = 0u;
           }
         }
-        v4i acc = seed;
+        v4i acc[TB];
+#pragma unroll
+        for (int u = 0; u < TB; ++u) acc[u] = seed;
 #pragma unroll
         for (int st = 0; st < GS; ++st) {
           const int h = st >> 1;
           const int o = 2 * (st & 1);
-          acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(unpack_pair(aw[b][h][o], aw[b][h][o + 1]),
-                                                      unpack_pair(ww[h][o], ww[h][o + 1]), acc,
-                                                      0, 0, 0);
+          const v4i wv = unpack_pair(ww[h][o], ww[h][o + 1]);
+#pragma unroll
+          for (int u = 0; u < TB; ++u)
+            acc[u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(
+                unpack_pair(aw[u][b][h][o], aw[u][b][h][o + 1]), wv, acc[u], 0, 0, 0);
         }
         if constexpr (kPartials) {
           int32_t* Pg = P + (size_t)(kq * NG + b) * (size_t)M * (size_t)N;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int row = 4 * q + r;
-            if (row < M)
-              Pg[(size_t)row * N + blk * kRows + c] = (GS > 4 ? acc[r] : acc[r] - kMagic) >> 8;
-          }
+          for (int u = 0; u < TB; ++u)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int row = 16 * u + 4 * q + r;
+              if (row < M)
+                Pg[(size_t)row * N + blk * kRows + c] =
+                    (GS > 4 ? acc[u][r] : acc[u][r] - kMagic) >> 8;
+            }
         } else {
           const float s =
               __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sv), b));
-          // Bit-cast the whole vector, then index: bit-casting a single element
-          // of an ext_vector is miscompiled (every element reads element 0).
-          const v4f accf = __builtin_bit_cast(v4f, acc);
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float pv = GS > 4 ? (float)acc[r] : accf[r] - 12582912.0f;
-            f[r] = __builtin_fmaf(s, pv, f[r]);
+          for (int u = 0; u < TB; ++u) {
+            // Bit-cast the whole vector, then index: bit-casting a single
+            // element of an ext_vector is miscompiled (every element reads
+            // element 0).
+            const v4f accf = __builtin_bit_cast(v4f, acc[u]);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float pv = GS > 4 ? (float)acc[u][r] : accf[r] - 12582912.0f;
+              f[u][r] = __builtin_fmaf(s, pv, f[u][r]);
+            }
           }
         }
       }
     }
     if constexpr (!kPartials) {
-      // The four quarters' sums of this block, added in the order kq = 0..3
-      // (part is double-buffered, so one barrier per block suffices).
-      part[tb & 1][kq][lane] = v4f{f[0], f[1], f[2], f[3]};
-      __syncthreads();
-      float sum = part[tb & 1][0][lane][kq];
+      // The W slices' sums of this block, added in the order kq = 0 .. W - 1.
+      const int pb = PB == 2 ? (tb & 1) : 0;
 #pragma unroll
-      for (int p = 1; p < kWaves; ++p) sum += part[tb & 1][p][lane][kq];
-      // out_scale = 2^-8 (undoes the 16 x 16 of the unpacked operands) / K (the
-      // unnormalized rotation; 1 without rotation), an exact power of two.
-      if (orow < M)
-        Y[(size_t)orow * N + blk * kRows + c] =
-            __builtin_bit_cast(uint16_t, (_Float16)((sum * oscale) * bcol));
+      for (int u = 0; u < TB; ++u) part[pb][kq][u][lane] = v4f{f[u][0], f[u][1], f[u][2], f[u][3]};
+      __syncthreads();
+#pragma unroll
+      for (int x = 0; x < NX; ++x) {
+        const int pi = kq + x * W;
+        if (pi < 4 * TB) {
+          const int u = pi >> 2;
+          const int r = pi & 3;
+          float sum = part[pb][0][u][lane][r];
+#pragma unroll
+          for (int p = 1; p < W; ++p) sum += part[pb][p][u][lane][r];
+          const int row = 16 * u + 4 * q + r;
+          // out_scale = 2^-8 (undoes the 16 x 16 of the unpacked operands) / K
+          // (the unnormalized rotation; 1 without rotation), an exact power of two.
+          if (row < M)
+            Y[(size_t)row * N + blk * kRows + c] =
+                __builtin_bit_cast(uint16_t, (_Float16)((sum * oscale[x]) * bcol));
+        }
+      }
+      if constexpr (PB == 1) __syncthreads();  // every wave has read `part`
     }
   }
 }
 
-template <int K, bool kPartials>
+// Shapes each form of the kernel takes (K, g powers of two, g <= 512).
+// W = 4, one token block: every wave holds whole groups (K >= 4 g); K = 16384
+// with g <= 128 keeps 32 or 64 groups of token codes per wave, which do not fit
+// the registers next to the loop. W = 8, two token blocks: K = 8192 only. The
+// form compiles without spills wherever K >= 1024, K >= 8 g and TB K <= 16384,
+// but it beats the few-token kernel only where the weight stream dominates:
+// at K = 8192, N = 28672 it takes 28.1 / 30.3 / 31.6 us at M = 17 / 24 / 32
+// (row-major; 23.4 / 24.8 / 26.1 tiled) against 34.3 / 35.7 / 36.6 (27.3 /
+// 28.8 / 30.0); at K = 4096, N = 12288 it ties up to 32 tokens and loses with
+// three or four token blocks (13.7 against 12.7 us at M = 64); at K = 8192
+// three or four token blocks spill.
+constexpr bool stream_form_fits(int K, int W, int TB, int g) {
+  return W == 4 ? (TB == 1 && K >= 4 * g && !(K == 16384 && g <= 128))
+                : (W == 8 && TB == 2 && K == 8192 && K >= 8 * g);
+}
+
+template <int K, int W, int TB, bool kPartials>
 hipError_t launch_k(const uint8_t* Xq, const float* a_scale, const float* s_group,
                     const uint8_t* Wq, const float* w_scale, int M, int N, int g, uint16_t* Y,
                     int32_t* P, float out_scale, hipStream_t stream, bool tiled) {
   const int nblk = N / kRows;  // N % 16 == 0 (API precondition)
-#define RRS_STREAM_T(GS_, T_)                                                             \
-  {                                                                                       \
-    auto kern = gemm_stream_kernel<K, GS_, T_, kPartials>;                                \
-    kern<<<resident_grid(kern, nblk), kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq,    \
-                                                             w_scale, M, N, Y, P,         \
-                                                             out_scale);                  \
+#define RRS_STREAM_T(GS_, T_)                                                              \
+  {                                                                                        \
+    constexpr auto kern = gemm_stream_kernel<K, GS_, W, TB, T_, kPartials>;                \
+    kern<<<resident_grid<kern>(nblk, 64 * W), 64 * W, 0, stream>>>(Xq, a_scale, s_group,    \
+                                                                   Wq, w_scale, M, N, Y, P, \
+                                                                   out_scale);              \
   }
-#define RRS_STREAM(GS_)    \
-  if (tiled)               \
-    RRS_STREAM_T(GS_, true) \
-  else                     \
-    RRS_STREAM_T(GS_, false)
+#define RRS_STREAM(GS_)                             \
+  if constexpr (stream_form_fits(K, W, TB, GS_ * 64)) { \
+    if (tiled)                                      \
+      RRS_STREAM_T(GS_, true)                       \
+    else                                            \
+      RRS_STREAM_T(GS_, false)                      \
+  } else {                                          \
+    return hipErrorInvalidValue;                    \
+  }
   switch (g) {
-    case 64:
-      if constexpr (K <= 8192) {
-        RRS_STREAM(1)
-      } else {
-        return hipErrorInvalidValue;
-      }
-      break;
-    case 128:
-      if constexpr (K <= 8192) {
-        RRS_STREAM(2)
-      } else {
-        return hipErrorInvalidValue;
-      }
-      break;
-    case 256:
-      if constexpr (K >= 1024) {
-        RRS_STREAM(4)
-      } else {
-        return hipErrorInvalidValue;
-      }
-      break;
-    case 512:
-      if constexpr (K >= 2048) {
-        RRS_STREAM(8)
-      } else {
-        return hipErrorInvalidValue;
-      }
-      break;
+    case 64: RRS_STREAM(1) break;
+    case 128: RRS_STREAM(2) break;
+    case 256: RRS_STREAM(4) break;
+    case 512: RRS_STREAM(8) break;
     default: return hipErrorInvalidValue;
   }
 #undef RRS_STREAM
@@ -309,15 +362,16 @@ hipError_t launch_k(const uint8_t* Xq, const float* a_scale, const float* s_grou
   return hipGetLastError();
 }
 
-template <bool kPartials>
+template <int W, int TB, bool kPartials>
 hipError_t launch_any(const uint8_t* Xq, const float* a_scale, const float* s_group,
                       const uint8_t* Wq, const float* w_scale, int M, int N, int K, int g,
                       uint16_t* Y, int32_t* P, float out_scale, hipStream_t stream,
                       bool tiled) {
   switch (K) {
-#define RRS_K(K_) \
-  case K_: return launch_k<K_, kPartials>(Xq, a_scale, s_group, Wq, w_scale, M, N, g, Y, P, \
-                                           out_scale, stream, tiled)
+#define RRS_K(K_)                                                                        \
+  case K_:                                                                               \
+    return launch_k<K_, W, TB, kPartials>(Xq, a_scale, s_group, Wq, w_scale, M, N, g, Y, P, \
+                                          out_scale, stream, tiled)
     RRS_K(512);
     RRS_K(1024);
     RRS_K(2048);
@@ -329,13 +383,27 @@ hipError_t launch_any(const uint8_t* Xq, const float* a_scale, const float* s_gr
   }
 }
 
+// The form for M tokens: up to 16, four waves and one token block; 17 to 32,
+// eight waves (one workgroup per compute unit) and two token blocks, so the
+// weights still stream once.
+template <bool kPartials>
+hipError_t launch_tokens(const uint8_t* Xq, const float* a_scale, const float* s_group,
+                         const uint8_t* Wq, const float* w_scale, int M, int N, int K, int g,
+                         uint16_t* Y, int32_t* P, float out_scale, hipStream_t stream,
+                         bool tiled) {
+  if (M <= kMaxTokens)
+    return launch_any<4, 1, kPartials>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, P,
+                                       out_scale, stream, tiled);
+  return launch_any<8, 2, kPartials>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, P,
+                                     out_scale, stream, tiled);
+}
+
 }  // namespace
 
-// K = 16384 with g <= 128 keeps 32 or 64 groups of token codes per wave,
-// which do not fit the registers next to the loop: the few-token kernel takes
-// those shapes.
 bool stream_kernel_fits(int M, int K, int g) {
-  return M >= 1 && M <= kMaxTokens && K >= 4 * g && !(K == 16384 && g <= 128);
+  if (M < 1 || M > 2 * kMaxTokens) return false;
+  if (M <= kMaxTokens) return stream_form_fits(K, 4, 1, g);
+  return stream_form_fits(K, 8, 2, g);
 }
 
 hipError_t launch_w4a4_gemm_stream(const uint8_t* Xq, const float* a_scale,
@@ -343,15 +411,17 @@ hipError_t launch_w4a4_gemm_stream(const uint8_t* Xq, const float* a_scale,
                                    const float* w_scale, int M, int N, int K, int g,
                                    uint16_t* Y, float out_scale, hipStream_t stream,
                                    WqLayout lay) {
-  return launch_any<false>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, nullptr, out_scale,
-                           stream, lay.tiled);
+  if (!stream_kernel_fits(M, K, g)) return hipErrorInvalidValue;
+  return launch_tokens<false>(Xq, a_scale, s_group, Wq, w_scale, M, N, K, g, Y, nullptr,
+                              out_scale, stream, lay.tiled);
 }
 
 hipError_t launch_w4a4_gemm_stream_partials(const uint8_t* Xq, const uint8_t* Wq, int M, int N,
                                             int K, int g, int32_t* P, hipStream_t stream,
                                             WqLayout lay) {
-  return launch_any<true>(Xq, nullptr, nullptr, Wq, nullptr, M, N, K, g, nullptr, P, 0.0f,
-                          stream, lay.tiled);
+  if (!stream_kernel_fits(M, K, g)) return hipErrorInvalidValue;
+  return launch_tokens<true>(Xq, nullptr, nullptr, Wq, nullptr, M, N, K, g, nullptr, P, 0.0f,
+                             stream, lay.tiled);
 }
 
 }  // namespace rrs

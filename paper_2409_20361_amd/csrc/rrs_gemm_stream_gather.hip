@@ -168,12 +168,12 @@ hipError_t launch_gather_k(const uint8_t* Xq, const float* a_scale, const float*
                            hipStream_t stream, bool tiled) {
   const int nblk = N / kRows;
   if (tiled) {
-    auto kern = gemm_stream_gather_kernel<K, true>;
-    kern<<<resident_grid(kern, nblk), kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale,
+    constexpr auto kern = gemm_stream_gather_kernel<K, true>;
+    kern<<<resident_grid<kern>(nblk), kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale,
                                                              border, M, N, g, Y, out_scale);
   } else {
-    auto kern = gemm_stream_gather_kernel<K, false>;
-    kern<<<resident_grid(kern, nblk), kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale,
+    constexpr auto kern = gemm_stream_gather_kernel<K, false>;
+    kern<<<resident_grid<kern>(nblk), kThreads, 0, stream>>>(Xq, a_scale, s_group, Wq, w_scale,
                                                              border, M, N, g, Y, out_scale);
   }
   return hipGetLastError();

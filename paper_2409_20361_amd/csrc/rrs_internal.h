@@ -141,9 +141,11 @@ hipError_t launch_w4a4_gemm_decode(const uint8_t* Xq, const float* a_scale,
 hipError_t launch_w4a4_gemm_decode_partials(const uint8_t* Xq, const uint8_t* Wq, int M, int N,
                                             int K, int g, int32_t* P, hipStream_t stream);
 
-// Weight-streaming kernel for up to 16 tokens (rrs_gemm_stream.hip): each
+// Weight-streaming kernel for few tokens (rrs_gemm_stream.hip): each
 // workgroup copies 16 whole rows of Wq into LDS with direct-to-LDS loads.
-// Needs K >= 4 g. Both layouts, bit-identical results.
+// Up to 16 tokens: four waves, K >= 4 g (not K = 16384 with g <= 128). 17 to
+// 32 tokens at K = 8192: eight waves and two blocks of 16 tokens. Both
+// layouts, bit-identical results.
 bool stream_kernel_fits(int M, int K, int g);
 hipError_t launch_w4a4_gemm_stream(const uint8_t* Xq, const float* a_scale,
                                    const float* s_group, const uint8_t* Wq,

@@ -17,9 +17,10 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kRows = 16;  // weight rows (output columns) per column block
 constexpr int kMaxTokens = 16;
 
-template <int K>
+// W waves per workgroup, each streaming a 1/W slice of K.
+template <int K, int W = kWaves>
 struct StreamShape {
-  static constexpr int R = K / 2 / kWaves;            // packed bytes per row per wave
+  static constexpr int R = K / 2 / W;                 // packed bytes per row per wave
   static constexpr int SBW = R < 512 ? R : 512;        // bytes per row per sub-buffer
   static constexpr int SPB = R / SBW;                  // sub-buffers per block
   static constexpr int CPR = SBW / 16;                 // 16-byte chunks per row per sub-buffer
@@ -80,13 +81,14 @@ inline int cu_count() {
 // once (the surplus would wait for a whole earlier workgroup to finish):
 // as many per compute unit as the runtime's occupancy query allows (two for
 // most shapes: 72 KB of LDS each; one where a wave needs more than 256
-// registers), times the compute units. Cached per kernel.
-template <typename Kern>
-int resident_grid(Kern kern, int nblk) {
+// registers or the workgroup more than 80 KB of LDS), times the compute
+// units. Cached per kernel (one instantiation per kernel function).
+template <auto Kern>
+int resident_grid(int nblk, int threads = kThreads) {
   static int per_cu = 0;
   if (per_cu == 0) {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, kThreads, 0) != hipSuccess || n < 1)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, Kern, threads, 0) != hipSuccess || n < 1)
       n = 1;
     per_cu = n;
   }

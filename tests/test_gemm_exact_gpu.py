@@ -6,8 +6,10 @@ as an FMA by 0, and P_b / K is exact in binary32 (K is a power of two). The
 oracle therefore predicts Y bit for bit (Eq. 3 for one block), which checks
 each kernel's integer path and its accumulator encoding (the magic-number
 seed of the production loop) through the timed entry point, for every kernel
-the dispatch chooses: the weight-streaming kernel (up to 16 tokens, row-major
-Wq), the few-token kernel (one, two or four blocks of 16 tokens; two or four
+the dispatch chooses: the weight-streaming kernel (up to 16 tokens with four
+waves; 17 to 32 tokens at K = 8192 with eight waves and two token blocks; both
+weight layouts), the few-token kernel (one, two or four blocks of 16 tokens;
+two or four
 column blocks per workgroup, with a partly filled last workgroup; both weight
 layouts) and the main kernel (partial row and column tiles). With codes in
 [-2, 2] every |P_b| <= 4 g <= 2048 is an integer that fp16 holds exactly, so
@@ -48,10 +50,17 @@ CASES = [
     # weight-streaming kernel: row-major, M <= 16, K >= 4 g (R < 1 KB, = 1 KB, 2 KB per row)
     (1, 2048, 48, 64, False), (3, 512, 32, 128, False), (8, 4096, 80, 128, False),
     (16, 8192, 32, 256, False), (5, 16384, 16, 512, False), (11, 1024, 64, 256, False),
-    # few-token kernel, row-major: K < 4 g, and 17..64 tokens (two or four token
-    # blocks, four column blocks per workgroup, the last one partly filled)
+    # weight-streaming kernel, eight waves: 17..32 tokens at K = 8192 in two
+    # token blocks (the second ragged or full), both layouts, g = 64 (8-byte
+    # lane pieces) to g = 512 (no seed); N = 4112 gives the first workgroup a
+    # second column block
+    (17, 8192, 48, 128, False), (32, 8192, 48, 64, True), (24, 8192, 4112, 512, False),
+    (20, 8192, 4112, 256, True),
+    # few-token kernel, row-major: K < 4 g, and 17..64 tokens elsewhere (two or
+    # four token blocks, four column blocks per workgroup, the last one partly
+    # filled)
     (1, 1024, 48, 512, False), (17, 2048, 48, 128, False), (40, 4096, 80, 64, False),
-    (64, 2048, 16, 256, False),
+    (64, 2048, 16, 256, False), (40, 8192, 48, 128, False), (64, 16384, 32, 256, False),
     # few-token kernel, tiled weights
     (8, 4096, 48, 128, True), (24, 2048, 80, 512, True), (64, 8192, 32, 64, True),
     (16, 1024, 32, 64, True),
@@ -161,6 +170,8 @@ def test_partials_decode_full_rows():
 @pytest.mark.parametrize("M,K,N,g", [
     (1, 512, 16, 64), (16, 16384, 32, 512), (9, 8192, 48, 256), (4, 1024, 64, 128),
     (2, 1024, 16, 512),   # K < 4 g: the few-token kernel
+    # eight waves, two token blocks (K = 8192)
+    (32, 8192, 48, 128), (18, 8192, 4112, 64), (25, 8192, 32, 512),
 ])
 def test_partials_stream_kernel_edges(M, K, N, g):
     rng = np.random.default_rng(M + K + N + g)

@@ -286,6 +286,19 @@ def test_linear_ragged(M, K, N, g):
     _linear_case(w, label=f"ragged {M}x{K}x{N}/g{g}")
 
 
+@pytest.mark.parametrize("M", [32, 64])
+def test_linear_decode_shape_more_tokens(M):
+    # The decode layer (K = 8192, N = 28672) with 32 tokens (weight-streaming
+    # GEMM, eight waves, two token blocks) and 64 (the few-token GEMM), on
+    # every token and sampled output channels.
+    base = synth.WORKLOADS["decode"]
+    w = synth.custom("d", M, base.K, base.N, base.g, 40 + M, n_chan=82, n_spike=2,
+                     spike_mag=(100, 500))
+    rng = np.random.default_rng(M)
+    cols = np.unique(np.concatenate([[0, w.N - 1], rng.choice(w.N, 160, replace=False)]))
+    _linear_case(w, col_sample=cols, label=f"decode shape M={M}")
+
+
 @pytest.mark.parametrize("name", ["qkv", "decode", "gateup"])
 def test_linear_full_size_sampled(name):
     # The benchmark's shapes and launch configuration; outputs checked on a
