@@ -257,8 +257,10 @@ rrs_status rrs_linear_ex(const void* X, const void* Wq, const float* w_scale, in
  * Test hook for the failure path of the one-launch quantizers (not for
  * computing: use rrs_rotate_smooth_quant). Without a static reorder,
  * rrs_rotate_smooth_quant runs one launch for 2 to 16 tokens (one workgroup
- * per token row) and, at K <= 4096, for more tokens too (one workgroup per
- * compute unit, up to two rows per wave). The workgroups exchange their group
+ * per token row; at K >= 8192 up to 64 tokens for g >= K / 64 and up to 32
+ * for g = K / 128)
+ * and, at K <= 4096, for more tokens too (one workgroup per compute unit, up
+ * to two rows per wave). The workgroups exchange their group
  * maxima through the workspace (Eq. 1 takes the maximum over every token),
  * each polling, with a bound, until the words it needs have arrived. That
  * needs all workgroups of the launch to be resident at the same time, which
@@ -273,8 +275,8 @@ rrs_status rrs_linear_ex(const void* X, const void* Wq, const float* w_scale, in
  * in *failed (host pointer) if the exchange failed, else 0. Arguments
  * otherwise as rrs_rotate_smooth_quant with perm = NULL; RRS_ERR_SHAPE when
  * no one-launch kernel serves the shape, RRS_ERR_FLAGS for extra_rows < 0,
- * max_polls < 1 or more than 16 rows in all for the per-row kernel (256 for
- * the fused one). With RRS_DEBUG set, rrs_rotate_smooth_quant(_ex) and
+ * max_polls < 1 or more rows in all than the per-row kernel takes for the
+ * shape (16, or the 32 or 64 above; 256 for the fused one). With RRS_DEBUG set, rrs_rotate_smooth_quant(_ex) and
  * rrs_linear(_ex) make the same check after a call that used a one-launch
  * kernel and return RRS_ERR_TIMEOUT when it failed.
  */

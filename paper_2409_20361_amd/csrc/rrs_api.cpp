@@ -645,7 +645,9 @@ rrs_status rrs_test_quant_rows_wait(const void* X, int M, int K, int group_size,
   const bool rows = M >= 2 && rrs::quant_rows_used(M, K, group_size, nullptr, 0);
   const bool fused = rrs::fused_quant_used(M, K, group_size, nullptr, 0);
   if (!rows && !fused) return RRS_ERR_SHAPE;
-  if (extra_rows < 0 || max_polls < 1 || (rows && M + extra_rows > 16)) return RRS_ERR_FLAGS;
+  if (extra_rows < 0 || max_polls < 1 ||
+      (rows && M + extra_rows > rrs::quant_rows_max(K, group_size)))
+    return RRS_ERR_FLAGS;
   if (!is_aligned(X) || !is_aligned(Xq) || !is_aligned(a_scale) || !is_aligned(s_group) ||
       !is_aligned(workspace))
     return RRS_ERR_ALIGN;

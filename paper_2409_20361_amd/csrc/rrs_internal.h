@@ -229,6 +229,7 @@ hipError_t noalloc_scratch(void** ptr);
 // extra_rows rows that no workgroup writes (so every wait runs out) and give
 // up after max_polls rounds (0 = the default bound).
 bool quant_rows_fits(int M);
+int quant_rows_max(int K, int g);  // rows the per-row kernel takes (no runtime reorder)
 size_t quant_rows_workspace_bytes(int K, int g);
 hipError_t launch_quant_rows(const uint16_t* X, int M, int K, int g, bool rotate, uint8_t* Xq,
                              float* a_scale, float* s_group, void* workspace, hipStream_t stream,

@@ -7,12 +7,14 @@
 // rows exchange their group maxima within the launch: workgroup p rotates row
 // p and publishes the row's G group maxima as tagged words in the workspace
 // (the fence-free epoch protocol of rrs_device.h); every workgroup then reads
-// the M rows of words, forms s_b and r_b, and quantizes its own row. With
-// M <= 16 workgroups the rows are rotated in parallel instead of one after
-// another as in the one-workgroup kernel. A single row needs no exchange.
-// Beyond about 32 rows the M words per group the reduction reads cost more
-// than the second launch they save (27.5 us against 19.7 us at M = 64,
-// K = 8192, measured with an earlier, count-based exchange).
+// the M rows of words, forms s_b and r_b, and quantizes its own row. The rows
+// are rotated in parallel instead of one after another as in the
+// one-workgroup kernel. A single row needs no exchange. The threads of a
+// group share the reads of its M words (16 at most per thread), so up to 64
+// rows take one launch where a group spans four threads or more: at K = 8192
+// and g = 128, 8.1 to 9.1 us for 17 to 64 rows against about 19 us for the two
+// launches (an earlier form, where one thread per group read every row through
+// a count-based exchange, took 27.5 us at 64 rows).
 //
 // The exchange needs the M workgroups to be resident together, which a plain
 // launch of M <= 16 workgroups gets on an otherwise idle device but not when
@@ -27,7 +29,8 @@
 namespace rrs {
 namespace {
 
-constexpr int kMaxRows = 16;
+constexpr int kMaxRows = 16;      // exchanged words one thread waits for
+constexpr int kMaxRowsWide = 64;  // rows when a group's threads share the reads
 constexpr int kMaxPolls = 1 << 18;
 
 // LDS address of position q of the rotated row in position-major order: row
@@ -146,34 +149,46 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
   }
 
   // Maxima over the rows. With more than one row, every row's maxima are
-  // exchanged: the owner of span b publishes this row's maximum and reads
-  // span b of all nrows rows (all words requested at once, those not yet
-  // tagged requested again, within max_polls rounds).
+  // exchanged: the owner of span b publishes this row's maximum, and span b
+  // of all nrows rows is read (all words requested at once, those not yet
+  // tagged requested again, within max_polls rounds). When a span's tps
+  // threads share a wave they share the reads, thread k of the span taking
+  // rows k, k + tps, ... (up to kMaxRows each), and combine them with
+  // shuffles; otherwise the owner reads them all.
   const uint32_t tag = tag_lds;  // set before the barrier above
-  if (owner) {
-    float s = pm;
-    if (M > 1) {
-      publish_tagged(tagged + (size_t)p * W + b, tag, pm);
-      unsigned long long x[kMaxRows];
+  const bool share = tps <= 64;
+  const int sub = share ? (t & (tps - 1)) : 0;
+  const int nsub = share ? tps : 1;
+  float s = pm;
+  if (M > 1 && (share || owner)) {
+    if (owner) publish_tagged(tagged + (size_t)p * W + b, tag, pm);
+    unsigned long long x[kMaxRows];
 #pragma unroll
-      for (int i = 0; i < kMaxRows; ++i)
-        x[i] = i < nrows ? load_tagged(tagged + (size_t)i * W + b) : ((unsigned long long)tag << 32);
-      bool ok = false;
-      for (int round = 0;; ++round) {
-        ok = true;
-#pragma unroll
-        for (int i = 0; i < kMaxRows; ++i) ok = ok && has_tag(x[i], tag);
-        if (ok || round >= max_polls) break;
-        __builtin_amdgcn_s_sleep(1);
-#pragma unroll
-        for (int i = 0; i < kMaxRows; ++i)
-          if (i < nrows && !has_tag(x[i], tag)) x[i] = load_tagged(tagged + (size_t)i * W + b);
-      }
-      if (!ok) missed = 1;  // benign race: every writer writes 1
-      s = 0.0f;
-#pragma unroll
-      for (int i = 0; i < kMaxRows; ++i) s = fmaxf(s, __uint_as_float((uint32_t)x[i]));
+    for (int i = 0; i < kMaxRows; ++i) {
+      const int r = sub + i * nsub;
+      x[i] = r < nrows ? load_tagged(tagged + (size_t)r * W + b) : ((unsigned long long)tag << 32);
     }
+    bool ok = false;
+    for (int round = 0;; ++round) {
+      ok = true;
+#pragma unroll
+      for (int i = 0; i < kMaxRows; ++i) ok = ok && has_tag(x[i], tag);
+      if (ok || round >= max_polls) break;
+      __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+      for (int i = 0; i < kMaxRows; ++i) {
+        const int r = sub + i * nsub;
+        if (r < nrows && !has_tag(x[i], tag)) x[i] = load_tagged(tagged + (size_t)r * W + b);
+      }
+    }
+    if (!ok) missed = 1;  // benign race: every writer writes 1
+    s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kMaxRows; ++i) s = fmaxf(s, __uint_as_float((uint32_t)x[i]));
+  }
+  if (M > 1 && share)  // every lane of the wave takes part (tps is uniform)
+    for (int o = 1; o < tps; o <<= 1) s = fmaxf(s, __shfl_xor(s, o, 64));
+  if (owner) {
     if constexpr (kReorder) {
       key[b] = s;  // block b's key: its largest channel maximum
     } else {
@@ -283,8 +298,18 @@ hipError_t launch_k(const uint16_t* X, int M, int g, bool rotate, uint8_t* Xq, f
 
 bool quant_rows_fits(int M) { return M >= 1 && M <= kMaxRows; }
 
+// Rows the per-row kernel takes at (K, g) without a runtime reorder: 16, or
+// up to 64 where a group's threads share the reads (16 words each). Only from
+// K = 8192 on, where the alternative is the two-pass kernels; at K <= 4096
+// the one-launch fused kernel takes more tokens.
+int quant_rows_max(int K, int g) {
+  const int tps = g / (K / kRowThreads);  // threads per group
+  if (K < 8192 || tps < 1 || tps > 64) return kMaxRows;
+  return kMaxRows * tps < kMaxRowsWide ? kMaxRows * tps : kMaxRowsWide;
+}
+
 size_t quant_rows_workspace_bytes(int K, int g) {
-  return kQuantHeaderBytes + align256((size_t)kMaxRows * (K / g) * 8);
+  return kQuantHeaderBytes + align256((size_t)quant_rows_max(K, g) * (K / g) * 8);
 }
 
 bool quant_rows_reorder_fits(int M, int K) { return quant_rows_fits(M) && K <= 8192; }
@@ -324,7 +349,7 @@ hipError_t launch_quant_rows(const uint16_t* X, int M, int K, int g, bool rotate
   unsigned long long* tagged =
       reinterpret_cast<unsigned long long*>(static_cast<char*>(workspace) + kQuantHeaderBytes);
   const int nrows = M + extra_rows;  // rows of maxima the readers wait for
-  if (nrows > kMaxRows) return hipErrorInvalidValue;
+  if (nrows > quant_rows_max(K, g)) return hipErrorInvalidValue;
   const int polls = max_polls > 0 ? max_polls : kMaxPolls;
 #define RRS_ROWS_K(K_)                                                                   \
   launch_k<K_, false>(X, M, g, rotate, Xq, a_scale, s_group, nullptr, header, tagged, nrows, \
@@ -342,7 +367,7 @@ hipError_t launch_quant_rows(const uint16_t* X, int M, int K, int g, bool rotate
 }
 
 bool quant_rows_used(int M, int K, int g, const int32_t* perm, int flags) {
-  return quant_rows_fits(M) && !perm && !(flags & kSkipSmoothing) &&
+  return M >= 1 && M <= quant_rows_max(K, g) && !perm && !(flags & kSkipSmoothing) &&
          quant_rows_workspace_bytes(K, g) <= quant_two_pass_offset(K);
 }
 

@@ -468,15 +468,18 @@ def test_quant_rows_wait_hook_checks():
     for key in ("X", "Xq", "a", "s", "ws", "n"):
         assert _qwait(**{key: None}) == NULL, key
     assert _qwait(M=1) == SHAPE       # one row: no exchange
-    assert _qwait(M=17, K=8192) == SHAPE   # no one-launch kernel for this shape
+    assert _qwait(M=65, K=8192) == SHAPE   # no one-launch kernel for this shape
+    assert _qwait(M=33, K=8192, g=64) == SHAPE   # per-row up to 32 rows at g = K / 128
     assert _qwait(K=1000) == SHAPE
     assert _qwait(g=96) == GROUP
     assert _qwait(extra=-1) == FLAGS
     assert _qwait(polls=0) == FLAGS
     assert _qwait(M=4, extra=13) == FLAGS  # the per-row kernel waits for <= 16 rows
+    assert _qwait(M=60, K=8192, extra=5) == FLAGS  # <= 64 rows at K = 8192, g = 128
+    assert _qwait(M=30, K=8192, g=64, extra=3) == FLAGS  # <= 32 rows at g = 64
     assert _qwait(X=MIS) == ALIGN
     assert _qwait(wsb=16) == WS
-    assert _qwait(M=17, K=8192, X=None) == NULL   # null pointers first
+    assert _qwait(M=65, K=8192, X=None) == NULL   # null pointers first
 
 
 def _rwait(**kw):

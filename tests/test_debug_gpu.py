@@ -183,9 +183,11 @@ def test_debug_rejects_bad_block_order(debug_env):
 # ------------------------------------------------------------------ bounded wait
 
 @pytest.mark.parametrize("M,K,g", [(2, 8192, 128), (8, 8192, 128), (15, 1024, 64),
-                                   (300, 4096, 128), (2040, 4096, 128), (40, 1024, 64)])
+                                   (300, 4096, 128), (2040, 4096, 128), (40, 1024, 64),
+                                   (40, 8192, 128), (63, 8192, 256), (31, 8192, 64)])
 def test_one_launch_wait_runs_out_loudly(M, K, g):
-    # per-row kernel up to 16 tokens, fused kernel above (K <= 4096)
+    # per-row kernel up to 16 tokens (up to 32 / 64 at K = 8192 by g), fused
+    # kernel above (K <= 4096)
     rrs = _rrs()
     w = synth.custom("qw", M, K, 16, g, M + K, n_chan=max(1, K // 100), n_spike=2,
                      spike_mag=(100, 500))

@@ -1,6 +1,7 @@
 """rrs_rotate_smooth_quant through its one-launch kernels: one workgroup per
-token row for up to 16 tokens, and the fused kernel (every row rotated once,
-kept in registers) for more tokens at K <= 4096. Both exchange the workgroups'
+token row for up to 16 tokens (up to 32 or 64 at K >= 8192, where a group's
+threads share the reads of the exchanged words), and the fused kernel (every
+row rotated once, kept in registers) for more tokens at K <= 4096. Both exchange the workgroups'
 group maxima within the launch as epoch-tagged words in the workspace. Codes
 must equal the oracle's (boundary flips aside), alpha and s bit for bit, on a
 zeroed workspace and when one workspace serves consecutive calls of any shape
@@ -63,6 +64,19 @@ def test_rows_match_oracle(M, K, g):
     _check(_x(M, K, g, 5 * M + K + g), g, ws, f"rows {M}x{K}/g{g}")
     # one exchange (none for a single row): epoch 0 -> 1, no failure
     assert _words(ws)[:2] == ([1, 0] if M > 1 else [0, 0])
+
+
+@pytest.mark.parametrize("M,K,g", [
+    (17, 8192, 128), (33, 8192, 128), (64, 8192, 128), (32, 8192, 64), (50, 8192, 512),
+    (64, 16384, 256), (32, 16384, 128), (20, 8192, 256),
+])
+def test_rows_many_tokens_match_oracle(M, K, g):
+    # 17..64 rows at K >= 8192: one workgroup per row, the tps threads of a
+    # group reading rows k, k + tps, ... of the exchanged words
+    print(f"[case] quant rows (shared reads) M={M} K={K} g={g}", flush=True)
+    ws = _zeros(M, K, g)
+    _check(_x(M, K, g, 13 * M + K + g), g, ws, f"rows {M}x{K}/g{g}")
+    assert _words(ws)[:2] == [1, 0]
 
 
 @pytest.mark.parametrize("M", [4, 16])
