@@ -257,8 +257,8 @@ rrs_status rrs_linear_ex(const void* X, const void* Wq, const float* w_scale, in
  * Test hook for the failure path of the one-launch quantizers (not for
  * computing: use rrs_rotate_smooth_quant). Without a static reorder,
  * rrs_rotate_smooth_quant runs one launch for 2 to 16 tokens (one workgroup
- * per token row; at K >= 8192 up to 64 tokens for g >= K / 64 and up to 32
- * for g = K / 128)
+ * per token row; up to 64 tokens for g >= K / 64 and up to 32 for
+ * g = K / 128)
  * and, at K <= 4096, for more tokens too (one workgroup per compute unit, up
  * to two rows per wave). The workgroups exchange their group
  * maxima through the workspace (Eq. 1 takes the maximum over every token),

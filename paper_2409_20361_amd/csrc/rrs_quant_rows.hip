@@ -14,7 +14,8 @@
 // rows take one launch where a group spans four threads or more: at K = 8192
 // and g = 128, 8.1 to 9.1 us for 17 to 64 rows against about 19 us for the two
 // launches (an earlier form, where one thread per group read every row through
-// a count-based exchange, took 27.5 us at 64 rows).
+// a count-based exchange, took 27.5 us at 64 rows), and at K <= 4096 0.5 to
+// 0.9 us less than the fused many-token kernel.
 //
 // The exchange needs the M workgroups to be resident together, which a plain
 // launch of M <= 16 workgroups gets on an otherwise idle device but not when
@@ -299,12 +300,14 @@ hipError_t launch_k(const uint16_t* X, int M, int g, bool rotate, uint8_t* Xq, f
 bool quant_rows_fits(int M) { return M >= 1 && M <= kMaxRows; }
 
 // Rows the per-row kernel takes at (K, g) without a runtime reorder: 16, or
-// up to 64 where a group's threads share the reads (16 words each). Only from
-// K = 8192 on, where the alternative is the two-pass kernels; at K <= 4096
-// the one-launch fused kernel takes more tokens.
+// up to 64 where a group's threads share the reads (16 words each). From
+// 17 to 64 rows it beats the alternatives at every K: the two-pass kernels
+// from K = 8192 on (8.1-9.1 us against about 19 us at K = 8192, g = 128) and
+// the one-launch fused kernel at K <= 4096 (8.0-8.5 against 8.6-9.1 us at
+// K = 1024 to 4096; events, back-to-back calls).
 int quant_rows_max(int K, int g) {
   const int tps = g / (K / kRowThreads);  // threads per group
-  if (K < 8192 || tps < 1 || tps > 64) return kMaxRows;
+  if (tps < 1 || tps > 64) return kMaxRows;
   return kMaxRows * tps < kMaxRowsWide ? kMaxRows * tps : kMaxRowsWide;
 }
 

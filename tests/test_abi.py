@@ -474,7 +474,8 @@ def test_quant_rows_wait_hook_checks():
     assert _qwait(g=96) == GROUP
     assert _qwait(extra=-1) == FLAGS
     assert _qwait(polls=0) == FLAGS
-    assert _qwait(M=4, extra=13) == FLAGS  # the per-row kernel waits for <= 16 rows
+    assert _qwait(M=4, extra=61) == FLAGS  # the per-row kernel waits for <= 64 rows
+    assert _qwait(M=4, K=512, g=512, extra=13) == FLAGS  # <= 16 where one thread reads all
     assert _qwait(M=60, K=8192, extra=5) == FLAGS  # <= 64 rows at K = 8192, g = 128
     assert _qwait(M=30, K=8192, g=64, extra=3) == FLAGS  # <= 32 rows at g = 64
     assert _qwait(X=MIS) == ALIGN

@@ -184,10 +184,11 @@ def test_debug_rejects_bad_block_order(debug_env):
 
 @pytest.mark.parametrize("M,K,g", [(2, 8192, 128), (8, 8192, 128), (15, 1024, 64),
                                    (300, 4096, 128), (2040, 4096, 128), (40, 1024, 64),
-                                   (40, 8192, 128), (63, 8192, 256), (31, 8192, 64)])
+                                   (40, 8192, 128), (63, 8192, 256), (31, 8192, 64),
+                                   (90, 1024, 64)])
 def test_one_launch_wait_runs_out_loudly(M, K, g):
-    # per-row kernel up to 16 tokens (up to 32 / 64 at K = 8192 by g), fused
-    # kernel above (K <= 4096)
+    # per-row kernel up to 16 tokens (up to 32 / 64 by g), fused kernel above
+    # (K <= 4096)
     rrs = _rrs()
     w = synth.custom("qw", M, K, 16, g, M + K, n_chan=max(1, K // 100), n_spike=2,
                      spike_mag=(100, 500))
@@ -281,7 +282,7 @@ def test_quant_rows_hook_argument_checks():
         X.data_ptr(), M, 1024, 128, extra, polls, Xq.data_ptr(), a.data_ptr(), s.data_ptr(),
         ws.data_ptr(), ws.numel(), ctypes.byref(n), _stream())
     assert call(1, 1, 8) == -2       # one row: no one-launch exchange
-    assert call(4, 13, 8) == -9      # more than 16 rows in all for the per-row kernel
+    assert call(4, 61, 8) == -9      # more than 64 rows in all for the per-row kernel
     assert call(4, -1, 8) == -9
     assert call(4, 1, 0) == -9
     assert _untouched(Xq, a, s)

@@ -1,7 +1,7 @@
 """rrs_rotate_smooth_quant through its one-launch kernels: one workgroup per
-token row for up to 16 tokens (up to 32 or 64 at K >= 8192, where a group's
-threads share the reads of the exchanged words), and the fused kernel (every
-row rotated once, kept in registers) for more tokens at K <= 4096. Both exchange the workgroups'
+token row for up to 16 tokens (up to 32 or 64 where a group's threads share
+the reads of the exchanged words), and the fused kernel (every row rotated
+once, kept in registers) for more tokens at K <= 4096. Both exchange the workgroups'
 group maxima within the launch as epoch-tagged words in the workspace. Codes
 must equal the oracle's (boundary flips aside), alpha and s bit for bit, on a
 zeroed workspace and when one workspace serves consecutive calls of any shape
@@ -69,10 +69,11 @@ def test_rows_match_oracle(M, K, g):
 @pytest.mark.parametrize("M,K,g", [
     (17, 8192, 128), (33, 8192, 128), (64, 8192, 128), (32, 8192, 64), (50, 8192, 512),
     (64, 16384, 256), (32, 16384, 128), (20, 8192, 256),
+    (40, 4096, 128), (64, 1024, 64), (33, 2048, 256), (64, 512, 64),
 ])
 def test_rows_many_tokens_match_oracle(M, K, g):
-    # 17..64 rows at K >= 8192: one workgroup per row, the tps threads of a
-    # group reading rows k, k + tps, ... of the exchanged words
+    # 17..64 rows: one workgroup per row, the tps threads of a group reading
+    # rows k, k + tps, ... of the exchanged words
     print(f"[case] quant rows (shared reads) M={M} K={K} g={g}", flush=True)
     ws = _zeros(M, K, g)
     _check(_x(M, K, g, 13 * M + K + g), g, ws, f"rows {M}x{K}/g{g}")
@@ -89,11 +90,11 @@ def test_rows_without_rotation(M):
     assert _words(ws)[:2] == [1, 0]
 
 
-@pytest.mark.parametrize("M,K,g", [(17, 4096, 128), (300, 4096, 64), (2048, 4096, 128),
+@pytest.mark.parametrize("M,K,g", [(65, 4096, 128), (300, 4096, 64), (2048, 4096, 128),
                                    (4096, 4096, 128), (3000, 2048, 512), (777, 512, 128),
                                    (5000, 1024, 256), (1000, 2048, 256), (1024, 4096, 128)])
 def test_fused_match_oracle(M, K, g):
-    # more than 16 tokens at K <= 4096: the fused one-launch kernel (one or
+    # more than 64 tokens at K <= 4096: the fused one-launch kernel (one or
     # two rows per wave; 4096 rows at K = 4096 is its largest single-slot
     # case, 5000 at K = 1024 takes two slots)
     print(f"[case] quant fused M={M} K={K} g={g}", flush=True)
