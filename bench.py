@@ -364,9 +364,11 @@ def few_token_bench(torch, rrs, synth, reps=50):
     """Few-token layers at the decode shape (K=8192, N=28672, g=128) for
     M = 1, 2, 4, 8, 16, 32, 64: quantizer, GEMM and the whole layer, each timed
     with HIP events around 50 back-to-back calls, weights cycling through 4
-    copies. Up to M = 16 the quantizer is one launch with one workgroup per
-    row; the GEMM is the weight-streaming kernel up to M = 32 (eight waves
-    from 17 tokens) and the few-token kernel at M = 64. The *_tiled entries
+    copies. At M = 1 and 2 the layer is one launch (every workgroup of the
+    GEMM quantizes the rows itself); otherwise the quantizer is one launch
+    with one workgroup per row and the GEMM the weight-streaming kernel up to
+    M = 32 (eight waves from 17 tokens) or the few-token kernel at M = 64.
+    The *_tiled entries
     run the same calls on the tiled weight layout."""
     dev = torch.device("cuda:0")
     base = synth.WORKLOADS["decode"]

@@ -215,7 +215,12 @@ size_t rrs_linear_workspace_bytes(int M, int K, int group_size);
 
 /*
  * One RRS linear layer: rrs_rotate_smooth_quant followed by rrs_w4a4_gemm,
- * with Xq, a_scale and s_group kept in the workspace.
+ * with Xq, a_scale and s_group kept in the workspace. For one or two tokens
+ * at K = 2048, 4096 or 8192 (K >= 4 group_size, no perm, no RRS_SKIP_*
+ * flag) the layer is a single launch in which every workgroup of the
+ * weight-streaming GEMM quantizes the token rows itself (Section 3.3: the
+ * rotation is online, inside the layer call); Y is bit-identical to the two
+ * calls, and Xq, a_scale and s_group are then not written to the workspace.
  *   X in: M x K float16; Wq, w_scale from rrs_prepare_weight (same perm);
  *   Y out: M x N float16.
  */

@@ -385,6 +385,12 @@ rrs_status linear_run(const void* X, const void* Wq, const float* w_scale, int M
   float* s = reinterpret_cast<float*>(ws);
 
   hipStream_t st = static_cast<hipStream_t>(stream);
+  // One or two tokens: the whole layer in one launch (no exchange, so no
+  // wait to check).
+  if (!perm && (flags & kQuantFlags) == 0 && rrs::layer_one_launch_fits(M, K, group_size))
+    return from_hip(rrs::launch_layer_one_launch(
+        static_cast<const uint16_t*>(X), M, N, K, group_size, static_cast<const uint8_t*>(Wq),
+        w_scale, static_cast<uint16_t*>(Y), out_scale(K, flags), st, layout(flags)));
   hipError_t e = rrs::launch_rotate_smooth_quant(static_cast<const uint16_t*>(X), M, K,
                                                  group_size, perm, flags & kQuantFlags, xq, a,
                                                  s, qws, st);

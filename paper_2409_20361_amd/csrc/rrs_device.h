@@ -134,6 +134,46 @@ __device__ __forceinline__ void fwht_row(float (&v)[FwhtShape<K>::E], float* lds
   fwht_windows<K, 1, kRot>(v, lds, t);
 }
 
+// LDS address of position q of the rotated row in position-major order: row
+// a = q / E (E floats) holds positions [a E, a E + E), thread a's share; its
+// 4-float chunks are permuted by h(a) so that both the strided writes of the
+// rotation's output (position t + 256 e from thread t) and the 128-bit chunk
+// reads of the owner are free of bank conflicts.
+template <int E>
+__device__ __forceinline__ int pos_addr(int q) {
+  constexpr int CH = E < 4 ? E : 4;  // floats per chunk
+  constexpr int NCH = E / CH;        // chunks per row
+  constexpr int S = ilog2(64 / E);   // rows per 64 banks = 2^S
+  const int a = q / E;
+  const int b = q % E;
+  const int h = NCH > 1 ? (a >> S) & (NCH - 1) : 0;
+  return a * E + ((b / CH) ^ h) * CH + b % CH;
+}
+
+// Thread t's E consecutive positions [t E, t E + E) of a row stored with
+// pos_addr<E>, read as 128-bit chunks in the permuted order (E >= 4) or one
+// by one.
+template <int E>
+__device__ __forceinline__ void read_positions(const float* row, int t, float (&v)[E]) {
+  constexpr int CH = E < 4 ? E : 4;
+  constexpr int NCH = E / CH;
+  const int h = NCH > 1 ? (t >> ilog2(64 / E)) & (NCH - 1) : 0;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const float* src = row + t * E + (c ^ h) * CH;
+    if constexpr (CH == 4) {
+      const float4 x = *reinterpret_cast<const float4*>(src);
+      v[4 * c] = x.x;
+      v[4 * c + 1] = x.y;
+      v[4 * c + 2] = x.z;
+      v[4 * c + 3] = x.w;
+    } else {
+#pragma unroll
+      for (int i = 0; i < CH; ++i) v[CH * c + i] = src[i];
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Reductions (values are non-negative and finite, so fmaxf is exact).
 // ---------------------------------------------------------------------------

@@ -69,6 +69,7 @@
 // fragment is unpacked once for both token blocks; the 2 x 4 (token block,
 // accumulator row) pairs of each lane are dealt to the eight waves for the
 // fixed-order sum and the stores.
+#include "rrs_device.h"
 #include "rrs_stream.h"
 
 namespace rrs {
@@ -81,12 +82,22 @@ using namespace stream;
 // weight operands. kPartials (test hook): instead of Y, write P[b][i][n] for
 // every group b, token i < M and column n, decoded from the same seeded
 // accumulators.
-template <int K, int GS, int W, int TB, bool kTiled, bool kPartials>
+//
+// MQ > 0 (the whole layer in one launch, MQ = M token rows of X): every
+// workgroup first rotates, smooths and quantizes the MQ rows itself, with the
+// arithmetic of the per-row quantizer (rrs_quant_rows.hip) and the maximum
+// over the rows taken locally instead of exchanged, so the codes and scales
+// are bit-identical to rrs_rotate_smooth_quant's; it works in the ring's last
+// slot of every wave and the partial-sum area (one contiguous region: the
+// ring is laid out slot by slot), which no load touches before the loop,
+// while the first RS - 1 sub-buffers of weights stream in. (Xq, a_scale and
+// s_group are intermediates of the layer and are not written.)
+template <int K, int GS, int W, int TB, bool kTiled, bool kPartials, int MQ = 0>
 __global__ __launch_bounds__(64 * W) void gemm_stream_kernel(
     const uint8_t* __restrict__ Xq, const float* __restrict__ a_scale,
     const float* __restrict__ s_group, const uint8_t* __restrict__ Wq,
     const float* __restrict__ w_scale, int M, int N, uint16_t* __restrict__ Y,
-    int32_t* __restrict__ P, float out_scale) {
+    int32_t* __restrict__ P, float out_scale, const uint16_t* __restrict__ X) {
   using S = StreamShape<K, W>;
   constexpr int g = GS * 64;
   constexpr int GB = g / 2;                   // packed bytes of a row per group
@@ -102,8 +113,18 @@ __global__ __launch_bounds__(64 * W) void gemm_stream_kernel(
   constexpr int kPartBytes = W * TB * 64 * 16;
   constexpr int PB = kRingBytes + 2 * kPartBytes <= 163840 ? 2 : 1;
   static_assert(kRingBytes + PB * kPartBytes <= 163840, "LDS of one workgroup");
-  __shared__ __attribute__((aligned(16))) uint8_t ring[kRingBytes];
-  __shared__ __attribute__((aligned(16))) v4f part[PB][W][TB][64];
+  struct alignas(16) Lds {
+    uint8_t ring[kRingBytes];
+    v4f part[PB][W][TB][64];  // follows the ring directly (kRingBytes % 16 == 0)
+  };
+  __shared__ Lds L;
+  uint8_t* const ring = L.ring;
+  auto& part = L.part;
+  static_assert(MQ == 0 || (W == 4 && TB == 1 && !kPartials), "one-launch layer: M <= 2");
+  constexpr int G = K / g;
+  __shared__ float qsg[MQ > 0 ? G : 1];  // s_b (one-launch layer)
+  __shared__ float qred[MQ > 0 ? 4 * MQ : 1];
+  __shared__ float qa[MQ > 0 ? MQ : 1];  // alpha of the rows
 
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -111,7 +132,14 @@ __global__ __launch_bounds__(64 * W) void gemm_stream_kernel(
   const int c = lane & 15;
   const int q = lane >> 4;
   constexpr size_t krow = (size_t)K / 2;
+  // Ring slot of item i of this wave: wave-major, or slot-major for MQ > 0.
   uint8_t* my = ring + kq * S::RS * S::SB;
+  auto slot_of = [&](int i) -> uint8_t* {
+    if constexpr (MQ > 0)
+      return ring + (i % S::RS) * (W * S::SB) + kq * S::SB;
+    else
+      return my + (i % S::RS) * S::SB;
+  };
   const int nblk = N / kRows;
   const int mine = (nblk - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x;
   const int items = mine * S::SPB;  // sub-buffers this wave streams, in order
@@ -123,7 +151,7 @@ __global__ __launch_bounds__(64 * W) void gemm_stream_kernel(
   auto issue = [&](int i) {
     const int blk = (int)blockIdx.x + (i / S::SPB) * (int)gridDim.x;
     const int sp = i % S::SPB;
-    uint8_t* dst = my + (i % S::RS) * S::SB;
+    uint8_t* dst = slot_of(i);
     const uint8_t* base = Wq + (size_t)blk * kRows * krow;
     if constexpr (kTiled) {
       const uint8_t* src = base + (size_t)(kq * S::R + sp * S::SBW) * kRows;
@@ -151,17 +179,100 @@ __global__ __launch_bounds__(64 * W) void gemm_stream_kernel(
       return c * S::SBW + 16 * (jc ^ (c & S::SW)) + 8 * e;
   };
 
+  // One-launch layer: the MQ rows of X are requested first, so that waiting
+  // for them (vector-memory loads retire in order) does not wait for the
+  // weight loads issued after them.
+  constexpr int EQ = MQ > 0 ? FwhtShape<K>::E : 8;
+  uint4 xraw[MQ > 0 ? MQ : 1][EQ / 8];
+  if constexpr (MQ > 0) {
+#pragma unroll
+    for (int r = 0; r < MQ; ++r)
+#pragma unroll
+      for (int w = 0; w < EQ / 8; ++w)
+        xraw[r][w] = reinterpret_cast<const uint4*>(X + (size_t)r * K + (size_t)t * EQ)[w];
+  }
+
   // Fill the ring: the first RS - 1 sub-buffers.
 #pragma unroll
   for (int i = 0; i < S::RS - 1; ++i)
     if (i < items) issue(i);
+
+  // One-launch layer: rotate, smooth and quantize the MQ rows (Section 3.3,
+  // then Section 3.2, Eq. 1-2) into codes in LDS.
+  const uint8_t* tok = Xq;
+  if constexpr (MQ > 0) {
+    constexpr int E = FwhtShape<K>::E;  // positions per thread (256 threads)
+    static_assert(E >= 8 && E <= 64, "packed 8 codes at a time");
+    static_assert((W * S::SB + PB * kPartBytes) >= lds_row_floats(K) * 4 &&
+                      (W * S::SB + PB * kPartBytes) >= MQ * K / 2,
+                  "scratch in the last ring slot and the partial sums");
+    float* scr = reinterpret_cast<float*>(ring + (S::RS - 1) * (W * S::SB));
+    float v[MQ][E];
+#pragma unroll
+    for (int r = 0; r < MQ; ++r) {
+#pragma unroll
+      for (int w = 0; w < E / 8; ++w) {
+        const uint32_t h4[4] = {xraw[r][w].x, xraw[r][w].y, xraw[r][w].z, xraw[r][w].w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          v[r][8 * w + 2 * k] = half_to_float(h4[k] & 0xFFFFu);
+          v[r][8 * w + 2 * k + 1] = half_to_float(h4[k] >> 16);
+        }
+      }
+      fwht_row<K, true>(v[r], scr, t);  // v[r][e] = y[t + 256 e]
+      __syncthreads();                  // the transform's last reads are done
+#pragma unroll
+      for (int e = 0; e < E; ++e) scr[pos_addr<E>(t + e * kRowThreads)] = v[r][e];
+      __syncthreads();
+      read_positions<E>(scr, t, v[r]);  // v[r][e] = y[t E + e]
+    }
+    // s_b: the largest |y| of group b over the rows; a group is tps threads
+    // of one wave (K >= 4 g).
+    constexpr int tps = g / E;
+    static_assert(tps >= 1 && tps <= 64, "a group inside one wave");
+    float pm = 0.0f;
+#pragma unroll
+    for (int r = 0; r < MQ; ++r)
+#pragma unroll
+      for (int e = 0; e < E; ++e) pm = fmaxf(pm, fabsf(v[r][e]));
+#pragma unroll
+    for (int o = 1; o < tps; o <<= 1) pm = fmaxf(pm, __shfl_xor(pm, o, 64));
+    const float rb = (pm == 0.0f) ? 0.0f : __fdiv_rn(1.0f, pm);  // r_b = fl(1 / s_b)
+    if ((t & (tps - 1)) == 0) qsg[t / tps] = pm;
+    // alpha_i: the largest fl(|y| r_b) of row i
+#pragma unroll
+    for (int r = 0; r < MQ; ++r) {
+      float lm = 0.0f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) lm = fmaxf(lm, fabsf(v[r][e]));
+      lm = wave_max(lm * rb);
+      if (lane == 0) qred[4 * r + kq] = lm;
+    }
+    __syncthreads();  // qred and qsg written, every read of scr done
+    uint8_t* codes = reinterpret_cast<uint8_t*>(scr);  // MQ rows of K/2 bytes
+#pragma unroll
+    for (int r = 0; r < MQ; ++r) {
+      const float a = fmaxf(fmaxf(qred[4 * r], qred[4 * r + 1]), fmaxf(qred[4 * r + 2], qred[4 * r + 3]));
+      const float inv = (a == 0.0f) ? 0.0f : __fdiv_rn(7.0f, a);
+      const float m = rb * inv;  // fl(r_b * inv_i)
+      uint32_t wd[E / 8];
+#pragma unroll
+      for (int w = 0; w < E / 8; ++w) wd[w] = quant_pack8(&v[r][8 * w], m);
+      const size_t off = (size_t)r * krow + (size_t)t * (E / 2);
+#pragma unroll
+      for (int w = 0; w < E / 8; ++w) *reinterpret_cast<uint32_t*>(codes + off + 4 * w) = wd[w];
+      if (t == 0) qa[r] = __fdiv_rn(a, 7.0f);
+    }
+    __syncthreads();  // codes, qa visible
+    tok = codes;
+  }
 
   // Token codes of the wave's slice (once per workgroup) and its group
   // scales (one per lane).
   uint32_t aw[TB][NG][NP][4];
 #pragma unroll
   for (int u = 0; u < TB; ++u) {
-    const uint8_t* abase = Xq + (size_t)min(16 * u + c, M - 1) * krow + (size_t)kq * S::R;
+    const uint8_t* abase = tok + (size_t)min(16 * u + c, M - 1) * krow + (size_t)kq * S::R;
 #pragma unroll
     for (int b = 0; b < NG; ++b) {
       if constexpr (GB >= 64) {
@@ -183,7 +294,10 @@ __global__ __launch_bounds__(64 * W) void gemm_stream_kernel(
     }
   }
   float sv = 0.0f;
-  if constexpr (!kPartials) sv = s_group[kq * NG + (lane < NG ? lane : 0)];
+  if constexpr (MQ > 0)
+    sv = qsg[kq * NG + (lane < NG ? lane : 0)];
+  else if constexpr (!kPartials)
+    sv = s_group[kq * NG + (lane < NG ? lane : 0)];
 
   constexpr int kMagic = 0x4B400000;  // bits of 1.5 * 2^23
   const v4i seed = GS > 4 ? v4i{0, 0, 0, 0} : v4i{kMagic, kMagic, kMagic, kMagic};
@@ -199,8 +313,14 @@ __global__ __launch_bounds__(64 * W) void gemm_stream_kernel(
     const int pi = kq + x * W;
     const int row = 16 * (pi >> 2) + 4 * q + (pi & 3);
     oscale[x] = 0.0f;
-    if constexpr (!kPartials) oscale[x] = a_scale[min(row, M - 1)] * out_scale;
+    if constexpr (MQ > 0)
+      oscale[x] = qa[min(row, M - 1)] * out_scale;
+    else if constexpr (!kPartials)
+      oscale[x] = a_scale[min(row, M - 1)] * out_scale;
   }
+  // One-launch layer: every wave has read its codes before the loop's first
+  // refill overwrites the scratch (the last ring slot).
+  if constexpr (MQ > 0) __syncthreads();
 
   for (int tb = 0; tb < mine; ++tb) {
     const int blk = (int)blockIdx.x + tb * (int)gridDim.x;
@@ -222,7 +342,7 @@ __global__ __launch_bounds__(64 * W) void gemm_stream_kernel(
       } else {
         wait_vm<0>();
       }
-      const uint8_t* buf = my + (i % S::RS) * S::SB;
+      const uint8_t* buf = slot_of(i);
 #pragma unroll
       for (int bl = 0; bl < NGS; ++bl) {
         const int b = sp * NGS + bl;  // group of the wave's slice
@@ -339,7 +459,7 @@ hipError_t launch_k(const uint8_t* Xq, const float* a_scale, const float* s_grou
     constexpr auto kern = gemm_stream_kernel<K, GS_, W, TB, T_, kPartials>;                \
     kern<<<resident_grid<kern>(nblk, 64 * W), 64 * W, 0, stream>>>(Xq, a_scale, s_group,    \
                                                                    Wq, w_scale, M, N, Y, P, \
-                                                                   out_scale);              \
+                                                                   out_scale, nullptr);     \
   }
 #define RRS_STREAM(GS_)                             \
   if constexpr (stream_form_fits(K, W, TB, GS_ * 64)) { \
@@ -398,7 +518,65 @@ hipError_t launch_tokens(const uint8_t* Xq, const float* a_scale, const float* s
                                      out_scale, stream, tiled);
 }
 
+// The one-launch layer: the same kernel with the quantizer of MQ rows in
+// front of the loop (four waves, one token block).
+template <int K, int MQ>
+hipError_t launch_layer_k(const uint16_t* X, const uint8_t* Wq, const float* w_scale, int N,
+                          int g, uint16_t* Y, float out_scale, hipStream_t stream, bool tiled) {
+  const int nblk = N / kRows;
+#define RRS_LAYER_T(GS_, T_)                                                                \
+  {                                                                                         \
+    constexpr auto kern = gemm_stream_kernel<K, GS_, 4, 1, T_, false, MQ>;                  \
+    kern<<<resident_grid<kern>(nblk), kThreads, 0, stream>>>(nullptr, nullptr, nullptr, Wq, \
+                                                             w_scale, MQ, N, Y, nullptr,    \
+                                                             out_scale, X);                 \
+  }
+#define RRS_LAYER(GS_)                                 \
+  if constexpr (stream_form_fits(K, 4, 1, GS_ * 64)) { \
+    if (tiled)                                         \
+      RRS_LAYER_T(GS_, true)                           \
+    else                                               \
+      RRS_LAYER_T(GS_, false)                          \
+  } else {                                             \
+    return hipErrorInvalidValue;                       \
+  }
+  switch (g) {
+    case 64: RRS_LAYER(1) break;
+    case 128: RRS_LAYER(2) break;
+    case 256: RRS_LAYER(4) break;
+    case 512: RRS_LAYER(8) break;
+    default: return hipErrorInvalidValue;
+  }
+#undef RRS_LAYER
+#undef RRS_LAYER_T
+  return hipGetLastError();
+}
+
 }  // namespace
+
+bool layer_one_launch_fits(int M, int K, int g) {
+  return (M == 1 || M == 2) && (K == 2048 || K == 4096 || K == 8192) &&
+         stream_form_fits(K, 4, 1, g);
+}
+
+hipError_t launch_layer_one_launch(const uint16_t* X, int M, int N, int K, int g,
+                                   const uint8_t* Wq, const float* w_scale, uint16_t* Y,
+                                   float out_scale, hipStream_t stream, WqLayout lay) {
+  if (!layer_one_launch_fits(M, K, g)) return hipErrorInvalidValue;
+#define RRS_LK(K_)                                                                          \
+  case K_:                                                                                  \
+    return M == 1 ? launch_layer_k<K_, 1>(X, Wq, w_scale, N, g, Y, out_scale, stream,       \
+                                          lay.tiled)                                        \
+                  : launch_layer_k<K_, 2>(X, Wq, w_scale, N, g, Y, out_scale, stream,       \
+                                          lay.tiled)
+  switch (K) {
+    RRS_LK(2048);
+    RRS_LK(4096);
+    RRS_LK(8192);
+    default: return hipErrorInvalidValue;
+  }
+#undef RRS_LK
+}
 
 bool stream_kernel_fits(int M, int K, int g) {
   if (M < 1 || M > 2 * kMaxTokens) return false;

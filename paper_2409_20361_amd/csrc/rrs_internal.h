@@ -155,6 +155,15 @@ hipError_t launch_w4a4_gemm_stream(const uint8_t* Xq, const float* a_scale,
 hipError_t launch_w4a4_gemm_stream_partials(const uint8_t* Xq, const uint8_t* Wq, int M, int N,
                                             int K, int g, int32_t* P, hipStream_t stream,
                                             WqLayout lay);
+// The whole layer for one or two tokens in one launch of the weight-streaming
+// kernel: every workgroup rotates, smooths and quantizes the rows itself,
+// with the arithmetic of rrs_rotate_smooth_quant, so Y is bit-identical to the
+// two launches. K = 2048, 4096 or 8192, K >= 4 g, rotation and smoothing on,
+// no static reorder.
+bool layer_one_launch_fits(int M, int K, int g);
+hipError_t launch_layer_one_launch(const uint16_t* X, int M, int N, int K, int g,
+                                   const uint8_t* Wq, const float* w_scale, uint16_t* Y,
+                                   float out_scale, hipStream_t stream, WqLayout lay);
 
 // Baselines of the kernel comparison (per-channel / sub-channel A4W4).
 hipError_t launch_quantize_sub_channel(const uint16_t* X, int M, int K, int g, int flags,

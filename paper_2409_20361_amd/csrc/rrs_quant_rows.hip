@@ -34,22 +34,6 @@ constexpr int kMaxRows = 16;      // exchanged words one thread waits for
 constexpr int kMaxRowsWide = 64;  // rows when a group's threads share the reads
 constexpr int kMaxPolls = 1 << 18;
 
-// LDS address of position q of the rotated row in position-major order: row
-// a = q / E (E floats) holds positions [a E, a E + E), thread a's share; its
-// 4-float chunks are permuted by h(a) so that both the strided writes of the
-// rotation's output (position t + 256 e from thread t) and the 128-bit chunk
-// reads of the owner are free of bank conflicts.
-template <int E>
-__device__ __forceinline__ int pos_addr(int q) {
-  constexpr int CH = E < 4 ? E : 4;  // floats per chunk
-  constexpr int NCH = E / CH;        // chunks per row
-  constexpr int S = ilog2(64 / E);   // rows per 64 banks = 2^S
-  const int a = q / E;
-  const int b = q % E;
-  const int h = NCH > 1 ? (a >> S) & (NCH - 1) : 0;
-  return a * E + ((b / CH) ^ h) * CH + b % CH;
-}
-
 // kReorder (runtime reorder, K <= 8192): the rows exchange their K/32 block
 // maxima instead of their group maxima; every workgroup then ranks the blocks
 // (keys largest first, equal keys in increasing block index), takes s_b over
@@ -69,7 +53,6 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
     float* __restrict__ a_scale, float* __restrict__ s_group, int32_t* __restrict__ block_order,
     uint32_t* header, unsigned long long* tagged, int nrows, int max_polls) {
   constexpr int E = FwhtShape<K>::E;  // this thread's channels: t + 256 e after the FWHT
-  constexpr int CH = E < 4 ? E : 4;
   constexpr int NB = K / kReorderBlock;
   static_assert(!kReorder || NB <= kRowThreads, "one block key per thread");
   static_assert(E <= 64 && (!kReorder || E <= kReorderBlock), "a thread's positions in one span");
@@ -105,24 +88,7 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
     tag_lds = next_epoch(epoch);
   }
   __syncthreads();
-  {
-    constexpr int NCH = E / CH;
-    const int h = NCH > 1 ? (t >> ilog2(64 / E)) & (NCH - 1) : 0;
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      const float* src = row + t * E + (c ^ h) * CH;
-      if constexpr (CH == 4) {
-        const float4 x = *reinterpret_cast<const float4*>(src);
-        v[4 * c] = x.x;
-        v[4 * c + 1] = x.y;
-        v[4 * c + 2] = x.z;
-        v[4 * c + 3] = x.w;
-      } else {
-#pragma unroll
-        for (int i = 0; i < CH; ++i) v[CH * c + i] = src[i];
-      }
-    }
-  }  // v[e] = y[t E + e]
+  read_positions<E>(row, t, v);  // v[e] = y[t E + e]
 
   // This row's maximum of each exchanged span: over the thread's E positions,
   // then over the tps threads of the span (shuffles within a wave, LDS across

@@ -286,6 +286,38 @@ def test_linear_ragged(M, K, N, g):
     _linear_case(w, label=f"ragged {M}x{K}x{N}/g{g}")
 
 
+@pytest.mark.parametrize("M,K,N,g", [
+    (1, 8192, 4112, 128), (2, 8192, 48, 64), (1, 4096, 272, 512), (2, 4096, 4112, 256),
+    (1, 2048, 80, 64), (2, 2048, 48, 512),
+])
+@pytest.mark.parametrize("tiled", [False, True])
+def test_linear_one_launch_layer(M, K, N, g, tiled):
+    # One or two tokens at K = 2048..8192: rrs_linear is one launch in which
+    # every workgroup quantizes the rows itself; Y must equal the two calls
+    # (quantizer, then GEMM) bit for bit, and the oracle within its bound.
+    rrs = _rrs()
+    w = synth.custom("l1", M, K, N, g, 3 * M + K + N + g, n_chan=max(1, K // 100),
+                     chan_factor=(20, 100), n_spike=2, spike_mag=(100, 500))
+    print(f"[case] one-launch layer M={M} K={K} N={N} g={g} tiled={tiled}", flush=True)
+    X = synth.activations(w)
+    W = synth.weights(w)
+    flags = rrs.WEIGHT_TILED if tiled else 0
+    Wq, beta = rrs.prepare_weight(to_gpu(W), flags=flags)
+    Xg = to_gpu(X)
+    Xq, a, s = rrs.rotate_smooth_quant(Xg, g)
+    Y2 = rrs.w4a4_gemm(Xq, a, s, Wq, beta, g, flags=flags)
+    ws = torch.full((rrs.linear_workspace_bytes(M, K, g),), 0, dtype=torch.uint8, device="cuda")
+    for rep in range(2):   # a reused workspace
+        Y = rrs.linear(Xg, Wq, beta, g, workspace=ws, flags=flags)
+        assert torch.equal(Y, Y2), f"one-launch layer differs from quant + gemm (call {rep})"
+    act = O.rotate_smooth_quant(X, g)
+    wq = O.prepare_weight(W)
+    P = O.group_partials(act.q, wq.q, g)
+    y_ref = O.output(P, act.s, act.alpha, wq.beta, norm=K)
+    check_y(to_np(Y).astype(np.float32), y_ref, P, act.s, act.alpha, wq.beta, K,
+            f"one-launch layer {M}x{K}x{N}")
+
+
 @pytest.mark.parametrize("M", [32, 64])
 def test_linear_decode_shape_more_tokens(M):
     # The decode layer (K = 8192, N = 28672) with 32 tokens (weight-streaming
