@@ -29,6 +29,9 @@ def _rrs():
 
 @pytest.mark.parametrize("M,K,N,g,reorder", [
     (8, 8192, 256, 128, False),    # one-launch few-token quantizer, few-token GEMM
+    (1, 4096, 4112, 128, False),   # the whole layer in one launch (one token)
+    (2, 8192, 512, 256, False),    # the whole layer in one launch (two tokens)
+    (40, 8192, 4112, 128, False),  # per-row quantizer (shared reads), few-token GEMM
     (300, 4096, 384, 128, False),  # two-launch quantizer, main GEMM
     (16, 2048, 128, 64, True),     # reorder: three quantizer launches, few-token gather
     (260, 1024, 256, 256, True),   # reorder: main-kernel gather

@@ -441,10 +441,11 @@ def test_ablation_ordering_channels_and_spikes(seed):
 
 
 def test_fwht_fp32_canonical_stage_order():
-    # The binary32 rounding order is this build's reading (stages h = 1, 2, 4,
-    # ...), not something the paper fixes. Check the vectorised oracle against
-    # that definition executed one scalar butterfly at a time, on data where the
-    # reverse order rounds differently (so the check has teeth).
+    # The binary32 rounding order is a reading the oracle and the kernels share
+    # (stages h = 1, 2, 4, ...), not something the paper fixes. Check the
+    # vectorised oracle against that definition executed one scalar butterfly
+    # at a time, on data where the reverse order rounds differently (so the
+    # check has teeth).
     K = 64
     rng = np.random.default_rng(77)
     x = (rng.standard_normal(K) * np.exp(rng.uniform(-8, 8, K))).astype(np.float16)
