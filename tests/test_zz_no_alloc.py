@@ -59,6 +59,8 @@ def test_no_alloc_decode_and_large_then_small():
     _compare(2048, 4096, 64, 128, 3)          # qkv's token count: a large workspace
     _compare(8, 8192, 112, 128, 4)            # decode shape, few-token kernels
     _compare(3, 1024, 32, 64, 5, perm=True)   # static reorder
+    _compare(2, 8192, 64, 128, 6)             # the layer in one launch (two tokens)
+    _compare(1, 4096, 48, 256, 7)             # the layer in one launch (one token)
 
 
 def test_no_alloc_rejects_oversize_without_enqueuing():
