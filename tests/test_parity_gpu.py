@@ -318,6 +318,50 @@ def test_linear_one_launch_layer(M, K, N, g, tiled):
             f"one-launch layer {M}x{K}x{N}")
 
 
+@pytest.mark.parametrize("K", [2048, 8192])
+@pytest.mark.parametrize("case", ["zero_row", "ones", "spike", "fp16_max"])
+def test_linear_one_launch_layer_degenerate(K, case):
+    # The one-launch layer's own copy of the quantizer on the quantizer's
+    # degenerate inputs: an all-zero token (alpha = 0), all-ones tokens (every
+    # group but the first has s_b = 0), a lone spike (Eq. 4: all codes +-7) and
+    # values at the fp16 limit. Y must equal the two calls bit for bit and the
+    # oracle within its bound.
+    rrs = _rrs()
+    g, N = 128, 48
+    X = np.zeros((2, K), np.float16)
+    if case == "ones":
+        X[0] = 1.0
+        X[1] = -2.0
+    elif case == "spike":
+        X[0, 123] = 300.0
+        X[1, 7] = -12.0
+    elif case == "fp16_max":
+        X[0, ::3] = 65504.0
+        X[1, 1::5] = -65504.0
+    else:   # zero_row: row 0 stays zero
+        X[1] = np.linspace(-3.0, 3.0, K).astype(np.float16)
+    W = synth.weights(synth.custom("dg", 2, K, N, g, 5 + K))
+    if case == "fp16_max":   # small weights keep Y inside the fp16 range
+        W = (W.astype(np.float32) * 1e-3).astype(np.float16)
+    print(f"[case] one-launch layer degenerate {case} K={K}", flush=True)
+    Wq, beta = rrs.prepare_weight(to_gpu(W))
+    Xg = to_gpu(X)
+    Xq, a, s = rrs.rotate_smooth_quant(Xg, g)
+    Y2 = rrs.w4a4_gemm(Xq, a, s, Wq, beta, g)
+    for M in (1, 2):
+        Y = rrs.linear(Xg[:M].contiguous(), Wq, beta, g)
+        Xq1, a1, s1 = rrs.rotate_smooth_quant(Xg[:M].contiguous(), g)
+        Yq = rrs.w4a4_gemm(Xq1, a1, s1, Wq, beta, g)
+        assert torch.equal(Y, Yq), f"{case} M={M}: one-launch layer differs from quant + gemm"
+    act = O.rotate_smooth_quant(X, g)
+    wq = O.prepare_weight(W)
+    P = O.group_partials(act.q, wq.q, g)
+    y_ref = O.output(P, act.s, act.alpha, wq.beta, norm=K)
+    check_y(to_np(Y).astype(np.float32), y_ref, P, act.s, act.alpha, wq.beta, K,
+            f"one-launch layer {case}")
+    assert torch.equal(Y, Y2)
+
+
 @pytest.mark.parametrize("M", [32, 64])
 def test_linear_decode_shape_more_tokens(M):
     # The decode layer (K = 8192, N = 28672) with 32 tokens (weight-streaming
