@@ -17,7 +17,9 @@ K further steps that also give the breakdown (their per-kernel events add
 their own cost to each step, reported as step_us_with_kernel_events).
 A decode-shaped measurement (M=8, K=8192, N=28672) reports HBM GB/s of the
 GEMM over algorithmic bytes, cycling through 4 weight copies (470 MB, more
-than the 256 MB Infinity Cache) so that every call streams its weight from HBM.
+than the 256 MB Infinity Cache) so that every call streams its weight from HBM:
+back to back (one event pair around the calls, as a decode loop issues them),
+and with an event after every call (*_per_call_events, gaps included).
 Further objects on the same line: few-token layers at the decode shape
 (M = 1..64), the gate/up and large prefill configurations against their own
 rooflines, the runtime-reorder comparison, the kernel comparison of the three
@@ -197,29 +199,47 @@ def decode_bench(args, torch, rrs, synth):
         prewarm(torch, lambda: rrs.w4a4_gemm(Xq, a, s, copies[next(it) % 4], beta, w.g, out=Y,
                                              flags=flags))
         torch.cuda.synchronize()
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
-        ev[0].record()
-        for i in range(n):
-            rrs.w4a4_gemm(Xq, a, s, copies[i % 4], beta, w.g, out=Y, flags=flags)
-            ev[i + 1].record()
-        torch.cuda.synchronize()
-        g_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(n)]
-        ev2 = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
-        ev2[0].record()
-        for i in range(n):
-            rrs.linear(X, copies[i % 4], beta, w.g, workspace=lws, out=Y, flags=flags)
-            ev2[i + 1].record()
-        torch.cuda.synchronize()
-        l_ms = [ev2[i].elapsed_time(ev2[i + 1]) for i in range(n)]
+
+        def back_to_back(fn):
+            # n calls between one event pair, as a decode loop issues them
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for i in range(n):
+                fn(i)
+            e1.record()
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / n
+
+        def per_call(fn):
+            # an event after every call: each record drains the stream, so
+            # these include the gap before every launch
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+            ev[0].record()
+            for i in range(n):
+                fn(i)
+                ev[i + 1].record()
+            torch.cuda.synchronize()
+            return [ev[i].elapsed_time(ev[i + 1]) for i in range(n)]
+
+        gemm = lambda i: rrs.w4a4_gemm(Xq, a, s, copies[i % 4], beta, w.g, out=Y, flags=flags)  # noqa: E731
+        lin = lambda i: rrs.linear(X, copies[i % 4], beta, w.g, workspace=lws, out=Y,  # noqa: E731
+                                   flags=flags)
+        gb = back_to_back(gemm)
+        lb = back_to_back(lin)
+        g_ms = per_call(gemm)
+        l_ms = per_call(lin)
         gm = sum(g_ms) / n
         lm = sum(l_ms) / n
         return {
-            "gemm_us": round(gm * 1e3, 3),
-            "gemm_us_min": round(min(g_ms) * 1e3, 3),
-            "gemm_GBps": round(alg / (gm * 1e-3) / 1e9, 1),
-            "gemm_frac_hbm": round(alg / (gm * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-            "linear_us": round(lm * 1e3, 3),
-            "linear_GBps": round(alg / (lm * 1e-3) / 1e9, 1),
+            "gemm_us": round(gb * 1e3, 3),
+            "gemm_GBps": round(alg / (gb * 1e-3) / 1e9, 1),
+            "gemm_frac_hbm": round(alg / (gb * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "linear_us": round(lb * 1e3, 3),
+            "linear_GBps": round(alg / (lb * 1e-3) / 1e9, 1),
+            "gemm_us_per_call_events": round(gm * 1e3, 3),
+            "gemm_us_per_call_events_min": round(min(g_ms) * 1e3, 3),
+            "linear_us_per_call_events": round(lm * 1e3, 3),
         }
 
     out = {"config": {"workload": "decode", "M": w.M, "K": w.K, "N": w.N, "group_size": w.g},
