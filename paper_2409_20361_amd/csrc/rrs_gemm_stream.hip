@@ -65,10 +65,11 @@
 // an eighth of K (16 rows x 512 bytes per block, the same 16 KB ring per wave)
 // and holding the codes of two blocks of 16 tokens (64 registers per block,
 // half of what a quarter of K would take), one workgroup of 512 threads per
-// compute unit (128 KB of ring and 32 KB of partial sums). Every weight
-// fragment is unpacked once for both token blocks; the 2 x 4 (token block,
-// accumulator row) pairs of each lane are dealt to the eight waves for the
-// fixed-order sum and the stores.
+// compute unit (128 KB of ring and 32 KB of partial sums), each workgroup
+// streaming one contiguous range of column blocks. Every weight fragment is
+// unpacked once for both token blocks; the 2 x 4 (token block, accumulator
+// row) pairs of each lane are dealt to the eight waves for the fixed-order sum
+// and the stores.
 #include "rrs_device.h"
 #include "rrs_stream.h"
 
@@ -141,7 +142,15 @@ __global__ __launch_bounds__(64 * W) void gemm_stream_kernel(
       return my + (i % S::RS) * S::SB;
   };
   const int nblk = N / kRows;
-  const int mine = (nblk - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x;
+  // Column blocks of this workgroup: w, w + grid, ... with four waves (two
+  // workgroups per compute unit); one contiguous range with eight (one per
+  // compute unit), which streams 1-2 us faster there and 1.5 us slower with
+  // four (decode shape, back-to-back calls).
+  constexpr bool kRange = W == 8;
+  const int b_lo = kRange ? (int)(((long long)blockIdx.x * nblk) / (int)gridDim.x) : (int)blockIdx.x;
+  const int b_step = kRange ? 1 : (int)gridDim.x;
+  const int mine = kRange ? (int)(((long long)(blockIdx.x + 1) * nblk) / (int)gridDim.x) - b_lo
+                          : (nblk - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x;
   const int items = mine * S::SPB;  // sub-buffers this wave streams, in order
 
   // Direct loads of item i (sub-buffer i % SPB of column block i / SPB) into
@@ -149,7 +158,7 @@ __global__ __launch_bounds__(64 * W) void gemm_stream_kernel(
   // chunks permuted; tiled: each instruction one tile (the block's 16 rows are
   // one 16-row block, n0 a multiple of 16).
   auto issue = [&](int i) {
-    const int blk = (int)blockIdx.x + (i / S::SPB) * (int)gridDim.x;
+    const int blk = b_lo + (i / S::SPB) * b_step;
     const int sp = i % S::SPB;
     uint8_t* dst = slot_of(i);
     const uint8_t* base = Wq + (size_t)blk * kRows * krow;
@@ -323,7 +332,7 @@ __global__ __launch_bounds__(64 * W) void gemm_stream_kernel(
   if constexpr (MQ > 0) __syncthreads();
 
   for (int tb = 0; tb < mine; ++tb) {
-    const int blk = (int)blockIdx.x + tb * (int)gridDim.x;
+    const int blk = b_lo + tb * b_step;
     float bcol = 0.0f;  // beta of this lane's column, requested early
     if constexpr (!kPartials) bcol = w_scale[blk * kRows + c];
     float f[TB][4];
