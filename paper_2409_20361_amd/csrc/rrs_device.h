@@ -287,7 +287,36 @@ __device__ __forceinline__ uint32_t quant_pack8(const float* v, float m) {
   return lo | hi;
 }
 
-// Store E/2 packed bytes (E nibbles, low nibble = even index) at dst.
+// The order of the runtime reorder as one unsigned 64-bit sort key per block:
+// the block key's bits above the complemented block index. Keys are
+// non-negative and finite, so their bit patterns order as the keys do, and a
+// larger sort key means a larger key, or an equal key and a smaller index.
+__device__ __forceinline__ unsigned long long block_sort_key(float key, int b) {
+  return ((unsigned long long)__float_as_uint(key) << 32) |
+         (unsigned long long)(0xFFFFFFFFu - (uint32_t)b);
+}
+__device__ __forceinline__ float sort_key_value(unsigned long long k) {
+  return __uint_as_float((uint32_t)(k >> 32));
+}
+
+// Rank of sort key `me` among the NB sort keys in LDS: how many are larger
+// (two keys per 128-bit broadcast read, one 64-bit compare each; the rank of
+// the float keys with their tie rule took about five operations per key).
+template <int NB>
+__device__ __forceinline__ int block_rank(const unsigned long long* sk, unsigned long long me) {
+  static_assert(NB % 2 == 0, "pairs of keys");
+  int rank = 0;
+#pragma unroll 8
+  for (int q = 0; q < NB / 2; ++q) {
+    const uint4 v = reinterpret_cast<const uint4*>(sk)[q];
+    const unsigned long long k0 = ((unsigned long long)v.y << 32) | v.x;
+    const unsigned long long k1 = ((unsigned long long)v.w << 32) | v.z;
+    rank += (k0 > me) ? 1 : 0;
+    rank += (k1 > me) ? 1 : 0;
+  }
+  return rank;
+}
+
 // ---------------------------------------------------------------------------
 // Runtime reorder (Fig. 4 step (1) at run time), computed by every workgroup
 // of the quantizer's second pass: the key of block b (32 consecutive
@@ -299,8 +328,8 @@ __device__ __forceinline__ uint32_t quant_pack8(const float* v, float m) {
 // ---------------------------------------------------------------------------
 template <int NT, int NB>
 __device__ __forceinline__ void block_order_wg(const float* __restrict__ part, int nrows,
-                                               float* red, float* key, int* sblk, float* skey,
-                                               int tid) {
+                                               float* red, unsigned long long* key, int* sblk,
+                                               float* skey, int tid) {
   static_assert(NB % 4 == 0 && NB / 4 <= NT, "float4 columns, one per thread at least");
   constexpr int NQ = NB / 4;   // float4 columns of a partial row
   constexpr int NS = NT / NQ;  // row slices
@@ -335,23 +364,14 @@ __device__ __forceinline__ void block_order_wg(const float* __restrict__ part, i
   for (int b = tid; b < NB; b += NT) {
     float k = red[b];
     for (int q = 1; q < NS; ++q) k = fmaxf(k, red[q * NB + b]);
-    key[b] = k;
+    key[b] = block_sort_key(k, b);
   }
   __syncthreads();
   for (int b = tid; b < NB; b += NT) {
-    const float c = key[b];
-    int rank = 0;
-#pragma unroll 4
-    for (int q = 0; q < NB / 4; ++q) {
-      const float4 k4 = reinterpret_cast<const float4*>(key)[q];
-      const int j = 4 * q;
-      rank += (k4.x > c || (k4.x == c && j < b)) ? 1 : 0;
-      rank += (k4.y > c || (k4.y == c && j + 1 < b)) ? 1 : 0;
-      rank += (k4.z > c || (k4.z == c && j + 2 < b)) ? 1 : 0;
-      rank += (k4.w > c || (k4.w == c && j + 3 < b)) ? 1 : 0;
-    }
+    const unsigned long long me = key[b];
+    const int rank = block_rank<NB>(key, me);
     sblk[rank] = b;
-    skey[rank] = c;
+    skey[rank] = sort_key_value(me);
   }
   __syncthreads();
 }

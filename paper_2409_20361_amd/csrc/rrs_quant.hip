@@ -188,7 +188,7 @@ __global__ __launch_bounds__(Teams<K>::threads) void quant_kernel(
   __shared__ __attribute__((aligned(16))) float slots[slot_floats<K>()];
   __shared__ float rg[256];
   __shared__ float red[16];
-  __shared__ __attribute__((aligned(16))) float key[kOrder ? NB : 4];
+  __shared__ __attribute__((aligned(16))) unsigned long long key[kOrder ? NB : 2];
   __shared__ float skey[kOrder ? NB : 1];
   __shared__ int sblk[kOrder ? NB : 1];
   __shared__ __attribute__((aligned(16))) float ored[kOrder ? 4 * kThreads : 4];

@@ -61,7 +61,7 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
   __shared__ float red[4];
   __shared__ float rg[256];
   __shared__ float sg[256];
-  __shared__ __attribute__((aligned(16))) float key[kReorder ? NB : 4];
+  __shared__ __attribute__((aligned(16))) unsigned long long key[kReorder ? NB : 2];
   __shared__ float skey[kReorder ? NB : 1];
   __shared__ int sblk[kReorder ? NB : 1];
   __shared__ int missed;
@@ -157,7 +157,7 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
     for (int o = 1; o < tps; o <<= 1) s = fmaxf(s, __shfl_xor(s, o, 64));
   if (owner) {
     if constexpr (kReorder) {
-      key[b] = s;  // block b's key: its largest channel maximum
+      key[b] = block_sort_key(s, b);  // block b's key: its largest channel maximum
     } else {
       rg[b] = (s == 0.0f) ? 0.0f : __fdiv_rn(1.0f, s);  // s_b and r_b = fl(1 / s_b)
       sg[b] = s;
@@ -166,21 +166,12 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
   __syncthreads();
   if constexpr (kReorder) {
     // Rank of block t: blocks with a larger key, or an equal key and a smaller
-    // index, come first (broadcast LDS reads).
+    // index, come first: one compare of the 64-bit sort keys per block.
     if (t < NB) {
-      const float c = key[t];
-      int rank = 0;
-#pragma unroll 4
-      for (int q = 0; q < NB / 4; ++q) {
-        const float4 k4 = reinterpret_cast<const float4*>(key)[q];
-        const int bb = 4 * q;
-        rank += (k4.x > c || (k4.x == c && bb < t)) ? 1 : 0;
-        rank += (k4.y > c || (k4.y == c && bb + 1 < t)) ? 1 : 0;
-        rank += (k4.z > c || (k4.z == c && bb + 2 < t)) ? 1 : 0;
-        rank += (k4.w > c || (k4.w == c && bb + 3 < t)) ? 1 : 0;
-      }
+      const unsigned long long me = key[t];
+      const int rank = block_rank<NB>(key, me);
       sblk[rank] = t;
-      skey[rank] = c;
+      skey[rank] = sort_key_value(me);
     }
     __syncthreads();
     // s_b over the sorted blocks of group b.

@@ -202,7 +202,7 @@ __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
   __shared__ __attribute__((aligned(16))) float rows[kQuantWaves * S::RW * S::RF];
   __shared__ float rg[GMAX];
   __shared__ __attribute__((aligned(16))) float red[kOrder ? 4 * NT : NT];
-  __shared__ __attribute__((aligned(16))) float key[kOrder ? NB : 4];
+  __shared__ __attribute__((aligned(16))) unsigned long long key[kOrder ? NB : 2];
   __shared__ float skey[kOrder ? NB : 1];
   __shared__ int sblk[kOrder ? NB : 1];
 
@@ -394,7 +394,7 @@ __global__ __launch_bounds__(WAVES * 64) void rot_quant_fused_kernel(
   __shared__ float wmax[WAVES][kOrder ? NB : GMAX];
   __shared__ float red[NT];
   __shared__ float rg[GMAX];
-  __shared__ __attribute__((aligned(16))) float key[kOrder ? NB : 4];
+  __shared__ __attribute__((aligned(16))) unsigned long long key[kOrder ? NB : 2];
   __shared__ float skey[kOrder ? NB : 1];
   __shared__ int sblk[kOrder ? NB : 1];
   __shared__ int missed;
@@ -555,7 +555,7 @@ __global__ __launch_bounds__(WAVES * 64) void rot_quant_fused_kernel(
         m2 = fmaxf(m2, mm);
       }
       if (!ok2) missed = 1;  // benign race: every writer writes 1
-      if (serve && tp == 0) key[bb] = m2;
+      if (serve && tp == 0) key[bb] = block_sort_key(m2, bb);
     }
     __syncthreads();
     if (tid == 0) {
@@ -567,21 +567,12 @@ __global__ __launch_bounds__(WAVES * 64) void rot_quant_fused_kernel(
         __hip_atomic_store(header + kEpochWord, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     // Rank of block t: blocks with a larger key, or an equal key and a smaller
-    // index, come first (broadcast LDS reads).
+    // index, come first: one compare of the 64-bit sort keys per block.
     if (tid < NB) {
-      const float c = key[tid];
-      int rank = 0;
-#pragma unroll 4
-      for (int q = 0; q < NB / 4; ++q) {
-        const float4 k4 = reinterpret_cast<const float4*>(key)[q];
-        const int b4 = 4 * q;
-        rank += (k4.x > c || (k4.x == c && b4 < tid)) ? 1 : 0;
-        rank += (k4.y > c || (k4.y == c && b4 + 1 < tid)) ? 1 : 0;
-        rank += (k4.z > c || (k4.z == c && b4 + 2 < tid)) ? 1 : 0;
-        rank += (k4.w > c || (k4.w == c && b4 + 3 < tid)) ? 1 : 0;
-      }
+      const unsigned long long me = key[tid];
+      const int rank = block_rank<NB>(key, me);
       sblk[rank] = tid;
-      skey[rank] = c;
+      skey[rank] = sort_key_value(me);
     }
     __syncthreads();
     const bool failed = missed != 0;  // uniform over the workgroup
