@@ -317,19 +317,84 @@ __device__ __forceinline__ int block_rank(const unsigned long long* sk, unsigned
   return rank;
 }
 
+// Count of the entries of A larger than x, for A of L distinct sort keys in
+// LDS in decreasing order (L a power of two): a binary search, log2(L) + 1
+// dependent reads.
+template <int L>
+__device__ __forceinline__ int count_greater(const unsigned long long* A, unsigned long long x) {
+  int lo = 0;  // A[0 .. lo - 1] > x
+#pragma unroll
+  for (int s = L / 2; s >= 1; s >>= 1)
+    if (A[lo + s - 1] > x) lo += s;
+  return lo + (A[lo] > x ? 1 : 0);
+}
+
+// The runtime reorder's ranking: key holds the NB sort keys (block_sort_key);
+// on return sblk[p] is the block at sorted position p and skey[p] its key. The
+// blocks fall into lists of L = min(NB, 64); a block's rank is the number of
+// larger sort keys in its own list (block_rank, broadcast reads) plus, for
+// every other list, the number of larger ones in that list once sorted
+// (count_greater). The sort keys are distinct, so the ranks are a permutation
+// and equal to the count over all NB keys. srt is NB entries of LDS scratch.
+// All NT threads of the workgroup call it; it ends with a barrier.
+template <int NB, int NT>
+__device__ __forceinline__ void rank_blocks(const unsigned long long* key, unsigned long long* srt,
+                                            int* sblk, float* skey, int tid) {
+  constexpr int L = NB < 64 ? NB : 64;
+  constexpr int NL = NB / L;
+  constexpr int PER = (NB + NT - 1) / NT;  // blocks per thread
+  static_assert(NB % L == 0 && (L & (L - 1)) == 0, "lists of a power of two");
+  unsigned long long me[PER];
+  int r[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int b = tid + i * NT;
+    me[i] = 0;
+    r[i] = 0;
+    if (b < NB) {
+      me[i] = key[b];
+      r[i] = block_rank<L>(key + (b / L) * L, me[i]);
+      if constexpr (NL > 1) srt[(b / L) * L + r[i]] = me[i];
+    }
+  }
+  if constexpr (NL > 1) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int b = tid + i * NT;
+      if (b < NB) {
+        const int own = b / L;
+#pragma unroll
+        for (int w = 0; w < NL; ++w)
+          if (w != own) r[i] += count_greater<L>(srt + w * L, me[i]);
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int b = tid + i * NT;
+    if (b < NB) {
+      sblk[r[i]] = b;
+      skey[r[i]] = sort_key_value(me[i]);
+    }
+  }
+  __syncthreads();
+}
+
 // ---------------------------------------------------------------------------
 // Runtime reorder (Fig. 4 step (1) at run time), computed by every workgroup
 // of the quantizer's second pass: the key of block b (32 consecutive
 // channels) is the largest of the nrows partial rows part[r][b] (r < nrows,
 // NB = K / 32 entries per row); keys are ranked largest first, equal keys in
 // increasing block index. On return (after a barrier) sblk[p] is the block at
-// sorted position p and skey[p] its key. `red` holds at least 4 NT floats.
-// All NT threads of the workgroup must call it.
+// sorted position p and skey[p] its key. `red` holds at least 4 NT floats,
+// `key` and `srt` NB entries each. All NT threads of the workgroup must call it.
 // ---------------------------------------------------------------------------
 template <int NT, int NB>
 __device__ __forceinline__ void block_order_wg(const float* __restrict__ part, int nrows,
-                                               float* red, unsigned long long* key, int* sblk,
-                                               float* skey, int tid) {
+                                               float* red, unsigned long long* key,
+                                               unsigned long long* srt, int* sblk, float* skey,
+                                               int tid) {
   static_assert(NB % 4 == 0 && NB / 4 <= NT, "float4 columns, one per thread at least");
   constexpr int NQ = NB / 4;   // float4 columns of a partial row
   constexpr int NS = NT / NQ;  // row slices
@@ -367,13 +432,7 @@ __device__ __forceinline__ void block_order_wg(const float* __restrict__ part, i
     key[b] = block_sort_key(k, b);
   }
   __syncthreads();
-  for (int b = tid; b < NB; b += NT) {
-    const unsigned long long me = key[b];
-    const int rank = block_rank<NB>(key, me);
-    sblk[rank] = b;
-    skey[rank] = sort_key_value(me);
-  }
-  __syncthreads();
+  rank_blocks<NB, NT>(key, srt, sblk, skey, tid);
 }
 
 template <int E>

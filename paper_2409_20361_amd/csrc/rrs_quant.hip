@@ -189,6 +189,7 @@ __global__ __launch_bounds__(Teams<K>::threads) void quant_kernel(
   __shared__ float rg[256];
   __shared__ float red[16];
   __shared__ __attribute__((aligned(16))) unsigned long long key[kOrder ? NB : 2];
+  __shared__ __attribute__((aligned(16))) unsigned long long srt[kOrder ? NB : 2];
   __shared__ float skey[kOrder ? NB : 1];
   __shared__ int sblk[kOrder ? NB : 1];
   __shared__ __attribute__((aligned(16))) float ored[kOrder ? 4 * kThreads : 4];
@@ -215,7 +216,7 @@ __global__ __launch_bounds__(Teams<K>::threads) void quant_kernel(
     }
     __syncthreads();
   } else if constexpr (kOrder) {
-    block_order_wg<kThreads, NB>(gpart, nparts, ored, key, sblk, skey, tid);
+    block_order_wg<kThreads, NB>(gpart, nparts, ored, key, srt, sblk, skey, tid);
     if (tid < G) {
       const int per = g / kReorderBlock;
       float s = 0.0f;

@@ -62,6 +62,7 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
   __shared__ float rg[256];
   __shared__ float sg[256];
   __shared__ __attribute__((aligned(16))) unsigned long long key[kReorder ? NB : 2];
+  __shared__ __attribute__((aligned(16))) unsigned long long srt[kReorder ? NB : 2];
   __shared__ float skey[kReorder ? NB : 1];
   __shared__ int sblk[kReorder ? NB : 1];
   __shared__ int missed;
@@ -165,15 +166,8 @@ __global__ __launch_bounds__(kRowThreads) void quant_rows_kernel(
   }
   __syncthreads();
   if constexpr (kReorder) {
-    // Rank of block t: blocks with a larger key, or an equal key and a smaller
-    // index, come first: one compare of the 64-bit sort keys per block.
-    if (t < NB) {
-      const unsigned long long me = key[t];
-      const int rank = block_rank<NB>(key, me);
-      sblk[rank] = t;
-      skey[rank] = sort_key_value(me);
-    }
-    __syncthreads();
+    // Blocks with a larger key, or an equal key and a smaller index, first.
+    rank_blocks<NB, kRowThreads>(key, srt, sblk, skey, t);
     // s_b over the sorted blocks of group b.
     if (t < G) {
       const int per = g / kReorderBlock;

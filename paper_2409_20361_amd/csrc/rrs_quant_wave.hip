@@ -203,6 +203,7 @@ __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
   __shared__ float rg[GMAX];
   __shared__ __attribute__((aligned(16))) float red[kOrder ? 4 * NT : NT];
   __shared__ __attribute__((aligned(16))) unsigned long long key[kOrder ? NB : 2];
+  __shared__ __attribute__((aligned(16))) unsigned long long srt[kOrder ? NB : 2];
   __shared__ float skey[kOrder ? NB : 1];
   __shared__ int sblk[kOrder ? NB : 1];
 
@@ -267,7 +268,7 @@ __global__ __launch_bounds__(kQuantWaves * 64) void quant_wave_kernel(
     }
     __syncthreads();
   } else if constexpr (kOrder) {
-    block_order_wg<NT, NB>(gpart, nparts, red, key, sblk, skey, tid);
+    block_order_wg<NT, NB>(gpart, nparts, red, key, srt, sblk, skey, tid);
     if (tid < G) {
       const int per = g / kReorderBlock;
       float sv = 0.0f;
@@ -395,6 +396,7 @@ __global__ __launch_bounds__(WAVES * 64) void rot_quant_fused_kernel(
   __shared__ float red[NT];
   __shared__ float rg[GMAX];
   __shared__ __attribute__((aligned(16))) unsigned long long key[kOrder ? NB : 2];
+  __shared__ __attribute__((aligned(16))) unsigned long long srt[kOrder ? NB : 2];
   __shared__ float skey[kOrder ? NB : 1];
   __shared__ int sblk[kOrder ? NB : 1];
   __shared__ int missed;
@@ -566,15 +568,8 @@ __global__ __launch_bounds__(WAVES * 64) void rot_quant_fused_kernel(
       if (blockIdx.x == 0)
         __hip_atomic_store(header + kEpochWord, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    // Rank of block t: blocks with a larger key, or an equal key and a smaller
-    // index, come first: one compare of the 64-bit sort keys per block.
-    if (tid < NB) {
-      const unsigned long long me = key[tid];
-      const int rank = block_rank<NB>(key, me);
-      sblk[rank] = tid;
-      skey[rank] = sort_key_value(me);
-    }
-    __syncthreads();
+    // Blocks with a larger key, or an equal key and a smaller index, first.
+    rank_blocks<NB, NT>(key, srt, sblk, skey, tid);
     const bool failed = missed != 0;  // uniform over the workgroup
     // s_b over the sorted blocks of group b.
     if (tid < G) {
