@@ -35,7 +35,12 @@ __global__ __launch_bounds__(kThreads) void gemm_stream_gather_kernel(
   constexpr int NB = K / kReorderBlock;  // blocks of a row
   constexpr int NBW = NB / kWaves;       // blocks of a wave's quarter
   constexpr int BPS = S::SBW / 16;       // blocks per sub-buffer
+  constexpr int RPW = S::SB / (K / 2);   // token rows staged per wave
+  constexpr int RPR = kWaves * RPW;      // token rows staged per round
+  static_assert(RPW >= 1 && S::SB % (K / 2) == 0, "whole token rows per sub-buffer");
+  static_assert(NB % 16 == 0, "the chunk swizzle stays inside a row");
   static_assert(NBW <= 64 && S::R % 16 == 0, "one lane per block of the quarter");
+  static_assert(BPS % 4 == 0, "blocks of a sub-buffer in fours");
   __shared__ __attribute__((aligned(16))) uint8_t ring[kWaves * S::RS * S::SB];
   __shared__ __attribute__((aligned(16))) v4f part[2][kWaves][64];
   __shared__ int inv[NB];     // natural block -> position block
@@ -48,6 +53,7 @@ __global__ __launch_bounds__(kThreads) void gemm_stream_gather_kernel(
   const int q = lane >> 4;
   constexpr size_t krow = (size_t)K / 2;
   uint8_t* my = ring + kq * S::RS * S::SB;
+  uint8_t* stage = ring + (S::RS - 1) * S::SB;  // + w RS SB: wave w's staged rows
   const int nblk = N / kRows;
   const int mine = (nblk - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x;
   const int items = mine * S::SPB;
@@ -82,6 +88,23 @@ __global__ __launch_bounds__(kThreads) void gemm_stream_gather_kernel(
       return c * S::SBW + 16 * (jc ^ (c & S::SW)) + 4 * q;
   };
 
+  // Copy of token rows r0 + w RPW .. r0 + w RPW + RPW - 1 (those below M) into
+  // the last sub-buffer of wave w's ring, by wave w. Position block j of row r
+  // lands in 16-byte chunk j ^ (r & 15) of the row's copy, so that the 16 token
+  // rows of one block fall in different LDS banks when gathered.
+  auto stage_rows = [&](int r0) {
+#pragma unroll
+    for (int ii = 0; ii < S::NL; ++ii) {
+      const int off = 1024 * ii + 16 * lane;  // byte of this wave's rows
+      const int r = r0 + kq * RPW + off / (int)krow;
+      const int j = ((off % (int)krow) >> 4) ^ (r & 15);
+      if (r < M)
+        __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(Xq + (size_t)r * krow + 16 * j),
+                                         (lds_ptr_t)(stage + kq * S::RS * S::SB + 1024 * ii),
+                                         16, 0, 0);
+    }
+  };
+  stage_rows(0);
 #pragma unroll
   for (int i = 0; i < S::RS - 1; ++i)
     if (i < items) issue(i);
@@ -101,15 +124,32 @@ __global__ __launch_bounds__(kThreads) void gemm_stream_gather_kernel(
   __syncthreads();
 
   // Token row c (row M - 1 for c >= M, never stored): dword q of the position
-  // block of every natural block of this wave's quarter.
-  const uint8_t* arow = Xq + (size_t)min(c, M - 1) * krow + 4 * q;
+  // block of every natural block of this wave's quarter. The rows are copied
+  // whole into LDS first, into the last sub-buffer of every wave's ring (the
+  // prefetch above leaves it empty), RPW rows per wave and RPR per round;
+  // gathered straight from global memory, one load touched a cache line per
+  // token row and block, 16 times the lines of the whole copy.
+  const int rc = min(c, M - 1);
   uint32_t aw[NBW];
+  for (int r0 = 0; r0 < M; r0 += RPR) {
+    if (r0 > 0) {
+      __syncthreads();  // the previous round's rows have been read
+      stage_rows(r0);
+    }
+    if (r0 == 0 && items >= S::RS - 1)
+      wait_vm<(S::RS - 1) * S::NL>();  // the copy, issued before the prefetch
+    else
+      wait_vm<0>();
+    __syncthreads();
+    if (rc >= r0 && rc < r0 + RPR) {
+      const uint8_t* arow = stage + ((rc - r0) / RPW) * S::RS * S::SB +
+                            ((rc - r0) % RPW) * krow + 4 * q;
 #pragma unroll
-  for (int b = 0; b < NBW; ++b) {
-    aw[b] = *reinterpret_cast<const uint32_t*>(arow + 16 * inv[kq * NBW + b]);
-    // eight loads at a time: all 64 addresses at once would need 128 registers
-    if (b % 8 == 7) __builtin_amdgcn_sched_barrier(0);
+      for (int b = 0; b < NBW; ++b)
+        aw[b] = *reinterpret_cast<const uint32_t*>(arow + 16 * (inv[kq * NBW + b] ^ (rc & 15)));
+    }
   }
+  __syncthreads();  // the ring's last sub-buffers are free again
   const float sv = sbl[kq * NBW + (lane < NBW ? lane : 0)];
 
   constexpr int kMagic = 0x4B400000;  // bits of 1.5 * 2^23
@@ -131,23 +171,35 @@ __global__ __launch_bounds__(kThreads) void gemm_stream_gather_kernel(
         wait_vm<0>();
       }
       const uint8_t* buf = my + (i % S::RS) * S::SB;
+      // Four blocks at a time: their weight words are read together and their
+      // four products issued back to back, so the LDS latency and the MFMA
+      // latency are paid once per four blocks; the rescales then follow in
+      // natural block order (the fp32 sum's order is unchanged).
 #pragma unroll
-      for (int bl = 0; bl < BPS; ++bl) {
-        const int b = sp * BPS + bl;  // natural block of the wave's quarter
-        const uint32_t w = *reinterpret_cast<const uint32_t*>(buf + woff(bl));
-        const v4i acc = __builtin_amdgcn_mfma_i32_16x16x32_i8(unpack_dword(aw[b]),
-                                                              unpack_dword(w), seed, 0, 0, 0);
-        const float s =
-            __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sv), b));
-        const v4f accf = __builtin_bit_cast(v4f, acc);
+      for (int bl = 0; bl < BPS; bl += 4) {
+        uint32_t w[4];
+        v4i acc[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          f[r] = __builtin_fmaf(s, accf[r] - 12582912.0f, f[r]);
-          // Pin the update here: otherwise every block's rescale sinks to the
-          // end of the column block and all 64 accumulators stay live.
-          asm volatile("" : "+v"(f[r]));
+        for (int u = 0; u < 4; ++u) w[u] = *reinterpret_cast<const uint32_t*>(buf + woff(bl + u));
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          acc[u] = __builtin_amdgcn_mfma_i32_16x16x32_i8(unpack_dword(aw[sp * BPS + bl + u]),
+                                                         unpack_dword(w[u]), seed, 0, 0, 0);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int b = sp * BPS + bl + u;  // natural block of the wave's quarter
+          const float s = __builtin_bit_cast(
+              float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sv), b));
+          const v4f accf = __builtin_bit_cast(v4f, acc[u]);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            f[r] = __builtin_fmaf(s, accf[r] - 12582912.0f, f[r]);
+            // Pin the update here: otherwise every block's rescale sinks to
+            // the end of the column block and all 64 accumulators stay live.
+            asm volatile("" : "+v"(f[r]));
+          }
         }
-        if (bl % 4 == 3) __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     part[tb & 1][kq][lane] = v4f{f[0], f[1], f[2], f[3]};
