@@ -115,19 +115,33 @@ def test_quant_reorder_full_size():
     _quant_case(synth.activations(w), w.g, 0, "qkv")
 
 
-def test_quant_reorder_ties():
-    rrs = _rrs()
+@pytest.mark.parametrize("M,K", [(8, 1024), (8, 8192), (40, 8192)])
+def test_quant_reorder_ties(M, K):
     # all-zero input: every key is 0, the order is the identity, all codes 0
-    X = np.zeros((8, 1024), np.float16)
-    act, order, (Xq, a, s, bo) = _quant_case(X, 128, 0, "zeros")
-    np.testing.assert_array_equal(to_np(bo), np.arange(1024 // BLOCK))
+    X = np.zeros((M, K), np.float16)
+    act, order, (Xq, a, s, bo) = _quant_case(X, 128, 0, f"zeros {M}x{K}")
+    np.testing.assert_array_equal(to_np(bo), np.arange(K // BLOCK))
     assert not to_np(Xq).any()
-    # repeated blocks without rotation: equal keys keep increasing block index
-    rng = np.random.default_rng(9)
-    base = rng.uniform(-1, 1, size=(40, BLOCK))
-    scale = rng.choice([1.0, 2.0, 4.0], size=4096 // BLOCK)
+
+
+# Repeated blocks without rotation: every block is the same block scaled by 1,
+# 2 or 4 (exact in fp16), so the K/32 keys take three values and equal keys
+# fall in every list of 64 the ranking merges; equal keys keep increasing
+# block index. One launch per row (M <= 16), the many-token one-launch kernel
+# (K <= 4096) and the two-launch form (K = 8192 / 16384 with more rows).
+@pytest.mark.parametrize("M,K", [(40, 4096), (3000, 4096), (1, 8192), (8, 8192), (16, 8192),
+                                 (40, 8192), (20, 16384), (2, 512)])
+def test_quant_reorder_repeated_blocks(M, K):
+    rrs = _rrs()
+    rng = np.random.default_rng(9 + M + K)
+    base = rng.uniform(-1, 1, size=(M, BLOCK))
+    scale = rng.choice([1.0, 2.0, 4.0], size=K // BLOCK)
     X = np.concatenate([base * c for c in scale], axis=1).astype(np.float16)
-    _quant_case(X, 128, rrs.SKIP_ROTATION, "repeated blocks")
+    act, order, _ = _quant_case(X, 128, rrs.SKIP_ROTATION, f"repeated blocks {M}x{K}")
+    # the oracle's order itself: blocks of scale 4, then 2, then 1, each run in
+    # increasing block index
+    expect = np.concatenate([np.flatnonzero(scale == c) for c in (4.0, 2.0, 1.0)])
+    np.testing.assert_array_equal(order, expect)
 
 
 def _tol_terms(act_q, wq_q, s, g, M):
