@@ -602,7 +602,7 @@ def cpu_baseline(synth):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+        print(json.dumps({"error": "the benchmark measures one GPU (one process, no collectives); --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     import torch
