@@ -594,6 +594,22 @@ def test_reorder_sorted_and_largest_first(block):
     assert np.all(np.diff(act.s) <= 0)
 
 
+@pytest.mark.parametrize("block", [1, 32])
+def test_reorder_equal_keys_keep_index_order(block):
+    # Every block of `block` channels is one base block scaled by 1, 2 or 4
+    # (exact in fp16), so the keys take three values and most of them tie:
+    # the order is the blocks of scale 4, then 2, then 1, each run in
+    # increasing block index (Fig. 4 step (1) with equal keys in index order).
+    rng = np.random.default_rng(5)
+    nb = 1024 // block
+    base = rng.uniform(-1, 1, size=(6, block))
+    scale = rng.choice([1.0, 2.0, 4.0], size=nb)
+    X = np.concatenate([base * c for c in scale], axis=1).astype(np.float16)
+    _, order, _ = O.rotate_smooth_quant_reorder(X, 128, block, rotate=False)
+    expect = np.concatenate([np.flatnonzero(scale == c) for c in (4.0, 2.0, 1.0)])
+    np.testing.assert_array_equal(order, expect)
+
+
 def test_reorder_sum_of_scales_is_minimal_brute_force():
     # Cutting the sorted blocks into consecutive groups minimises the sum of
     # the group maxima over every assignment of blocks to positions: checked
